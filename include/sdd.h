@@ -1,0 +1,201 @@
+/*
+ * sdd.h -- C ABI of the MI355X (gfx950) hot path of verifier-skipped
+ * speculative diffusion decoding.
+ *
+ * Paper: "From Positionwise Confidence to Prefix Scheduling: Verifier Skipping
+ * in Speculative Decoding".  A diffusion drafter proposes a block
+ * x^_1..x^_gamma; the target model verifies it in one call and accepts a prefix
+ * of length L in {0..gamma} (Sec. 3.1 "Strict Decoding and Verifier
+ * Skipping"); a confidence scheduler may instead commit a prefix of length K
+ * without calling the target (Sec. 4.1 "Skip Policy", candidate skip length
+ * equation).
+ *
+ * Conventions for every function:
+ *  - returns SDD_OK (0) or a negative SDD_E* code; sdd_last_error() gives a
+ *    human-readable message for the last failure on the calling thread;
+ *  - argument errors are detected synchronously, before anything is launched;
+ *  - pointers documented as "device" are caller-owned device allocations
+ *    (e.g. from torch); the library never allocates device memory;
+ *  - work is enqueued on the given HIP stream and completes asynchronously;
+ *    the caller synchronizes before reading outputs;
+ *  - integer outputs are deterministic: reductions use fixed orders and no
+ *    floating-point atomics, so repeated calls give bit-identical results.
+ */
+#ifndef SDD_H
+#define SDD_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct ihipStream_t* sdd_stream_t; /* a hipStream_t; NULL = default stream */
+
+/* status codes */
+#define SDD_OK 0
+#define SDD_EINVAL (-1)       /* bad argument */
+#define SDD_ENOMEM (-2)       /* buffer too small / host allocation failed */
+#define SDD_EHIP (-3)         /* a HIP call or kernel launch failed */
+#define SDD_ECAPACITY (-4)    /* KV cache or workspace capacity exceeded */
+#define SDD_EUNSUPPORTED (-5) /* shape/dtype/mode combination not built */
+
+/* element types */
+#define SDD_F32 0
+#define SDD_BF16 1
+
+/* acceptance modes (Sec. 3.1; Appendix "Baselines and Sweep Settings") */
+#define SDD_GREEDY 0  /* accept x^_j iff it is the target argmax (lowest index on ties) */
+#define SDD_RATIO 1   /* accept iff u_j < p(x^_j)/q(x^_j) (min(1, p/q) test of [Leviathan 2023]) */
+#define SDD_TOPK 2    /* accept iff x^_j is among the k largest target logits */
+#define SDD_LENIENT 3 /* accept iff z(x^_j) - max_v z(v) >= log(lenience); lenience 1 = greedy */
+
+/* tensor kinds for sdd_model_load_tensor (row-major, PyTorch Linear [out][in]) */
+#define SDD_T_EMBED 0      /* [vocab][d_model] */
+#define SDD_T_LM_HEAD 1    /* [vocab][d_model] */
+#define SDD_T_FINAL_NORM 2 /* [d_model], fp32 */
+#define SDD_T_WQ 3         /* [n_q_heads*head_dim][d_model] */
+#define SDD_T_WK 4         /* [n_kv_heads*head_dim][d_model] */
+#define SDD_T_WV 5         /* [n_kv_heads*head_dim][d_model] */
+#define SDD_T_WO 6         /* [d_model][n_q_heads*head_dim] */
+#define SDD_T_WGATE 7      /* [d_ff][d_model] */
+#define SDD_T_WUP 8        /* [d_ff][d_model] */
+#define SDD_T_WDOWN 9      /* [d_model][d_ff] */
+#define SDD_T_ATTN_NORM 10 /* [d_model], fp32 */
+#define SDD_T_FFN_NORM 11  /* [d_model], fp32 */
+#define SDD_T_Q_NORM 12    /* [head_dim], fp32 */
+#define SDD_T_K_NORM 13    /* [head_dim], fp32 */
+
+/* Target decoder shape.  The paper names its verifier (Qwen3-32B, Sec. 5.1)
+ * but not its architecture; this is the pre-norm decoder of that family:
+ * RMSNorm, GQA attention with rotate-half RoPE (optionally per-head QK
+ * RMSNorm before RoPE), SwiGLU FFN, untied LM head, no biases. */
+typedef struct {
+  int n_layers, d_model, n_q_heads, n_kv_heads, head_dim, d_ff, vocab;
+  float rms_eps, rope_theta;
+  int qk_norm; /* 1: per-head RMSNorm on q and k before RoPE */
+  int dtype;   /* SDD_F32 or SDD_BF16: weights, KV cache and GEMM inputs */
+} sdd_model_config;
+
+typedef struct sdd_model sdd_model;
+typedef struct sdd_kv sdd_kv;
+
+const char* sdd_status_string(int status);
+const char* sdd_last_error(void);
+/* 1 if the library was built for gfx950 and a gfx950 device is current. */
+int sdd_device_ok(void);
+
+/* ---- model ------------------------------------------------------------ */
+
+/* Bytes of the device weight buffer for cfg.  Weights are stored in the
+ * library's MFMA-tiled layout, not row-major. */
+int sdd_weights_bytes(const sdd_model_config* cfg, size_t* bytes);
+
+/* Wraps a caller-owned device buffer of at least sdd_weights_bytes() bytes.
+ * The handle is host memory; destroy with sdd_model_destroy (the buffer stays
+ * the caller's).  Supported: head_dim 64 or 128, n_q_heads % n_kv_heads == 0,
+ * d_model, d_ff multiples of 32, vocab a multiple of 16. */
+int sdd_model_create(const sdd_model_config* cfg, void* weights, size_t bytes, sdd_model** out);
+int sdd_model_destroy(sdd_model* m);
+
+/* Fills every weight with the synthetic counter-based generator:
+ * w = round(sigma * sqrt(3)/65536 * S) with S the Irwin-Hall sum of the four
+ * 16-bit lanes of SplitMix64(key(seed, tensor) + index * golden), index the
+ * row-major position in the [out][in] matrix; norm gains are set to 1. */
+int sdd_model_init_random(sdd_model* m, uint64_t seed, float sigma, sdd_stream_t stream);
+
+/* Copies one row-major tensor (device pointer; model dtype for matrices and
+ * embeddings, fp32 for norm gains) into the tiled layout. */
+int sdd_model_load_tensor(sdd_model* m, int kind, int layer, const void* src, sdd_stream_t stream);
+
+/* ---- KV cache ---------------------------------------------------------- */
+
+/* Bytes of a KV cache for max_batch sequences of up to max_len positions. */
+int sdd_kv_bytes(const sdd_model_config* cfg, int max_batch, int max_len, size_t* bytes);
+/* Wraps a caller-owned device buffer and resets every sequence to empty
+ * (length 0, pending token 0) with a kernel on stream. */
+int sdd_kv_create(sdd_model* m, int max_batch, int max_len, void* buf, size_t bytes,
+                  sdd_stream_t stream, sdd_kv** out);
+int sdd_kv_destroy(sdd_kv* kv);
+/* Synchronous read of per-sequence state: len[max_batch], pending[max_batch]
+ * (host pointers, either may be NULL) and the sticky error word (bit0: a
+ * capacity overflow was refused on the device, bit1: a token outside
+ * [0, vocab) was replaced by 0). */
+int sdd_kv_state(sdd_kv* kv, int32_t* len, int32_t* pending, int32_t* error_bits,
+                 sdd_stream_t stream);
+
+/* Workspace for prefill/verify of up to max_rows rows per call. */
+int sdd_workspace_bytes(const sdd_model* m, int max_rows, size_t* bytes);
+/* Prepares a caller-owned device workspace (zeroes its counters with a
+ * kernel); needed once after allocation.  Every call leaves the counters zero
+ * again, so the workspace may be reused by any number of later calls on the
+ * same stream. */
+int sdd_workspace_init(void* ws, size_t bytes, sdd_stream_t stream);
+
+/* Prefill of sequence seq with tokens[0..n) (device int32): caches positions
+ * 0..n-2, sets len = n-1 and pending = tokens[n-1].  The prompt is processed
+ * in row chunks of at most max_rows of the workspace. */
+int sdd_kv_prefill(sdd_model* m, sdd_kv* kv, int seq, const int32_t* tokens, int n,
+                   void* ws, size_t ws_bytes, sdd_stream_t stream);
+
+/* Block verification (Sec. 3.1): for each of n_seq sequences (seq_ids,
+ * device int32[n_seq]) runs the causal decoder over the gamma+1 rows
+ * [pending, drafts[s][0..gamma)] at positions len..len+gamma against the
+ * sequence's cache.  Row j < gamma scores draft j; row gamma is the bonus
+ * position.  Outputs (device): logits fp32 [n_seq][gamma+1][vocab] and
+ * argmax int32 [n_seq][gamma+1] (lowest index on ties; may be NULL).  K/V of
+ * the rows are written at len..len+gamma but len is unchanged until
+ * sdd_kv_commit.  gamma = 0 is a plain decode step.  Sequences whose cache
+ * cannot hold the block are refused on the device (sticky error bit0; their
+ * outputs are left unwritten).  Requires n_seq*(gamma+1) <= max_rows of ws. */
+int sdd_verify_block(sdd_model* m, sdd_kv* kv, const int32_t* seq_ids, int n_seq,
+                     const int32_t* drafts, int gamma, float* logits, int32_t* argmax,
+                     void* ws, size_t ws_bytes, sdd_stream_t stream);
+
+/* Commit after acceptance (device int32 arrays): len += accepted_len + 1,
+ * pending = next_token (the target's correction or bonus token). */
+int sdd_kv_commit(sdd_kv* kv, const int32_t* seq_ids, int n_seq, const int32_t* accepted_len,
+                  const int32_t* next_token, sdd_stream_t stream);
+/* ---- acceptance and confidence ---------------------------------------- */
+
+/* Workspace bytes for sdd_accept / sdd_confidence_prefix at these shapes. */
+int sdd_rowstats_workspace_bytes(int B, int gamma, int V, size_t* bytes);
+
+/* Acceptance test (Sec. 3.1; lenience equation and top-k rule, Appendix
+ * "Baselines and Sweep Settings").  Device inputs:
+ *   draft     int32 [B][gamma]
+ *   p_logits  target logits [B][gamma+1][V], dtype p_dtype, contiguous
+ *   q_logits  drafter logits, RATIO only: row j of sequence b at
+ *             q_logits + b*q_seq_stride + j*V elements (dtype q_dtype)
+ *   uniforms  fp32 [B][gamma] in [0,1), RATIO only
+ * For j < gamma, row j decides draft j; L = first failing j (gamma if none);
+ * next_token = argmax of target row L (lowest index on ties).  A non-finite
+ * value in a deciding row, or a draft token outside [0,V), fails that
+ * position.  Outputs (device int32 [B]): accepted_len, next_token, and flags
+ * (may be NULL; bit0 non-finite value seen, bit1 draft token out of range).
+ * Errors: SDD_EINVAL for NULL required pointers, B <= 0, gamma < 0 or > 64,
+ * V <= 0, k < 1 (TOPK), lenience not in (0,1] (LENIENT). */
+int sdd_accept(const int32_t* draft, const void* p_logits, int p_dtype, const void* q_logits,
+               int q_dtype, size_t q_seq_stride, const float* uniforms, int B, int gamma, int V,
+               int mode, int k, float lenience, int32_t* accepted_len, int32_t* next_token,
+               int32_t* flags, void* ws, size_t ws_bytes, sdd_stream_t stream);
+
+/* Raw-confidence prefix (Sec. 4.1 local gate B_k = min_{j<=k} q_j; Sec. 4.2
+ * raw confidence = max softmax of the drafter row).  Row j < gamma of
+ * sequence b at logits + b*seq_stride + j*V elements.  skip_len[b] =
+ * max{k : B_k >= tau} = first j with q_j < tau (gamma if none), decided as
+ * fp32 log q_j >= fp32 log tau.  Optional outputs: log_conf fp32 [B][gamma];
+ * with draft != NULL, log_p_draft fp32 [B][gamma] = log softmax at the draft
+ * token.  A row with a non-finite value has log q = NaN and stops the prefix.
+ * Errors: SDD_EINVAL for NULL required pointers, B <= 0, gamma < 0 or > 64,
+ * V <= 0, tau NaN. */
+int sdd_confidence_prefix(const void* logits, int dtype, size_t seq_stride, int B, int gamma,
+                          int V, float tau, int32_t* skip_len, float* log_conf,
+                          const int32_t* draft, float* log_p_draft, void* ws, size_t ws_bytes,
+                          sdd_stream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* SDD_H */

@@ -1,0 +1,226 @@
+"""CPU oracle for verifier-skipped speculative diffusion decoding.
+
+TEST INFRASTRUCTURE ONLY.  Only tests/, ``__graft_entry__.smoke()`` and the
+``cpu_baseline`` leg of ``bench.py`` may import this package.  The GPU product
+path (``paper_2608_14787_amd``) never imports it and shares no code with it.
+
+A ctypes wrapper over ``libsdd_oracle.so`` (plain C, fp64; see sdd_oracle.c for
+the passages each function follows).
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+
+import numpy as np
+
+from . import build as _build
+
+GREEDY, RATIO, TOPK, LENIENT = 0, 1, 2, 3
+(EMBED, LM_HEAD, FINAL_NORM, WQ, WK, WV, WO, WGATE, WUP, WDOWN,
+ ATTN_NORM, FFN_NORM, Q_NORM, K_NORM) = range(14)
+
+_lib = None
+
+
+class _Cfg(C.Structure):
+    _fields_ = [("n_layers", C.c_int), ("d_model", C.c_int), ("n_q_heads", C.c_int),
+                ("n_kv_heads", C.c_int), ("head_dim", C.c_int), ("d_ff", C.c_int),
+                ("vocab", C.c_int), ("rms_eps", C.c_double), ("rope_theta", C.c_double),
+                ("qk_norm", C.c_int), ("bf16_weights", C.c_int)]
+
+
+def lib():
+    """Loads the oracle library, compiling it first if it is not built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_build.LIB):
+            _build.build()
+        L = C.CDLL(_build.LIB)
+        P = C.c_void_p
+        L.orc_splitmix64.restype = C.c_uint64
+        L.orc_splitmix64.argtypes = [C.c_uint64]
+        L.orc_weight_values.argtypes = [C.c_uint64, C.c_int, C.c_uint64, C.c_uint64, C.c_double, C.c_int, P]
+        L.orc_tensor_id.argtypes = [C.c_int, C.c_int]
+        L.orc_model_create.restype = P
+        L.orc_model_create.argtypes = [C.POINTER(_Cfg), C.c_uint64, C.c_double]
+        L.orc_model_free.argtypes = [P]
+        L.orc_model_set_tensor.argtypes = [P, C.c_int, C.c_int, P]
+        L.orc_forward_full.argtypes = [P, P, C.c_int, C.c_int, P]
+        L.orc_forward_full_hidden.argtypes = [P, P, C.c_int, C.c_int, P]
+        L.orc_kv_create.restype = P
+        L.orc_kv_create.argtypes = [P, C.c_int]
+        L.orc_kv_free.argtypes = [P]
+        L.orc_kv_len.argtypes = [P]
+        L.orc_kv_pending.argtypes = [P]
+        L.orc_kv_read.argtypes = [P, C.c_int, C.c_int, P, P]
+        L.orc_kv_prefill.argtypes = [P, P, C.c_int]
+        L.orc_verify.argtypes = [P, P, C.c_int, P]
+        L.orc_commit.argtypes = [P, C.c_int, C.c_int]
+        L.orc_accept.argtypes = [C.c_int, P, P, P, C.c_size_t, P, C.c_int, C.c_int, C.c_int,
+                                 C.c_int, C.c_double, P, P, P, P, P]
+        L.orc_confidence_prefix.argtypes = [P, C.c_size_t, C.c_int, C.c_int, C.c_int, C.c_double,
+                                            P, P, P, P]
+        _lib = L
+    return _lib
+
+
+def _p(a):
+    return None if a is None else a.ctypes.data_as(C.c_void_p)
+
+
+def splitmix64(x: int) -> int:
+    return lib().orc_splitmix64(x)
+
+
+def tensor_id(kind: int, layer: int = 0) -> int:
+    return lib().orc_tensor_id(kind, layer)
+
+
+def weight_values(seed: int, tid: int, start: int, count: int, sigma: float, bf16: bool) -> np.ndarray:
+    out = np.empty(count, np.float32)
+    lib().orc_weight_values(seed, tid, start, count, sigma, int(bf16), _p(out))
+    return out
+
+
+def tensor_shape(shape, kind: int):
+    d, hq, hk = shape.d_model, shape.n_q_heads * shape.head_dim, shape.n_kv_heads * shape.head_dim
+    return {EMBED: (shape.vocab, d), LM_HEAD: (shape.vocab, d), FINAL_NORM: (1, d),
+            ATTN_NORM: (1, d), FFN_NORM: (1, d), Q_NORM: (1, shape.head_dim),
+            K_NORM: (1, shape.head_dim), WQ: (hq, d), WK: (hk, d), WV: (hk, d), WO: (d, hq),
+            WGATE: (shape.d_ff, d), WUP: (shape.d_ff, d), WDOWN: (d, shape.d_ff)}[kind]
+
+
+class Model:
+    """The target decoder with synthetic weights (seed, sigma) held in host memory."""
+
+    def __init__(self, shape, seed: int = 0, sigma: float = 0.02):
+        self.shape = shape
+        c = _Cfg(shape.n_layers, shape.d_model, shape.n_q_heads, shape.n_kv_heads,
+                 shape.head_dim, shape.d_ff, shape.vocab, shape.rms_eps, shape.rope_theta,
+                 int(shape.qk_norm), int(shape.dtype == "bf16"))
+        self._h = lib().orc_model_create(C.byref(c), seed, sigma)
+        if not self._h:
+            raise MemoryError("oracle model creation failed")
+
+    def __del__(self):
+        if getattr(self, "_h", None):
+            lib().orc_model_free(self._h)
+            self._h = None
+
+    def set_tensor(self, kind: int, layer: int, values: np.ndarray):
+        v = np.ascontiguousarray(values, np.float32)
+        assert v.size == int(np.prod(tensor_shape(self.shape, kind)))
+        if lib().orc_model_set_tensor(self._h, kind, layer, _p(v)) != 0:
+            raise ValueError("bad tensor")
+
+    def forward_full(self, tokens, row0: int = 0) -> np.ndarray:
+        """Logits of rows [row0, n) from full recomputation (no cache)."""
+        t = np.ascontiguousarray(tokens, np.int32)
+        out = np.empty((len(t) - row0, self.shape.vocab), np.float64)
+        if lib().orc_forward_full(self._h, _p(t), len(t), row0, _p(out)) != 0:
+            raise ValueError("forward_full failed")
+        return out
+
+    def hidden_full(self, tokens, row0: int = 0) -> np.ndarray:
+        t = np.ascontiguousarray(tokens, np.int32)
+        out = np.empty((len(t) - row0, self.shape.d_model), np.float64)
+        if lib().orc_forward_full_hidden(self._h, _p(t), len(t), row0, _p(out)) != 0:
+            raise ValueError("forward_full failed")
+        return out
+
+
+class KV:
+    """One sequence's cache in the cached route."""
+
+    def __init__(self, model: Model, max_len: int):
+        self.model = model
+        self._h = lib().orc_kv_create(model._h, max_len)
+        if not self._h:
+            raise MemoryError("oracle kv creation failed")
+
+    def __del__(self):
+        if getattr(self, "_h", None):
+            lib().orc_kv_free(self._h)
+            self._h = None
+
+    @property
+    def len(self) -> int:
+        return lib().orc_kv_len(self._h)
+
+    @property
+    def pending(self) -> int:
+        return lib().orc_kv_pending(self._h)
+
+    def read(self, layer: int, pos: int):
+        s = self.model.shape
+        k = np.empty(s.n_kv_heads * s.head_dim, np.float64)
+        v = np.empty_like(k)
+        if lib().orc_kv_read(self._h, layer, pos, _p(k), _p(v)) != 0:
+            raise IndexError("kv read out of range")
+        return k, v
+
+    def prefill(self, tokens):
+        t = np.ascontiguousarray(tokens, np.int32)
+        if lib().orc_kv_prefill(self._h, _p(t), len(t)) != 0:
+            raise ValueError("prefill failed")
+
+    def verify(self, drafts) -> np.ndarray:
+        d = np.ascontiguousarray(drafts, np.int32)
+        out = np.empty((len(d) + 1, self.model.shape.vocab), np.float64)
+        rc = lib().orc_verify(self._h, _p(d) if len(d) else None, len(d), _p(out))
+        if rc != 0:
+            raise ValueError(f"verify failed ({rc})")
+        return out
+
+    def commit(self, accepted_len: int, next_token: int):
+        if lib().orc_commit(self._h, int(accepted_len), int(next_token)) != 0:
+            raise ValueError("commit failed")
+
+
+def accept(mode: int, draft, p, q=None, u=None, k: int = 1, lenience: float = 1.0):
+    """Acceptance test over target rows p [B, gamma+1, V] (fp32 values).
+
+    Returns dict(accepted_len, next_token, dec_margin, argmax_gap, flags).
+    q: drafter rows [B, >=gamma, V] (ratio mode), u: uniforms [B, gamma]."""
+    p = np.ascontiguousarray(p, np.float32)
+    B, R, V = p.shape
+    gamma = R - 1
+    draft = np.ascontiguousarray(np.asarray(draft, np.int32).reshape(B, gamma))
+    qs = 0
+    if q is not None:
+        q = np.ascontiguousarray(q, np.float32)
+        qs = q.shape[1] * V
+    if u is not None:
+        u = np.ascontiguousarray(u, np.float32).reshape(B, gamma)
+    L = np.empty(B, np.int32)
+    nxt = np.empty(B, np.int32)
+    fl = np.empty(B, np.int32)
+    dm = np.empty((B, max(gamma, 1)), np.float64)
+    gap = np.empty((B, gamma + 1), np.float64)
+    rc = lib().orc_accept(mode, _p(draft), _p(p), _p(q), qs, _p(u), B, gamma, V, int(k),
+                          float(lenience), _p(L), _p(nxt), _p(dm), _p(gap), _p(fl))
+    if rc != 0:
+        raise ValueError("invalid accept arguments")
+    return dict(accepted_len=L, next_token=nxt, dec_margin=dm[:, :gamma], argmax_gap=gap,
+                flags=fl)
+
+
+def confidence_prefix(logits, gamma: int, tau: float, draft=None):
+    """skip_len [B] and log_conf [B, gamma] from drafter rows logits [B, >=gamma, V]."""
+    z = np.ascontiguousarray(logits, np.float32)
+    B, R, V = z.shape
+    sk = np.empty(B, np.int32)
+    lc = np.empty((B, max(gamma, 1)), np.float64)
+    lp = None
+    if draft is not None:
+        draft = np.ascontiguousarray(np.asarray(draft, np.int32).reshape(B, gamma))
+        lp = np.empty((B, max(gamma, 1)), np.float64)
+    rc = lib().orc_confidence_prefix(_p(z), R * V, B, gamma, V, float(tau), _p(sk), _p(lc),
+                                     _p(draft), _p(lp))
+    if rc != 0:
+        raise ValueError("invalid confidence arguments")
+    out = dict(skip_len=sk, log_conf=lc[:, :gamma])
+    if lp is not None:
+        out["log_p_draft"] = lp[:, :gamma]
+    return out

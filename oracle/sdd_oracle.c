@@ -1,0 +1,700 @@
+/*
+ * CPU oracle for verifier-skipped speculative diffusion decoding.
+ *
+ * TEST INFRASTRUCTURE ONLY: loaded by tests/, the smoke entry and the
+ * benchmark's CPU-baseline leg, never by the GPU product path.  It shares no
+ * code with the HIP library.  Plain loops, IEEE double precision for every
+ * quantity of the method; the acceptance/confidence decisions that the paper
+ * takes on FP32 log-probabilities are taken in fp32 here as well.
+ *
+ * Parts and the passages they follow:
+ *   - decoder forward (target model): the paper names the verifier
+ *     (Qwen3-32B, Sec. 5.1 "Experimental Setup") but prints no architecture;
+ *     the textbook pre-norm decoder (RMSNorm, GQA attention with rotate-half
+ *     RoPE, optional per-head QK RMSNorm, SwiGLU FFN, untied LM head) is written
+ *     out literally.  Two independent routes: full recomputation over the whole
+ *     sequence with no cache (the paper's measured verifier, Appendix
+ *     "Evaluation and Throughput") and a cached block verify.
+ *   - strict greedy acceptance and the accepted length L (Sec. 3.1), lenience
+ *     (lenience equation, Appendix "Baselines and Sweep Settings"), top-k
+ *     membership (same appendix), and the distribution-preserving ratio test
+ *     min(1, p/q) that Sec. 3.1 cites.
+ *   - raw confidence q_j = max softmax and the local gate B_k = min_{j<=k} q_j
+ *     with K = max{k : B_k >= tau} (Sec. 4.1 candidate skip length, Sec. 4.2
+ *     raw confidence).
+ */
+#include "sdd_oracle.h"
+
+#include <math.h>
+#include <stdlib.h>
+#include <string.h>
+
+/* ------------------------------------------------------------------------ */
+/* Synthetic weights.  SplitMix64 (Steele, Lea and Flood, OOPSLA 2014) as a
+ * counter-based generator; the normal variate is the Irwin-Hall sum of four
+ * 16-bit uniforms, scaled to standard deviation sigma.  Integer arithmetic up
+ * to one fp32 multiply, so any IEEE implementation reproduces it bit for bit. */
+
+uint64_t orc_splitmix64(uint64_t x) {
+  uint64_t z = x + 0x9E3779B97F4A7C15ULL;
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ULL;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBULL;
+  return z ^ (z >> 31);
+}
+
+int orc_tensor_id(int kind, int layer) {
+  switch (kind) {
+    case ORC_EMBED: return 1;
+    case ORC_LM_HEAD: return 2;
+    case ORC_FINAL_NORM: return 3;
+    case ORC_WQ: return 16 + 16 * layer + 0;
+    case ORC_WK: return 16 + 16 * layer + 1;
+    case ORC_WV: return 16 + 16 * layer + 2;
+    case ORC_WO: return 16 + 16 * layer + 3;
+    case ORC_WGATE: return 16 + 16 * layer + 4;
+    case ORC_WUP: return 16 + 16 * layer + 5;
+    case ORC_WDOWN: return 16 + 16 * layer + 6;
+    case ORC_ATTN_NORM: return 16 + 16 * layer + 7;
+    case ORC_FFN_NORM: return 16 + 16 * layer + 8;
+    case ORC_Q_NORM: return 16 + 16 * layer + 9;
+    case ORC_K_NORM: return 16 + 16 * layer + 10;
+  }
+  return -1;
+}
+
+static float orc_round_bf16(float f) {
+  uint32_t u;
+  memcpy(&u, &f, 4);
+  if ((u & 0x7f800000u) == 0x7f800000u) return f; /* inf/nan untouched */
+  uint32_t lsb = (u >> 16) & 1u;
+  u += 0x7fffu + lsb; /* round to nearest, ties to even */
+  u &= 0xffff0000u;
+  memcpy(&f, &u, 4);
+  return f;
+}
+
+void orc_weight_values(uint64_t seed, int tensor_id, uint64_t start, uint64_t count,
+                       double sigma, int bf16, float* out) {
+  const uint64_t gamma = 0x9E3779B97F4A7C15ULL;
+  uint64_t key = orc_splitmix64(orc_splitmix64(seed) + (uint64_t)tensor_id);
+  float scale = (float)(sigma * 1.7320508075688772 / 65536.0);
+  for (uint64_t i = 0; i < count; ++i) {
+    uint64_t r = orc_splitmix64(key + (start + i) * gamma);
+    int32_t s = (int32_t)(r & 0xffff) + (int32_t)((r >> 16) & 0xffff) +
+                (int32_t)((r >> 32) & 0xffff) + (int32_t)(r >> 48) - 131070;
+    float w = (float)s * scale;
+    out[i] = bf16 ? orc_round_bf16(w) : w;
+  }
+}
+
+/* ------------------------------------------------------------------------ */
+/* Model */
+
+struct orc_model {
+  orc_config c;
+  float* embed;   /* [V][d] */
+  float* lm_head; /* [V][d] */
+  float* final_norm;
+  struct {
+    float *wq, *wk, *wv, *wo, *wg, *wu, *wd;
+    float *attn_norm, *ffn_norm, *q_norm, *k_norm;
+  } * L;
+};
+
+int orc_tensor_shape(const orc_config* c, int kind, int64_t* rows, int64_t* cols) {
+  int64_t d = c->d_model, hq = (int64_t)c->n_q_heads * c->head_dim,
+          hk = (int64_t)c->n_kv_heads * c->head_dim;
+  switch (kind) {
+    case ORC_EMBED: case ORC_LM_HEAD: *rows = c->vocab; *cols = d; return 0;
+    case ORC_FINAL_NORM: case ORC_ATTN_NORM: case ORC_FFN_NORM: *rows = 1; *cols = d; return 0;
+    case ORC_Q_NORM: case ORC_K_NORM: *rows = 1; *cols = c->head_dim; return 0;
+    case ORC_WQ: *rows = hq; *cols = d; return 0;
+    case ORC_WK: case ORC_WV: *rows = hk; *cols = d; return 0;
+    case ORC_WO: *rows = d; *cols = hq; return 0;
+    case ORC_WGATE: case ORC_WUP: *rows = c->d_ff; *cols = d; return 0;
+    case ORC_WDOWN: *rows = d; *cols = c->d_ff; return 0;
+  }
+  return -1;
+}
+
+static float** orc_slot(orc_model* m, int kind, int layer) {
+  switch (kind) {
+    case ORC_EMBED: return &m->embed;
+    case ORC_LM_HEAD: return &m->lm_head;
+    case ORC_FINAL_NORM: return &m->final_norm;
+    case ORC_WQ: return &m->L[layer].wq;
+    case ORC_WK: return &m->L[layer].wk;
+    case ORC_WV: return &m->L[layer].wv;
+    case ORC_WO: return &m->L[layer].wo;
+    case ORC_WGATE: return &m->L[layer].wg;
+    case ORC_WUP: return &m->L[layer].wu;
+    case ORC_WDOWN: return &m->L[layer].wd;
+    case ORC_ATTN_NORM: return &m->L[layer].attn_norm;
+    case ORC_FFN_NORM: return &m->L[layer].ffn_norm;
+    case ORC_Q_NORM: return &m->L[layer].q_norm;
+    case ORC_K_NORM: return &m->L[layer].k_norm;
+  }
+  return NULL;
+}
+
+static int orc_is_norm(int kind) {
+  return kind == ORC_FINAL_NORM || kind == ORC_ATTN_NORM || kind == ORC_FFN_NORM ||
+         kind == ORC_Q_NORM || kind == ORC_K_NORM;
+}
+
+static float* orc_make_tensor(const orc_config* c, int kind, int layer, uint64_t seed,
+                              double sigma) {
+  int64_t rows, cols;
+  orc_tensor_shape(c, kind, &rows, &cols);
+  int64_t n = rows * cols;
+  float* t = (float*)malloc((size_t)n * sizeof(float));
+  if (!t) return NULL;
+  if (orc_is_norm(kind)) { /* RMSNorm gains start at one */
+    for (int64_t i = 0; i < n; ++i) t[i] = 1.0f;
+    return t;
+  }
+  int id = orc_tensor_id(kind, layer);
+  const int64_t chunk = 1 << 16;
+#pragma omp parallel for schedule(static)
+  for (int64_t s = 0; s < n; s += chunk) {
+    int64_t cnt = (n - s < chunk) ? n - s : chunk;
+    orc_weight_values(seed, id, (uint64_t)s, (uint64_t)cnt, sigma, c->bf16_weights, t + s);
+  }
+  return t;
+}
+
+void orc_model_free(orc_model* m) {
+  if (!m) return;
+  free(m->embed);
+  free(m->lm_head);
+  free(m->final_norm);
+  if (m->L) {
+    for (int l = 0; l < m->c.n_layers; ++l) {
+      free(m->L[l].wq); free(m->L[l].wk); free(m->L[l].wv); free(m->L[l].wo);
+      free(m->L[l].wg); free(m->L[l].wu); free(m->L[l].wd);
+      free(m->L[l].attn_norm); free(m->L[l].ffn_norm);
+      free(m->L[l].q_norm); free(m->L[l].k_norm);
+    }
+    free(m->L);
+  }
+  free(m);
+}
+
+orc_model* orc_model_create(const orc_config* cfg, uint64_t seed, double sigma) {
+  if (!cfg || cfg->n_layers < 0 || cfg->d_model <= 0 || cfg->n_q_heads <= 0 ||
+      cfg->n_kv_heads <= 0 || cfg->n_q_heads % cfg->n_kv_heads || cfg->head_dim <= 0 ||
+      cfg->head_dim % 2 || cfg->d_ff <= 0 || cfg->vocab <= 0)
+    return NULL;
+  orc_model* m = (orc_model*)calloc(1, sizeof(orc_model));
+  if (!m) return NULL;
+  m->c = *cfg;
+  m->L = calloc((size_t)(cfg->n_layers > 0 ? cfg->n_layers : 1), sizeof(*m->L));
+  int ok = m->L != NULL;
+  for (int kind = ORC_EMBED; ok && kind <= ORC_FINAL_NORM; ++kind) {
+    float** s = orc_slot(m, kind, 0);
+    *s = orc_make_tensor(cfg, kind, 0, seed, sigma);
+    ok = *s != NULL;
+  }
+  for (int l = 0; ok && l < cfg->n_layers; ++l)
+    for (int kind = ORC_WQ; ok && kind <= ORC_K_NORM; ++kind) {
+      float** s = orc_slot(m, kind, l);
+      *s = orc_make_tensor(cfg, kind, l, seed, sigma);
+      ok = *s != NULL;
+    }
+  if (!ok) {
+    orc_model_free(m);
+    return NULL;
+  }
+  return m;
+}
+
+int orc_model_set_tensor(orc_model* m, int kind, int layer, const float* src) {
+  if (!m || !src || kind < ORC_EMBED || kind > ORC_K_NORM) return -1;
+  if (kind >= ORC_WQ && (layer < 0 || layer >= m->c.n_layers)) return -1;
+  int64_t rows, cols;
+  orc_tensor_shape(&m->c, kind, &rows, &cols);
+  memcpy(*orc_slot(m, kind, layer), src, (size_t)(rows * cols) * sizeof(float));
+  return 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Decoder building blocks, fp64 */
+
+/* Y[r][n] = sum_k X[r][k] * W[n][k]  (PyTorch Linear convention W[out][in]) */
+static void linear(const float* W, int N, int K, const double* X, int R, double* Y) {
+#pragma omp parallel for schedule(static)
+  for (int n = 0; n < N; ++n) {
+    const float* w = W + (size_t)n * K;
+    for (int r = 0; r < R; ++r) {
+      const double* x = X + (size_t)r * K;
+      double acc = 0.0;
+      for (int k = 0; k < K; ++k) acc += x[k] * (double)w[k];
+      Y[(size_t)r * N + n] = acc;
+    }
+  }
+}
+
+/* RMSNorm: y = x / sqrt(mean(x^2) + eps) * g */
+static void rmsnorm(const double* x, int d, const float* g, double eps, double* y) {
+  double ss = 0.0;
+  for (int i = 0; i < d; ++i) ss += x[i] * x[i];
+  double inv = 1.0 / sqrt(ss / d + eps);
+  for (int i = 0; i < d; ++i) y[i] = x[i] * inv * (double)g[i];
+}
+
+/* Rotate-half RoPE at absolute position pos: pairs (i, i + hd/2) rotate by
+ * pos * theta^(-2i/hd). */
+static void rope(double* v, int hd, int pos, double theta) {
+  int h = hd / 2;
+  for (int i = 0; i < h; ++i) {
+    double inv_freq = pow(theta, -2.0 * i / hd);
+    double a = pos * inv_freq, c = cos(a), s = sin(a);
+    double x0 = v[i], x1 = v[i + h];
+    v[i] = x0 * c - x1 * s;
+    v[i + h] = x1 * c + x0 * s;
+  }
+}
+
+static double silu(double g) { return g / (1.0 + exp(-g)); }
+
+/* q/k projections of R rows at positions pos0.., with optional QK-norm and
+ * RoPE applied in place. */
+static void qk_post(const orc_model* m, int l, double* q, double* k, int R, int pos0) {
+  const orc_config* c = &m->c;
+  int hd = c->head_dim, hq = c->n_q_heads, hk = c->n_kv_heads;
+  double* tmp = (double*)malloc(sizeof(double) * hd);
+  for (int r = 0; r < R; ++r) {
+    for (int h = 0; h < hq; ++h) {
+      double* v = q + ((size_t)r * hq + h) * hd;
+      if (c->qk_norm) {
+        rmsnorm(v, hd, m->L[l].q_norm, c->rms_eps, tmp);
+        memcpy(v, tmp, sizeof(double) * hd);
+      }
+      rope(v, hd, pos0 + r, c->rope_theta);
+    }
+    for (int h = 0; h < hk; ++h) {
+      double* v = k + ((size_t)r * hk + h) * hd;
+      if (c->qk_norm) {
+        rmsnorm(v, hd, m->L[l].k_norm, c->rms_eps, tmp);
+        memcpy(v, tmp, sizeof(double) * hd);
+      }
+      rope(v, hd, pos0 + r, c->rope_theta);
+    }
+  }
+  free(tmp);
+}
+
+/* Residual FFN block on R rows: x += down(silu(gate(h)) * up(h)), h = RMSNorm(x). */
+static void ffn_block(const orc_model* m, int l, double* x, int R) {
+  const orc_config* c = &m->c;
+  int d = c->d_model, f = c->d_ff;
+  double* h = (double*)malloc(sizeof(double) * (size_t)R * d);
+  double* g = (double*)malloc(sizeof(double) * (size_t)R * f);
+  double* u = (double*)malloc(sizeof(double) * (size_t)R * f);
+  double* y = (double*)malloc(sizeof(double) * (size_t)R * d);
+  for (int r = 0; r < R; ++r) rmsnorm(x + (size_t)r * d, d, m->L[l].ffn_norm, c->rms_eps, h + (size_t)r * d);
+  linear(m->L[l].wg, f, d, h, R, g);
+  linear(m->L[l].wu, f, d, h, R, u);
+  for (size_t i = 0; i < (size_t)R * f; ++i) g[i] = silu(g[i]) * u[i];
+  linear(m->L[l].wd, d, f, g, R, y);
+  for (size_t i = 0; i < (size_t)R * d; ++i) x[i] += y[i];
+  free(h); free(g); free(u); free(y);
+}
+
+/* final RMSNorm + LM head on R rows */
+static void lm_head(const orc_model* m, const double* x, int R, double* logits) {
+  const orc_config* c = &m->c;
+  int d = c->d_model;
+  double* h = (double*)malloc(sizeof(double) * (size_t)R * d);
+  for (int r = 0; r < R; ++r) rmsnorm(x + (size_t)r * d, d, m->final_norm, c->rms_eps, h + (size_t)r * d);
+  linear(m->lm_head, c->vocab, d, h, R, logits);
+  free(h);
+}
+
+static void embed_rows(const orc_model* m, const int32_t* tok, int R, double* x) {
+  int d = m->c.d_model;
+  for (int r = 0; r < R; ++r)
+    for (int i = 0; i < d; ++i) x[(size_t)r * d + i] = (double)m->embed[(size_t)tok[r] * d + i];
+}
+
+static int tokens_ok(const orc_model* m, const int32_t* tok, int n) {
+  for (int i = 0; i < n; ++i)
+    if (tok[i] < 0 || tok[i] >= m->c.vocab) return 0;
+  return 1;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Route 1: full recomputation, no cache.  Every row attends to rows 0..i of
+ * the same pass (causal mask). */
+
+static int forward_full_x(const orc_model* m, const int32_t* tokens, int n, double* x) {
+  const orc_config* c = &m->c;
+  int d = c->d_model, hd = c->head_dim, hq = c->n_q_heads, hk = c->n_kv_heads;
+  int grp = hq / hk;
+  size_t nq = (size_t)hq * hd, nk = (size_t)hk * hd;
+  double* h = (double*)malloc(sizeof(double) * (size_t)n * d);
+  double* q = (double*)malloc(sizeof(double) * (size_t)n * nq);
+  double* k = (double*)malloc(sizeof(double) * (size_t)n * nk);
+  double* v = (double*)malloc(sizeof(double) * (size_t)n * nk);
+  double* o = (double*)malloc(sizeof(double) * (size_t)n * nq);
+  double* y = (double*)malloc(sizeof(double) * (size_t)n * d);
+  embed_rows(m, tokens, n, x);
+  double scale = 1.0 / sqrt((double)hd);
+  for (int l = 0; l < c->n_layers; ++l) {
+    for (int r = 0; r < n; ++r) rmsnorm(x + (size_t)r * d, d, m->L[l].attn_norm, c->rms_eps, h + (size_t)r * d);
+    linear(m->L[l].wq, (int)nq, d, h, n, q);
+    linear(m->L[l].wk, (int)nk, d, h, n, k);
+    linear(m->L[l].wv, (int)nk, d, h, n, v);
+    qk_post(m, l, q, k, n, 0);
+#pragma omp parallel for schedule(dynamic)
+    for (int i = 0; i < n; ++i) {
+      double* s = (double*)malloc(sizeof(double) * (size_t)(i + 1));
+      for (int hh = 0; hh < hq; ++hh) {
+        int kh = hh / grp;
+        const double* qi = q + ((size_t)i * hq + hh) * hd;
+        double mx = -INFINITY;
+        for (int j = 0; j <= i; ++j) {
+          const double* kj = k + ((size_t)j * hk + kh) * hd;
+          double dot = 0.0;
+          for (int t = 0; t < hd; ++t) dot += qi[t] * kj[t];
+          s[j] = dot * scale;
+          if (s[j] > mx) mx = s[j];
+        }
+        double den = 0.0;
+        for (int j = 0; j <= i; ++j) { s[j] = exp(s[j] - mx); den += s[j]; }
+        double* oi = o + ((size_t)i * hq + hh) * hd;
+        for (int t = 0; t < hd; ++t) {
+          double acc = 0.0;
+          for (int j = 0; j <= i; ++j) acc += s[j] * v[((size_t)j * hk + kh) * hd + t];
+          oi[t] = acc / den;
+        }
+      }
+      free(s);
+    }
+    linear(m->L[l].wo, d, (int)nq, o, n, y);
+    for (size_t i = 0; i < (size_t)n * d; ++i) x[i] += y[i];
+    ffn_block(m, l, x, n);
+  }
+  free(h); free(q); free(k); free(v); free(o); free(y);
+  return 0;
+}
+
+int orc_forward_full(const orc_model* m, const int32_t* tokens, int n, int row0, double* logits) {
+  if (!m || !tokens || !logits || n <= 0 || row0 < 0 || row0 >= n || !tokens_ok(m, tokens, n)) return -1;
+  int d = m->c.d_model;
+  double* x = (double*)malloc(sizeof(double) * (size_t)n * d);
+  forward_full_x(m, tokens, n, x);
+  lm_head(m, x + (size_t)row0 * d, n - row0, logits);
+  free(x);
+  return 0;
+}
+
+int orc_forward_full_hidden(const orc_model* m, const int32_t* tokens, int n, int row0, double* hidden) {
+  if (!m || !tokens || !hidden || n <= 0 || row0 < 0 || row0 >= n || !tokens_ok(m, tokens, n)) return -1;
+  int d = m->c.d_model;
+  double* x = (double*)malloc(sizeof(double) * (size_t)n * d);
+  forward_full_x(m, tokens, n, x);
+  memcpy(hidden, x + (size_t)row0 * d, sizeof(double) * (size_t)(n - row0) * d);
+  free(x);
+  return 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Route 2: cached.  The cache holds K (after QK-norm and RoPE) and V of every
+ * committed position; a block of R rows at positions len..len+R-1 appends its
+ * own K/V and attends to positions 0..its own. */
+
+struct orc_kv {
+  const orc_model* m;
+  int max_len, len, pending;
+  double* k; /* [layers][max_len][Hkv*hd] */
+  double* v;
+};
+
+orc_kv* orc_kv_create(const orc_model* m, int max_len) {
+  if (!m || max_len <= 0) return NULL;
+  orc_kv* kv = (orc_kv*)calloc(1, sizeof(orc_kv));
+  size_t per = (size_t)m->c.n_kv_heads * m->c.head_dim;
+  size_t nl = (size_t)(m->c.n_layers > 0 ? m->c.n_layers : 1);
+  kv->m = m;
+  kv->max_len = max_len;
+  kv->k = (double*)calloc(nl * max_len * per, sizeof(double));
+  kv->v = (double*)calloc(nl * max_len * per, sizeof(double));
+  if (!kv->k || !kv->v) {
+    orc_kv_free(kv);
+    return NULL;
+  }
+  return kv;
+}
+
+void orc_kv_free(orc_kv* kv) {
+  if (!kv) return;
+  free(kv->k);
+  free(kv->v);
+  free(kv);
+}
+
+int orc_kv_len(const orc_kv* kv) { return kv ? kv->len : -1; }
+int orc_kv_pending(const orc_kv* kv) { return kv ? kv->pending : -1; }
+
+int orc_kv_read(const orc_kv* kv, int layer, int pos, double* k, double* v) {
+  if (!kv || layer < 0 || layer >= kv->m->c.n_layers || pos < 0 || pos >= kv->max_len) return -1;
+  size_t per = (size_t)kv->m->c.n_kv_heads * kv->m->c.head_dim;
+  size_t off = ((size_t)layer * kv->max_len + pos) * per;
+  if (k) memcpy(k, kv->k + off, per * sizeof(double));
+  if (v) memcpy(v, kv->v + off, per * sizeof(double));
+  return 0;
+}
+
+/* Runs R rows at positions pos0.. through all layers, appending K/V. */
+static void block_forward(orc_kv* kv, const int32_t* tok, int R, int pos0, double* x) {
+  const orc_model* m = kv->m;
+  const orc_config* c = &m->c;
+  int d = c->d_model, hd = c->head_dim, hq = c->n_q_heads, hk = c->n_kv_heads;
+  int grp = hq / hk;
+  size_t nq = (size_t)hq * hd, nk = (size_t)hk * hd;
+  double* h = (double*)malloc(sizeof(double) * (size_t)R * d);
+  double* q = (double*)malloc(sizeof(double) * (size_t)R * nq);
+  double* k = (double*)malloc(sizeof(double) * (size_t)R * nk);
+  double* v = (double*)malloc(sizeof(double) * (size_t)R * nk);
+  double* o = (double*)malloc(sizeof(double) * (size_t)R * nq);
+  double* y = (double*)malloc(sizeof(double) * (size_t)R * d);
+  embed_rows(m, tok, R, x);
+  double scale = 1.0 / sqrt((double)hd);
+  for (int l = 0; l < c->n_layers; ++l) {
+    double* K = kv->k + (size_t)l * kv->max_len * nk;
+    double* V = kv->v + (size_t)l * kv->max_len * nk;
+    for (int r = 0; r < R; ++r) rmsnorm(x + (size_t)r * d, d, m->L[l].attn_norm, c->rms_eps, h + (size_t)r * d);
+    linear(m->L[l].wq, (int)nq, d, h, R, q);
+    linear(m->L[l].wk, (int)nk, d, h, R, k);
+    linear(m->L[l].wv, (int)nk, d, h, R, v);
+    qk_post(m, l, q, k, R, pos0);
+    memcpy(K + (size_t)pos0 * nk, k, sizeof(double) * (size_t)R * nk);
+    memcpy(V + (size_t)pos0 * nk, v, sizeof(double) * (size_t)R * nk);
+#pragma omp parallel for schedule(dynamic)
+    for (int r = 0; r < R; ++r) {
+      int last = pos0 + r;
+      double* s = (double*)malloc(sizeof(double) * (size_t)(last + 1));
+      for (int hh = 0; hh < hq; ++hh) {
+        int kh = hh / grp;
+        const double* qi = q + ((size_t)r * hq + hh) * hd;
+        double mx = -INFINITY;
+        for (int j = 0; j <= last; ++j) {
+          const double* kj = K + (size_t)j * nk + (size_t)kh * hd;
+          double dot = 0.0;
+          for (int t = 0; t < hd; ++t) dot += qi[t] * kj[t];
+          s[j] = dot * scale;
+          if (s[j] > mx) mx = s[j];
+        }
+        double den = 0.0;
+        for (int j = 0; j <= last; ++j) { s[j] = exp(s[j] - mx); den += s[j]; }
+        double* oi = o + ((size_t)r * hq + hh) * hd;
+        for (int t = 0; t < hd; ++t) {
+          double acc = 0.0;
+          for (int j = 0; j <= last; ++j) acc += s[j] * V[(size_t)j * nk + (size_t)kh * hd + t];
+          oi[t] = acc / den;
+        }
+      }
+      free(s);
+    }
+    linear(m->L[l].wo, d, (int)nq, o, R, y);
+    for (size_t i = 0; i < (size_t)R * d; ++i) x[i] += y[i];
+    ffn_block(m, l, x, R);
+  }
+  free(h); free(q); free(k); free(v); free(o); free(y);
+}
+
+int orc_kv_prefill(orc_kv* kv, const int32_t* tokens, int n) {
+  if (!kv || !tokens || n <= 0 || n > kv->max_len || !tokens_ok(kv->m, tokens, n)) return -1;
+  int d = kv->m->c.d_model;
+  if (n > 1) {
+    double* x = (double*)malloc(sizeof(double) * (size_t)(n - 1) * d);
+    block_forward(kv, tokens, n - 1, 0, x);
+    free(x);
+  }
+  kv->len = n - 1;
+  kv->pending = tokens[n - 1];
+  return 0;
+}
+
+int orc_verify(orc_kv* kv, const int32_t* drafts, int gamma, double* logits) {
+  if (!kv || gamma < 0 || !logits || (gamma > 0 && !drafts)) return -1;
+  if (kv->len + gamma + 1 > kv->max_len) return -4;
+  if (!tokens_ok(kv->m, drafts, gamma)) return -1;
+  int R = gamma + 1, d = kv->m->c.d_model;
+  int32_t* tok = (int32_t*)malloc(sizeof(int32_t) * R);
+  tok[0] = kv->pending;
+  for (int j = 0; j < gamma; ++j) tok[j + 1] = drafts[j];
+  double* x = (double*)malloc(sizeof(double) * (size_t)R * d);
+  block_forward(kv, tok, R, kv->len, x);
+  lm_head(kv->m, x, R, logits);
+  free(x);
+  free(tok);
+  return 0;
+}
+
+int orc_commit(orc_kv* kv, int accepted_len, int next_token) {
+  if (!kv || accepted_len < 0 || next_token < 0 || next_token >= kv->m->c.vocab) return -1;
+  if (kv->len + accepted_len + 1 > kv->max_len) return -4;
+  kv->len += accepted_len + 1;
+  kv->pending = next_token;
+  return 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Acceptance */
+
+static int row_finite(const float* z, int V) {
+  for (int v = 0; v < V; ++v)
+    if (!isfinite(z[v])) return 0;
+  return 1;
+}
+
+/* argmax with the lowest index among equal maxima; NaN never wins */
+static int row_argmax(const float* z, int V) {
+  int best = -1;
+  for (int v = 0; v < V; ++v) {
+    if (isnan(z[v])) continue;
+    if (best < 0 || z[v] > z[best]) best = v;
+  }
+  return best < 0 ? 0 : best;
+}
+
+static double row_lse(const float* z, int V) {
+  double mx = -INFINITY;
+  for (int v = 0; v < V; ++v)
+    if ((double)z[v] > mx) mx = z[v];
+  double s = 0.0;
+  for (int v = 0; v < V; ++v) s += exp((double)z[v] - mx);
+  return mx + log(s);
+}
+
+/* largest value among v != x */
+static double max_excluding(const float* z, int V, int x) {
+  double mx = -INFINITY;
+  for (int v = 0; v < V; ++v)
+    if (v != x && (double)z[v] > mx) mx = z[v];
+  return mx;
+}
+
+/* k-th largest (1-based) value among v != x; -inf if fewer than k values */
+static int cmp_desc(const void* a, const void* b) {
+  double x = *(const double*)a, y = *(const double*)b;
+  return (x < y) - (x > y);
+}
+static double kth_excluding(const float* z, int V, int x, int k) {
+  if (k > V - 1) return -INFINITY;
+  double* t = (double*)malloc(sizeof(double) * (size_t)V);
+  int n = 0;
+  for (int v = 0; v < V; ++v)
+    if (v != x) t[n++] = z[v];
+  qsort(t, (size_t)n, sizeof(double), cmp_desc);
+  double r = t[k - 1];
+  free(t);
+  return r;
+}
+
+int orc_accept(int mode, const int32_t* draft, const float* p, const float* q,
+               size_t q_seq_stride, const float* u, int B, int gamma, int V, int k,
+               double lenience, int32_t* accepted_len, int32_t* next_token,
+               double* dec_margin, double* argmax_gap, int32_t* flags) {
+  if (!p || !accepted_len || !next_token || B <= 0 || gamma < 0 || V <= 0) return -1;
+  if (gamma > 0 && !draft) return -1;
+  if (mode == ORC_TOPK && k < 1) return -1;
+  if (mode == ORC_LENIENT && !(lenience > 0.0 && lenience <= 1.0)) return -1;
+  if (mode == ORC_RATIO && (!q || !u)) return -1;
+  if (mode < ORC_GREEDY || mode > ORC_LENIENT) return -1;
+  const float log_len32 = (float)log(lenience);
+  for (int b = 0; b < B; ++b) {
+    int L = gamma, fl = 0;
+    for (int j = 0; j < gamma; ++j) {
+      const float* z = p + ((size_t)b * (gamma + 1) + j) * V;
+      int x = draft[(size_t)b * gamma + j];
+      int pass;
+      double margin = INFINITY;
+      if (x < 0 || x >= V) {
+        pass = 0;
+        fl |= 2;
+      } else if (!row_finite(z, V) ||
+                 (mode == ORC_RATIO && !row_finite(q + (size_t)b * q_seq_stride + (size_t)j * V, V))) {
+        pass = 0;
+        fl |= 1;
+      } else if (mode == ORC_GREEDY || (mode == ORC_LENIENT && lenience == 1.0)) {
+        /* strict: the draft token must be the target argmax (lowest index) */
+        pass = row_argmax(z, V) == x;
+        margin = fabs((double)z[x] - max_excluding(z, V, x));
+      } else if (mode == ORC_TOPK) {
+        /* rank of x: strictly larger values, plus equal values at lower index */
+        long rank = 0;
+        for (int v = 0; v < V; ++v)
+          if (z[v] > z[x] || (z[v] == z[x] && v < x)) ++rank;
+        pass = rank < k;
+        margin = fabs((double)z[x] - kth_excluding(z, V, x, k));
+      } else if (mode == ORC_LENIENT) {
+        /* z(x) - max_v z(v) >= log(lenience), decided in fp32 */
+        float zmax = z[row_argmax(z, V)];
+        float diff = z[x] - zmax;
+        pass = diff >= log_len32;
+        margin = fabs((double)diff - (double)log_len32);
+      } else {
+        /* ratio: accept iff u < p(x)/q(x), i.e. log u < lp - lq */
+        const float* zq = q + (size_t)b * q_seq_stride + (size_t)j * V;
+        double lp = (double)z[x] - row_lse(z, V);
+        double lq = (double)zq[x] - row_lse(zq, V);
+        double uu = u[(size_t)b * gamma + j];
+        double lu = uu > 0.0 ? log(uu) : -INFINITY;
+        pass = lu < lp - lq;
+        margin = fabs(lu - (lp - lq));
+      }
+      if (dec_margin) dec_margin[(size_t)b * gamma + j] = margin;
+      if (!pass) {
+        L = j;
+        break;
+      }
+    }
+    if (dec_margin)
+      for (int j = L + 1; j < gamma; ++j) dec_margin[(size_t)b * gamma + j] = INFINITY;
+    const float* zL = p + ((size_t)b * (gamma + 1) + L) * V;
+    if (!row_finite(zL, V)) fl |= 1;
+    accepted_len[b] = L;
+    next_token[b] = row_argmax(zL, V);
+    if (flags) flags[b] = fl;
+    if (argmax_gap)
+      for (int j = 0; j <= gamma; ++j) {
+        const float* z = p + ((size_t)b * (gamma + 1) + j) * V;
+        int a = row_argmax(z, V);
+        argmax_gap[(size_t)b * (gamma + 1) + j] = (double)z[a] - max_excluding(z, V, a);
+      }
+  }
+  return 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Confidence prefix */
+
+int orc_confidence_prefix(const float* logits, size_t seq_stride, int B, int gamma, int V,
+                          double tau, int32_t* skip_len, double* log_conf,
+                          const int32_t* draft, double* log_p_draft) {
+  if (!logits || !skip_len || B <= 0 || gamma < 0 || V <= 0 || isnan(tau)) return -1;
+  /* q_j >= tau  <=>  log q_j >= log tau; decided on fp32 values */
+  const float log_tau32 = tau > 0.0 ? (float)log(tau) : -INFINITY;
+  for (int b = 0; b < B; ++b) {
+    int K = gamma;
+    for (int j = 0; j < gamma; ++j) {
+      const float* z = logits + (size_t)b * seq_stride + (size_t)j * V;
+      double lc = NAN;
+      if (row_finite(z, V)) lc = (double)z[row_argmax(z, V)] - row_lse(z, V);
+      if (log_conf) log_conf[(size_t)b * gamma + j] = lc;
+      if (draft && log_p_draft) {
+        int x = draft[(size_t)b * gamma + j];
+        log_p_draft[(size_t)b * gamma + j] =
+            (x >= 0 && x < V && row_finite(z, V)) ? (double)z[x] - row_lse(z, V) : NAN;
+      }
+      /* the local gate B_k = min_{j<=k} q_j first falls below tau at the
+       * first position whose own score does */
+      if (K == gamma && !((float)lc >= log_tau32)) K = j;
+    }
+    skip_len[b] = K;
+  }
+  return 0;
+}

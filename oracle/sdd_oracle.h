@@ -1,0 +1,108 @@
+/*
+ * CPU oracle for verifier-skipped speculative diffusion decoding.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Only tests/, the smoke entry and the CPU-baseline
+ * leg of the benchmark may load this library.  The GPU product path never
+ * links, imports or calls it, and it shares no code with the GPU path.
+ *
+ * Plain, slow, obviously correct: every floating-point quantity of the method
+ * is computed in IEEE double precision, except where the paper fixes fp32 (the
+ * acceptance and confidence decisions are taken in fp32, the precision the
+ * paper uses for target log-probabilities, Appendix "Evaluation and
+ * Throughput").  Weights are synthetic bf16 (or fp32) values held exactly in
+ * float storage.
+ *
+ * Paper: "From Positionwise Confidence to Prefix Scheduling: Verifier Skipping
+ * in Speculative Decoding".
+ */
+#ifndef SDD_ORACLE_H
+#define SDD_ORACLE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Decoder shape (the paper names Qwen3-32B / Qwen2.5-7B-class targets but
+ * prints no architecture; the textbook pre-norm decoder is written out). */
+typedef struct {
+  int n_layers, d_model, n_q_heads, n_kv_heads, head_dim, d_ff, vocab;
+  double rms_eps, rope_theta;
+  int qk_norm;      /* 1: per-head RMSNorm of q and k before RoPE */
+  int bf16_weights; /* 1: weights are bf16 values; 0: fp32 values */
+} orc_config;
+
+/* Tensor kinds for orc_model_set_tensor / orc_weight_values. */
+enum {
+  ORC_EMBED = 0, ORC_LM_HEAD = 1, ORC_FINAL_NORM = 2,
+  ORC_WQ = 3, ORC_WK = 4, ORC_WV = 5, ORC_WO = 6,
+  ORC_WGATE = 7, ORC_WUP = 8, ORC_WDOWN = 9,
+  ORC_ATTN_NORM = 10, ORC_FFN_NORM = 11, ORC_Q_NORM = 12, ORC_K_NORM = 13
+};
+
+/* Acceptance modes (Appendix "Baselines and Sweep Settings"; Sec. 3.1). */
+enum { ORC_GREEDY = 0, ORC_RATIO = 1, ORC_TOPK = 2, ORC_LENIENT = 3 };
+
+/* Counter-based synthetic weight generator (SplitMix64 + Irwin-Hall(4)). */
+uint64_t orc_splitmix64(uint64_t x);
+int orc_tensor_id(int kind, int layer);
+void orc_weight_values(uint64_t seed, int tensor_id, uint64_t start, uint64_t count,
+                       double sigma, int bf16, float* out);
+
+typedef struct orc_model orc_model;
+orc_model* orc_model_create(const orc_config* cfg, uint64_t seed, double sigma);
+void orc_model_free(orc_model* m);
+/* shape of a tensor kind: rows x cols (row-major, PyTorch Linear [out][in]) */
+int orc_tensor_shape(const orc_config* cfg, int kind, int64_t* rows, int64_t* cols);
+int orc_model_set_tensor(orc_model* m, int kind, int layer, const float* src);
+
+/* Full recompute (the paper's verifier: no KV cache).  Causal forward over
+ * tokens[0..n); writes logits of rows [row0, n) to logits[(n-row0) * V]. */
+int orc_forward_full(const orc_model* m, const int32_t* tokens, int n, int row0, double* logits);
+/* Same, but returns the final hidden rows (after the last layer, before the
+ * final norm) for rows [row0, n): hidden[(n-row0) * d]. */
+int orc_forward_full_hidden(const orc_model* m, const int32_t* tokens, int n, int row0, double* hidden);
+
+/* Cached mode: one sequence, K/V of every layer kept in fp64. */
+typedef struct orc_kv orc_kv;
+orc_kv* orc_kv_create(const orc_model* m, int max_len);
+void orc_kv_free(orc_kv* kv);
+int orc_kv_len(const orc_kv* kv);
+int orc_kv_pending(const orc_kv* kv);
+/* K/V of the cache: layer, position -> k[Hkv*hd], v[Hkv*hd] (fp64). */
+int orc_kv_read(const orc_kv* kv, int layer, int pos, double* k, double* v);
+/* Prefill: caches tokens[0..n-1), len = n-1, pending = tokens[n-1]. */
+int orc_kv_prefill(orc_kv* kv, const int32_t* tokens, int n);
+/* Verify: rows [pending, drafts[0..gamma)] at positions len..len+gamma;
+ * logits[(gamma+1) * V].  K/V rows are written but len is unchanged. */
+int orc_verify(orc_kv* kv, const int32_t* drafts, int gamma, double* logits);
+/* Commit: len += L + 1, pending = next. */
+int orc_commit(orc_kv* kv, int accepted_len, int next_token);
+
+/* Acceptance test over target rows p[B][gamma+1][V] (fp32 values).
+ * Ratio mode also reads drafter rows q (row j of sequence b at
+ * q + b*q_seq_stride + j*V) and uniforms u[B][gamma].
+ * Outputs accepted_len[B], next_token[B]; optional margins:
+ *   dec_margin[B][gamma]   distance of each decision from its threshold
+ *   argmax_gap[B][gamma+1] top-1 minus top-2 value of each target row
+ *   flags[B]               bit0: a non-finite value was seen in a decisive row
+ *                          bit1: a draft token outside [0, V) */
+int orc_accept(int mode, const int32_t* draft, const float* p, const float* q,
+               size_t q_seq_stride, const float* u, int B, int gamma, int V, int k,
+               double lenience, int32_t* accepted_len, int32_t* next_token,
+               double* dec_margin, double* argmax_gap, int32_t* flags);
+
+/* Raw-confidence prefix (Sec. 4.1-4.2): log conf_j = max_v z_j - LSE(z_j);
+ * skip_len = first j with conf_j < tau (gamma if none).  Rows of sequence b
+ * start at logits + b*seq_stride, row j at +j*V.  log_conf[B][gamma] and
+ * p_draft[B][gamma] (probability of draft[b][j] if draft != NULL) optional. */
+int orc_confidence_prefix(const float* logits, size_t seq_stride, int B, int gamma, int V,
+                          double tau, int32_t* skip_len, double* log_conf,
+                          const int32_t* draft, double* log_p_draft);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

@@ -1,0 +1,174 @@
+"""Pins of the oracle's target decoder (CPU only).
+
+The paper names its verifier but prints no architecture, so the decoder is
+pinned by (a) agreement of its two independent routes -- full recomputation
+with no cache, the paper's measured verifier (Appendix "Evaluation and
+Throughput"), and the cached block verify; (b) closed forms (one-token
+sequences, zeroed residual branches); (c) a composition of
+torch.nn.functional library ops in float64 at the tiny shape.
+"""
+import numpy as np
+import pytest
+import torch
+import torch.nn.functional as F
+
+import oracle
+import workloads as W
+
+SMALL = W.ModelShape(2, 64, 4, 2, 16, 96, 200, 1e-6, 1e4, True, "f32")
+SMALL_BF16 = W.ModelShape(2, 64, 8, 2, 16, 96, 200, 1e-6, 1e6, False, "bf16")
+
+
+def _weights(shape, seed=0, sigma=0.02):
+    out = {}
+    bf16 = shape.dtype == "bf16"
+    for kind in [oracle.EMBED, oracle.LM_HEAD]:
+        r, c = oracle.tensor_shape(shape, kind)
+        out[kind] = oracle.weight_values(seed, oracle.tensor_id(kind), 0, r * c, sigma, bf16).reshape(r, c)
+    for l in range(shape.n_layers):
+        for kind in [oracle.WQ, oracle.WK, oracle.WV, oracle.WO, oracle.WGATE, oracle.WUP, oracle.WDOWN]:
+            r, c = oracle.tensor_shape(shape, kind)
+            out[(kind, l)] = oracle.weight_values(seed, oracle.tensor_id(kind, l), 0, r * c, sigma,
+                                                  bf16).reshape(r, c)
+    return out
+
+
+def _rope_torch(x, pos, theta):
+    # x [n, heads, hd]; rotate-half with inv_freq theta^(-2i/hd)
+    hd = x.shape[-1]
+    inv = theta ** (-torch.arange(0, hd // 2, dtype=torch.float64) * 2 / hd)
+    ang = pos[:, None].double() * inv[None, :]
+    cos = torch.cat([ang.cos(), ang.cos()], -1)[:, None, :]
+    sin = torch.cat([ang.sin(), ang.sin()], -1)[:, None, :]
+    x1, x2 = x[..., : hd // 2], x[..., hd // 2:]
+    return x * cos + torch.cat([-x2, x1], -1) * sin
+
+
+def _torch_reference(shape, w, tokens):
+    """Decoder as a composition of torch.nn.functional ops, float64 on the CPU."""
+    t = lambda a: torch.from_numpy(np.asarray(a, np.float64))
+    d, hd, hq, hk = shape.d_model, shape.head_dim, shape.n_q_heads, shape.n_kv_heads
+    n = len(tokens)
+    x = F.embedding(torch.from_numpy(np.asarray(tokens, np.int64)), t(w[oracle.EMBED]))
+    pos = torch.arange(n)
+    one = torch.ones(d, dtype=torch.float64)
+    for l in range(shape.n_layers):
+        h = F.rms_norm(x, (d,), one, eps=shape.rms_eps)
+        q = F.linear(h, t(w[(oracle.WQ, l)])).view(n, hq, hd)
+        k = F.linear(h, t(w[(oracle.WK, l)])).view(n, hk, hd)
+        v = F.linear(h, t(w[(oracle.WV, l)])).view(n, hk, hd)
+        if shape.qk_norm:
+            q = F.rms_norm(q, (hd,), torch.ones(hd, dtype=torch.float64), eps=shape.rms_eps)
+            k = F.rms_norm(k, (hd,), torch.ones(hd, dtype=torch.float64), eps=shape.rms_eps)
+        q, k = _rope_torch(q, pos, shape.rope_theta), _rope_torch(k, pos, shape.rope_theta)
+        o = F.scaled_dot_product_attention(q.transpose(0, 1), k.transpose(0, 1), v.transpose(0, 1),
+                                           is_causal=True, enable_gqa=True)
+        x = x + F.linear(o.transpose(0, 1).reshape(n, hq * hd), t(w[(oracle.WO, l)]))
+        h = F.rms_norm(x, (d,), one, eps=shape.rms_eps)
+        a = F.silu(F.linear(h, t(w[(oracle.WGATE, l)]))) * F.linear(h, t(w[(oracle.WUP, l)]))
+        x = x + F.linear(a, t(w[(oracle.WDOWN, l)]))
+    h = F.rms_norm(x, (d,), one, eps=shape.rms_eps)
+    return F.linear(h, t(w[oracle.LM_HEAD])).numpy()
+
+
+@pytest.mark.parametrize("shape", [SMALL, SMALL_BF16], ids=["qknorm-f32", "gqa4-bf16"])
+def test_matches_torch_functional_composition(shape):
+    toks = W.prompt(1, 13, shape.vocab)
+    m = oracle.Model(shape)
+    got = m.forward_full(toks)
+    want = _torch_reference(shape, _weights(shape), toks)
+    np.testing.assert_allclose(got, want, rtol=0, atol=1e-10 * np.abs(want).max())
+
+
+def test_tiny_shape_matches_torch_functional():
+    shape = W.TINY
+    toks = W.prompt(2, 20, shape.vocab)
+    m = oracle.Model(shape)
+    want = _torch_reference(shape, _weights(shape), toks)
+    np.testing.assert_allclose(m.forward_full(toks, 10), want[10:], rtol=0, atol=1e-10 * np.abs(want).max())
+
+
+@pytest.mark.parametrize("shape", [SMALL, W.TINY], ids=["small", "tiny"])
+def test_cached_verify_equals_full_recompute(shape):
+    m = oracle.Model(shape)
+    toks = W.prompt(3, 30, shape.vocab)
+    kv = oracle.KV(m, 64)
+    kv.prefill(toks[:20])  # caches 0..18, pending = toks[19]
+    assert kv.len == 19 and kv.pending == toks[19]
+    drafts = toks[20:26]
+    got = kv.verify(drafts)  # rows at positions 19..25
+    want = m.forward_full(toks[:26], 19)
+    np.testing.assert_allclose(got, want, rtol=0, atol=1e-11 * np.abs(want).max())
+    # gamma = 0 is a decode step: the last row of the full recompute
+    got0 = kv.verify([])
+    np.testing.assert_allclose(got0, want[:1], rtol=0, atol=1e-11 * np.abs(want).max())
+
+
+def test_commit_then_decode_equals_fresh_prefill():
+    shape = SMALL
+    m = oracle.Model(shape)
+    toks = W.prompt(4, 40, shape.vocab)
+    kv = oracle.KV(m, 64)
+    kv.prefill(toks[:10])
+    drafts = toks[10:17]
+    kv.verify(drafts)
+    L, nxt = 3, int(toks[30])
+    kv.commit(L, nxt)  # keeps [pending, d0, d1, d2] = toks[9:13], pending = nxt
+    assert kv.len == 13 and kv.pending == nxt
+    a = kv.verify(toks[31:33])
+    seq = np.concatenate([toks[:13], [nxt], toks[31:33]]).astype(np.int32)
+    kv2 = oracle.KV(m, 64)
+    kv2.prefill(seq[:14])
+    b = kv2.verify(seq[14:])
+    np.testing.assert_allclose(a, b, rtol=0, atol=1e-11 * np.abs(b).max())
+    np.testing.assert_allclose(a, m.forward_full(seq, 13), rtol=0, atol=1e-11 * np.abs(b).max())
+
+
+def test_single_token_closed_form():
+    # one position: attention returns v itself; RoPE at position 0 is the identity
+    shape = SMALL_BF16.with_layers(1)
+    m = oracle.Model(shape)
+    w = _weights(shape)
+    tok = 5
+    x = w[oracle.EMBED][tok].astype(np.float64)
+    rms = lambda a: a / np.sqrt((a * a).mean() + shape.rms_eps)
+    h = rms(x)
+    v = w[(oracle.WV, 0)].astype(np.float64) @ h
+    grp = shape.n_q_heads // shape.n_kv_heads
+    o = np.concatenate([v.reshape(shape.n_kv_heads, -1)[hh // grp] for hh in range(shape.n_q_heads)])
+    x = x + w[(oracle.WO, 0)].astype(np.float64) @ o
+    h = rms(x)
+    g = w[(oracle.WGATE, 0)].astype(np.float64) @ h
+    u = w[(oracle.WUP, 0)].astype(np.float64) @ h
+    x = x + w[(oracle.WDOWN, 0)].astype(np.float64) @ (g / (1 + np.exp(-g)) * u)
+    want = w[oracle.LM_HEAD].astype(np.float64) @ rms(x)
+    np.testing.assert_allclose(m.forward_full([tok])[0], want, rtol=0, atol=1e-12)
+    # K cached at position 0 is the un-rotated projection
+    kv = oracle.KV(m, 4)
+    kv.prefill([tok, 1])
+    k0, v0 = kv.read(0, 0)
+    np.testing.assert_allclose(k0, w[(oracle.WK, 0)].astype(np.float64) @ rms(w[oracle.EMBED][tok].astype(np.float64)), atol=1e-12)
+
+
+def test_zeroed_branches_give_embedding_logits():
+    shape = SMALL
+    m = oracle.Model(shape)
+    w = _weights(shape)
+    for l in range(shape.n_layers):
+        m.set_tensor(oracle.WO, l, np.zeros(oracle.tensor_shape(shape, oracle.WO), np.float32))
+        m.set_tensor(oracle.WDOWN, l, np.zeros(oracle.tensor_shape(shape, oracle.WDOWN), np.float32))
+    toks = W.prompt(5, 9, shape.vocab)
+    e = w[oracle.EMBED][toks].astype(np.float64)
+    h = e / np.sqrt((e * e).mean(-1, keepdims=True) + shape.rms_eps)
+    want = h @ w[oracle.LM_HEAD].astype(np.float64).T
+    np.testing.assert_allclose(m.forward_full(toks), want, rtol=0, atol=1e-12)
+
+
+def test_capacity_and_bad_tokens():
+    m = oracle.Model(SMALL)
+    kv = oracle.KV(m, 8)
+    kv.prefill([1, 2, 3])
+    with pytest.raises(ValueError):
+        kv.verify([1, 2, 3, 4, 5, 6])  # 2 + 7 rows > 8
+    with pytest.raises(ValueError):
+        kv.verify([SMALL.vocab])
