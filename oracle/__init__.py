@@ -178,7 +178,8 @@ class KV:
             raise ValueError("commit failed")
 
 
-def accept(mode: int, draft, p, q=None, u=None, k: int = 1, lenience: float = 1.0):
+def accept(mode: int, draft, p, q=None, u=None, k: int = 1, lenience: float = 1.0,
+           margins: bool = True):
     """Acceptance test over target rows p [B, gamma+1, V] (fp32 values).
 
     Returns dict(accepted_len, next_token, dec_margin, argmax_gap, flags).
@@ -196,14 +197,14 @@ def accept(mode: int, draft, p, q=None, u=None, k: int = 1, lenience: float = 1.
     L = np.empty(B, np.int32)
     nxt = np.empty(B, np.int32)
     fl = np.empty(B, np.int32)
-    dm = np.empty((B, max(gamma, 1)), np.float64)
-    gap = np.empty((B, gamma + 1), np.float64)
+    dm = np.empty((B, max(gamma, 1)), np.float64) if margins else None
+    gap = np.empty((B, gamma + 1), np.float64) if margins else None
     rc = lib().orc_accept(mode, _p(draft), _p(p), _p(q), qs, _p(u), B, gamma, V, int(k),
                           float(lenience), _p(L), _p(nxt), _p(dm), _p(gap), _p(fl))
     if rc != 0:
         raise ValueError("invalid accept arguments")
-    return dict(accepted_len=L, next_token=nxt, dec_margin=dm[:, :gamma], argmax_gap=gap,
-                flags=fl)
+    return dict(accepted_len=L, next_token=nxt, dec_margin=None if dm is None else dm[:, :gamma],
+                argmax_gap=gap, flags=fl)
 
 
 def confidence_prefix(logits, gamma: int, tau: float, draft=None):

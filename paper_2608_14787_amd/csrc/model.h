@@ -1,0 +1,72 @@
+// Device data layout of the target decoder, the KV cache and the per-call
+// workspace (internal to libsdd).
+#pragma once
+
+#include "sdd_internal.h"
+
+// Weight matrices ([out][in] = [N][K]) are stored as 1 KiB tiles of 16 rows x
+// KT columns (KT = 32 for bf16, 16 for fp32).  Inside a tile, lane l of a wave
+// reads 16 contiguous bytes holding row (l % 16) and the EPL = 16/sizeof(T)
+// consecutive columns starting at (l / 16) * EPL: exactly one MFMA A-operand
+// fragment per lane, so a wave streams a tile with one coalesced 16-byte load
+// per lane.  Tiles are ordered row-tile major, column-tile minor, so the K-run
+// of a 16-row strip is contiguous.  Q, K and V projections are fused into one
+// matrix (rows [Wq; Wk; Wv]); gate and up projections are fused and
+// interleaved per 16-row tile (tile 2t = gate rows 16t.., tile 2t+1 = up rows
+// 16t..), so that one column group holds matching gate/up outputs.
+struct sdd_model {
+  sdd_model_config cfg;
+  char* base;
+  size_t bytes;
+  int es;    // element size of weights/activations: 2 (bf16) or 4 (fp32)
+  int ktile; // columns per tile
+  int n_cu;  // compute units of the device
+  size_t off_embed, off_lm, off_final_norm;
+  struct Layer {
+    size_t qkv, o, gu, down, attn_norm, ffn_norm, q_norm, k_norm;
+  };
+  Layer* layers;
+};
+
+struct sdd_kv {
+  sdd_model* m;
+  int max_batch, max_len;
+  char* base;
+  size_t bytes;
+  int32_t* len;      // [max_batch]
+  int32_t* pending;  // [max_batch]
+  int32_t* err;      // sticky error bits
+  float* rope;       // [max_len][head_dim/2][2] (cos, sin)
+  char* k;           // [layers][max_batch][n_kv_heads][max_len][head_dim]
+  char* v;
+  size_t layer_stride;  // bytes per layer of k (and of v)
+};
+
+namespace sdd {
+
+inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+// tiled matrix bytes
+inline size_t tiled_bytes(int64_t N, int64_t K, int ktile) {
+  return (size_t)ceil_div(N, 16) * (size_t)ceil_div(K, ktile) * 1024;
+}
+
+struct RowInfo {
+  int seq;    // KV slot
+  int pos;    // absolute position
+  int valid;  // 0: refused (capacity), rows of that block are skipped
+  int pad;
+};
+
+// Per-call workspace carve-up for up to max_rows rows.
+struct WsLayout {
+  size_t rowinfo, x, xa, rs, ss_part, q, ao, ffh, part, cnt, amax, attn_part, total;
+  int mp;         // padded rows
+  int max_groups; // column groups of the widest GEMM
+  int n_wg;       // GEMM workgroups
+  int attn_splits_max;
+};
+
+WsLayout ws_layout(const sdd_model* m, int max_rows);
+
+}  // namespace sdd

@@ -1,0 +1,558 @@
+// Vocab-wide row reductions for the acceptance test and the confidence
+// prefix (gfx950).
+//
+// Acceptance (Sec. 3.1; lenience equation and top-k rule in Appendix
+// "Baselines and Sweep Settings"): for every target row j < gamma decide
+// whether draft j passes; L = first failure; next token = argmax of row L.
+// Confidence (Sec. 4.1 local gate, Sec. 4.2 raw confidence): q_j = max softmax
+// of drafter row j; skip length = first j with q_j < tau.
+//
+// Both are HBM-bound streams over [B][rows][V] logits.  Each row is split into
+// C equal chunks; one 256-thread workgroup loads its chunk into registers with
+// 16-byte loads (one pass over HBM), reduces max / first-argmax / sum-exp /
+// rank counts in registers, then across the wave with shuffles and across the
+// four waves through LDS, and writes one record.  The last workgroup of a
+// sequence to finish (arrival counter) combines that sequence's records in a
+// fixed order, so results are bit-reproducible, and takes the decisions; it
+// resets the counter so the workspace can be reused.
+#include "sdd_internal.h"
+
+namespace sdd {
+
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kMaxVecPerThread = 24;
+
+struct RowRec {
+  float m;    // row max over the chunk (NaN ignored)
+  int arg;    // first index of the max (-1 if the chunk held only NaN)
+  float s;    // sum over finite values of exp(z - m)
+  int cnt;    // top-k rank count: z > z_x, or z == z_x at a lower index
+  float qm;   // drafter row max (ratio mode)
+  float qs;   // drafter row sum exp (ratio mode)
+  int flags;  // bit0: non-finite value in the target chunk; bit2: in the drafter chunk
+  int pad;
+};
+
+struct Job {
+  const void* p;  // rows to reduce
+  size_t p_seq_stride, p_row_stride;
+  const void* q;  // drafter rows (ratio)
+  size_t q_seq_stride;
+  const int32_t* draft;
+  const float* u;
+  int B, gamma, V, rows, C, chunk;
+  int mode, k;
+  float log_len;  // fp32 log(lenience)
+  float log_tau;  // fp32 log(tau)
+  RowRec* recs;
+  int* counters;
+  int32_t* out_len;
+  int32_t* out_next;
+  int32_t* out_flags;
+  float* out_log_conf;
+  float* out_log_pdraft;
+};
+
+enum Kind { kAccept = 0, kConfidence = 1 };
+
+__device__ inline bool better(float m2, int a2, float m1, int a1) {
+  if (a2 < 0) return false;
+  if (a1 < 0) return true;
+  return m2 > m1 || (m2 == m1 && a2 < a1);
+}
+
+__device__ inline float exp_shift(float z, float m) {  // exp(z - m) for finite z, m
+  return __expf(z - m);
+}
+
+// Block-wide combine of (m, arg, s) and an int count; result valid in thread 0.
+struct BlockRed {
+  float m[kThreads / kWave];
+  int a[kThreads / kWave];
+  float s[kThreads / kWave];
+  int c[kThreads / kWave];
+  int f[kThreads / kWave];
+};
+
+template <bool kSum>
+__device__ void block_reduce(float& m, int& a, float& s, int& cnt, int& fl, BlockRed* red) {
+  // wave level
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    float m2 = __shfl_xor(m, o);
+    int a2 = __shfl_xor(a, o);
+    int c2 = __shfl_xor(cnt, o);
+    int f2 = __shfl_xor(fl, o);
+    if (kSum) {
+      float s2 = __shfl_xor(s, o);
+      // combine sums relative to the larger max (finite maxima only)
+      float mm = fmaxf(m, m2);
+      float sa = (s > 0.f) ? s * __expf(m - mm) : 0.f;
+      float sb = (s2 > 0.f) ? s2 * __expf(m2 - mm) : 0.f;
+      s = sa + sb;
+    }
+    if (better(m2, a2, m, a)) {
+      m = m2;
+      a = a2;
+    }
+    cnt += c2;
+    fl |= f2;
+  }
+  const int w = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+  if (lane == 0) {
+    red->m[w] = m;
+    red->a[w] = a;
+    red->s[w] = s;
+    red->c[w] = cnt;
+    red->f[w] = fl;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    float M = red->m[0];
+    int A = red->a[0];
+    int Cn = red->c[0], F = red->f[0];
+    for (int i = 1; i < kThreads / kWave; ++i) {
+      if (better(red->m[i], red->a[i], M, A)) {
+        M = red->m[i];
+        A = red->a[i];
+      }
+      Cn += red->c[i];
+      F |= red->f[i];
+    }
+    float S = 0.f;
+    if (kSum) {
+      float mx = -INFINITY;
+      for (int i = 0; i < kThreads / kWave; ++i)
+        if (red->s[i] > 0.f) mx = fmaxf(mx, red->m[i]);
+      for (int i = 0; i < kThreads / kWave; ++i)
+        if (red->s[i] > 0.f) S += red->s[i] * __expf(red->m[i] - mx);
+      // express relative to the chunk max M (== mx whenever finite values exist)
+      if (S > 0.f && mx != M) S *= __expf(mx - M);
+    }
+    m = M;
+    a = A;
+    s = S;
+    cnt = Cn;
+    fl = F;
+  }
+}
+
+// Loads this thread's share of a chunk into registers.
+template <typename T, int VEC>
+__device__ inline int load_chunk(const T* row, int base, int n, uint4* regs) {
+  int nv = 0;
+#pragma unroll
+  for (int i = 0; i < kMaxVecPerThread; ++i) {
+    int e = (i * kThreads + (int)threadIdx.x) * VEC;
+    if (e < n) {
+      if constexpr (VEC > 1) {
+        regs[i] = load_nt16(row + base + e);
+      } else {
+        regs[i].x = __builtin_bit_cast(uint32_t, Elem<T>::to_f32(row[base + e]));
+      }
+      nv = i + 1;
+    }
+  }
+  return nv;
+}
+
+template <typename T, int VEC>
+__device__ inline void unpack(const uint4& r, float* v) {
+  if constexpr (VEC > 1) {
+    unpack16(r, v, T());
+  } else {
+    v[0] = __builtin_bit_cast(float, r.x);
+  }
+}
+
+// Per-thread statistics over the registers: max, first argmax, non-finite flag,
+// sum exp relative to the thread max, rank count against (zx, x).
+template <typename T, int VEC, bool kSum, bool kCount>
+__device__ inline void thread_stats(const uint4* regs, int nv, int base, float zx, int x, float& m,
+                                    int& a, float& s, int& cnt, int& fl) {
+  m = -INFINITY;
+  a = -1;
+  fl = 0;
+  cnt = 0;
+#pragma unroll
+  for (int i = 0; i < kMaxVecPerThread; ++i) {
+    if (i < nv) {
+      float v[VEC];
+      unpack<T, VEC>(regs[i], v);
+      const int e0 = base + (i * kThreads + (int)threadIdx.x) * VEC;
+#pragma unroll
+      for (int t = 0; t < VEC; ++t) {
+        float z = v[t];
+        if (!__builtin_isfinite(z)) fl = 1;
+        if (!__builtin_isnan(z) && (a < 0 || z > m)) {
+          m = z;
+          a = e0 + t;
+        }
+        if (kCount) cnt += (z > zx || (z == zx && e0 + t < x)) ? 1 : 0;
+      }
+    }
+  }
+  s = 0.f;
+  if (kSum && a >= 0 && __builtin_isfinite(m)) {
+#pragma unroll
+    for (int i = 0; i < kMaxVecPerThread; ++i) {
+      if (i < nv) {
+        float v[VEC];
+        unpack<T, VEC>(regs[i], v);
+#pragma unroll
+        for (int t = 0; t < VEC; ++t)
+          if (__builtin_isfinite(v[t])) s += exp_shift(v[t], m);
+      }
+    }
+  }
+}
+
+// Combines the C chunk records of one row in chunk order.
+struct RowStats {
+  float m, s, qm, qs;
+  int arg, cnt, flags;
+};
+
+__device__ inline RowStats combine_row(const RowRec* r, int C) {
+  RowStats o;
+  o.m = -INFINITY;
+  o.arg = -1;
+  o.cnt = 0;
+  o.flags = 0;
+  o.qm = -INFINITY;
+  for (int c = 0; c < C; ++c) {
+    if (better(r[c].m, r[c].arg, o.m, o.arg)) {
+      o.m = r[c].m;
+      o.arg = r[c].arg;
+    }
+    o.cnt += r[c].cnt;
+    o.flags |= r[c].flags;
+    if (r[c].qs > 0.f) o.qm = fmaxf(o.qm, r[c].qm);
+  }
+  o.s = 0.f;
+  o.qs = 0.f;
+  for (int c = 0; c < C; ++c) {
+    if (r[c].s > 0.f) o.s += r[c].s * __expf(r[c].m - o.m);
+    if (r[c].qs > 0.f) o.qs += r[c].qs * __expf(r[c].qm - o.qm);
+  }
+  return o;
+}
+
+template <typename T, typename TQ, int VEC, int KIND, bool kSum, bool kCount, bool kQ>
+__global__ void __launch_bounds__(kThreads) rowstats_kernel(Job job) {
+  __shared__ BlockRed red;
+  __shared__ int s_last;
+  __shared__ int s_pass[72];
+  __shared__ int s_arg[72];
+  __shared__ int s_flag[72];
+
+  const int c = blockIdx.x % job.C;
+  const int rowid = blockIdx.x / job.C;  // b * rows + j
+  const int b = rowid / job.rows, j = rowid % job.rows;
+  const int base = c * job.chunk;
+  const int n = min(job.chunk, job.V - base);
+
+  const T* row = reinterpret_cast<const T*>(job.p) + (size_t)b * job.p_seq_stride + (size_t)j * job.p_row_stride;
+  int x = -1;
+  float zx = 0.f;
+  if (job.draft != nullptr && j < job.gamma) {
+    x = job.draft[(size_t)b * job.gamma + j];
+    if (x >= 0 && x < job.V) zx = Elem<T>::to_f32(row[x]);
+  }
+
+  uint4 regs[kMaxVecPerThread];
+  int nv = load_chunk<T, VEC>(row, base, n, regs);
+  uint4 qregs[kQ ? kMaxVecPerThread : 1];
+  int qnv = 0;
+  const bool has_q = kQ && j < job.gamma;
+  const TQ* qrow = nullptr;
+  if (kQ && has_q) {
+    qrow = reinterpret_cast<const TQ*>(job.q) + (size_t)b * job.q_seq_stride + (size_t)j * job.V;
+    qnv = load_chunk<TQ, VEC>(qrow, base, n, qregs);
+  }
+
+  float m, s;
+  int a, cnt, fl;
+  thread_stats<T, VEC, kSum, kCount>(regs, nv, base, zx, x, m, a, s, cnt, fl);
+  block_reduce<kSum>(m, a, s, cnt, fl, &red);
+  RowRec rec;
+  rec.m = m;
+  rec.arg = a;
+  rec.s = s;
+  rec.cnt = cnt;
+  rec.flags = fl;
+  rec.qm = -INFINITY;
+  rec.qs = 0.f;
+  rec.pad = 0;
+  if (kQ) {
+    __syncthreads();
+    float qm = -INFINITY, qs = 0.f;
+    int qa = -1, qc = 0, qf = 0;
+    if (has_q) thread_stats<TQ, VEC, true, false>(qregs, qnv, base, 0.f, -1, qm, qa, qs, qc, qf);
+    block_reduce<true>(qm, qa, qs, qc, qf, &red);
+    rec.qm = qm;
+    rec.qs = qs;
+    rec.flags |= qf ? 4 : 0;
+  }
+
+  if (threadIdx.x == 0) {
+    job.recs[blockIdx.x] = rec;
+    __threadfence();
+    int old = atomicAdd(&job.counters[b], 1);
+    s_last = (old == job.rows * job.C - 1);
+  }
+  __syncthreads();
+  if (!s_last) return;
+  __threadfence();
+
+  // ---- last workgroup of sequence b: combine and decide ----
+  const int t = threadIdx.x;
+  const RowRec* recs = job.recs + (size_t)b * job.rows * job.C;
+  if (t < job.rows) {
+    const RowStats st = combine_row(recs + t * job.C, job.C);
+    const bool bad = (st.flags & 1) != 0;
+    s_arg[t] = st.arg < 0 ? 0 : st.arg;
+    s_flag[t] = bad ? 1 : 0;
+    if (KIND == kAccept) {
+      int pass = 0;
+      if (t < job.gamma) {
+        const int xx = job.draft[(size_t)b * job.gamma + t];
+        if (xx < 0 || xx >= job.V) {
+          pass = 0;
+          s_flag[t] |= 2;
+        } else if (bad || (kQ && (st.flags & 4))) {
+          pass = 0;
+          s_flag[t] |= 1;
+        } else {
+          const T* rr = reinterpret_cast<const T*>(job.p) + (size_t)b * job.p_seq_stride + (size_t)t * job.p_row_stride;
+          const float z = Elem<T>::to_f32(rr[xx]);
+          if (job.mode == SDD_GREEDY) {
+            pass = st.arg == xx;
+          } else if (job.mode == SDD_TOPK) {
+            pass = st.cnt < job.k;
+          } else if (job.mode == SDD_LENIENT) {
+            const float diff = z - st.m;
+            pass = diff >= job.log_len;
+          } else {  // SDD_RATIO: log u < (z - LSE_p) - (zq - LSE_q)
+            const TQ* qr = reinterpret_cast<const TQ*>(job.q) + (size_t)b * job.q_seq_stride + (size_t)t * job.V;
+            const float zq = Elem<TQ>::to_f32(qr[xx]);
+            const float lp = z - (st.m + logf(st.s));
+            const float lq = zq - (st.qm + logf(st.qs));
+            const float uu = job.u[(size_t)b * job.gamma + t];
+            const float lu = uu > 0.f ? logf(uu) : -INFINITY;
+            pass = lu < lp - lq;
+          }
+        }
+      }
+      s_pass[t] = pass;
+    } else {
+      const float lc = bad ? __builtin_nanf("") : -logf(st.s);
+      s_pass[t] = (lc >= job.log_tau) ? 1 : 0;
+      if (job.out_log_conf) job.out_log_conf[(size_t)b * job.gamma + t] = lc;
+      if (job.out_log_pdraft && job.draft) {
+        const int xx = job.draft[(size_t)b * job.gamma + t];
+        float lp = __builtin_nanf("");
+        if (!bad && xx >= 0 && xx < job.V) {
+          const T* rr = reinterpret_cast<const T*>(job.p) + (size_t)b * job.p_seq_stride + (size_t)t * job.p_row_stride;
+          lp = Elem<T>::to_f32(rr[xx]) - st.m - logf(st.s);
+        }
+        job.out_log_pdraft[(size_t)b * job.gamma + t] = lp;
+      }
+    }
+  }
+  __syncthreads();
+  if (t == 0) {
+    if (KIND == kAccept) {
+      int L = job.gamma, fl = 0;
+      for (int jj = 0; jj < job.gamma; ++jj) {
+        fl |= s_flag[jj] & 2;
+        if (!s_pass[jj]) {
+          fl |= s_flag[jj];
+          L = jj;
+          break;
+        }
+      }
+      fl |= s_flag[L] & 1;
+      job.out_len[b] = L;
+      job.out_next[b] = s_arg[L];
+      if (job.out_flags) job.out_flags[b] = fl;
+    } else {
+      int K = job.gamma;
+      for (int jj = 0; jj < job.gamma; ++jj)
+        if (!s_pass[jj]) {
+          K = jj;
+          break;
+        }
+      job.out_len[b] = K;
+    }
+    job.counters[b] = 0;  // ready for the next call
+  }
+}
+
+__global__ void fill_i32_kernel(int32_t* p, int n, int v) {
+  int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) p[i] = v;
+}
+
+int choose_vec(const void* p, size_t seq_stride, size_t row_stride, int V, int esize, const void* q,
+               size_t q_seq_stride) {
+  const int vec = 16 / esize;
+  auto al = [&](const void* ptr, size_t s1, size_t s2) {
+    return ptr == nullptr ||
+           (((uintptr_t)ptr % 16) == 0 && (s1 * esize) % 16 == 0 && (s2 * esize) % 16 == 0);
+  };
+  if (V % vec == 0 && al(p, seq_stride, row_stride) && al(q, q_seq_stride, (size_t)V)) return vec;
+  return 1;
+}
+
+int chunks_for(int nrows, int V, int vec) {
+  const int per_wg_max = kThreads * vec * kMaxVecPerThread;
+  int c = (int)ceil_div(4096, (int64_t)(nrows > 0 ? nrows : 1));  // ~4096 workgroups in total
+  c = max(c, (int)ceil_div(V, per_wg_max));
+  c = min(c, (int)ceil_div(V, kThreads * vec));  // at least one vector per thread
+  return max(c, (int)ceil_div(V, per_wg_max));
+}
+
+size_t counters_region(int B) { return ((size_t)B * sizeof(int) + 255) / 256 * 256; }
+
+size_t rowstats_ws(int B, int rows, int V) {
+  size_t best = 0;
+  for (int vec : {1, 4, 8}) {
+    int C = chunks_for(B * rows, V, vec);
+    size_t need = (size_t)B * rows * C * sizeof(RowRec);
+    best = best > need ? best : need;
+  }
+  return counters_region(B) + best;
+}
+
+template <int KIND, bool kSum, bool kCount, bool kQ, typename T, typename TQ>
+int launch_t(Job& job, int vec, hipStream_t st) {
+  const int blocks = job.B * job.rows * job.C;
+  if (vec == 1)
+    hipLaunchKernelGGL((rowstats_kernel<T, TQ, 1, KIND, kSum, kCount, kQ>), dim3(blocks), dim3(kThreads), 0, st, job);
+  else if (vec == 4)
+    hipLaunchKernelGGL((rowstats_kernel<T, TQ, 4, KIND, kSum, kCount, kQ>), dim3(blocks), dim3(kThreads), 0, st, job);
+  else
+    hipLaunchKernelGGL((rowstats_kernel<T, TQ, 8, KIND, kSum, kCount, kQ>), dim3(blocks), dim3(kThreads), 0, st, job);
+  return check_launch("rowstats_kernel");
+}
+
+}  // namespace
+}  // namespace sdd
+
+using namespace sdd;
+
+extern "C" int sdd_rowstats_workspace_bytes(int B, int gamma, int V, size_t* bytes) {
+  SDD_REQUIRE(bytes != nullptr, "bytes is NULL");
+  SDD_REQUIRE(B > 0 && gamma >= 0 && gamma <= 64 && V > 0, "bad shape B=%d gamma=%d V=%d", B, gamma, V);
+  *bytes = rowstats_ws(B, gamma + 1, V);
+  return SDD_OK;
+}
+
+static int setup_ws(Job& job, void* ws, size_t ws_bytes, int vec) {
+  job.C = chunks_for(job.B * job.rows, job.V, vec);
+  job.chunk = (int)ceil_div(ceil_div(job.V, job.C), vec) * vec;
+  job.C = (int)ceil_div(job.V, job.chunk);
+  size_t need = rowstats_ws(job.B, job.rows, job.V);
+  if (ws == nullptr || ws_bytes < need)
+    return fail(SDD_ENOMEM, "rowstats workspace needs %zu bytes, got %zu", need, ws_bytes);
+  if ((uintptr_t)ws % 16) return fail(SDD_EINVAL, "workspace must be 16-byte aligned");
+  job.counters = reinterpret_cast<int*>(ws);
+  job.recs = reinterpret_cast<RowRec*>(reinterpret_cast<char*>(ws) + counters_region(job.B));
+  return SDD_OK;
+}
+
+extern "C" int sdd_accept(const int32_t* draft, const void* p_logits, int p_dtype, const void* q_logits,
+                          int q_dtype, size_t q_seq_stride, const float* uniforms, int B, int gamma, int V,
+                          int mode, int k, float lenience, int32_t* accepted_len, int32_t* next_token,
+                          int32_t* flags, void* ws, size_t ws_bytes, sdd_stream_t stream) {
+  SDD_REQUIRE(p_logits && accepted_len && next_token, "NULL required pointer");
+  SDD_REQUIRE(B > 0 && gamma >= 0 && gamma <= 64 && V > 0, "bad shape B=%d gamma=%d V=%d", B, gamma, V);
+  SDD_REQUIRE(gamma == 0 || draft, "draft is NULL");
+  SDD_REQUIRE(mode >= SDD_GREEDY && mode <= SDD_LENIENT, "bad mode %d", mode);
+  SDD_REQUIRE(mode != SDD_TOPK || k >= 1, "top-k needs k >= 1 (k=%d)", k);
+  SDD_REQUIRE(mode != SDD_LENIENT || (lenience > 0.f && lenience <= 1.f), "lenience must be in (0,1]");
+  SDD_REQUIRE(p_dtype == SDD_F32 || p_dtype == SDD_BF16, "bad p dtype");
+  const bool ratio = mode == SDD_RATIO && gamma > 0;
+  if (ratio) {
+    SDD_REQUIRE(q_logits && uniforms, "ratio mode needs drafter logits and uniforms");
+    SDD_REQUIRE(q_dtype == p_dtype, "ratio mode needs drafter and target logits of one dtype");
+    SDD_REQUIRE(q_seq_stride >= (size_t)gamma * V, "q_seq_stride too small");
+  }
+  Job job{};
+  job.p = p_logits;
+  job.p_row_stride = (size_t)V;
+  job.p_seq_stride = (size_t)(gamma + 1) * V;
+  job.q = ratio ? q_logits : nullptr;
+  job.q_seq_stride = q_seq_stride;
+  job.draft = gamma > 0 ? draft : nullptr;
+  job.u = uniforms;
+  job.B = B;
+  job.gamma = gamma;
+  job.V = V;
+  job.rows = gamma + 1;
+  job.mode = (mode == SDD_LENIENT && lenience == 1.f) ? SDD_GREEDY : mode;
+  job.k = k;
+  job.log_len = (float)std::log((double)lenience);
+  job.out_len = accepted_len;
+  job.out_next = next_token;
+  job.out_flags = flags;
+  const int es = p_dtype == SDD_F32 ? 4 : 2;
+  const int vec = choose_vec(p_logits, job.p_seq_stride, job.p_row_stride, V, es, job.q, q_seq_stride);
+  int rc = setup_ws(job, ws, ws_bytes, vec);
+  if (rc) return rc;
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  const bool bf = p_dtype == SDD_BF16;
+  switch (job.mode) {
+    case SDD_GREEDY:
+    case SDD_LENIENT:
+      return bf ? launch_t<kAccept, false, false, false, uint16_t, uint16_t>(job, vec, st)
+                : launch_t<kAccept, false, false, false, float, float>(job, vec, st);
+    case SDD_TOPK:
+      return bf ? launch_t<kAccept, false, true, false, uint16_t, uint16_t>(job, vec, st)
+                : launch_t<kAccept, false, true, false, float, float>(job, vec, st);
+    default:
+      if (!ratio)  // gamma == 0: only the bonus row's argmax is needed
+        return bf ? launch_t<kAccept, false, false, false, uint16_t, uint16_t>(job, vec, st)
+                  : launch_t<kAccept, false, false, false, float, float>(job, vec, st);
+      return bf ? launch_t<kAccept, true, false, true, uint16_t, uint16_t>(job, vec, st)
+                : launch_t<kAccept, true, false, true, float, float>(job, vec, st);
+  }
+}
+
+extern "C" int sdd_confidence_prefix(const void* logits, int dtype, size_t seq_stride, int B, int gamma,
+                                     int V, float tau, int32_t* skip_len, float* log_conf,
+                                     const int32_t* draft, float* log_p_draft, void* ws, size_t ws_bytes,
+                                     sdd_stream_t stream) {
+  SDD_REQUIRE(logits && skip_len, "NULL required pointer");
+  SDD_REQUIRE(B > 0 && gamma >= 0 && gamma <= 64 && V > 0, "bad shape B=%d gamma=%d V=%d", B, gamma, V);
+  SDD_REQUIRE(!__builtin_isnan(tau), "tau is NaN");
+  SDD_REQUIRE(dtype == SDD_F32 || dtype == SDD_BF16, "bad dtype");
+  SDD_REQUIRE(seq_stride >= (size_t)gamma * V, "seq_stride too small");
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  if (gamma == 0) {
+    hipLaunchKernelGGL(fill_i32_kernel, dim3((B + 255) / 256), dim3(256), 0, st, skip_len, B, 0);
+    return check_launch("fill_i32_kernel");
+  }
+  Job job{};
+  job.p = logits;
+  job.p_row_stride = (size_t)V;
+  job.p_seq_stride = seq_stride;
+  job.draft = draft;
+  job.B = B;
+  job.gamma = gamma;
+  job.V = V;
+  job.rows = gamma;
+  job.log_tau = tau > 0.f ? (float)std::log((double)tau) : -INFINITY;
+  job.out_len = skip_len;
+  job.out_log_conf = log_conf;
+  job.out_log_pdraft = draft ? log_p_draft : nullptr;
+  const int es = dtype == SDD_F32 ? 4 : 2;
+  const int vec = choose_vec(logits, seq_stride, (size_t)V, V, es, nullptr, 0);
+  int rc = setup_ws(job, ws, ws_bytes, vec);
+  if (rc) return rc;
+  return dtype == SDD_BF16 ? launch_t<kConfidence, true, false, false, uint16_t, uint16_t>(job, vec, st)
+                           : launch_t<kConfidence, true, false, false, float, float>(job, vec, st);
+}

@@ -1,0 +1,100 @@
+// Internal helpers shared by the HIP translation units of libsdd (gfx950 only).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <cstdarg>
+#include <cstdio>
+#include <string>
+
+#include "../../include/sdd.h"
+
+namespace sdd {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kWave = 64;
+
+// ---- error reporting ------------------------------------------------------
+void set_error(const char* fmt, ...);
+int fail(int code, const char* fmt, ...);
+int check_launch(const char* what);
+
+#define SDD_REQUIRE(cond, ...)                   \
+  do {                                           \
+    if (!(cond)) return sdd::fail(SDD_EINVAL, __VA_ARGS__); \
+  } while (0)
+
+#define SDD_HIP(call)                                                             \
+  do {                                                                            \
+    hipError_t e_ = (call);                                                       \
+    if (e_ != hipSuccess)                                                         \
+      return sdd::fail(SDD_EHIP, "%s: %s", #call, hipGetErrorString(e_));         \
+  } while (0)
+
+// ---- bf16 <-> fp32 (bit-level; round to nearest even) ----------------------
+__host__ __device__ inline float bf16_to_f32(uint16_t b) {
+  return __builtin_bit_cast(float, (uint32_t)b << 16);
+}
+__host__ __device__ inline uint16_t f32_to_bf16(float f) {
+  uint32_t u = __builtin_bit_cast(uint32_t, f);
+  if ((u & 0x7f800000u) == 0x7f800000u) return (uint16_t)((u >> 16) | ((u & 0xffffu) ? 0x40u : 0u));
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+template <typename T> struct Elem;
+template <> struct Elem<float> {
+  static constexpr int kVec = 4;  // elements per 16-byte load
+  __device__ static inline float load(const float* p) { return *p; }
+  __device__ static inline float to_f32(float x) { return x; }
+  __device__ static inline float from_f32(float x) { return x; }
+};
+template <> struct Elem<uint16_t> {
+  static constexpr int kVec = 8;
+  __device__ static inline float load(const uint16_t* p) { return bf16_to_f32(*p); }
+  __device__ static inline float to_f32(uint16_t x) { return bf16_to_f32(x); }
+  __device__ static inline uint16_t from_f32(float x) { return f32_to_bf16(x); }
+};
+
+// unpack a 16-byte vector into fp32 values
+__device__ inline void unpack16(const uint4& v, float* out, float) {
+  out[0] = __builtin_bit_cast(float, v.x);
+  out[1] = __builtin_bit_cast(float, v.y);
+  out[2] = __builtin_bit_cast(float, v.z);
+  out[3] = __builtin_bit_cast(float, v.w);
+}
+__device__ inline void unpack16(const uint4& v, float* out, uint16_t) {
+  const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    out[2 * i] = __builtin_bit_cast(float, w[i] << 16);
+    out[2 * i + 1] = __builtin_bit_cast(float, w[i] & 0xffff0000u);
+  }
+}
+
+// 16-byte streaming load that bypasses cache residency (data read once)
+__device__ inline uint4 load_nt16(const void* p) {
+  u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
+__device__ inline uint4 load16(const void* p) { return *reinterpret_cast<const uint4*>(p); }
+
+__host__ __device__ inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+// wave-level reductions (64 lanes)
+__device__ inline float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
+  return v;
+}
+__device__ inline float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+
+}  // namespace sdd
