@@ -95,7 +95,7 @@ int sdd_weights_bytes(const sdd_model_config* cfg, size_t* bytes);
 /* Wraps a caller-owned device buffer of at least sdd_weights_bytes() bytes.
  * The handle is host memory; destroy with sdd_model_destroy (the buffer stays
  * the caller's).  Supported: head_dim 64 or 128, n_q_heads % n_kv_heads == 0,
- * d_model, d_ff multiples of 32, vocab a multiple of 16. */
+ * d_model and vocab multiples of 32, d_ff a multiple of 32 (bf16) or 16 (fp32). */
 int sdd_model_create(const sdd_model_config* cfg, void* weights, size_t bytes, sdd_model** out);
 int sdd_model_destroy(sdd_model* m);
 
@@ -121,7 +121,8 @@ int sdd_kv_destroy(sdd_kv* kv);
 /* Synchronous read of per-sequence state: len[max_batch], pending[max_batch]
  * (host pointers, either may be NULL) and the sticky error word (bit0: a
  * capacity overflow was refused on the device, bit1: a token outside
- * [0, vocab) was replaced by 0). */
+ * [0, vocab) was replaced by 0, bit2: a sequence id outside [0, max_batch)
+ * was refused). */
 int sdd_kv_state(sdd_kv* kv, int32_t* len, int32_t* pending, int32_t* error_bits,
                  sdd_stream_t stream);
 

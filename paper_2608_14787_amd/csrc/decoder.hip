@@ -1,0 +1,1001 @@
+// Block verification forward pass of the target decoder on gfx950.
+//
+// One verify call (Sec. 3.1: the target scores a drafted block and accepts a
+// prefix) runs the gamma drafts plus one bonus position of every sequence
+// through the decoder against its KV cache.  At gamma + 1 = 33 rows each
+// projection is a skinny, weight-streaming contraction, so the call is bound
+// by reading the weights from HBM once.
+//
+// Kernels of one call:
+//   embed        gathers token rows, the residual stream x (fp32), the GEMM
+//                input xa = T(x * g) and the RMSNorm row scale r
+//   per layer:   gemm<QKV>   fused q/k/v projection; epilogue: row scale, per-head
+//                            QK RMSNorm, rotate-half RoPE, K/V append to the cache
+//                attention   causal GQA attention of the block rows over the cache
+//                gemm<RESID> output projection + residual; epilogue also writes the
+//                            next GEMM input and the next RMSNorm row scale
+//                gemm<SWIGLU> fused gate/up projection; epilogue silu(gate) * up
+//                gemm<RESID> down projection + residual
+//   gemm<LOGITS> final norm (row scale) + LM head, fp32 logits and row argmax
+//
+// The GEMMs are stream-K over (column group, k-tile) units: every workgroup
+// gets an equal contiguous share of the weight bytes, whatever the matrix
+// shape, so all compute units stream the same amount.  A column group whose
+// K-range is split between workgroups is reduced by its last-arriving
+// contributor, which sums the partials in a fixed order (deterministic).
+#include <algorithm>
+#include <cmath>
+#include <new>
+
+#include "model.h"
+
+namespace sdd {
+
+enum Epi { EPI_QKV = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_LOGITS = 3 };
+
+constexpr int kGemmThreads = 256;
+constexpr int kMaxPassRows = 64;  // rows per GEMM pass (TB <= 4 row tiles of 16)
+
+struct GemmArgs {
+  const char* W;  // tiled weights
+  int KT;         // k-tiles per row strip
+  int G;          // column groups
+  int N;          // valid output columns
+  const char* X;  // activations, row-major [rows][ldx], element type T
+  int ldx;
+  int m0, M;      // rows of this pass
+  int mp;         // padded row stride of per-row scratch
+  int n_wg;
+  float* part;    // partial tiles [n_wg][2][M][NG*16]
+  int* cnt;       // arrival counter per column group
+  int* done;      // groups-finished counter
+  const RowInfo* rows;
+  const float* rs;  // RMSNorm row scale of the input (NULL: none)
+  float eps;
+  // EPI_QKV
+  char* q_out;
+  int hq, hkv, hd, qk_norm;
+  const float* qn;
+  const float* kn;
+  const float* rope;
+  int max_len;
+  char* kc;
+  char* vc;
+  // EPI_RESID
+  float* x;
+  char* xa;
+  int d;
+  const float* g_next;
+  float* ss_part;
+  float* rs_out;
+  // EPI_SWIGLU
+  char* ffh;
+  int dff;
+  // EPI_LOGITS
+  float* logits;
+  int V;
+  float* amax_v;
+  int* amax_i;
+  int* argmax_out;
+};
+
+template <typename T>
+__device__ inline void mma_tile(const uint4& a, const uint4& b, f32x4& acc) {
+  if constexpr (sizeof(T) == 2) {
+    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), acc, 0,
+                                                  0, 0);
+  } else {
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__builtin_bit_cast(float, a.x), __builtin_bit_cast(float, b.x), acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__builtin_bit_cast(float, a.y), __builtin_bit_cast(float, b.y), acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__builtin_bit_cast(float, a.z), __builtin_bit_cast(float, b.z), acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__builtin_bit_cast(float, a.w), __builtin_bit_cast(float, b.w), acc, 0, 0, 0);
+  }
+}
+
+template <typename T>
+__device__ inline void store_t(char* base, int64_t idx, float v) {
+  reinterpret_cast<T*>(base)[idx] = Elem<T>::from_f32(v);
+}
+
+// owner of unit x: the workgroup whose share [w*U/n, (w+1)*U/n) contains x
+__device__ inline int unit_owner(int64_t x, int64_t U, int n) { return (int)(((x + 1) * n + U - 1) / U - 1); }
+__device__ inline int64_t unit_start(int w, int64_t U, int n) { return (int64_t)w * U / n; }
+
+template <typename T, int NG>
+__device__ void epilogue_qkv(const GemmArgs& a, const float* tile, int g, int layer_unused) {
+  constexpr int C = NG * 16;  // == head_dim
+  const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+  const int h = g;
+  const bool is_q = h < a.hq, is_k = !is_q && h < a.hq + a.hkv;
+  for (int mm = wave; mm < a.M; mm += kGemmThreads / kWave) {
+    const int m = a.m0 + mm;
+    const RowInfo ri = a.rows[m];
+    if (!ri.valid) continue;
+    const float r = a.rs ? a.rs[m] : 1.f;
+    float y[C / 64 > 0 ? C / 64 : 1];
+    if constexpr (C == 128) {
+      y[0] = tile[mm * C + lane] * r;
+      y[1] = tile[mm * C + lane + 64] * r;
+    } else {
+      y[0] = tile[mm * C + lane] * r;
+    }
+    if (is_q || is_k) {
+      if (a.qk_norm) {
+        float ss = (C == 128) ? y[0] * y[0] + y[C == 128 ? 1 : 0] * y[C == 128 ? 1 : 0] : y[0] * y[0];
+        ss = wave_sum(ss);
+        const float inv = 1.f / sqrtf(ss / (float)C + a.eps);
+        const float* gn = is_q ? a.qn : a.kn;
+        y[0] *= inv * gn[lane];
+        if constexpr (C == 128) y[1] *= inv * gn[lane + 64];
+      }
+      const float* rp = a.rope + (size_t)ri.pos * (C / 2) * 2;
+      if constexpr (C == 128) {
+        const float c = rp[2 * lane], s = rp[2 * lane + 1];
+        const float y0 = y[0], y1 = y[1];
+        y[0] = y0 * c - y1 * s;
+        y[1] = y1 * c + y0 * s;
+      } else {
+        const int i = lane % 32;
+        const float c = rp[2 * i], s = rp[2 * i + 1];
+        const float other = __shfl_xor(y[0], 32);
+        y[0] = lane < 32 ? y[0] * c - other * s : y[0] * c + other * s;
+      }
+    }
+    char* dst;
+    int64_t base;
+    if (is_q) {
+      dst = a.q_out;
+      base = ((int64_t)m * a.hq + h) * C;
+    } else {
+      const int kh = is_k ? h - a.hq : h - a.hq - a.hkv;
+      dst = is_k ? a.kc : a.vc;
+      base = (((int64_t)ri.seq * a.hkv + kh) * a.max_len + ri.pos) * C;
+    }
+    store_t<T>(dst, base + lane, y[0]);
+    if constexpr (C == 128) store_t<T>(dst, base + lane + 64, y[1]);
+  }
+}
+
+template <typename T, int NG>
+__device__ void epilogue_resid(const GemmArgs& a, const float* tile, int g) {
+  constexpr int C = NG * 16;
+  const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+  for (int mm = wave; mm < a.M; mm += kGemmThreads / kWave) {
+    const int m = a.m0 + mm;
+    float ss = 0.f;
+    for (int c = lane; c < C; c += kWave) {
+      const int64_t n = (int64_t)g * C + c;
+      const float xv = a.x[(int64_t)m * a.d + n] + tile[mm * C + c];
+      a.x[(int64_t)m * a.d + n] = xv;
+      store_t<T>(a.xa, (int64_t)m * a.d + n, xv * a.g_next[n]);
+      ss += xv * xv;
+    }
+    ss = wave_sum(ss);
+    if (lane == 0) a.ss_part[(int64_t)g * a.mp + m] = ss;
+  }
+}
+
+template <typename T, int NG>
+__device__ void epilogue_swiglu(const GemmArgs& a, const float* tile, int g) {
+  constexpr int C = NG * 16, P = NG / 2;
+  const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+  for (int mm = wave; mm < a.M; mm += kGemmThreads / kWave) {
+    const int m = a.m0 + mm;
+    const float r = a.rs ? a.rs[m] : 1.f;
+    for (int idx = lane; idx < P * 16; idx += kWave) {
+      const int t = idx / 16, j = idx % 16;
+      const float gt = tile[mm * C + (2 * t) * 16 + j] * r;
+      const float up = tile[mm * C + (2 * t + 1) * 16 + j] * r;
+      const float hv = gt / (1.f + expf(-gt)) * up;
+      store_t<T>(a.ffh, (int64_t)m * a.dff + ((int64_t)g * P + t) * 16 + j, hv);
+    }
+  }
+}
+
+__device__ inline bool arg_better(float v2, int i2, float v1, int i1) {
+  if (i2 < 0 || v2 != v2) return false;
+  if (i1 < 0) return true;
+  return v2 > v1 || (v2 == v1 && i2 < i1);
+}
+
+template <int NG>
+__device__ void epilogue_logits(const GemmArgs& a, const float* tile, int g) {
+  constexpr int C = NG * 16;
+  const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+  for (int mm = wave; mm < a.M; mm += kGemmThreads / kWave) {
+    const int m = a.m0 + mm;
+    const RowInfo ri = a.rows[m];
+    const float r = a.rs ? a.rs[m] : 1.f;
+    float bv = -INFINITY;
+    int bi = -1;
+    for (int c = lane; c < C; c += kWave) {
+      const int n = g * C + c;
+      if (n >= a.V) break;
+      const float v = tile[mm * C + c] * r;
+      if (ri.valid) a.logits[(int64_t)m * a.V + n] = v;
+      if (arg_better(v, n, bv, bi)) {
+        bv = v;
+        bi = n;
+      }
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+      const float v2 = __shfl_xor(bv, o);
+      const int i2 = __shfl_xor(bi, o);
+      if (arg_better(v2, i2, bv, bi)) {
+        bv = v2;
+        bi = i2;
+      }
+    }
+    if (lane == 0) {
+      a.amax_v[(int64_t)g * a.mp + m] = bv;
+      a.amax_i[(int64_t)g * a.mp + m] = bi;
+    }
+  }
+}
+
+// After every column group of a RESID / LOGITS GEMM pass is final, the last
+// group to finish reduces the per-group row statistics in group order.
+template <int EPI>
+__device__ void finish_rows(const GemmArgs& a) {
+  __shared__ int s_last_done;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    __threadfence();
+    const int old = atomicAdd(a.done, 1);
+    s_last_done = old == a.G - 1;
+  }
+  __syncthreads();
+  if (!s_last_done) return;
+  __threadfence();
+  for (int mm = threadIdx.x; mm < a.M; mm += kGemmThreads) {
+    const int m = a.m0 + mm;
+    if constexpr (EPI == EPI_RESID) {
+      float s = 0.f;
+      for (int g = 0; g < a.G; ++g) s += a.ss_part[(int64_t)g * a.mp + m];
+      a.rs_out[m] = 1.f / sqrtf(s / (float)a.d + a.eps);
+    } else {
+      float bv = -INFINITY;
+      int bi = -1;
+      for (int g = 0; g < a.G; ++g) {
+        const float v = a.amax_v[(int64_t)g * a.mp + m];
+        const int i = a.amax_i[(int64_t)g * a.mp + m];
+        if (arg_better(v, i, bv, bi)) {
+          bv = v;
+          bi = i;
+        }
+      }
+      if (a.argmax_out && a.rows[m].valid) a.argmax_out[m] = bi < 0 ? 0 : bi;
+    }
+  }
+  if (threadIdx.x == 0) *a.done = 0;
+}
+
+template <typename T, int TB, int NG, int EPI>
+__global__ void __launch_bounds__(kGemmThreads, 2) gemm_kernel(GemmArgs a) {
+  constexpr int C = NG * 16;
+  constexpr int NACC = NG * TB;
+  constexpr int EPL = 16 / sizeof(T);
+  constexpr int KTILE = 4 * EPL;
+  // reduction buffer for waves 2,3 (later reused as the output tile)
+  __shared__ f32x4 red[2][NACC][kWave];
+  __shared__ int s_flag;
+  float* tile = reinterpret_cast<float*>(&red[1][0][0]);
+  static_assert(NACC * kWave * 4 >= TB * 16 * C, "tile must fit the reduction buffer");
+
+  const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+  const int64_t U = (int64_t)a.G * a.KT;
+  const int w = blockIdx.x;
+  const int64_t u0 = unit_start(w, U, a.n_wg), u1 = unit_start(w + 1, U, a.n_wg);
+  const uint4* W = reinterpret_cast<const uint4*>(a.W);
+  const int MC = a.M * C;
+
+  for (int64_t u = u0; u < u1;) {
+    const int g = (int)(u / a.KT);
+    const int kb = (int)(u % a.KT);
+    const int ke = (int)std::min<int64_t>(a.KT, kb + (u1 - u));
+    const bool full = kb == 0 && ke == a.KT;
+    const int which = (g == (int)(u0 / a.KT)) ? 0 : 1;
+    u += ke - kb;
+
+    // ---- stream this segment: each wave takes a quarter of the k-tiles ----
+    const int S = ke - kb;
+    const int ka = kb + S * wave / 4, kz = kb + S * (wave + 1) / 4;
+    f32x4 acc[NACC];
+#pragma unroll
+    for (int i = 0; i < NACC; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+    const uint4* Wg = W + (int64_t)g * NG * a.KT * kWave + lane;
+    const char* Xl = a.X + ((int64_t)(a.m0 + lane % 16) * a.ldx + (lane / 16) * EPL) * sizeof(T);
+    const int64_t xrow16 = (int64_t)16 * a.ldx * sizeof(T);
+    uint4 wa0[NG], wa1[NG], xb0[TB], xb1[TB];
+    auto load = [&](int kt, uint4* wa, uint4* xb) {
+#pragma unroll
+      for (int nt = 0; nt < NG; ++nt) wa[nt] = load_nt16(Wg + ((int64_t)nt * a.KT + kt) * kWave);
+#pragma unroll
+      for (int tb = 0; tb < TB; ++tb) xb[tb] = load16(Xl + tb * xrow16 + (int64_t)kt * KTILE * sizeof(T));
+    };
+    auto mma = [&](const uint4* wa, const uint4* xb) {
+#pragma unroll
+      for (int nt = 0; nt < NG; ++nt)
+#pragma unroll
+        for (int tb = 0; tb < TB; ++tb) mma_tile<T>(wa[nt], xb[tb], acc[nt * TB + tb]);
+    };
+    if (ka < kz) load(ka, wa0, xb0);
+    for (int kt = ka; kt < kz; kt += 2) {
+      if (kt + 1 < kz) load(kt + 1, wa1, xb1);
+      mma(wa0, xb0);
+      if (kt + 1 < kz) {
+        if (kt + 2 < kz) load(kt + 2, wa0, xb0);
+        mma(wa1, xb1);
+      }
+    }
+
+    // ---- reduce the four waves: (w0 + w2) + (w1 + w3), fixed order ----
+    __syncthreads();  // previous segment's tile readers are done
+    if (wave >= 2)
+#pragma unroll
+      for (int i = 0; i < NACC; ++i) red[wave - 2][i][lane] = acc[i];
+    __syncthreads();
+    if (wave < 2)
+#pragma unroll
+      for (int i = 0; i < NACC; ++i) acc[i] += red[wave][i][lane];
+    __syncthreads();
+    if (wave == 1)
+#pragma unroll
+      for (int i = 0; i < NACC; ++i) red[0][i][lane] = acc[i];
+    __syncthreads();
+    if (wave == 0) {
+#pragma unroll
+      for (int i = 0; i < NACC; ++i) acc[i] += red[0][i][lane];
+      // acc[nt*TB+tb] element e: row tb*16 + lane%16, column nt*16 + 4*(lane/16) + e
+#pragma unroll
+      for (int nt = 0; nt < NG; ++nt)
+#pragma unroll
+        for (int tb = 0; tb < TB; ++tb)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) tile[(tb * 16 + lane % 16) * C + nt * 16 + 4 * (lane / 16) + e] = acc[nt * TB + tb][e];
+    }
+    __syncthreads();
+
+    if (!full) {
+      // ---- split column group: publish the partial, last contributor reduces ----
+      float* my = a.part + ((int64_t)w * 2 + which) * MC;
+      for (int i = threadIdx.x; i < MC; i += kGemmThreads) my[i] = tile[i];
+      __syncthreads();
+      const int wf = unit_owner((int64_t)g * a.KT, U, a.n_wg);
+      const int wl = unit_owner((int64_t)(g + 1) * a.KT - 1, U, a.n_wg);
+      if (threadIdx.x == 0) {
+        __threadfence();
+        const int old = atomicAdd(&a.cnt[g], 1);
+        s_flag = old == wl - wf;
+      }
+      __syncthreads();
+      if (!s_flag) continue;
+      __threadfence();
+      for (int i = threadIdx.x; i < MC; i += kGemmThreads) {
+        float s = 0.f;
+        for (int ww = wf; ww <= wl; ++ww) {
+          const int wh = (g == (int)(unit_start(ww, U, a.n_wg) / a.KT)) ? 0 : 1;
+          s += a.part[((int64_t)ww * 2 + wh) * MC + i];
+        }
+        tile[i] = s;
+      }
+      if (threadIdx.x == 0) a.cnt[g] = 0;
+      __syncthreads();
+    }
+
+    // ---- epilogue on the final tile of column group g ----
+    if constexpr (EPI == EPI_QKV) epilogue_qkv<T, NG>(a, tile, g, 0);
+    if constexpr (EPI == EPI_RESID) epilogue_resid<T, NG>(a, tile, g);
+    if constexpr (EPI == EPI_SWIGLU) epilogue_swiglu<T, NG>(a, tile, g);
+    if constexpr (EPI == EPI_LOGITS) epilogue_logits<NG>(a, tile, g);
+    if constexpr (EPI == EPI_RESID || EPI == EPI_LOGITS) finish_rows<EPI>(a);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Attention: one workgroup per (row, query head).  Scores of a chunk of
+// positions go to LDS; the softmax is carried online across chunks.
+constexpr int kAttnChunk = 1024;
+
+struct AttnArgs {
+  const char* q;  // [rows][hq][hd]
+  const char* kc;
+  const char* vc;
+  char* out;      // [rows][hq*hd]
+  const RowInfo* rows;
+  int m0, hq, hkv, hd, max_len;
+  float scale;
+};
+
+template <typename T>
+__global__ void __launch_bounds__(256) attention_kernel(AttnArgs a) {
+  __shared__ float qs[128];
+  __shared__ float sc[kAttnChunk];
+  __shared__ float red[8];
+  __shared__ float acc2[256];
+  const int m = a.m0 + blockIdx.x, h = blockIdx.y;
+  const int tid = threadIdx.x, lane = tid % kWave, wave = tid / kWave;
+  const RowInfo ri = a.rows[m];
+  const int hd = a.hd;
+  T* outp = reinterpret_cast<T*>(a.out) + ((int64_t)m * a.hq + h) * hd;
+  if (!ri.valid) {
+    for (int d = tid; d < hd; d += 256) outp[d] = Elem<T>::from_f32(0.f);
+    return;
+  }
+  const int kh = h / (a.hq / a.hkv);
+  const T* qp = reinterpret_cast<const T*>(a.q) + ((int64_t)m * a.hq + h) * hd;
+  for (int d = tid; d < hd; d += 256) qs[d] = Elem<T>::to_f32(qp[d]) * a.scale;
+  __syncthreads();
+  const int64_t hb = ((int64_t)ri.seq * a.hkv + kh) * a.max_len;
+  const T* K = reinterpret_cast<const T*>(a.kc) + hb * hd;
+  const T* Vp = reinterpret_cast<const T*>(a.vc) + hb * hd;
+  const int npos = ri.pos + 1;
+  float run_m = -INFINITY, run_l = 0.f;
+  const int dsub = tid / hd, dd = tid % hd;  // PV: (sub-group, dim)
+  const int nsub = 256 / hd;
+  float acc = 0.f;
+  for (int p0 = 0; p0 < npos; p0 += kAttnChunk) {
+    const int n = min(kAttnChunk, npos - p0);
+    float lmax = -INFINITY;
+    for (int i = tid; i < n; i += 256) {
+      const T* kr = K + (int64_t)(p0 + i) * hd;
+      float s = 0.f;
+      for (int d = 0; d < hd; ++d) s += qs[d] * Elem<T>::to_f32(kr[d]);
+      sc[i] = s;
+      lmax = fmaxf(lmax, s);
+    }
+    lmax = wave_max(lmax);
+    if (lane == 0) red[wave] = lmax;
+    __syncthreads();
+    float cm = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+    const float new_m = fmaxf(run_m, cm);
+    float lsum = 0.f;
+    for (int i = tid; i < n; i += 256) {
+      const float e = expf(sc[i] - new_m);
+      sc[i] = e;
+      lsum += e;
+    }
+    lsum = wave_sum(lsum);
+    __syncthreads();
+    if (lane == 0) red[4 + wave] = lsum;
+    __syncthreads();
+    const float csum = (red[4] + red[5]) + (red[6] + red[7]);
+    const float alpha = expf(run_m - new_m);
+    run_l = run_l * alpha + csum;
+    run_m = new_m;
+    acc *= alpha;
+    if (dsub < nsub)
+      for (int i = dsub; i < n; i += nsub) acc += sc[i] * Elem<T>::to_f32(Vp[(int64_t)(p0 + i) * hd + dd]);
+    __syncthreads();
+  }
+  if (dsub < nsub) acc2[dsub * hd + dd] = acc;
+  __syncthreads();
+  if (tid < hd) {
+    float o = 0.f;
+    for (int s = 0; s < nsub; ++s) o += acc2[s * hd + tid];
+    outp[tid] = Elem<T>::from_f32(o / run_l);
+  }
+}
+
+// ---------------------------------------------------------------------------
+struct EmbedArgs {
+  const char* E;  // [V][d]
+  const float* g; // attention-norm gain of layer 0 (or final norm when there are no layers)
+  float* x;
+  char* xa;
+  float* rs;
+  RowInfo* rows;
+  int d, V, R, gamma, max_len, max_batch;
+  float eps;
+  // verify
+  const int32_t* seq_ids;
+  const int32_t* drafts;
+  const int32_t* kv_len;
+  const int32_t* pending;
+  // prefill
+  const int32_t* tokens;
+  int seq, pos0, prefill;
+  int32_t* err;
+};
+
+template <typename T>
+__global__ void __launch_bounds__(256) embed_kernel(EmbedArgs a) {
+  __shared__ float red[4];
+  __shared__ int s_tok;
+  const int m = blockIdx.x, tid = threadIdx.x;
+  if (tid == 0) {
+    int seq, pos, tok, valid;
+    if (a.prefill) {
+      seq = a.seq;
+      pos = a.pos0 + m;
+      tok = a.tokens[m];
+      valid = pos < a.max_len;
+    } else {
+      const int s = m / a.R, r = m % a.R;
+      seq = a.seq_ids[s];
+      if (seq < 0 || seq >= a.max_batch) {  // refused: no cache slot to read or write
+        if (r == 0) atomicOr(a.err, 4);
+        seq = 0;
+        pos = 0;
+        tok = 0;
+        valid = 0;
+      } else {
+        const int len = a.kv_len[seq];
+        pos = len + r;
+        tok = r == 0 ? a.pending[seq] : a.drafts[(int64_t)s * a.gamma + r - 1];
+        valid = len + a.R <= a.max_len;
+        if (!valid && r == 0) atomicOr(a.err, 1);
+      }
+    }
+    if (tok < 0 || tok >= a.V) {
+      atomicOr(a.err, 2);
+      tok = 0;
+    }
+    RowInfo ri;
+    ri.seq = seq;
+    ri.pos = valid ? pos : 0;
+    ri.valid = valid;
+    ri.pad = 0;
+    a.rows[m] = ri;
+    s_tok = tok;
+  }
+  __syncthreads();
+  const T* e = reinterpret_cast<const T*>(a.E) + (int64_t)s_tok * a.d;
+  float ss = 0.f;
+  for (int i = tid; i < a.d; i += 256) {
+    const float v = Elem<T>::to_f32(e[i]);
+    a.x[(int64_t)m * a.d + i] = v;
+    store_t<T>(a.xa, (int64_t)m * a.d + i, v * a.g[i]);
+    ss += v * v;
+  }
+  ss = wave_sum(ss);
+  if (tid % kWave == 0) red[tid / kWave] = ss;
+  __syncthreads();
+  if (tid == 0) a.rs[m] = 1.f / sqrtf(((red[0] + red[1]) + (red[2] + red[3])) / (float)a.d + a.eps);
+}
+
+__global__ void commit_kernel(int32_t* len, int32_t* pending, int32_t* err, const int32_t* seq_ids, int n,
+                              const int32_t* L, const int32_t* nxt, int max_len, int max_batch, int V) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  const int s = seq_ids[i];
+  if (s < 0 || s >= max_batch) {
+    atomicOr(err, 4);
+    return;
+  }
+  const int l = L[i], t = nxt[i];
+  if (l < 0 || len[s] + l + 1 > max_len || t < 0 || t >= V) {
+    atomicOr(err, 1);
+    return;
+  }
+  len[s] += l + 1;
+  pending[s] = t;
+}
+
+__global__ void prefill_finish_kernel(int32_t* len, int32_t* pending, int32_t* err, int seq, int n,
+                                      const int32_t* tokens, int V) {
+  if (threadIdx.x != 0 || blockIdx.x != 0) return;
+  int t = tokens[n - 1];
+  if (t < 0 || t >= V) {
+    atomicOr(err, 2);
+    t = 0;
+  }
+  len[seq] = n - 1;
+  pending[seq] = t;
+}
+
+__global__ void kv_init_kernel(int32_t* len, int32_t* pending, int32_t* err, int max_batch, float* rope, int max_len,
+                               int half, double theta) {
+  const int64_t n = (int64_t)max_len * half;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
+    const int pos = (int)(i / half), j = (int)(i % half);
+    const double inv_freq = pow(theta, -2.0 * j / (2.0 * half));
+    const double ang = (double)pos * inv_freq;
+    rope[2 * i] = (float)cos(ang);
+    rope[2 * i + 1] = (float)sin(ang);
+  }
+  if (blockIdx.x == 0) {
+    for (int i = threadIdx.x; i < max_batch; i += blockDim.x) {
+      len[i] = 0;
+      pending[i] = 0;
+    }
+    if (threadIdx.x == 0) *err = 0;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Host side
+
+static int pick_ng(int64_t ntiles, bool pairs) {
+  for (int ng : {8, 4, 2}) {
+    if (ntiles % ng == 0 && (!pairs || ng % 2 == 0)) return ng;
+  }
+  return pairs ? 2 : 1;
+}
+
+static size_t counters_bytes(const sdd_model* m) {
+  const int64_t g = ceil_div(m->cfg.vocab, 16) + ceil_div(2 * (int64_t)m->cfg.d_ff, 16) + 64;
+  return align_up((size_t)g * 4 + 64, 256);
+}
+
+WsLayout ws_layout(const sdd_model* m, int max_rows) {
+  WsLayout L{};
+  const sdd_model_config& c = m->cfg;
+  const int es = m->es;
+  const int mp = (int)align_up((size_t)std::max(1, max_rows), 16);
+  const int64_t d = c.d_model, hq = (int64_t)c.n_q_heads * c.head_dim;
+  L.mp = mp;
+  L.n_wg = 2 * m->n_cu;
+  L.max_groups = (int)ceil_div(std::max<int64_t>(c.vocab, std::max<int64_t>(2 * (int64_t)c.d_ff, d)), 16);
+  size_t off = 0;
+  auto take = [&](size_t b) {
+    size_t o = off;
+    off = align_up(off + b, 256);
+    return o;
+  };
+  L.cnt = take(counters_bytes(m));  // first: survives calls with other row counts
+  L.rowinfo = take((size_t)mp * sizeof(RowInfo));
+  L.x = take((size_t)mp * d * 4);
+  L.xa = take((size_t)mp * d * es);
+  L.rs = take((size_t)mp * 4);
+  L.ss_part = take((size_t)ceil_div(d, 16) * mp * 4);
+  L.q = take((size_t)mp * hq * es);
+  L.ao = take((size_t)mp * hq * es);
+  L.ffh = take((size_t)mp * c.d_ff * es);
+  L.part = take((size_t)L.n_wg * 2 * kMaxPassRows * 128 * 4);
+  L.amax = take((size_t)L.max_groups * mp * 8);
+  L.attn_part = 0;
+  L.total = off;
+  return L;
+}
+
+struct CallCtx {
+  sdd_model* m;
+  sdd_kv* kv;
+  char* ws;
+  WsLayout L;
+  hipStream_t st;
+};
+
+template <typename T, int NG, int EPI>
+static void launch_gemm_tb(int tb, const GemmArgs& a, int nblocks, hipStream_t st) {
+  switch (tb) {
+    case 1: hipLaunchKernelGGL((gemm_kernel<T, 1, NG, EPI>), dim3(nblocks), dim3(kGemmThreads), 0, st, a); break;
+    case 2: hipLaunchKernelGGL((gemm_kernel<T, 2, NG, EPI>), dim3(nblocks), dim3(kGemmThreads), 0, st, a); break;
+    case 3: hipLaunchKernelGGL((gemm_kernel<T, 3, NG, EPI>), dim3(nblocks), dim3(kGemmThreads), 0, st, a); break;
+    default: hipLaunchKernelGGL((gemm_kernel<T, 4, NG, EPI>), dim3(nblocks), dim3(kGemmThreads), 0, st, a); break;
+  }
+}
+
+template <typename T, int EPI>
+static void launch_gemm_ng(int ng, int tb, const GemmArgs& a, int nblocks, hipStream_t st) {
+  switch (ng) {
+    case 8: launch_gemm_tb<T, 8, EPI>(tb, a, nblocks, st); break;
+    case 4: launch_gemm_tb<T, 4, EPI>(tb, a, nblocks, st); break;
+    default: launch_gemm_tb<T, 2, EPI>(tb, a, nblocks, st); break;
+  }
+}
+
+// Runs one GEMM over rows [0, M) in passes of at most 64 rows.
+static int run_gemm(CallCtx& cx, int epi, size_t w_off, int64_t N, int K, const char* X, GemmArgs a, int M, int ng) {
+  const sdd_model* m = cx.m;
+  a.W = m->base + w_off;
+  a.KT = (int)ceil_div(K, m->ktile);
+  const int64_t ntiles = ceil_div(N, 16);
+  a.G = (int)(ntiles / ng);
+  a.N = (int)N;
+  a.X = X;
+  a.ldx = K;
+  a.mp = cx.L.mp;
+  a.part = reinterpret_cast<float*>(cx.ws + cx.L.part);
+  a.cnt = reinterpret_cast<int*>(cx.ws + cx.L.cnt) + 16;
+  a.done = reinterpret_cast<int*>(cx.ws + cx.L.cnt);
+  a.rows = reinterpret_cast<const RowInfo*>(cx.ws + cx.L.rowinfo);
+  a.eps = m->cfg.rms_eps;
+  const int64_t U = (int64_t)a.G * a.KT;
+  const int nblocks = (int)std::min<int64_t>(U, cx.L.n_wg);
+  a.n_wg = nblocks;
+  for (int m0 = 0; m0 < M; m0 += kMaxPassRows) {
+    a.m0 = m0;
+    a.M = std::min(kMaxPassRows, M - m0);
+    const int tb = (int)ceil_div(a.M, 16);
+    if (m->es == 2) {
+      switch (epi) {
+        case EPI_QKV: launch_gemm_ng<uint16_t, EPI_QKV>(ng, tb, a, nblocks, cx.st); break;
+        case EPI_RESID: launch_gemm_ng<uint16_t, EPI_RESID>(ng, tb, a, nblocks, cx.st); break;
+        case EPI_SWIGLU: launch_gemm_ng<uint16_t, EPI_SWIGLU>(ng, tb, a, nblocks, cx.st); break;
+        default: launch_gemm_ng<uint16_t, EPI_LOGITS>(ng, tb, a, nblocks, cx.st); break;
+      }
+    } else {
+      switch (epi) {
+        case EPI_QKV: launch_gemm_ng<float, EPI_QKV>(ng, tb, a, nblocks, cx.st); break;
+        case EPI_RESID: launch_gemm_ng<float, EPI_RESID>(ng, tb, a, nblocks, cx.st); break;
+        case EPI_SWIGLU: launch_gemm_ng<float, EPI_SWIGLU>(ng, tb, a, nblocks, cx.st); break;
+        default: launch_gemm_ng<float, EPI_LOGITS>(ng, tb, a, nblocks, cx.st); break;
+      }
+    }
+    int rc = check_launch("gemm_kernel");
+    if (rc) return rc;
+  }
+  return SDD_OK;
+}
+
+// Forward of M rows whose RowInfo/x/xa/rs were written by embed_kernel.
+static int forward_rows(CallCtx& cx, int M, float* logits, int32_t* argmax) {
+  sdd_model* m = cx.m;
+  sdd_kv* kv = cx.kv;
+  const sdd_model_config& c = m->cfg;
+  const int64_t d = c.d_model, hd = c.head_dim, hq = c.n_q_heads * hd, hk = c.n_kv_heads * hd;
+  char* ws = cx.ws;
+  const WsLayout& L = cx.L;
+  float* x = reinterpret_cast<float*>(ws + L.x);
+  char* xa = ws + L.xa;
+  float* rs = reinterpret_cast<float*>(ws + L.rs);
+  int rc;
+  for (int l = 0; l < c.n_layers; ++l) {
+    const sdd_model::Layer& Ly = m->layers[l];
+    // q/k/v + QK-norm + RoPE + cache append
+    {
+      GemmArgs a{};
+      a.rs = rs;
+      a.q_out = ws + L.q;
+      a.hq = c.n_q_heads;
+      a.hkv = c.n_kv_heads;
+      a.hd = c.head_dim;
+      a.qk_norm = c.qk_norm;
+      a.qn = reinterpret_cast<const float*>(m->base + Ly.q_norm);
+      a.kn = reinterpret_cast<const float*>(m->base + Ly.k_norm);
+      a.rope = kv->rope;
+      a.max_len = kv->max_len;
+      a.kc = kv->k + (size_t)l * kv->layer_stride;
+      a.vc = kv->v + (size_t)l * kv->layer_stride;
+      if ((rc = run_gemm(cx, EPI_QKV, Ly.qkv, hq + 2 * hk, (int)d, xa, a, M, (int)(hd / 16)))) return rc;
+    }
+    // attention
+    {
+      AttnArgs a{};
+      a.q = ws + L.q;
+      a.kc = kv->k + (size_t)l * kv->layer_stride;
+      a.vc = kv->v + (size_t)l * kv->layer_stride;
+      a.out = ws + L.ao;
+      a.rows = reinterpret_cast<const RowInfo*>(ws + L.rowinfo);
+      a.m0 = 0;
+      a.hq = c.n_q_heads;
+      a.hkv = c.n_kv_heads;
+      a.hd = c.head_dim;
+      a.max_len = kv->max_len;
+      a.scale = 1.f / sqrtf((float)c.head_dim);
+      if (m->es == 2)
+        hipLaunchKernelGGL(attention_kernel<uint16_t>, dim3(M, c.n_q_heads), dim3(256), 0, cx.st, a);
+      else
+        hipLaunchKernelGGL(attention_kernel<float>, dim3(M, c.n_q_heads), dim3(256), 0, cx.st, a);
+      if ((rc = check_launch("attention_kernel"))) return rc;
+    }
+    // output projection + residual; next input scaled by the FFN norm gain
+    {
+      GemmArgs a{};
+      a.rs = nullptr;
+      a.x = x;
+      a.xa = xa;
+      a.d = (int)d;
+      a.g_next = reinterpret_cast<const float*>(m->base + Ly.ffn_norm);
+      a.ss_part = reinterpret_cast<float*>(ws + L.ss_part);
+      a.rs_out = rs;
+      if ((rc = run_gemm(cx, EPI_RESID, Ly.o, d, (int)hq, ws + L.ao, a, M, pick_ng(d / 16, false)))) return rc;
+    }
+    // gate/up + SwiGLU
+    {
+      GemmArgs a{};
+      a.rs = rs;
+      a.ffh = ws + L.ffh;
+      a.dff = c.d_ff;
+      if ((rc = run_gemm(cx, EPI_SWIGLU, Ly.gu, 2 * (int64_t)c.d_ff, (int)d, xa, a, M, pick_ng(2 * (int64_t)c.d_ff / 16, true))))
+        return rc;
+    }
+    // down projection + residual; next input scaled by the next norm gain
+    {
+      GemmArgs a{};
+      a.rs = nullptr;
+      a.x = x;
+      a.xa = xa;
+      a.d = (int)d;
+      a.g_next = reinterpret_cast<const float*>(
+          m->base + (l + 1 < c.n_layers ? m->layers[l + 1].attn_norm : m->off_final_norm));
+      a.ss_part = reinterpret_cast<float*>(ws + L.ss_part);
+      a.rs_out = rs;
+      if ((rc = run_gemm(cx, EPI_RESID, Ly.down, d, c.d_ff, ws + L.ffh, a, M, pick_ng(d / 16, false)))) return rc;
+    }
+  }
+  if (logits) {
+    GemmArgs a{};
+    a.rs = rs;
+    a.logits = logits;
+    a.V = c.vocab;
+    a.amax_v = reinterpret_cast<float*>(ws + L.amax);
+    a.amax_i = reinterpret_cast<int*>(ws + L.amax + (size_t)L.max_groups * L.mp * 4);
+    a.argmax_out = argmax;
+    if ((rc = run_gemm(cx, EPI_LOGITS, m->off_lm, c.vocab, (int)d, xa, a, M, pick_ng(c.vocab / 16, false)))) return rc;
+  }
+  return SDD_OK;
+}
+
+static int launch_embed(CallCtx& cx, EmbedArgs e, int M) {
+  sdd_model* m = cx.m;
+  const sdd_model_config& c = m->cfg;
+  e.E = m->base + m->off_embed;
+  e.g = reinterpret_cast<const float*>(m->base + (c.n_layers > 0 ? m->layers[0].attn_norm : m->off_final_norm));
+  e.x = reinterpret_cast<float*>(cx.ws + cx.L.x);
+  e.xa = cx.ws + cx.L.xa;
+  e.rs = reinterpret_cast<float*>(cx.ws + cx.L.rs);
+  e.rows = reinterpret_cast<RowInfo*>(cx.ws + cx.L.rowinfo);
+  e.d = c.d_model;
+  e.V = c.vocab;
+  e.max_len = cx.kv->max_len;
+  e.max_batch = cx.kv->max_batch;
+  e.eps = c.rms_eps;
+  e.err = cx.kv->err;
+  if (m->es == 2)
+    hipLaunchKernelGGL(embed_kernel<uint16_t>, dim3(M), dim3(256), 0, cx.st, e);
+  else
+    hipLaunchKernelGGL(embed_kernel<float>, dim3(M), dim3(256), 0, cx.st, e);
+  return check_launch("embed_kernel");
+}
+
+}  // namespace sdd
+
+using namespace sdd;
+
+extern "C" int sdd_kv_bytes(const sdd_model_config* cfg, int max_batch, int max_len, size_t* bytes) {
+  SDD_REQUIRE(cfg && bytes, "NULL pointer");
+  SDD_REQUIRE(max_batch > 0 && max_len > 0, "bad max_batch/max_len");
+  const int es = cfg->dtype == SDD_BF16 ? 2 : 4;
+  size_t hdr = align_up((size_t)(2 * max_batch + 1) * 4, 256);
+  size_t rope = align_up((size_t)max_len * cfg->head_dim * 4, 256);
+  size_t per_layer = align_up((size_t)max_batch * cfg->n_kv_heads * max_len * cfg->head_dim * es, 256);
+  *bytes = hdr + rope + 2 * per_layer * (size_t)std::max(1, cfg->n_layers);
+  return SDD_OK;
+}
+
+extern "C" int sdd_kv_create(sdd_model* m, int max_batch, int max_len, void* buf, size_t bytes, sdd_stream_t stream,
+                             sdd_kv** out) {
+  SDD_REQUIRE(m && buf && out, "NULL pointer");
+  size_t need = 0;
+  int rc = sdd_kv_bytes(&m->cfg, max_batch, max_len, &need);
+  if (rc) return rc;
+  if (bytes < need) return fail(SDD_ENOMEM, "KV buffer needs %zu bytes, got %zu", need, bytes);
+  SDD_REQUIRE((uintptr_t)buf % 256 == 0, "KV buffer must be 256-byte aligned");
+  sdd_kv* kv = new (std::nothrow) sdd_kv();
+  if (!kv) return fail(SDD_ENOMEM, "host allocation failed");
+  const sdd_model_config& c = m->cfg;
+  kv->m = m;
+  kv->max_batch = max_batch;
+  kv->max_len = max_len;
+  kv->base = reinterpret_cast<char*>(buf);
+  kv->bytes = bytes;
+  kv->len = reinterpret_cast<int32_t*>(kv->base);
+  kv->pending = kv->len + max_batch;
+  kv->err = kv->pending + max_batch;
+  size_t hdr = align_up((size_t)(2 * max_batch + 1) * 4, 256);
+  kv->rope = reinterpret_cast<float*>(kv->base + hdr);
+  size_t rope = align_up((size_t)max_len * c.head_dim * 4, 256);
+  kv->layer_stride = align_up((size_t)max_batch * c.n_kv_heads * max_len * c.head_dim * m->es, 256);
+  kv->k = kv->base + hdr + rope;
+  kv->v = kv->k + kv->layer_stride * (size_t)std::max(1, c.n_layers);
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  const int64_t n = (int64_t)max_len * (c.head_dim / 2);
+  hipLaunchKernelGGL(kv_init_kernel, dim3((int)std::min<int64_t>(ceil_div(n, 256), 4096)), dim3(256), 0, st, kv->len,
+                     kv->pending, kv->err, max_batch, kv->rope, max_len, c.head_dim / 2, (double)c.rope_theta);
+  rc = check_launch("kv_init_kernel");
+  if (rc) {
+    delete kv;
+    return rc;
+  }
+  *out = kv;
+  return SDD_OK;
+}
+
+extern "C" int sdd_kv_destroy(sdd_kv* kv) {
+  delete kv;
+  return SDD_OK;
+}
+
+extern "C" int sdd_kv_state(sdd_kv* kv, int32_t* len, int32_t* pending, int32_t* error_bits, sdd_stream_t stream) {
+  SDD_REQUIRE(kv != nullptr, "kv is NULL");
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  if (len) SDD_HIP(hipMemcpyAsync(len, kv->len, (size_t)kv->max_batch * 4, hipMemcpyDeviceToHost, st));
+  if (pending) SDD_HIP(hipMemcpyAsync(pending, kv->pending, (size_t)kv->max_batch * 4, hipMemcpyDeviceToHost, st));
+  if (error_bits) SDD_HIP(hipMemcpyAsync(error_bits, kv->err, 4, hipMemcpyDeviceToHost, st));
+  SDD_HIP(hipStreamSynchronize(st));
+  return SDD_OK;
+}
+
+extern "C" int sdd_workspace_bytes(const sdd_model* m, int max_rows, size_t* bytes) {
+  SDD_REQUIRE(m && bytes, "NULL pointer");
+  SDD_REQUIRE(max_rows > 0 && max_rows <= 65536, "bad max_rows %d", max_rows);
+  *bytes = ws_layout(m, max_rows).total;
+  return SDD_OK;
+}
+
+static int make_ctx(CallCtx& cx, sdd_model* m, sdd_kv* kv, void* ws, size_t ws_bytes, int rows, hipStream_t st) {
+  SDD_REQUIRE(m && kv && ws, "NULL pointer");
+  SDD_REQUIRE(kv->m == m, "KV cache belongs to another model");
+  SDD_REQUIRE((uintptr_t)ws % 256 == 0, "workspace must be 256-byte aligned");
+  cx.m = m;
+  cx.kv = kv;
+  cx.ws = reinterpret_cast<char*>(ws);
+  cx.L = ws_layout(m, rows);
+  cx.st = st;
+  if (cx.L.total > ws_bytes)
+    return fail(SDD_ECAPACITY, "workspace of %zu bytes is too small for %d rows (%zu needed)", ws_bytes, rows, cx.L.total);
+  return SDD_OK;
+}
+
+extern "C" int sdd_kv_prefill(sdd_model* m, sdd_kv* kv, int seq, const int32_t* tokens, int n, void* ws,
+                              size_t ws_bytes, sdd_stream_t stream) {
+  SDD_REQUIRE(m && kv && tokens, "NULL pointer");
+  SDD_REQUIRE(seq >= 0 && seq < kv->max_batch, "bad seq %d", seq);
+  SDD_REQUIRE(n >= 1, "prefill needs at least one token");
+  if (n - 1 > kv->max_len) return fail(SDD_ECAPACITY, "prompt of %d tokens exceeds max_len %d", n, kv->max_len);
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  // largest chunk whose layout fits the workspace
+  int chunk = 0;
+  for (int r : {256, 128, 64, 32, 16}) {
+    if (ws_layout(m, r).total <= ws_bytes) {
+      chunk = r;
+      break;
+    }
+  }
+  if (chunk == 0) return fail(SDD_ECAPACITY, "workspace too small for prefill");
+  for (int c0 = 0; c0 < n - 1; c0 += chunk) {
+    const int rows = std::min(chunk, n - 1 - c0);
+    CallCtx cx;
+    int rc = make_ctx(cx, m, kv, ws, ws_bytes, chunk, st);
+    if (rc) return rc;
+    EmbedArgs e{};
+    e.prefill = 1;
+    e.seq = seq;
+    e.pos0 = c0;
+    e.tokens = tokens + c0;
+    e.R = rows;
+    if ((rc = launch_embed(cx, e, rows))) return rc;
+    if ((rc = forward_rows(cx, rows, nullptr, nullptr))) return rc;
+  }
+  hipLaunchKernelGGL(prefill_finish_kernel, dim3(1), dim3(64), 0, st, kv->len, kv->pending, kv->err, seq, n, tokens,
+                     m->cfg.vocab);
+  return check_launch("prefill_finish_kernel");
+}
+
+extern "C" int sdd_verify_block(sdd_model* m, sdd_kv* kv, const int32_t* seq_ids, int n_seq, const int32_t* drafts,
+                                int gamma, float* logits, int32_t* argmax, void* ws, size_t ws_bytes,
+                                sdd_stream_t stream) {
+  SDD_REQUIRE(m && kv && seq_ids && logits, "NULL pointer");
+  SDD_REQUIRE(n_seq > 0 && n_seq <= kv->max_batch, "bad n_seq %d", n_seq);
+  SDD_REQUIRE(gamma >= 0 && gamma <= 64, "gamma must be in [0, 64]");
+  SDD_REQUIRE(gamma == 0 || drafts, "drafts is NULL");
+  if (gamma + 1 > kv->max_len) return fail(SDD_ECAPACITY, "block of %d rows exceeds max_len", gamma + 1);
+  const int R = gamma + 1, M = n_seq * R;
+  CallCtx cx;
+  int rc = make_ctx(cx, m, kv, ws, ws_bytes, M, reinterpret_cast<hipStream_t>(stream));
+  if (rc) return rc;
+  EmbedArgs e{};
+  e.prefill = 0;
+  e.seq_ids = seq_ids;
+  e.drafts = drafts;
+  e.kv_len = kv->len;
+  e.pending = kv->pending;
+  e.R = R;
+  e.gamma = gamma;
+  if ((rc = launch_embed(cx, e, M))) return rc;
+  return forward_rows(cx, M, logits, argmax);
+}
+
+extern "C" int sdd_kv_commit(sdd_kv* kv, const int32_t* seq_ids, int n_seq, const int32_t* accepted_len,
+                             const int32_t* next_token, sdd_stream_t stream) {
+  SDD_REQUIRE(kv && seq_ids && accepted_len && next_token, "NULL pointer");
+  SDD_REQUIRE(n_seq > 0 && n_seq <= kv->max_batch, "bad n_seq %d", n_seq);
+  hipLaunchKernelGGL(commit_kernel, dim3((n_seq + 255) / 256), dim3(256), 0, reinterpret_cast<hipStream_t>(stream),
+                     kv->len, kv->pending, kv->err, seq_ids, n_seq, accepted_len, next_token, kv->max_len,
+                     kv->max_batch, kv->m->cfg.vocab);
+  return check_launch("commit_kernel");
+}

@@ -1,0 +1,39 @@
+"""Helpers shared by the GPU tests (no method arithmetic)."""
+import numpy as np
+import torch
+
+import workloads as W
+
+
+def untile(buf: np.ndarray, rows: int, cols: int, dtype: str) -> np.ndarray:
+    """Decodes libsdd's documented tiled weight layout back to a row-major [rows][cols] matrix.
+
+    Tiles of 16 rows x ktile columns (ktile 32 for bf16, 16 for fp32), 1 KiB each, ordered row-tile
+    major; lane l of a tile holds row l%16 and EPL = 16/sizeof(elem) columns from (l//16)*EPL."""
+    es = 2 if dtype == "bf16" else 4
+    epl = 16 // es
+    kt = 4 * epl
+    NT, KT = -(-rows // 16), -(-cols // kt)
+    if dtype == "bf16":
+        vals = W.bf16_bits_to_f32(buf[: NT * KT * 1024].view(np.uint16))
+    else:
+        vals = buf[: NT * KT * 1024].view(np.float32)
+    a = vals.reshape(NT, KT, 4, 16, epl).transpose(0, 3, 1, 2, 4).reshape(NT * 16, KT * kt)
+    return a[:rows, :cols]
+
+
+def to_dev_i32(a) -> torch.Tensor:
+    return torch.from_numpy(np.ascontiguousarray(a, np.int32)).cuda()
+
+
+def row_tol_ok(got: np.ndarray, want: np.ndarray, rel: float):
+    """Per-row max |got - want| <= rel * max |want| (the logit-scale tolerance)."""
+    err = np.abs(got - want).max(-1)
+    scale = np.abs(want).max(-1)
+    return err <= rel * scale, err / scale
+
+
+def argmax_near_tie(z: np.ndarray, tol: np.ndarray) -> np.ndarray:
+    """True where the top-2 gap of a row is below tol (an argmax that rounding may flip)."""
+    s = np.sort(z, axis=-1)
+    return (s[..., -1] - s[..., -2]) < tol

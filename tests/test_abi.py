@@ -1,0 +1,62 @@
+"""The C-ABI library loads and exports every function include/sdd.h declares; host-side argument
+checks return the documented status codes without touching a GPU."""
+import ctypes as C
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared():
+    src = open(os.path.join(ROOT, "include", "sdd.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(sdd_[a-z_0-9]+)\s*\(", src)))
+
+
+@pytest.fixture(scope="module")
+def S():
+    from paper_2608_14787_amd import sdd
+    if not os.path.exists(sdd.LIB_PATH):
+        from paper_2608_14787_amd import build
+        build.build()
+    return sdd
+
+
+def test_every_declared_symbol_is_exported(S):
+    names = _declared()
+    assert len(names) >= 18
+    lib = C.CDLL(S.LIB_PATH)
+    missing = [n for n in names if not hasattr(lib, n)]
+    assert not missing, missing
+
+
+def test_host_side_argument_errors(S):
+    L = S.lib()
+    assert L.sdd_status_string(S.EINVAL).decode() == "invalid argument"
+    out = C.c_size_t()
+    assert L.sdd_rowstats_workspace_bytes(0, 4, 10, C.byref(out)) == S.EINVAL
+    assert L.sdd_rowstats_workspace_bytes(2, 65, 10, C.byref(out)) == S.EINVAL
+    assert L.sdd_rowstats_workspace_bytes(2, 4, 10, C.byref(out)) == S.OK and out.value > 0
+    cfg = S.ModelConfig(2, 256, 4, 2, 64, 688, 4096, 1e-6, 1e4, 0, S.F32)
+    assert L.sdd_weights_bytes(C.byref(cfg), C.byref(out)) == S.OK
+    # 14.2 MB of fp32 weights for the tiny decoder (plus alignment)
+    assert 14.0e6 < out.value < 14.6e6
+    bad = S.ModelConfig(2, 256, 4, 2, 96, 688, 4096, 1e-6, 1e4, 0, S.F32)
+    assert L.sdd_weights_bytes(C.byref(bad), C.byref(out)) == S.EUNSUPPORTED
+    bad = S.ModelConfig(2, 256, 5, 2, 64, 688, 4096, 1e-6, 1e4, 0, S.F32)
+    assert L.sdd_weights_bytes(C.byref(bad), C.byref(out)) == S.EINVAL
+    # accept: NULL required pointers, bad mode parameters, bad shapes
+    P = C.c_void_p(16)
+    args = lambda **kw: [kw.get("draft", P), kw.get("p", P), S.BF16, None, S.BF16, 0, None, kw.get("B", 2),
+                         kw.get("gamma", 4), 100, kw.get("mode", S.GREEDY), kw.get("k", 1), kw.get("len", 1.0),
+                         P, P, None, P, 1 << 20, None]
+    assert L.sdd_accept(*args(p=None)) == S.EINVAL
+    assert L.sdd_accept(*args(B=0)) == S.EINVAL
+    assert L.sdd_accept(*args(gamma=65)) == S.EINVAL
+    assert L.sdd_accept(*args(mode=S.TOPK, k=0)) == S.EINVAL
+    assert L.sdd_accept(*args(mode=S.LENIENT, len=1.5)) == S.EINVAL
+    assert L.sdd_accept(*args(mode=S.RATIO)) == S.EINVAL  # ratio needs q and uniforms
+    assert L.sdd_confidence_prefix(P, S.BF16, 400, 2, 4, 100, float("nan"), P, None, None, None, P, 1 << 20, None) == S.EINVAL
+    assert L.sdd_confidence_prefix(P, S.BF16, 10, 2, 4, 100, 0.5, P, None, None, None, P, 1 << 20, None) == S.EINVAL
