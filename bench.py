@@ -1,0 +1,238 @@
+#!/usr/bin/env python3
+"""Benchmark of the verify hot path on one MI355X.
+
+One step = one pass of the whole hot path over one block: the pre-call
+confidence prefix on the drafter's logits, the gamma = 32 block verification
+(causal decoder forward of gamma + 1 rows against the KV cache, fp32 logits),
+the acceptance test and the commit.  Default workload: the Qwen3-32B-shaped
+target (64 layers, d 5120, 64/8 heads x 128, QK-norm, FFN 25600, V 151936,
+bf16, random weights) with a 1024-token prompt, 16 rounds of gamma = 32
+(each round appends the accepted tokens).  Drafts follow the target's own
+greedy continuation (precomputed, untimed) with 20% of the tokens replaced,
+so accepted lengths vary as in speculative decoding.
+
+Prints one JSON line (see the contract in the repository docs).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+import numpy as np  # noqa: E402
+
+import workloads as W  # noqa: E402
+
+METRIC = "verify-call ms & tokens verified/s at γ=32, Qwen3-32B shape; % HBM peak"
+HBM_PEAK_GBS = 8000.0  # MI355X HBM3E
+TAU = 0.7
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=16)
+    p.add_argument("--warmup", type=int, default=2)
+    p.add_argument("--workload", default="qwen32b", choices=["qwen32b", "qwen7b", "tiny"])
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--drafts", default="greedy", choices=["greedy", "random"])
+    p.add_argument("--all-kernels", action="store_true", help="report every kernel class (extra pass)")
+    return p.parse_args()
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+SHAPES = {"qwen32b": (W.QWEN32B, W.QWEN32B_PROMPT, W.GAMMA),
+          "qwen7b": (W.QWEN7B, W.QWEN7B_PROMPT, W.GAMMA),
+          "tiny": (W.TINY, W.TINY_PROMPT, W.GAMMA_TINY)}
+
+
+def layer_params(s: W.ModelShape) -> int:
+    d, hd = s.d_model, s.head_dim
+    return d * (s.n_q_heads + 2 * s.n_kv_heads) * hd + s.n_q_heads * hd * d + 3 * d * s.d_ff
+
+
+def cpu_baseline(shape: W.ModelShape, gamma: int) -> dict:
+    """The oracle on this host: one gamma-row verify through 1 layer + LM head, scaled to all layers."""
+    import oracle
+
+    s1 = shape.with_layers(1)
+    log("cpu baseline: building 1-layer oracle model")
+    m = oracle.Model(s1, W.WEIGHT_SEED, W.WEIGHT_SIGMA)
+    kv = oracle.KV(m, 64)
+    kv.prefill(W.prompt(101, 16, shape.vocab))
+    drafts = W.prompt(102, gamma, shape.vocab)
+    t0 = time.perf_counter()
+    kv.verify(drafts)
+    t = time.perf_counter() - t0
+    lp, lm = layer_params(shape), shape.vocab * shape.d_model
+    scale = (shape.n_layers * lp + lm) / (lp + lm)
+    call_s = t * scale
+    return {"value": gamma / call_s, "unit": "drafted tokens verified/s", "cores": oracle.num_threads(),
+            "kind": "oracle",
+            "sample": (f"one gamma={gamma} verify call ({gamma + 1} rows) through 1 of {shape.n_layers} layers plus "
+                       f"the LM head, 16-token cache, fp64 oracle: {t:.2f} s, scaled by the MAC ratio {scale:.1f} "
+                       f"to {call_s:.1f} s per full call")}
+
+
+def main():
+    a = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if a.gpus != 1 or world != 1:
+        print("bench.py measures one GPU: this build has no multi-GPU path (no collectives); "
+              "run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    from paper_2608_14787_amd import sdd
+    if not os.path.exists(sdd.LIB_PATH):
+        raise SystemExit("libsdd.so is not built: run `python __graft_entry__.py` first")
+    torch.cuda.set_device(0)
+    assert sdd.device_ok(), "needs a gfx950 GPU"
+
+    shape, P, gamma = SHAPES[a.workload]
+    V = shape.vocab
+    rounds = a.warmup + a.steps
+    log(f"workload {a.workload}: {shape}")
+    t0 = time.perf_counter()
+    model = sdd.Model(shape)
+    model.init_random(W.WEIGHT_SEED, W.WEIGHT_SIGMA)
+    torch.cuda.synchronize()
+    log(f"weights {model.weight_bytes / 1e9:.2f} GB generated in {time.perf_counter() - t0:.2f} s")
+
+    # committed tokens per round average about 5 at a 20% replacement rate; past the end of the
+    # continuation, drafts repeat its last token and are rejected
+    n_cont = rounds * 12 + gamma if a.drafts == "greedy" else 0
+    max_len = P + rounds * (gamma + 1) + n_cont + gamma + 8
+    kv = sdd.KVCache(model, 2, max_len)
+    ws = model.workspace(256)
+    prompt = torch.from_numpy(W.prompt(1, P, V)).cuda()
+    t0 = time.perf_counter()
+    kv.prefill(0, prompt, ws)
+    torch.cuda.synchronize()
+    log(f"prefill {P} tokens: {time.perf_counter() - t0:.2f} s")
+
+    # greedy continuation of the prompt (untimed): decode steps on slot 1
+    one = torch.tensor([1], dtype=torch.int32, device="cuda")
+    zero = torch.zeros(1, dtype=torch.int32, device="cuda")
+    cont = torch.zeros(max(n_cont, 1), dtype=torch.int32, device="cuda")
+    if n_cont:
+        kv.prefill(1, prompt, ws)
+        lg1 = torch.empty((1, 1, V), dtype=torch.float32, device="cuda")
+        am1 = torch.empty((1, 1), dtype=torch.int32, device="cuda")
+        nodraft = torch.empty((1, 0), dtype=torch.int32, device="cuda")
+        t0 = time.perf_counter()
+        for i in range(n_cont):
+            kv.verify(one, nodraft, lg1, am1, ws)
+            cont[i] = am1[0, 0]
+            kv.commit(one, zero, am1[0])
+        torch.cuda.synchronize()
+        log(f"greedy continuation of {n_cont} tokens: {time.perf_counter() - t0:.2f} s")
+
+    # per-round draft corruption (20% replaced) and drafter logits for the confidence prefix
+    g = W.rng(7)
+    mask = torch.from_numpy(g.random((rounds, gamma)) < (0.2 if n_cont else 1.0)).cuda()
+    repl = torch.from_numpy(g.integers(0, V, size=(rounds, gamma)).astype(np.int32)).cuda()
+    dl_bits = W.to_bf16_bits(W.rng(8).standard_normal((rounds, gamma + 1, V), dtype=np.float32) * np.float32(3.0))
+    drafter = torch.from_numpy(dl_bits.view(np.int16)).cuda().view(torch.bfloat16).view(rounds, 1, gamma + 1, V)
+
+    len_ptr = kv.device_len_ptr()
+    kv_len = torch.as_strided(kv.buf, (4,), (1,), (len_ptr - kv.buf.data_ptr())).view(torch.int32)
+    ar = torch.arange(gamma, dtype=torch.int32, device="cuda")
+    seq0 = torch.zeros(1, dtype=torch.int32, device="cuda")
+    drafts = torch.empty((1, gamma), dtype=torch.int32, device="cuda")
+    logits = torch.empty((1, gamma + 1, V), dtype=torch.float32, device="cuda")
+    am = torch.empty((1, gamma + 1), dtype=torch.int32, device="cuda")
+    acc_ws = sdd.rowstats_workspace(1, gamma, V)
+    conf_ws = sdd.rowstats_workspace(1, gamma, V)
+    outs = tuple(torch.empty(1, dtype=torch.int32, device="cuda") for _ in range(3))
+    skip = torch.empty(1, dtype=torch.int32, device="cuda")
+    accepted = torch.zeros(rounds, dtype=torch.int32, device="cuda")
+
+    def step(r):
+        # drafter stand-in: the next gamma continuation tokens after the cache, 20% replaced
+        idx = (kv_len[0] + 1 - P + ar).clamp_(0, max(n_cont - 1, 0)).long()
+        torch.where(mask[r], repl[r], cont[idx], out=drafts[0])
+        sdd.confidence_prefix(drafter[r], gamma, TAU, ws=conf_ws, out=skip)
+        kv.verify(seq0, drafts, logits, am, ws)
+        L, nxt, _ = sdd.accept(drafts, logits, sdd.GREEDY, ws=acc_ws, out=outs)
+        kv.commit(seq0, L, nxt)
+        accepted[r] = L[0]
+
+    for r in range(a.warmup):
+        step(r)
+    torch.cuda.synchronize()
+    dom = sdd.PROF_GEMM_GATEUP
+    sdd.profile_start(dom, 64 * a.steps * 4 + 16)
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    ev0.record()
+    for r in range(a.warmup, rounds):
+        step(r)
+    ev1.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms = ev0.elapsed_time(ev1) / a.steps
+    n_dom, tot_dom, mn_dom, mx_dom = sdd.profile_read(dom)
+    sdd.profile_stop()
+    acc_l = accepted[a.warmup:].cpu().numpy()
+    final_len = int(kv.state()[0][0])
+    log(f"timed {a.steps} steps: {ms:.3f} ms/step (wall {wall * 1e3 / a.steps:.3f}), "
+        f"accepted lengths {acc_l.tolist()}, final len {final_len}")
+
+    # algorithmic bytes
+    d, dff = shape.d_model, shape.d_ff
+    es = 2 if shape.dtype == "bf16" else 4
+    R = gamma + 1
+    gu_bytes = 2 * dff * d * es + R * d * es + R * dff * es  # weights + input rows + output rows
+    dom_ms = tot_dom / max(n_dom, 1)
+    achieved = gu_bytes / (dom_ms * 1e-3) / 1e9
+    weights_streamed = shape.n_layers * layer_params(shape) * es + V * d * es
+    kv_bytes = shape.n_layers * 2 * shape.n_kv_heads * shape.head_dim * es * (final_len - acc_l.mean() / 2)
+    call_bytes = weights_streamed + kv_bytes + R * V * 4
+    result = {
+        "metric": METRIC,
+        "value": gamma * 1e3 / ms,
+        "unit": "drafted tokens verified/s",
+        "n_gpus": 1, "steps": a.steps, "warmup": a.warmup,
+        "ms_per_step": ms,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": shape.dtype, "data": "synthetic",
+        "config": {"workload": f"{a.workload}-verify-gamma{gamma}", "layers": shape.n_layers,
+                   "d_model": d, "heads": f"{shape.n_q_heads}/{shape.n_kv_heads}x{shape.head_dim}",
+                   "d_ff": dff, "vocab": V, "prompt": P, "gamma": gamma, "batch": 1,
+                   "rounds": a.steps, "drafts": a.drafts, "tau": TAU},
+        "verify_calls_per_s": 1e3 / ms,
+        "accepted_tokens_per_s": float((acc_l + 1).sum()) * 1e3 / (ms * a.steps),
+        "call_hbm_frac": call_bytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
+        "call_bytes": call_bytes,
+        "roofline": {"bound": "hbm", "kernel": "gemm_kernel gate/up (SwiGLU epilogue)",
+                     "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
+                     "traffic": None, "bytes_per_launch": gu_bytes, "launches": n_dom,
+                     "avg_ms": dom_ms, "min_ms": mn_dom, "max_ms": mx_dom},
+    }
+    if a.all_kernels:
+        sdd.profile_start(0x1FF, 4096)
+        step(rounds - 1)
+        torch.cuda.synchronize()
+        names = {"embed": 1, "qkv": 2, "attention": 4, "o_proj": 8, "gate_up": 16, "down": 32, "lm_head": 64,
+                 "accept": 128, "confidence": 256}
+        result["kernels_ms_per_step"] = {k: sdd.profile_read(v)[1] for k, v in names.items()}
+        sdd.profile_stop()
+    if not a.no_cpu_baseline:
+        del model, kv, ws, drafter
+        torch.cuda.empty_cache()
+        result["cpu_baseline"] = cpu_baseline(shape, gamma)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -126,6 +126,11 @@ int sdd_kv_destroy(sdd_kv* kv);
 int sdd_kv_state(sdd_kv* kv, int32_t* len, int32_t* pending, int32_t* error_bits,
                  sdd_stream_t stream);
 
+/* Device pointers to the per-sequence length and pending-token arrays
+ * (int32[max_batch] each), valid while kv exists; lets callers build the next
+ * block on the device without a host round trip.  Read-only for callers. */
+int sdd_kv_device_state(sdd_kv* kv, const int32_t** len, const int32_t** pending);
+
 /* Workspace for prefill/verify of up to max_rows rows per call. */
 int sdd_workspace_bytes(const sdd_model* m, int max_rows, size_t* bytes);
 /* Prepares a caller-owned device workspace (zeroes its counters with a
@@ -195,6 +200,32 @@ int sdd_confidence_prefix(const void* logits, int dtype, size_t seq_stride, int 
                           int V, float tau, int32_t* skip_len, float* log_conf,
                           const int32_t* draft, float* log_p_draft, void* ws, size_t ws_bytes,
                           sdd_stream_t stream);
+
+/* ---- launch timing (benchmarks) ----------------------------------------- */
+
+/* Kernel classes */
+#define SDD_PROF_EMBED 1u
+#define SDD_PROF_GEMM_QKV 2u
+#define SDD_PROF_ATTN 4u
+#define SDD_PROF_GEMM_O 8u
+#define SDD_PROF_GEMM_GATEUP 16u
+#define SDD_PROF_GEMM_DOWN 32u
+#define SDD_PROF_GEMM_LM 64u
+#define SDD_PROF_ACCEPT 128u
+#define SDD_PROF_CONF 256u
+
+/* Starts timing: until sdd_profile_stop, each launch of a class in
+ * class_mask is bracketed by two HIP events on its own stream (at most
+ * max_launches launches are recorded; events are allocated here, on the
+ * host thread, not during the launches).  Not thread-safe: one profiling
+ * session per process. */
+int sdd_profile_start(unsigned class_mask, int max_launches);
+/* Waits for the recorded events and returns, over the launches of the
+ * classes in cls: count, total, min and max duration in ms (min/max may be
+ * NULL). */
+int sdd_profile_read(unsigned cls, int* launches, double* total_ms, double* min_ms, double* max_ms);
+/* Stops timing and releases the events. */
+int sdd_profile_stop(void);
 
 #ifdef __cplusplus
 }

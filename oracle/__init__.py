@@ -69,6 +69,10 @@ def _p(a):
     return None if a is None else a.ctypes.data_as(C.c_void_p)
 
 
+def num_threads() -> int:
+    return lib().orc_num_threads()
+
+
 def splitmix64(x: int) -> int:
     return lib().orc_splitmix64(x)
 

@@ -45,6 +45,9 @@ enum {
 /* Acceptance modes (Appendix "Baselines and Sweep Settings"; Sec. 3.1). */
 enum { ORC_GREEDY = 0, ORC_RATIO = 1, ORC_TOPK = 2, ORC_LENIENT = 3 };
 
+/* Threads the oracle's parallel loops use. */
+int orc_num_threads(void);
+
 /* Counter-based synthetic weight generator (SplitMix64 + Irwin-Hall(4)). */
 uint64_t orc_splitmix64(uint64_t x);
 int orc_tensor_id(int kind, int layer);

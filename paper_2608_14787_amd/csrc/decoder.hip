@@ -141,18 +141,23 @@ __device__ void epilogue_qkv(const GemmArgs& a, const float* tile, int g, int la
         y[0] = lane < 32 ? y[0] * c - other * s : y[0] * c + other * s;
       }
     }
-    char* dst;
-    int64_t base;
-    if (is_q) {
-      dst = a.q_out;
-      base = ((int64_t)m * a.hq + h) * C;
-    } else {
-      const int kh = is_k ? h - a.hq : h - a.hq - a.hkv;
-      dst = is_k ? a.kc : a.vc;
-      base = (((int64_t)ri.seq * a.hkv + kh) * a.max_len + ri.pos) * C;
+    if (is_q || is_k) {
+      char* dst;
+      int64_t base;
+      if (is_q) {
+        dst = a.q_out;
+        base = ((int64_t)m * a.hq + h) * C;
+      } else {
+        dst = a.kc;
+        base = (((int64_t)ri.seq * a.hkv + (h - a.hq)) * a.max_len + ri.pos) * C;
+      }
+      store_t<T>(dst, base + lane, y[0]);
+      if constexpr (C == 128) store_t<T>(dst, base + lane + 64, y[1]);
+    } else {  // V cache is transposed: [seq][kv head][dim][position]
+      const int64_t base = ((int64_t)ri.seq * a.hkv + (h - a.hq - a.hkv)) * C;
+      store_t<T>(a.vc, (base + lane) * a.max_len + ri.pos, y[0]);
+      if constexpr (C == 128) store_t<T>(a.vc, (base + lane + 64) * a.max_len + ri.pos, y[1]);
     }
-    store_t<T>(dst, base + lane, y[0]);
-    if constexpr (C == 128) store_t<T>(dst, base + lane + 64, y[1]);
   }
 }
 
@@ -283,7 +288,7 @@ __global__ void __launch_bounds__(kGemmThreads, 2) gemm_kernel(GemmArgs a) {
   float* tile = reinterpret_cast<float*>(&red[1][0][0]);
   static_assert(NACC * kWave * 4 >= TB * 16 * C, "tile must fit the reduction buffer");
 
-  const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave), lane = threadIdx.x % kWave;
   const int64_t U = (int64_t)a.G * a.KT;
   const int w = blockIdx.x;
   const int64_t u0 = unit_start(w, U, a.n_wg), u1 = unit_start(w + 1, U, a.n_wg);
@@ -300,19 +305,22 @@ __global__ void __launch_bounds__(kGemmThreads, 2) gemm_kernel(GemmArgs a) {
 
     // ---- stream this segment: each wave takes a quarter of the k-tiles ----
     const int S = ke - kb;
-    const int ka = kb + S * wave / 4, kz = kb + S * (wave + 1) / 4;
+    const int ka = __builtin_amdgcn_readfirstlane(kb + S * wave / 4);
+    const int kz = __builtin_amdgcn_readfirstlane(kb + S * (wave + 1) / 4);
     f32x4 acc[NACC];
 #pragma unroll
     for (int i = 0; i < NACC; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
-    const uint4* Wg = W + (int64_t)g * NG * a.KT * kWave + lane;
+    const uint4* Wg = W + (int64_t)g * NG * a.KT * kWave + lane;  // k-step kt: NG contiguous tiles
     const char* Xl = a.X + ((int64_t)(a.m0 + lane % 16) * a.ldx + (lane / 16) * EPL) * sizeof(T);
     const int64_t xrow16 = (int64_t)16 * a.ldx * sizeof(T);
     uint4 wa0[NG], wa1[NG], xb0[TB], xb1[TB];
     auto load = [&](int kt, uint4* wa, uint4* xb) {
 #pragma unroll
-      for (int nt = 0; nt < NG; ++nt) wa[nt] = load_nt16(Wg + ((int64_t)nt * a.KT + kt) * kWave);
+      for (int nt = 0; nt < NG; ++nt) wa[nt] = load_nt16(Wg + ((int64_t)kt * NG + nt) * kWave);
 #pragma unroll
       for (int tb = 0; tb < TB; ++tb) xb[tb] = load16(Xl + tb * xrow16 + (int64_t)kt * KTILE * sizeof(T));
+      // keep the next stage's loads ahead of this stage's MFMAs
+      __builtin_amdgcn_sched_barrier(0);
     };
     auto mma = [&](const uint4* wa, const uint4* xb) {
 #pragma unroll
@@ -320,14 +328,22 @@ __global__ void __launch_bounds__(kGemmThreads, 2) gemm_kernel(GemmArgs a) {
 #pragma unroll
         for (int tb = 0; tb < TB; ++tb) mma_tile<T>(wa[nt], xb[tb], acc[nt * TB + tb]);
     };
-    if (ka < kz) load(ka, wa0, xb0);
-    for (int kt = ka; kt < kz; kt += 2) {
-      if (kt + 1 < kz) load(kt + 1, wa1, xb1);
+    // Two register stages; the steady-state loop issues its loads
+    // unconditionally so that each MFMA batch waits only for its own stage.
+    int kt = ka;
+    if (kt < kz) load(kt, wa0, xb0);
+    for (; kt + 2 < kz; kt += 2) {
+      load(kt + 1, wa1, xb1);
       mma(wa0, xb0);
-      if (kt + 1 < kz) {
-        if (kt + 2 < kz) load(kt + 2, wa0, xb0);
-        mma(wa1, xb1);
-      }
+      load(kt + 2, wa0, xb0);
+      mma(wa1, xb1);
+    }
+    if (kt + 1 < kz) {
+      load(kt + 1, wa1, xb1);
+      mma(wa0, xb0);
+      mma(wa1, xb1);
+    } else if (kt < kz) {
+      mma(wa0, xb0);
     }
 
     // ---- reduce the four waves: (w0 + w2) + (w1 + w3), fixed order ----
@@ -394,8 +410,9 @@ __global__ void __launch_bounds__(kGemmThreads, 2) gemm_kernel(GemmArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// Attention: one workgroup per (row, query head).  Scores of a chunk of
-// positions go to LDS; the softmax is carried online across chunks.
+// Attention, plain VALU version (fp32 models): one workgroup per (row, query
+// head).  Scores of a chunk of positions go to LDS; the softmax is carried
+// online across chunks.
 constexpr int kAttnChunk = 1024;
 
 struct AttnArgs {
@@ -466,7 +483,7 @@ __global__ void __launch_bounds__(256) attention_kernel(AttnArgs a) {
     run_m = new_m;
     acc *= alpha;
     if (dsub < nsub)
-      for (int i = dsub; i < n; i += nsub) acc += sc[i] * Elem<T>::to_f32(Vp[(int64_t)(p0 + i) * hd + dd]);
+      for (int i = dsub; i < n; i += nsub) acc += sc[i] * Elem<T>::to_f32(Vp[(int64_t)dd * a.max_len + p0 + i]);
     __syncthreads();
   }
   if (dsub < nsub) acc2[dsub * hd + dd] = acc;
@@ -476,6 +493,181 @@ __global__ void __launch_bounds__(256) attention_kernel(AttnArgs a) {
     for (int s = 0; s < nsub; ++s) o += acc2[s * hd + tid];
     outp[tid] = Elem<T>::from_f32(o / run_l);
   }
+}
+
+// ---------------------------------------------------------------------------
+// Attention on MFMA (bf16 models).  Grid: (KV split, group of 64 query
+// vectors, sequence x KV head).  The query vectors of one KV head are the
+// block's rows times the heads that share it (GQA); each wave owns 16 of them.
+// Per 32 cache positions a wave computes S^T = K Q^T with K rows as the MFMA A
+// operand, so each lane ends up holding 8 scores of its own query column,
+// exactly the P^T fragment that O^T = V^T P^T takes as its B operand; V is
+// cached transposed so the A operand is two contiguous 8-byte reads.  The
+// softmax is online across positions; splits of the cache are combined by the
+// last-arriving workgroup in split order.
+struct AttnMfmaArgs {
+  const uint16_t* q;   // [rows][hq][HD]
+  const uint16_t* kc;  // layer base [seq][hkv][max_len][HD]
+  const uint16_t* vc;  // layer base [seq][hkv][HD][max_len]
+  uint16_t* out;       // [rows][hq*HD]
+  const RowInfo* rows;
+  float* part_o;       // [nb*hkv][n_splits][QV][HD]
+  float* part_ml;      // [nb*hkv][n_splits][QV][2]
+  int* cnt;            // [nb*hkv][qgroups]
+  int nb, R, hq, hkv, grp, max_len, n_splits, split_len, qgroups;
+  float scale;
+};
+
+__device__ inline uint2 load4_bf16(const uint16_t* row, int p, int end) {
+  if (p + 3 < end) return *reinterpret_cast<const uint2*>(row + p);
+  uint16_t t[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) t[i] = (p + i < end) ? row[p + i] : (uint16_t)0;
+  return make_uint2((uint32_t)t[0] | ((uint32_t)t[1] << 16), (uint32_t)t[2] | ((uint32_t)t[3] << 16));
+}
+
+template <int HD>
+__global__ void __launch_bounds__(256) attention_mfma_kernel(AttnMfmaArgs a) {
+  constexpr int KK = HD / 32, DB = HD / 16;
+  __shared__ int s_last;
+  const int split = blockIdx.x, qg = blockIdx.y, bk = blockIdx.z;
+  if (bk >= a.nb * a.hkv || qg >= a.qgroups) return;  // launch larger than the block set
+  const int blk = bk / a.hkv, kvh = bk % a.hkv;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave), lane = threadIdx.x % kWave;
+  const int QV = a.R * a.grp;
+  const int qv = (qg * 4 + wave) * 16 + lane % 16;
+  const bool qok = qv < QV;
+  const int r = qok ? qv / a.grp : 0, hh = qok ? qv % a.grp : 0;
+  const int m = blk * a.R + r;
+  const RowInfo first = a.rows[blk * a.R], last = a.rows[blk * a.R + a.R - 1];
+  const int kv_end = first.valid ? last.pos + 1 : 0;
+  const int qpos = a.rows[m].pos;
+  const int p_begin = __builtin_amdgcn_readfirstlane(split * a.split_len);
+  const int p_end = __builtin_amdgcn_readfirstlane(min(kv_end, p_begin + a.split_len));
+  const int64_t head = (int64_t)first.seq * a.hkv + kvh;
+  const uint16_t* K = a.kc + head * a.max_len * HD;
+  const uint16_t* Vt = a.vc + head * HD * a.max_len;
+
+  uint4 qf[KK];
+  const uint16_t* Q = a.q + ((int64_t)m * a.hq + kvh * a.grp + hh) * HD;
+#pragma unroll
+  for (int kk = 0; kk < KK; ++kk) qf[kk] = qok ? load16(Q + 32 * kk + 8 * (lane / 16)) : make_uint4(0, 0, 0, 0);
+
+  f32x4 o[DB];
+#pragma unroll
+  for (int db = 0; db < DB; ++db) o[db] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float mrun = -INFINITY, lrun = 0.f;
+  const int g4 = 4 * (lane / 16);
+  for (int p = p_begin; p < p_end; p += 32) {
+    f32x4 sacc[2];
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+      sacc[b] = f32x4{0.f, 0.f, 0.f, 0.f};
+      const int kp = p + 16 * b + lane % 16;
+#pragma unroll
+      for (int kk = 0; kk < KK; ++kk) {
+        const uint4 kf = kp < kv_end ? load16(K + (int64_t)kp * HD + 32 * kk + 8 * (lane / 16)) : make_uint4(0, 0, 0, 0);
+        sacc[b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kf), __builtin_bit_cast(bf16x8, qf[kk]),
+                                                          sacc[b], 0, 0, 0);
+      }
+    }
+    // sacc[b][i]: position p + 16 b + g4 + i, query column lane % 16
+    float sv[8];
+    float mloc = -INFINITY;
+#pragma unroll
+    for (int b = 0; b < 2; ++b)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int kp = p + 16 * b + g4 + i;
+        const float v = (qok && kp <= qpos && kp < kv_end) ? sacc[b][i] * a.scale : -INFINITY;
+        sv[b * 4 + i] = v;
+        mloc = fmaxf(mloc, v);
+      }
+    mloc = fmaxf(mloc, __shfl_xor(mloc, 16));
+    mloc = fmaxf(mloc, __shfl_xor(mloc, 32));
+    const float mnew = fmaxf(mrun, mloc);
+    const float alpha = mrun == -INFINITY ? 0.f : __expf(mrun - mnew);
+    float lsum = 0.f;
+    uint16_t pb[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const float e = sv[i] == -INFINITY ? 0.f : __expf(sv[i] - mnew);
+      lsum += e;
+      pb[i] = f32_to_bf16(e);
+    }
+    lrun = lrun * alpha + lsum;
+    mrun = mnew;
+    const uint4 pf = make_uint4((uint32_t)pb[0] | ((uint32_t)pb[1] << 16), (uint32_t)pb[2] | ((uint32_t)pb[3] << 16),
+                                (uint32_t)pb[4] | ((uint32_t)pb[5] << 16), (uint32_t)pb[6] | ((uint32_t)pb[7] << 16));
+#pragma unroll
+    for (int db = 0; db < DB; ++db) {
+      const uint16_t* vrow = Vt + (int64_t)(16 * db + lane % 16) * a.max_len;
+      const uint2 v0 = load4_bf16(vrow, p + g4, kv_end), v1 = load4_bf16(vrow, p + 16 + g4, kv_end);
+      const uint4 vf = make_uint4(v0.x, v0.y, v1.x, v1.y);
+      o[db] *= alpha;
+      o[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, vf), __builtin_bit_cast(bf16x8, pf), o[db],
+                                                      0, 0, 0);
+    }
+  }
+  // full softmax denominator of query lane%16: the four lanes of its column
+  float ltot = lrun + __shfl_xor(lrun, 16);
+  ltot += __shfl_xor(ltot, 32);
+  const int h = kvh * a.grp + hh;
+  if (a.n_splits == 1) {
+    if (qok) {
+      const float inv = ltot > 0.f ? 1.f / ltot : 0.f;
+      uint16_t* dst = a.out + ((int64_t)m * a.hq + h) * HD;
+#pragma unroll
+      for (int db = 0; db < DB; ++db)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) dst[16 * db + g4 + i] = f32_to_bf16(o[db][i] * inv);
+    }
+    return;
+  }
+  // publish this split, the last workgroup of (bk, qg) combines in split order
+  const int64_t sbase = ((int64_t)bk * a.n_splits + split) * QV;
+  if (qok) {
+    float* po = a.part_o + (sbase + qv) * HD;
+#pragma unroll
+    for (int db = 0; db < DB; ++db)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) po[16 * db + g4 + i] = o[db][i];
+    if (lane < 16) {
+      a.part_ml[(sbase + qv) * 2] = mrun;
+      a.part_ml[(sbase + qv) * 2 + 1] = ltot;
+    }
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    __threadfence();
+    const int old = atomicAdd(&a.cnt[bk * a.qgroups + qg], 1);
+    s_last = old == a.n_splits - 1;
+  }
+  __syncthreads();
+  if (!s_last) return;
+  __threadfence();
+  const int q0 = qg * 64;
+  for (int e = threadIdx.x; e < 64 * HD; e += 256) {
+    const int qq = q0 + e / HD, dim = e % HD;
+    if (qq >= QV) break;
+    float M = -INFINITY;
+    for (int sp = 0; sp < a.n_splits; ++sp)
+      M = fmaxf(M, a.part_ml[(((int64_t)bk * a.n_splits + sp) * QV + qq) * 2]);
+    float L = 0.f, O = 0.f;
+    if (M != -INFINITY) {
+      for (int sp = 0; sp < a.n_splits; ++sp) {
+        const int64_t id = ((int64_t)bk * a.n_splits + sp) * QV + qq;
+        const float ms = a.part_ml[id * 2];
+        if (ms == -INFINITY) continue;
+        const float f = __expf(ms - M);
+        L += a.part_ml[id * 2 + 1] * f;
+        O += a.part_o[id * HD + dim] * f;
+      }
+    }
+    const int rr = qq / a.grp, hq2 = kvh * a.grp + qq % a.grp;
+    a.out[((int64_t)(blk * a.R + rr) * a.hq + hq2) * HD + dim] = f32_to_bf16(L > 0.f ? O / L : 0.f);
+  }
+  if (threadIdx.x == 0) a.cnt[bk * a.qgroups + qg] = 0;
 }
 
 // ---------------------------------------------------------------------------
@@ -607,16 +799,19 @@ __global__ void kv_init_kernel(int32_t* len, int32_t* pending, int32_t* err, int
 // ---------------------------------------------------------------------------
 // Host side
 
-static int pick_ng(int64_t ntiles, bool pairs) {
-  for (int ng : {8, 4, 2}) {
-    if (ntiles % ng == 0 && (!pairs || ng % 2 == 0)) return ng;
-  }
-  return pairs ? 2 : 1;
+
+// Counter region at the start of every workspace, sized by the model only, so
+// that it stays at one place whatever the row count of a call: [0, 16) group
+// completion counters, then one arrival counter per GEMM column group, then
+// kAttnCounters attention split counters.
+constexpr int kAttnCounters = 65536;
+
+static int64_t gemm_counter_count(const sdd_model* m) {
+  return ceil_div(m->cfg.vocab, 16) + ceil_div(2 * (int64_t)m->cfg.d_ff, 16) + ceil_div(m->cfg.d_model, 16) + 64;
 }
 
 static size_t counters_bytes(const sdd_model* m) {
-  const int64_t g = ceil_div(m->cfg.vocab, 16) + ceil_div(2 * (int64_t)m->cfg.d_ff, 16) + 64;
-  return align_up((size_t)g * 4 + 64, 256);
+  return align_up((size_t)(16 + gemm_counter_count(m) + kAttnCounters) * 4, 256);
 }
 
 WsLayout ws_layout(const sdd_model* m, int max_rows) {
@@ -645,7 +840,10 @@ WsLayout ws_layout(const sdd_model* m, int max_rows) {
   L.ffh = take((size_t)mp * c.d_ff * es);
   L.part = take((size_t)L.n_wg * 2 * kMaxPassRows * 128 * 4);
   L.amax = take((size_t)L.max_groups * mp * 8);
-  L.attn_part = 0;
+  // attention split partials: room for attn_qs (query vector, split) pairs
+  L.attn_splits_max = (int)std::max<int64_t>((int64_t)mp * c.n_q_heads * 4, (int64_t)64 * c.n_q_heads * 16);
+  L.attn_part = take((size_t)L.attn_splits_max * (c.head_dim + 2) * 4);
+  L.attn_cnt = L.cnt + (size_t)(16 + gemm_counter_count(m)) * 4;
   L.total = off;
   return L;
 }
@@ -678,7 +876,8 @@ static void launch_gemm_ng(int ng, int tb, const GemmArgs& a, int nblocks, hipSt
 }
 
 // Runs one GEMM over rows [0, M) in passes of at most 64 rows.
-static int run_gemm(CallCtx& cx, int epi, size_t w_off, int64_t N, int K, const char* X, GemmArgs a, int M, int ng) {
+static int run_gemm(CallCtx& cx, int epi, unsigned prof, size_t w_off, int64_t N, int K, const char* X, GemmArgs a,
+                    int M, int ng) {
   const sdd_model* m = cx.m;
   a.W = m->base + w_off;
   a.KT = (int)ceil_div(K, m->ktile);
@@ -700,6 +899,7 @@ static int run_gemm(CallCtx& cx, int epi, size_t w_off, int64_t N, int K, const 
     a.m0 = m0;
     a.M = std::min(kMaxPassRows, M - m0);
     const int tb = (int)ceil_div(a.M, 16);
+    prof_begin(prof, cx.st);
     if (m->es == 2) {
       switch (epi) {
         case EPI_QKV: launch_gemm_ng<uint16_t, EPI_QKV>(ng, tb, a, nblocks, cx.st); break;
@@ -715,6 +915,7 @@ static int run_gemm(CallCtx& cx, int epi, size_t w_off, int64_t N, int K, const 
         default: launch_gemm_ng<float, EPI_LOGITS>(ng, tb, a, nblocks, cx.st); break;
       }
     }
+    prof_end(prof, cx.st);
     int rc = check_launch("gemm_kernel");
     if (rc) return rc;
   }
@@ -722,7 +923,8 @@ static int run_gemm(CallCtx& cx, int epi, size_t w_off, int64_t N, int K, const 
 }
 
 // Forward of M rows whose RowInfo/x/xa/rs were written by embed_kernel.
-static int forward_rows(CallCtx& cx, int M, float* logits, int32_t* argmax) {
+static int forward_rows(CallCtx& cx, int nb, int R, float* logits, int32_t* argmax) {
+  const int M = nb * R;
   sdd_model* m = cx.m;
   sdd_kv* kv = cx.kv;
   const sdd_model_config& c = m->cfg;
@@ -750,10 +952,42 @@ static int forward_rows(CallCtx& cx, int M, float* logits, int32_t* argmax) {
       a.max_len = kv->max_len;
       a.kc = kv->k + (size_t)l * kv->layer_stride;
       a.vc = kv->v + (size_t)l * kv->layer_stride;
-      if ((rc = run_gemm(cx, EPI_QKV, Ly.qkv, hq + 2 * hk, (int)d, xa, a, M, (int)(hd / 16)))) return rc;
+      if ((rc = run_gemm(cx, EPI_QKV, PROF_GEMM_QKV, Ly.qkv, hq + 2 * hk, (int)d, xa, a, M, m->ng_qkv))) return rc;
     }
     // attention
-    {
+    if (m->es == 2) {
+      AttnMfmaArgs a{};
+      a.q = reinterpret_cast<const uint16_t*>(ws + L.q);
+      a.kc = reinterpret_cast<const uint16_t*>(kv->k + (size_t)l * kv->layer_stride);
+      a.vc = reinterpret_cast<const uint16_t*>(kv->v + (size_t)l * kv->layer_stride);
+      a.out = reinterpret_cast<uint16_t*>(ws + L.ao);
+      a.rows = reinterpret_cast<const RowInfo*>(ws + L.rowinfo);
+      a.R = R;
+      a.hq = c.n_q_heads;
+      a.hkv = c.n_kv_heads;
+      a.grp = c.n_q_heads / c.n_kv_heads;
+      a.max_len = kv->max_len;
+      a.qgroups = (int)ceil_div((int64_t)R * a.grp, 64);
+      a.nb = nb;
+      const int64_t base = (int64_t)nb * a.hkv * a.qgroups;  // (sequence x KV head, query group) pairs
+      int ns = (int)std::min<int64_t>(16, std::max<int64_t>(1, ceil_div(2 * m->n_cu, base)));
+      ns = (int)std::min<int64_t>(ns, std::max<int64_t>(1, L.attn_splits_max / ((int64_t)M * c.n_q_heads)));
+      if (base > kAttnCounters) ns = 1;
+      a.split_len = (int)align_up((size_t)ceil_div(kv->max_len, ns), 32);
+      a.n_splits = (int)ceil_div(kv->max_len, a.split_len);
+      a.part_o = reinterpret_cast<float*>(ws + L.attn_part);
+      a.part_ml = a.part_o + (size_t)L.attn_splits_max * c.head_dim;
+      a.cnt = reinterpret_cast<int*>(ws + L.attn_cnt);
+      a.scale = 1.f / sqrtf((float)c.head_dim);
+      const dim3 grid(a.n_splits, a.qgroups, (unsigned)(nb * a.hkv));
+      prof_begin(PROF_ATTN, cx.st);
+      if (c.head_dim == 128)
+        hipLaunchKernelGGL(attention_mfma_kernel<128>, grid, dim3(256), 0, cx.st, a);
+      else
+        hipLaunchKernelGGL(attention_mfma_kernel<64>, grid, dim3(256), 0, cx.st, a);
+      prof_end(PROF_ATTN, cx.st);
+      if ((rc = check_launch("attention_mfma_kernel"))) return rc;
+    } else {
       AttnArgs a{};
       a.q = ws + L.q;
       a.kc = kv->k + (size_t)l * kv->layer_stride;
@@ -766,10 +1000,9 @@ static int forward_rows(CallCtx& cx, int M, float* logits, int32_t* argmax) {
       a.hd = c.head_dim;
       a.max_len = kv->max_len;
       a.scale = 1.f / sqrtf((float)c.head_dim);
-      if (m->es == 2)
-        hipLaunchKernelGGL(attention_kernel<uint16_t>, dim3(M, c.n_q_heads), dim3(256), 0, cx.st, a);
-      else
-        hipLaunchKernelGGL(attention_kernel<float>, dim3(M, c.n_q_heads), dim3(256), 0, cx.st, a);
+      prof_begin(PROF_ATTN, cx.st);
+      hipLaunchKernelGGL(attention_kernel<float>, dim3(M, c.n_q_heads), dim3(256), 0, cx.st, a);
+      prof_end(PROF_ATTN, cx.st);
       if ((rc = check_launch("attention_kernel"))) return rc;
     }
     // output projection + residual; next input scaled by the FFN norm gain
@@ -782,7 +1015,7 @@ static int forward_rows(CallCtx& cx, int M, float* logits, int32_t* argmax) {
       a.g_next = reinterpret_cast<const float*>(m->base + Ly.ffn_norm);
       a.ss_part = reinterpret_cast<float*>(ws + L.ss_part);
       a.rs_out = rs;
-      if ((rc = run_gemm(cx, EPI_RESID, Ly.o, d, (int)hq, ws + L.ao, a, M, pick_ng(d / 16, false)))) return rc;
+      if ((rc = run_gemm(cx, EPI_RESID, PROF_GEMM_O, Ly.o, d, (int)hq, ws + L.ao, a, M, m->ng_o))) return rc;
     }
     // gate/up + SwiGLU
     {
@@ -790,7 +1023,7 @@ static int forward_rows(CallCtx& cx, int M, float* logits, int32_t* argmax) {
       a.rs = rs;
       a.ffh = ws + L.ffh;
       a.dff = c.d_ff;
-      if ((rc = run_gemm(cx, EPI_SWIGLU, Ly.gu, 2 * (int64_t)c.d_ff, (int)d, xa, a, M, pick_ng(2 * (int64_t)c.d_ff / 16, true))))
+      if ((rc = run_gemm(cx, EPI_SWIGLU, PROF_GEMM_GU, Ly.gu, 2 * (int64_t)c.d_ff, (int)d, xa, a, M, m->ng_gu)))
         return rc;
     }
     // down projection + residual; next input scaled by the next norm gain
@@ -804,7 +1037,7 @@ static int forward_rows(CallCtx& cx, int M, float* logits, int32_t* argmax) {
           m->base + (l + 1 < c.n_layers ? m->layers[l + 1].attn_norm : m->off_final_norm));
       a.ss_part = reinterpret_cast<float*>(ws + L.ss_part);
       a.rs_out = rs;
-      if ((rc = run_gemm(cx, EPI_RESID, Ly.down, d, c.d_ff, ws + L.ffh, a, M, pick_ng(d / 16, false)))) return rc;
+      if ((rc = run_gemm(cx, EPI_RESID, PROF_GEMM_DOWN, Ly.down, d, c.d_ff, ws + L.ffh, a, M, m->ng_down))) return rc;
     }
   }
   if (logits) {
@@ -815,7 +1048,7 @@ static int forward_rows(CallCtx& cx, int M, float* logits, int32_t* argmax) {
     a.amax_v = reinterpret_cast<float*>(ws + L.amax);
     a.amax_i = reinterpret_cast<int*>(ws + L.amax + (size_t)L.max_groups * L.mp * 4);
     a.argmax_out = argmax;
-    if ((rc = run_gemm(cx, EPI_LOGITS, m->off_lm, c.vocab, (int)d, xa, a, M, pick_ng(c.vocab / 16, false)))) return rc;
+    if ((rc = run_gemm(cx, EPI_LOGITS, PROF_GEMM_LM, m->off_lm, c.vocab, (int)d, xa, a, M, m->ng_lm))) return rc;
   }
   return SDD_OK;
 }
@@ -835,10 +1068,12 @@ static int launch_embed(CallCtx& cx, EmbedArgs e, int M) {
   e.max_batch = cx.kv->max_batch;
   e.eps = c.rms_eps;
   e.err = cx.kv->err;
+  prof_begin(PROF_EMBED, cx.st);
   if (m->es == 2)
     hipLaunchKernelGGL(embed_kernel<uint16_t>, dim3(M), dim3(256), 0, cx.st, e);
   else
     hipLaunchKernelGGL(embed_kernel<float>, dim3(M), dim3(256), 0, cx.st, e);
+  prof_end(PROF_EMBED, cx.st);
   return check_launch("embed_kernel");
 }
 
@@ -910,6 +1145,13 @@ extern "C" int sdd_kv_state(sdd_kv* kv, int32_t* len, int32_t* pending, int32_t*
   return SDD_OK;
 }
 
+extern "C" int sdd_kv_device_state(sdd_kv* kv, const int32_t** len, const int32_t** pending) {
+  SDD_REQUIRE(kv != nullptr, "kv is NULL");
+  if (len) *len = kv->len;
+  if (pending) *pending = kv->pending;
+  return SDD_OK;
+}
+
 extern "C" int sdd_workspace_bytes(const sdd_model* m, int max_rows, size_t* bytes) {
   SDD_REQUIRE(m && bytes, "NULL pointer");
   SDD_REQUIRE(max_rows > 0 && max_rows <= 65536, "bad max_rows %d", max_rows);
@@ -959,7 +1201,7 @@ extern "C" int sdd_kv_prefill(sdd_model* m, sdd_kv* kv, int seq, const int32_t* 
     e.tokens = tokens + c0;
     e.R = rows;
     if ((rc = launch_embed(cx, e, rows))) return rc;
-    if ((rc = forward_rows(cx, rows, nullptr, nullptr))) return rc;
+    if ((rc = forward_rows(cx, 1, rows, nullptr, nullptr))) return rc;
   }
   hipLaunchKernelGGL(prefill_finish_kernel, dim3(1), dim3(64), 0, st, kv->len, kv->pending, kv->err, seq, n, tokens,
                      m->cfg.vocab);
@@ -987,7 +1229,7 @@ extern "C" int sdd_verify_block(sdd_model* m, sdd_kv* kv, const int32_t* seq_ids
   e.R = R;
   e.gamma = gamma;
   if ((rc = launch_embed(cx, e, M))) return rc;
-  return forward_rows(cx, M, logits, argmax);
+  return forward_rows(cx, n_seq, R, logits, argmax);
 }
 
 extern "C" int sdd_kv_commit(sdd_kv* kv, const int32_t* seq_ids, int n_seq, const int32_t* accepted_len,

@@ -9,8 +9,10 @@
 // reads 16 contiguous bytes holding row (l % 16) and the EPL = 16/sizeof(T)
 // consecutive columns starting at (l / 16) * EPL: exactly one MFMA A-operand
 // fragment per lane, so a wave streams a tile with one coalesced 16-byte load
-// per lane.  Tiles are ordered row-tile major, column-tile minor, so the K-run
-// of a 16-row strip is contiguous.  Q, K and V projections are fused into one
+// per lane.  Row tiles are grouped NG at a time (NG in {8, 4, 2}, per matrix);
+// tile (nt, kt) sits at index ((nt / NG) * KT + kt) * NG + nt % NG, so one
+// k-step of a column group is NG KiB of contiguous memory and a group's whole
+// K-run is contiguous.  Q, K and V projections are fused into one
 // matrix (rows [Wq; Wk; Wv]); gate and up projections are fused and
 // interleaved per 16-row tile (tile 2t = gate rows 16t.., tile 2t+1 = up rows
 // 16t..), so that one column group holds matching gate/up outputs.
@@ -22,6 +24,7 @@ struct sdd_model {
   int ktile; // columns per tile
   int n_cu;  // compute units of the device
   size_t off_embed, off_lm, off_final_norm;
+  int ng_qkv, ng_o, ng_gu, ng_down, ng_lm;  // row tiles per column group
   struct Layer {
     size_t qkv, o, gu, down, attn_norm, ffn_norm, q_norm, k_norm;
   };
@@ -38,13 +41,21 @@ struct sdd_kv {
   int32_t* err;      // sticky error bits
   float* rope;       // [max_len][head_dim/2][2] (cos, sin)
   char* k;           // [layers][max_batch][n_kv_heads][max_len][head_dim]
-  char* v;
+  char* v;               // [layers][max_batch][n_kv_heads][head_dim][max_len] (transposed)
   size_t layer_stride;  // bytes per layer of k (and of v)
 };
 
 namespace sdd {
 
 inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+// Row tiles per column group: the largest of 8, 4, 2 dividing the tile count
+// (even for the gate/up interleave, which pairs tiles).
+inline int pick_ng(int64_t ntiles, bool pairs) {
+  for (int ng : {8, 4, 2})
+    if (ntiles % ng == 0 && (!pairs || ng % 2 == 0)) return ng;
+  return pairs ? 2 : 1;
+}
 
 // tiled matrix bytes
 inline size_t tiled_bytes(int64_t N, int64_t K, int ktile) {
@@ -60,7 +71,7 @@ struct RowInfo {
 
 // Per-call workspace carve-up for up to max_rows rows.
 struct WsLayout {
-  size_t rowinfo, x, xa, rs, ss_part, q, ao, ffh, part, cnt, amax, attn_part, total;
+  size_t rowinfo, x, xa, rs, ss_part, q, ao, ffh, part, cnt, amax, attn_part, attn_cnt, total;
   int mp;         // padded rows
   int max_groups; // column groups of the widest GEMM
   int n_wg;       // GEMM workgroups

@@ -430,12 +430,15 @@ size_t rowstats_ws(int B, int rows, int V) {
 template <int KIND, bool kSum, bool kCount, bool kQ, typename T, typename TQ>
 int launch_t(Job& job, int vec, hipStream_t st) {
   const int blocks = job.B * job.rows * job.C;
+  const unsigned prof = KIND == kAccept ? PROF_ACCEPT : PROF_CONF;
+  prof_begin(prof, st);
   if (vec == 1)
     hipLaunchKernelGGL((rowstats_kernel<T, TQ, 1, KIND, kSum, kCount, kQ>), dim3(blocks), dim3(kThreads), 0, st, job);
   else if (vec == 4)
     hipLaunchKernelGGL((rowstats_kernel<T, TQ, 4, KIND, kSum, kCount, kQ>), dim3(blocks), dim3(kThreads), 0, st, job);
   else
     hipLaunchKernelGGL((rowstats_kernel<T, TQ, 8, KIND, kSum, kCount, kQ>), dim3(blocks), dim3(kThreads), 0, st, job);
+  prof_end(prof, st);
   return check_launch("rowstats_kernel");
 }
 

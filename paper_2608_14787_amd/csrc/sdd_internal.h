@@ -98,3 +98,14 @@ __device__ inline float wave_sum(float v) {
 }
 
 }  // namespace sdd
+
+namespace sdd {
+// Kernel classes for launch timing (sdd_profile_*).
+enum ProfClass : unsigned {
+  PROF_EMBED = 1u, PROF_GEMM_QKV = 2u, PROF_ATTN = 4u, PROF_GEMM_O = 8u, PROF_GEMM_GU = 16u,
+  PROF_GEMM_DOWN = 32u, PROF_GEMM_LM = 64u, PROF_ACCEPT = 128u, PROF_CONF = 256u
+};
+// Bracket a launch with events on its stream when timing of cls is enabled.
+void prof_begin(unsigned cls, hipStream_t st);
+void prof_end(unsigned cls, hipStream_t st);
+}  // namespace sdd

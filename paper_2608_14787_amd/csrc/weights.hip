@@ -39,7 +39,7 @@ __device__ inline float synth_value(uint64_t key, uint64_t idx, float scale) {
 // Source of a tiled matrix: rows of a fused matrix map to (part, logical row).
 struct TiledSrc {
   int kind;  // 0 plain, 1 fused q/k/v, 2 gate/up interleaved per 16-row tile
-  int K, ktile, KT;
+  int K, ktile, KT, ng;
   int64_t N;      // physical rows
   int n0, n1;     // fused q/k/v row boundaries
   uint64_t key[3];
@@ -70,10 +70,12 @@ __global__ void fill_tiled_kernel(char* dst, TiledSrc s, int only_part) {
   const int64_t slices = ceil_div(s.N, 16) * (int64_t)s.KT * 64;
   for (int64_t id = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; id < slices;
        id += (int64_t)gridDim.x * blockDim.x) {
-    const int64_t tile = id / 64;
+    const int64_t tile = id / 64;  // physical: ((nt / ng) * KT + kt) * ng + nt % ng
     const int lane = (int)(id % 64);
-    const int64_t nt = tile / s.KT;
-    const int kt = (int)(tile % s.KT);
+    const int64_t grp = tile / ((int64_t)s.KT * s.ng);
+    const int64_t rem = tile % ((int64_t)s.KT * s.ng);
+    const int kt = (int)(rem / s.ng);
+    const int64_t nt = grp * s.ng + rem % s.ng;
     const int64_t row = nt * 16 + lane % 16;
     const int k0 = kt * s.ktile + (lane / 16) * EPL;
     int part = 0;
@@ -148,6 +150,11 @@ static size_t plan_weights(const sdd_model_config* c, sdd_model* m) {
     m->off_embed = e;
     m->off_lm = lm;
     m->off_final_norm = fn;
+    m->ng_qkv = (int)(hd / 16);
+    m->ng_o = pick_ng(d / 16, false);
+    m->ng_gu = pick_ng(2 * (int64_t)c->d_ff / 16, true);
+    m->ng_down = pick_ng(d / 16, false);
+    m->ng_lm = pick_ng(c->vocab / 16, false);
   }
   for (int l = 0; l < c->n_layers; ++l) {
     sdd_model::Layer L;
@@ -166,7 +173,8 @@ static size_t plan_weights(const sdd_model_config* c, sdd_model* m) {
 
 static int launch_blocks(int64_t work) { return (int)std::max<int64_t>(1, std::min<int64_t>(ceil_div(work, 256), 8192)); }
 
-static int fill_tiled(sdd_model* m, char* dst, TiledSrc s, int only_part, hipStream_t st) {
+static int fill_tiled(sdd_model* m, char* dst, TiledSrc s, int ng, int only_part, hipStream_t st) {
+  s.ng = ng;
   s.ktile = m->ktile;
   s.KT = (int)ceil_div(s.K, s.ktile);
   s.bf16 = m->cfg.dtype == SDD_BF16;
@@ -245,7 +253,8 @@ extern "C" int sdd_model_init_random(sdd_model* m, uint64_t seed, float sigma, s
                          reinterpret_cast<float*>(m->base + m->off_embed), ne, key, scale, (const float*)nullptr);
     if ((rc = check_launch("fill_rowmajor_kernel"))) return rc;
   }
-  auto gen = [&](char* dst, int kind, int64_t N, int K, uint64_t k0, uint64_t k1, uint64_t k2, int n0, int n1) {
+  auto gen = [&](char* dst, int ng, int kind, int64_t N, int K, uint64_t k0, uint64_t k1, uint64_t k2, int n0,
+                 int n1) {
     TiledSrc s{};
     s.kind = kind;
     s.K = K;
@@ -257,9 +266,9 @@ extern "C" int sdd_model_init_random(sdd_model* m, uint64_t seed, float sigma, s
     s.key[2] = k2;
     s.scale = scale;
     s.gen = 1;
-    return fill_tiled(m, dst, s, -1, st);
+    return fill_tiled(m, dst, s, ng, -1, st);
   };
-  if ((rc = gen(m->base + m->off_lm, 0, c.vocab, (int)d, tensor_key(seed, tensor_id(SDD_T_LM_HEAD, 0)), 0, 0, 0, 0)))
+  if ((rc = gen(m->base + m->off_lm, m->ng_lm, 0, c.vocab, (int)d, tensor_key(seed, tensor_id(SDD_T_LM_HEAD, 0)), 0, 0, 0, 0)))
     return rc;
   auto ones = [&](size_t off, int64_t n) {
     hipLaunchKernelGGL(fill_f32_kernel, dim3(launch_blocks(n)), dim3(256), 0, st,
@@ -270,11 +279,11 @@ extern "C" int sdd_model_init_random(sdd_model* m, uint64_t seed, float sigma, s
   for (int l = 0; l < c.n_layers; ++l) {
     const sdd_model::Layer& L = m->layers[l];
     auto key = [&](int kind) { return tensor_key(seed, tensor_id(kind, l)); };
-    if ((rc = gen(m->base + L.qkv, 1, hq + 2 * hk, (int)d, key(SDD_T_WQ), key(SDD_T_WK), key(SDD_T_WV), (int)hq, (int)hk)))
+    if ((rc = gen(m->base + L.qkv, m->ng_qkv, 1, hq + 2 * hk, (int)d, key(SDD_T_WQ), key(SDD_T_WK), key(SDD_T_WV), (int)hq, (int)hk)))
       return rc;
-    if ((rc = gen(m->base + L.o, 0, d, (int)hq, key(SDD_T_WO), 0, 0, 0, 0))) return rc;
-    if ((rc = gen(m->base + L.gu, 2, 2 * (int64_t)c.d_ff, (int)d, key(SDD_T_WGATE), key(SDD_T_WUP), 0, 0, 0))) return rc;
-    if ((rc = gen(m->base + L.down, 0, d, c.d_ff, key(SDD_T_WDOWN), 0, 0, 0, 0))) return rc;
+    if ((rc = gen(m->base + L.o, m->ng_o, 0, d, (int)hq, key(SDD_T_WO), 0, 0, 0, 0))) return rc;
+    if ((rc = gen(m->base + L.gu, m->ng_gu, 2, 2 * (int64_t)c.d_ff, (int)d, key(SDD_T_WGATE), key(SDD_T_WUP), 0, 0, 0))) return rc;
+    if ((rc = gen(m->base + L.down, m->ng_down, 0, d, c.d_ff, key(SDD_T_WDOWN), 0, 0, 0, 0))) return rc;
     if ((rc = ones(L.attn_norm, d)) || (rc = ones(L.ffn_norm, d)) || (rc = ones(L.q_norm, hd)) || (rc = ones(L.k_norm, hd)))
       return rc;
   }
@@ -293,7 +302,7 @@ extern "C" int sdd_model_load_tensor(sdd_model* m, int kind, int layer, const vo
                        reinterpret_cast<float*>(m->base + off), n, 0.f, reinterpret_cast<const float*>(src));
     return check_launch("fill_f32_kernel");
   };
-  auto tiled = [&](size_t off, int skind, int64_t N, int K, int part, int n0, int n1) {
+  auto tiled = [&](size_t off, int ng, int skind, int64_t N, int K, int part, int n0, int n1) {
     TiledSrc s{};
     s.kind = skind;
     s.K = K;
@@ -302,7 +311,7 @@ extern "C" int sdd_model_load_tensor(sdd_model* m, int kind, int layer, const vo
     s.n1 = n1;
     s.src[part] = src;
     s.gen = 0;
-    return fill_tiled(m, m->base + off, s, part, st);
+    return fill_tiled(m, m->base + off, s, ng, part, st);
   };
   if (kind == SDD_T_EMBED) {
     const int64_t ne = (int64_t)c.vocab * d;
@@ -316,17 +325,17 @@ extern "C" int sdd_model_load_tensor(sdd_model* m, int kind, int layer, const vo
                          reinterpret_cast<const float*>(src));
     return check_launch("fill_rowmajor_kernel");
   }
-  if (kind == SDD_T_LM_HEAD) return tiled(m->off_lm, 0, c.vocab, (int)d, 0, 0, 0);
+  if (kind == SDD_T_LM_HEAD) return tiled(m->off_lm, m->ng_lm, 0, c.vocab, (int)d, 0, 0, 0);
   if (kind == SDD_T_FINAL_NORM) return copy_f32(m->off_final_norm, d);
   const sdd_model::Layer& L = m->layers[layer];
   switch (kind) {
-    case SDD_T_WQ: return tiled(L.qkv, 1, hq + 2 * hk, (int)d, 0, (int)hq, (int)hk);
-    case SDD_T_WK: return tiled(L.qkv, 1, hq + 2 * hk, (int)d, 1, (int)hq, (int)hk);
-    case SDD_T_WV: return tiled(L.qkv, 1, hq + 2 * hk, (int)d, 2, (int)hq, (int)hk);
-    case SDD_T_WO: return tiled(L.o, 0, d, (int)hq, 0, 0, 0);
-    case SDD_T_WGATE: return tiled(L.gu, 2, 2 * (int64_t)c.d_ff, (int)d, 0, 0, 0);
-    case SDD_T_WUP: return tiled(L.gu, 2, 2 * (int64_t)c.d_ff, (int)d, 1, 0, 0);
-    case SDD_T_WDOWN: return tiled(L.down, 0, d, c.d_ff, 0, 0, 0);
+    case SDD_T_WQ: return tiled(L.qkv, m->ng_qkv, 1, hq + 2 * hk, (int)d, 0, (int)hq, (int)hk);
+    case SDD_T_WK: return tiled(L.qkv, m->ng_qkv, 1, hq + 2 * hk, (int)d, 1, (int)hq, (int)hk);
+    case SDD_T_WV: return tiled(L.qkv, m->ng_qkv, 1, hq + 2 * hk, (int)d, 2, (int)hq, (int)hk);
+    case SDD_T_WO: return tiled(L.o, m->ng_o, 0, d, (int)hq, 0, 0, 0);
+    case SDD_T_WGATE: return tiled(L.gu, m->ng_gu, 2, 2 * (int64_t)c.d_ff, (int)d, 0, 0, 0);
+    case SDD_T_WUP: return tiled(L.gu, m->ng_gu, 2, 2 * (int64_t)c.d_ff, (int)d, 1, 0, 0);
+    case SDD_T_WDOWN: return tiled(L.down, m->ng_down, 0, d, c.d_ff, 0, 0, 0);
     case SDD_T_ATTN_NORM: return copy_f32(L.attn_norm, d);
     case SDD_T_FFN_NORM: return copy_f32(L.ffn_norm, d);
     case SDD_T_Q_NORM: return copy_f32(L.q_norm, hd);

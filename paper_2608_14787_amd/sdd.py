@@ -55,6 +55,7 @@ _SIGS = {
     "sdd_kv_create": (I, [P, I, I, P, SZ, P, P]),
     "sdd_kv_destroy": (I, [P]),
     "sdd_kv_state": (I, [P, P, P, P, P]),
+    "sdd_kv_device_state": (I, [P, P, P]),
     "sdd_workspace_bytes": (I, [P, I, P]),
     "sdd_workspace_init": (I, [P, SZ, P]),
     "sdd_kv_prefill": (I, [P, P, I, P, I, P, SZ, P]),
@@ -63,7 +64,13 @@ _SIGS = {
     "sdd_rowstats_workspace_bytes": (I, [I, I, I, P]),
     "sdd_accept": (I, [P, P, I, P, I, SZ, P, I, I, I, I, I, F, P, P, P, P, SZ, P]),
     "sdd_confidence_prefix": (I, [P, I, SZ, I, I, I, F, P, P, P, P, P, SZ, P]),
+    "sdd_profile_start": (I, [C.c_uint, I]),
+    "sdd_profile_read": (I, [C.c_uint, P, P, P, P]),
+    "sdd_profile_stop": (I, []),
 }
+
+PROF_EMBED, PROF_GEMM_QKV, PROF_ATTN, PROF_GEMM_O = 1, 2, 4, 8
+PROF_GEMM_GATEUP, PROF_GEMM_DOWN, PROF_GEMM_LM, PROF_ACCEPT, PROF_CONF = 16, 32, 64, 128, 256
 
 
 def lib() -> C.CDLL:
@@ -165,6 +172,22 @@ def confidence_prefix(logits: torch.Tensor, gamma: int, tau: float, *, draft=Non
     return sk, (lc[:, :gamma] if lc is not None else None), (lp[:, :gamma] if lp is not None else None)
 
 
+def profile_start(class_mask: int, max_launches: int = 65536):
+    """Brackets launches of the given kernel classes with HIP events until profile_stop()."""
+    _check(lib().sdd_profile_start(class_mask, max_launches))
+
+
+def profile_read(cls: int):
+    """(launches, total_ms, min_ms, max_ms) over the recorded launches of the classes in cls."""
+    n, tot, mn, mx = C.c_int(), C.c_double(), C.c_double(), C.c_double()
+    _check(lib().sdd_profile_read(cls, C.byref(n), C.byref(tot), C.byref(mn), C.byref(mx)))
+    return n.value, tot.value, mn.value, mx.value
+
+
+def profile_stop():
+    _check(lib().sdd_profile_stop())
+
+
 # ---- decoder ------------------------------------------------------------------------------
 
 
@@ -226,6 +249,12 @@ class KVCache:
         _check(lib().sdd_kv_state(self.handle, ln.ctypes.data_as(C.c_void_p), pd.ctypes.data_as(C.c_void_p),
                                   eb.ctypes.data_as(C.c_void_p), _stream(stream)))
         return ln, pd, int(eb[0])
+
+    def device_len_ptr(self) -> int:
+        """Device address of the int32[max_batch] length array."""
+        p = C.c_void_p()
+        _check(lib().sdd_kv_device_state(self.handle, C.byref(p), None))
+        return p.value
 
     def prefill(self, seq: int, tokens: torch.Tensor, ws: torch.Tensor, stream=None):
         _check(lib().sdd_kv_prefill(self.model.handle, self.handle, seq, _ptr(tokens), tokens.numel(),
