@@ -176,7 +176,7 @@ __device__ void epilogue_resid(const GemmArgs& a, const float* tile, int g) {
       ss += xv * xv;
     }
     ss = wave_sum(ss);
-    if (lane == 0) a.ss_part[(int64_t)g * a.mp + m] = ss;
+    if (lane == 0) st_coherent(&a.ss_part[(int64_t)g * a.mp + m], ss);
   }
 }
 
@@ -233,8 +233,8 @@ __device__ void epilogue_logits(const GemmArgs& a, const float* tile, int g) {
       }
     }
     if (lane == 0) {
-      a.amax_v[(int64_t)g * a.mp + m] = bv;
-      a.amax_i[(int64_t)g * a.mp + m] = bi;
+      st_coherent(&a.amax_v[(int64_t)g * a.mp + m], bv);
+      st_coherent(&a.amax_i[(int64_t)g * a.mp + m], bi);
     }
   }
 }
@@ -244,27 +244,19 @@ __device__ void epilogue_logits(const GemmArgs& a, const float* tile, int g) {
 template <int EPI>
 __device__ void finish_rows(const GemmArgs& a) {
   __shared__ int s_last_done;
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    __threadfence();
-    const int old = atomicAdd(a.done, 1);
-    s_last_done = old == a.G - 1;
-  }
-  __syncthreads();
-  if (!s_last_done) return;
-  __threadfence();
+  if (!arrive_last(a.done, a.G, &s_last_done)) return;
   for (int mm = threadIdx.x; mm < a.M; mm += kGemmThreads) {
     const int m = a.m0 + mm;
     if constexpr (EPI == EPI_RESID) {
       float s = 0.f;
-      for (int g = 0; g < a.G; ++g) s += a.ss_part[(int64_t)g * a.mp + m];
+      for (int g = 0; g < a.G; ++g) s += ld_coherent(&a.ss_part[(int64_t)g * a.mp + m]);
       a.rs_out[m] = 1.f / sqrtf(s / (float)a.d + a.eps);
     } else {
       float bv = -INFINITY;
       int bi = -1;
       for (int g = 0; g < a.G; ++g) {
-        const float v = a.amax_v[(int64_t)g * a.mp + m];
-        const int i = a.amax_i[(int64_t)g * a.mp + m];
+        const float v = ld_coherent(&a.amax_v[(int64_t)g * a.mp + m]);
+        const int i = ld_coherent(&a.amax_i[(int64_t)g * a.mp + m]);
         if (arg_better(v, i, bv, bi)) {
           bv = v;
           bi = i;
@@ -273,11 +265,10 @@ __device__ void finish_rows(const GemmArgs& a) {
       if (a.argmax_out && a.rows[m].valid) a.argmax_out[m] = bi < 0 ? 0 : bi;
     }
   }
-  if (threadIdx.x == 0) *a.done = 0;
 }
 
 template <typename T, int TB, int NG, int EPI>
-__global__ void __launch_bounds__(kGemmThreads, 2) gemm_kernel(GemmArgs a) {
+__global__ void __launch_bounds__(kGemmThreads, 1) gemm_kernel(GemmArgs a) {
   constexpr int C = NG * 16;
   constexpr int NACC = NG * TB;
   constexpr int EPL = 16 / sizeof(T);
@@ -313,13 +304,17 @@ __global__ void __launch_bounds__(kGemmThreads, 2) gemm_kernel(GemmArgs a) {
     const uint4* Wg = W + (int64_t)g * NG * a.KT * kWave + lane;  // k-step kt: NG contiguous tiles
     const char* Xl = a.X + ((int64_t)(a.m0 + lane % 16) * a.ldx + (lane / 16) * EPL) * sizeof(T);
     const int64_t xrow16 = (int64_t)16 * a.ldx * sizeof(T);
-    uint4 wa0[NG], wa1[NG], xb0[TB], xb1[TB];
+    uint4 wa0[NG], wa1[NG], wa2[NG], wa3[NG], xb0[TB], xb1[TB], xb2[TB], xb3[TB];
+    // Stage loads are unconditional (the k-tile index is clamped to the last
+    // one, so a tail reloads a tile already read) so that the compiler can wait
+    // for exactly the oldest stage.
     auto load = [&](int kt, uint4* wa, uint4* xb) {
+      kt = min(kt, kz - 1);
 #pragma unroll
       for (int nt = 0; nt < NG; ++nt) wa[nt] = load_nt16(Wg + ((int64_t)kt * NG + nt) * kWave);
 #pragma unroll
       for (int tb = 0; tb < TB; ++tb) xb[tb] = load16(Xl + tb * xrow16 + (int64_t)kt * KTILE * sizeof(T));
-      // keep the next stage's loads ahead of this stage's MFMAs
+      // keep the next stages' loads ahead of this stage's MFMAs
       __builtin_amdgcn_sched_barrier(0);
     };
     auto mma = [&](const uint4* wa, const uint4* xb) {
@@ -328,22 +323,27 @@ __global__ void __launch_bounds__(kGemmThreads, 2) gemm_kernel(GemmArgs a) {
 #pragma unroll
         for (int tb = 0; tb < TB; ++tb) mma_tile<T>(wa[nt], xb[tb], acc[nt * TB + tb]);
     };
-    // Two register stages; the steady-state loop issues its loads
-    // unconditionally so that each MFMA batch waits only for its own stage.
+    // Four register stages, three in flight while one is consumed.
     int kt = ka;
-    if (kt < kz) load(kt, wa0, xb0);
-    for (; kt + 2 < kz; kt += 2) {
+    if (kt < kz) {
+      load(kt, wa0, xb0);
       load(kt + 1, wa1, xb1);
-      mma(wa0, xb0);
-      load(kt + 2, wa0, xb0);
-      mma(wa1, xb1);
-    }
-    if (kt + 1 < kz) {
-      load(kt + 1, wa1, xb1);
-      mma(wa0, xb0);
-      mma(wa1, xb1);
-    } else if (kt < kz) {
-      mma(wa0, xb0);
+      load(kt + 2, wa2, xb2);
+      for (; kt + 4 <= kz; kt += 4) {
+        load(kt + 3, wa3, xb3);
+        mma(wa0, xb0);
+        load(kt + 4, wa0, xb0);
+        mma(wa1, xb1);
+        load(kt + 5, wa1, xb1);
+        mma(wa2, xb2);
+        load(kt + 6, wa2, xb2);
+        mma(wa3, xb3);
+      }
+      // 0..3 k-tiles left, already loaded in stages 0..2
+      const int left = kz - kt;
+      if (left > 0) mma(wa0, xb0);
+      if (left > 1) mma(wa1, xb1);
+      if (left > 2) mma(wa2, xb2);
     }
 
     // ---- reduce the four waves: (w0 + w2) + (w1 + w3), fixed order ----
@@ -376,27 +376,33 @@ __global__ void __launch_bounds__(kGemmThreads, 2) gemm_kernel(GemmArgs a) {
     if (!full) {
       // ---- split column group: publish the partial, last contributor reduces ----
       float* my = a.part + ((int64_t)w * 2 + which) * MC;
-      for (int i = threadIdx.x; i < MC; i += kGemmThreads) my[i] = tile[i];
-      __syncthreads();
+      for (int i = threadIdx.x; i < MC; i += kGemmThreads) st_coherent(&my[i], tile[i]);
       const int wf = unit_owner((int64_t)g * a.KT, U, a.n_wg);
       const int wl = unit_owner((int64_t)(g + 1) * a.KT - 1, U, a.n_wg);
-      if (threadIdx.x == 0) {
-        __threadfence();
-        const int old = atomicAdd(&a.cnt[g], 1);
-        s_flag = old == wl - wf;
-      }
-      __syncthreads();
-      if (!s_flag) continue;
-      __threadfence();
-      for (int i = threadIdx.x; i < MC; i += kGemmThreads) {
-        float s = 0.f;
-        for (int ww = wf; ww <= wl; ++ww) {
-          const int wh = (g == (int)(unit_start(ww, U, a.n_wg) / a.KT)) ? 0 : 1;
-          s += a.part[((int64_t)ww * 2 + wh) * MC + i];
+      if (!arrive_last(&a.cnt[g], wl - wf + 1, &s_flag)) continue;
+      // sum the contributors in workgroup order; each thread keeps its EPT
+      // elements in registers and issues one contributor's loads together
+      constexpr int EPT = TB * 16 * C / kGemmThreads;
+      float sum[EPT];
+#pragma unroll
+      for (int e = 0; e < EPT; ++e) sum[e] = 0.f;
+      for (int ww = wf; ww <= wl; ++ww) {
+        const int wh = (g == (int)(unit_start(ww, U, a.n_wg) / a.KT)) ? 0 : 1;
+        float* src = a.part + ((int64_t)ww * 2 + wh) * MC;
+        float v[EPT];
+#pragma unroll
+        for (int e = 0; e < EPT; ++e) {
+          const int i = threadIdx.x + e * kGemmThreads;
+          v[e] = i < MC ? ld_coherent(&src[i]) : 0.f;
         }
-        tile[i] = s;
+#pragma unroll
+        for (int e = 0; e < EPT; ++e) sum[e] += v[e];
       }
-      if (threadIdx.x == 0) a.cnt[g] = 0;
+#pragma unroll
+      for (int e = 0; e < EPT; ++e) {
+        const int i = threadIdx.x + e * kGemmThreads;
+        if (i < MC) tile[i] = sum[e];
+      }
       __syncthreads();
     }
 
@@ -496,25 +502,24 @@ __global__ void __launch_bounds__(256) attention_kernel(AttnArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// Attention on MFMA (bf16 models).  Grid: (KV split, group of 64 query
-// vectors, sequence x KV head).  The query vectors of one KV head are the
-// block's rows times the heads that share it (GQA); each wave owns 16 of them.
-// Per 32 cache positions a wave computes S^T = K Q^T with K rows as the MFMA A
-// operand, so each lane ends up holding 8 scores of its own query column,
-// exactly the P^T fragment that O^T = V^T P^T takes as its B operand; V is
-// cached transposed so the A operand is two contiguous 8-byte reads.  The
-// softmax is online across positions; splits of the cache are combined by the
-// last-arriving workgroup in split order.
+// Attention on MFMA (bf16 models).  One workgroup of kAttnWaves waves per (16
+// query vectors, sequence x KV head).  The query vectors of one KV head are the
+// block's rows times the heads that share it (GQA).  The waves split the cache
+// positions into 32-position steps taken round-robin; per step a wave
+// computes S^T = K Q^T with K rows as the MFMA A operand, so each lane ends up
+// holding 8 scores of its own query column, exactly the P^T fragment that
+// O^T = V^T P^T takes as its B operand; V is cached transposed so the A operand
+// is two contiguous 8-byte reads.  The softmax is online within a wave; the
+// waves' partial (max, sum, O) are combined through LDS in wave order.
+constexpr int kAttnWaves = 8;
+
 struct AttnMfmaArgs {
   const uint16_t* q;   // [rows][hq][HD]
   const uint16_t* kc;  // layer base [seq][hkv][max_len][HD]
   const uint16_t* vc;  // layer base [seq][hkv][HD][max_len]
   uint16_t* out;       // [rows][hq*HD]
   const RowInfo* rows;
-  float* part_o;       // [nb*hkv][n_splits][QV][HD]
-  float* part_ml;      // [nb*hkv][n_splits][QV][2]
-  int* cnt;            // [nb*hkv][qgroups]
-  int nb, R, hq, hkv, grp, max_len, n_splits, split_len, qgroups;
+  int nb, R, hq, hkv, grp, max_len, qblocks;
   float scale;
 };
 
@@ -527,23 +532,25 @@ __device__ inline uint2 load4_bf16(const uint16_t* row, int p, int end) {
 }
 
 template <int HD>
-__global__ void __launch_bounds__(256) attention_mfma_kernel(AttnMfmaArgs a) {
+__global__ void __launch_bounds__(kAttnWaves * 64) attention_mfma_kernel(AttnMfmaArgs a) {
   constexpr int KK = HD / 32, DB = HD / 16;
-  __shared__ int s_last;
-  const int split = blockIdx.x, qg = blockIdx.y, bk = blockIdx.z;
-  if (bk >= a.nb * a.hkv || qg >= a.qgroups) return;  // launch larger than the block set
+  __shared__ float s_o[kAttnWaves][16][HD + 1];
+  __shared__ float s_m[kAttnWaves][16], s_l[kAttnWaves][16];
+  const int qb = blockIdx.x, bk = blockIdx.y;
+  if (bk >= a.nb * a.hkv || qb >= a.qblocks) return;  // launch larger than the block set
   const int blk = bk / a.hkv, kvh = bk % a.hkv;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave), lane = threadIdx.x % kWave;
   const int QV = a.R * a.grp;
-  const int qv = (qg * 4 + wave) * 16 + lane % 16;
+  const int qv = qb * 16 + lane % 16;
   const bool qok = qv < QV;
   const int r = qok ? qv / a.grp : 0, hh = qok ? qv % a.grp : 0;
   const int m = blk * a.R + r;
   const RowInfo first = a.rows[blk * a.R], last = a.rows[blk * a.R + a.R - 1];
-  const int kv_end = first.valid ? last.pos + 1 : 0;
+  // positions this query block can see: up to its last row's position
+  const int r_hi = min(a.R - 1, (qb * 16 + 15) / a.grp);
+  const int kv_end = __builtin_amdgcn_readfirstlane(first.valid ? a.rows[blk * a.R + r_hi].pos + 1 : 0);
+  (void)last;
   const int qpos = a.rows[m].pos;
-  const int p_begin = __builtin_amdgcn_readfirstlane(split * a.split_len);
-  const int p_end = __builtin_amdgcn_readfirstlane(min(kv_end, p_begin + a.split_len));
   const int64_t head = (int64_t)first.seq * a.hkv + kvh;
   const uint16_t* K = a.kc + head * a.max_len * HD;
   const uint16_t* Vt = a.vc + head * HD * a.max_len;
@@ -558,18 +565,35 @@ __global__ void __launch_bounds__(256) attention_mfma_kernel(AttnMfmaArgs a) {
   for (int db = 0; db < DB; ++db) o[db] = f32x4{0.f, 0.f, 0.f, 0.f};
   float mrun = -INFINITY, lrun = 0.f;
   const int g4 = 4 * (lane / 16);
-  for (int p = p_begin; p < p_end; p += 32) {
+  // Fixed assignment of 32-position steps to waves (step t to wave t % waves),
+  // independent of the other rows of the block: a row's result does not
+  // depend on how rows are batched, so a block verify reproduces decode steps
+  // bit for bit.  Steps past a row's own position are fully masked and leave
+  // its running state unchanged.
+  for (int p = 32 * wave; p < kv_end; p += 32 * kAttnWaves) {
+    uint4 kf[2][KK];
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+      const int kp = p + 16 * b + lane % 16;
+#pragma unroll
+      for (int kk = 0; kk < KK; ++kk)
+        kf[b][kk] = kp < kv_end ? load16(K + (int64_t)kp * HD + 32 * kk + 8 * (lane / 16)) : make_uint4(0, 0, 0, 0);
+    }
+    uint4 vf[DB];
+#pragma unroll
+    for (int db = 0; db < DB; ++db) {
+      const uint16_t* vrow = Vt + (int64_t)(16 * db + lane % 16) * a.max_len;
+      const uint2 v0 = load4_bf16(vrow, p + g4, kv_end), v1 = load4_bf16(vrow, p + 16 + g4, kv_end);
+      vf[db] = make_uint4(v0.x, v0.y, v1.x, v1.y);
+    }
     f32x4 sacc[2];
 #pragma unroll
     for (int b = 0; b < 2; ++b) {
       sacc[b] = f32x4{0.f, 0.f, 0.f, 0.f};
-      const int kp = p + 16 * b + lane % 16;
 #pragma unroll
-      for (int kk = 0; kk < KK; ++kk) {
-        const uint4 kf = kp < kv_end ? load16(K + (int64_t)kp * HD + 32 * kk + 8 * (lane / 16)) : make_uint4(0, 0, 0, 0);
-        sacc[b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kf), __builtin_bit_cast(bf16x8, qf[kk]),
-                                                          sacc[b], 0, 0, 0);
-      }
+      for (int kk = 0; kk < KK; ++kk)
+        sacc[b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kf[b][kk]),
+                                                          __builtin_bit_cast(bf16x8, qf[kk]), sacc[b], 0, 0, 0);
     }
     // sacc[b][i]: position p + 16 b + g4 + i, query column lane % 16
     float sv[8];
@@ -601,73 +625,45 @@ __global__ void __launch_bounds__(256) attention_mfma_kernel(AttnMfmaArgs a) {
                                 (uint32_t)pb[4] | ((uint32_t)pb[5] << 16), (uint32_t)pb[6] | ((uint32_t)pb[7] << 16));
 #pragma unroll
     for (int db = 0; db < DB; ++db) {
-      const uint16_t* vrow = Vt + (int64_t)(16 * db + lane % 16) * a.max_len;
-      const uint2 v0 = load4_bf16(vrow, p + g4, kv_end), v1 = load4_bf16(vrow, p + 16 + g4, kv_end);
-      const uint4 vf = make_uint4(v0.x, v0.y, v1.x, v1.y);
       o[db] *= alpha;
-      o[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, vf), __builtin_bit_cast(bf16x8, pf), o[db],
-                                                      0, 0, 0);
+      o[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, vf[db]), __builtin_bit_cast(bf16x8, pf),
+                                                      o[db], 0, 0, 0);
     }
   }
-  // full softmax denominator of query lane%16: the four lanes of its column
+  // softmax denominator of query lane%16 over this wave's positions
   float ltot = lrun + __shfl_xor(lrun, 16);
   ltot += __shfl_xor(ltot, 32);
-  const int h = kvh * a.grp + hh;
-  if (a.n_splits == 1) {
-    if (qok) {
-      const float inv = ltot > 0.f ? 1.f / ltot : 0.f;
-      uint16_t* dst = a.out + ((int64_t)m * a.hq + h) * HD;
+  // publish the wave's partial to LDS: o[db][i] is O^T[16 db + g4 + i][query lane%16]
 #pragma unroll
-      for (int db = 0; db < DB; ++db)
+  for (int db = 0; db < DB; ++db)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) dst[16 * db + g4 + i] = f32_to_bf16(o[db][i] * inv);
-    }
-    return;
-  }
-  // publish this split, the last workgroup of (bk, qg) combines in split order
-  const int64_t sbase = ((int64_t)bk * a.n_splits + split) * QV;
-  if (qok) {
-    float* po = a.part_o + (sbase + qv) * HD;
-#pragma unroll
-    for (int db = 0; db < DB; ++db)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) po[16 * db + g4 + i] = o[db][i];
-    if (lane < 16) {
-      a.part_ml[(sbase + qv) * 2] = mrun;
-      a.part_ml[(sbase + qv) * 2 + 1] = ltot;
-    }
+    for (int i = 0; i < 4; ++i) s_o[wave][lane % 16][16 * db + g4 + i] = o[db][i];
+  if (lane < 16) {
+    s_m[wave][lane] = mrun;
+    s_l[wave][lane] = ltot;
   }
   __syncthreads();
-  if (threadIdx.x == 0) {
-    __threadfence();
-    const int old = atomicAdd(&a.cnt[bk * a.qgroups + qg], 1);
-    s_last = old == a.n_splits - 1;
-  }
-  __syncthreads();
-  if (!s_last) return;
-  __threadfence();
-  const int q0 = qg * 64;
-  for (int e = threadIdx.x; e < 64 * HD; e += 256) {
-    const int qq = q0 + e / HD, dim = e % HD;
-    if (qq >= QV) break;
+  // combine the waves in wave order
+  for (int e = threadIdx.x; e < 16 * HD; e += kAttnWaves * 64) {
+    const int q = e / HD, dim = e % HD;
+    const int qq = qb * 16 + q;
+    if (qq >= QV) continue;
     float M = -INFINITY;
-    for (int sp = 0; sp < a.n_splits; ++sp)
-      M = fmaxf(M, a.part_ml[(((int64_t)bk * a.n_splits + sp) * QV + qq) * 2]);
+#pragma unroll
+    for (int w = 0; w < kAttnWaves; ++w) M = fmaxf(M, s_m[w][q]);
     float L = 0.f, O = 0.f;
     if (M != -INFINITY) {
-      for (int sp = 0; sp < a.n_splits; ++sp) {
-        const int64_t id = ((int64_t)bk * a.n_splits + sp) * QV + qq;
-        const float ms = a.part_ml[id * 2];
-        if (ms == -INFINITY) continue;
-        const float f = __expf(ms - M);
-        L += a.part_ml[id * 2 + 1] * f;
-        O += a.part_o[id * HD + dim] * f;
+#pragma unroll
+      for (int w = 0; w < kAttnWaves; ++w) {
+        const float ms = s_m[w][q];
+        const float f = ms == -INFINITY ? 0.f : __expf(ms - M);
+        L += s_l[w][q] * f;
+        O += s_o[w][q][dim] * f;
       }
     }
     const int rr = qq / a.grp, hq2 = kvh * a.grp + qq % a.grp;
     a.out[((int64_t)(blk * a.R + rr) * a.hq + hq2) * HD + dim] = f32_to_bf16(L > 0.f ? O / L : 0.f);
   }
-  if (threadIdx.x == 0) a.cnt[bk * a.qgroups + qg] = 0;
 }
 
 // ---------------------------------------------------------------------------
@@ -802,16 +798,14 @@ __global__ void kv_init_kernel(int32_t* len, int32_t* pending, int32_t* err, int
 
 // Counter region at the start of every workspace, sized by the model only, so
 // that it stays at one place whatever the row count of a call: [0, 16) group
-// completion counters, then one arrival counter per GEMM column group, then
-// kAttnCounters attention split counters.
-constexpr int kAttnCounters = 65536;
+// completion counters, then one arrival counter per GEMM column group.
 
 static int64_t gemm_counter_count(const sdd_model* m) {
   return ceil_div(m->cfg.vocab, 16) + ceil_div(2 * (int64_t)m->cfg.d_ff, 16) + ceil_div(m->cfg.d_model, 16) + 64;
 }
 
 static size_t counters_bytes(const sdd_model* m) {
-  return align_up((size_t)(16 + gemm_counter_count(m) + kAttnCounters) * 4, 256);
+  return align_up((size_t)(16 + gemm_counter_count(m)) * 4, 256);
 }
 
 WsLayout ws_layout(const sdd_model* m, int max_rows) {
@@ -821,7 +815,7 @@ WsLayout ws_layout(const sdd_model* m, int max_rows) {
   const int mp = (int)align_up((size_t)std::max(1, max_rows), 16);
   const int64_t d = c.d_model, hq = (int64_t)c.n_q_heads * c.head_dim;
   L.mp = mp;
-  L.n_wg = 2 * m->n_cu;
+  L.n_wg = m->n_cu;  // one 256-thread GEMM workgroup per compute unit
   L.max_groups = (int)ceil_div(std::max<int64_t>(c.vocab, std::max<int64_t>(2 * (int64_t)c.d_ff, d)), 16);
   size_t off = 0;
   auto take = [&](size_t b) {
@@ -840,10 +834,6 @@ WsLayout ws_layout(const sdd_model* m, int max_rows) {
   L.ffh = take((size_t)mp * c.d_ff * es);
   L.part = take((size_t)L.n_wg * 2 * kMaxPassRows * 128 * 4);
   L.amax = take((size_t)L.max_groups * mp * 8);
-  // attention split partials: room for attn_qs (query vector, split) pairs
-  L.attn_splits_max = (int)std::max<int64_t>((int64_t)mp * c.n_q_heads * 4, (int64_t)64 * c.n_q_heads * 16);
-  L.attn_part = take((size_t)L.attn_splits_max * (c.head_dim + 2) * 4);
-  L.attn_cnt = L.cnt + (size_t)(16 + gemm_counter_count(m)) * 4;
   L.total = off;
   return L;
 }
@@ -962,29 +952,20 @@ static int forward_rows(CallCtx& cx, int nb, int R, float* logits, int32_t* argm
       a.vc = reinterpret_cast<const uint16_t*>(kv->v + (size_t)l * kv->layer_stride);
       a.out = reinterpret_cast<uint16_t*>(ws + L.ao);
       a.rows = reinterpret_cast<const RowInfo*>(ws + L.rowinfo);
+      a.nb = nb;
       a.R = R;
       a.hq = c.n_q_heads;
       a.hkv = c.n_kv_heads;
       a.grp = c.n_q_heads / c.n_kv_heads;
       a.max_len = kv->max_len;
-      a.qgroups = (int)ceil_div((int64_t)R * a.grp, 64);
-      a.nb = nb;
-      const int64_t base = (int64_t)nb * a.hkv * a.qgroups;  // (sequence x KV head, query group) pairs
-      int ns = (int)std::min<int64_t>(16, std::max<int64_t>(1, ceil_div(2 * m->n_cu, base)));
-      ns = (int)std::min<int64_t>(ns, std::max<int64_t>(1, L.attn_splits_max / ((int64_t)M * c.n_q_heads)));
-      if (base > kAttnCounters) ns = 1;
-      a.split_len = (int)align_up((size_t)ceil_div(kv->max_len, ns), 32);
-      a.n_splits = (int)ceil_div(kv->max_len, a.split_len);
-      a.part_o = reinterpret_cast<float*>(ws + L.attn_part);
-      a.part_ml = a.part_o + (size_t)L.attn_splits_max * c.head_dim;
-      a.cnt = reinterpret_cast<int*>(ws + L.attn_cnt);
+      a.qblocks = (int)ceil_div((int64_t)R * a.grp, 16);
       a.scale = 1.f / sqrtf((float)c.head_dim);
-      const dim3 grid(a.n_splits, a.qgroups, (unsigned)(nb * a.hkv));
+      const dim3 grid(a.qblocks, nb * a.hkv);
       prof_begin(PROF_ATTN, cx.st);
       if (c.head_dim == 128)
-        hipLaunchKernelGGL(attention_mfma_kernel<128>, grid, dim3(256), 0, cx.st, a);
+        hipLaunchKernelGGL(attention_mfma_kernel<128>, grid, dim3(kAttnWaves * 64), 0, cx.st, a);
       else
-        hipLaunchKernelGGL(attention_mfma_kernel<64>, grid, dim3(256), 0, cx.st, a);
+        hipLaunchKernelGGL(attention_mfma_kernel<64>, grid, dim3(kAttnWaves * 64), 0, cx.st, a);
       prof_end(PROF_ATTN, cx.st);
       if ((rc = check_launch("attention_mfma_kernel"))) return rc;
     } else {

@@ -47,7 +47,7 @@ struct sdd_kv {
 
 namespace sdd {
 
-inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+__host__ __device__ inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
 // Row tiles per column group: the largest of 8, 4, 2 dividing the tile count
 // (even for the gate/up interleave, which pairs tiles).
@@ -71,11 +71,10 @@ struct RowInfo {
 
 // Per-call workspace carve-up for up to max_rows rows.
 struct WsLayout {
-  size_t rowinfo, x, xa, rs, ss_part, q, ao, ffh, part, cnt, amax, attn_part, attn_cnt, total;
+  size_t rowinfo, x, xa, rs, ss_part, q, ao, ffh, part, cnt, amax, total;
   int mp;         // padded rows
   int max_groups; // column groups of the widest GEMM
   int n_wg;       // GEMM workgroups
-  int attn_splits_max;
 };
 
 WsLayout ws_layout(const sdd_model* m, int max_rows);

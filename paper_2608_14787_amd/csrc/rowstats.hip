@@ -215,7 +215,7 @@ struct RowStats {
   int arg, cnt, flags;
 };
 
-__device__ inline RowStats combine_row(const RowRec* r, int C) {
+__device__ inline RowStats combine_row(RowRec* rp, int C) {
   RowStats o;
   o.m = -INFINITY;
   o.arg = -1;
@@ -223,19 +223,22 @@ __device__ inline RowStats combine_row(const RowRec* r, int C) {
   o.flags = 0;
   o.qm = -INFINITY;
   for (int c = 0; c < C; ++c) {
-    if (better(r[c].m, r[c].arg, o.m, o.arg)) {
-      o.m = r[c].m;
-      o.arg = r[c].arg;
+    const float m = ld_coherent(&rp[c].m);
+    const int arg = ld_coherent(&rp[c].arg);
+    if (better(m, arg, o.m, o.arg)) {
+      o.m = m;
+      o.arg = arg;
     }
-    o.cnt += r[c].cnt;
-    o.flags |= r[c].flags;
-    if (r[c].qs > 0.f) o.qm = fmaxf(o.qm, r[c].qm);
+    o.cnt += ld_coherent(&rp[c].cnt);
+    o.flags |= ld_coherent(&rp[c].flags);
+    if (ld_coherent(&rp[c].qs) > 0.f) o.qm = fmaxf(o.qm, ld_coherent(&rp[c].qm));
   }
   o.s = 0.f;
   o.qs = 0.f;
   for (int c = 0; c < C; ++c) {
-    if (r[c].s > 0.f) o.s += r[c].s * __expf(r[c].m - o.m);
-    if (r[c].qs > 0.f) o.qs += r[c].qs * __expf(r[c].qm - o.qm);
+    const float s = ld_coherent(&rp[c].s), qs = ld_coherent(&rp[c].qs);
+    if (s > 0.f) o.s += s * __expf(ld_coherent(&rp[c].m) - o.m);
+    if (qs > 0.f) o.qs += qs * __expf(ld_coherent(&rp[c].qm) - o.qm);
   }
   return o;
 }
@@ -298,18 +301,20 @@ __global__ void __launch_bounds__(kThreads) rowstats_kernel(Job job) {
   }
 
   if (threadIdx.x == 0) {
-    job.recs[blockIdx.x] = rec;
-    __threadfence();
-    int old = atomicAdd(&job.counters[b], 1);
-    s_last = (old == job.rows * job.C - 1);
+    RowRec* dst = &job.recs[blockIdx.x];
+    st_coherent(&dst->m, rec.m);
+    st_coherent(&dst->arg, rec.arg);
+    st_coherent(&dst->s, rec.s);
+    st_coherent(&dst->cnt, rec.cnt);
+    st_coherent(&dst->qm, rec.qm);
+    st_coherent(&dst->qs, rec.qs);
+    st_coherent(&dst->flags, rec.flags);
   }
-  __syncthreads();
-  if (!s_last) return;
-  __threadfence();
+  if (!arrive_last(&job.counters[b], job.rows * job.C, &s_last)) return;
 
   // ---- last workgroup of sequence b: combine and decide ----
   const int t = threadIdx.x;
-  const RowRec* recs = job.recs + (size_t)b * job.rows * job.C;
+  RowRec* recs = job.recs + (size_t)b * job.rows * job.C;
   if (t < job.rows) {
     const RowStats st = combine_row(recs + t * job.C, job.C);
     const bool bad = (st.flags & 1) != 0;
@@ -387,7 +392,6 @@ __global__ void __launch_bounds__(kThreads) rowstats_kernel(Job job) {
         }
       job.out_len[b] = K;
     }
-    job.counters[b] = 0;  // ready for the next call
   }
 }
 

@@ -85,6 +85,43 @@ __device__ inline uint4 load16(const void* p) { return *reinterpret_cast<const u
 
 __host__ __device__ inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
+// Cross-workgroup hand-off without cache-wide fences.  A device-scope fence on
+// this part writes back and invalidates a whole L2 (one per XCD), which costs
+// far more than the few kilobytes handed over.  Instead the published data and
+// the arrival counters use relaxed system-scope accesses, which go to the
+// memory side (coherent for every XCD) and bypass the L2 and L1; a publisher
+// waits for its stores to complete before it arrives, and the last arriver
+// reads the data back with the same coherent loads.
+template <typename T>
+__device__ inline void st_coherent(T* p, T v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+}
+template <typename T>
+__device__ inline T ld_coherent(T* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+}
+// Waits until every memory operation this thread issued has completed.
+__device__ inline void wait_stores() {
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+  __builtin_amdgcn_s_waitcnt(0);
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+}
+// Every thread of the block must call this after its coherent stores; returns
+// (in all threads) whether this block is the last of `expected` arrivals on
+// *cnt.  The last arriver finds the counter back at zero for the next use.
+__device__ inline bool arrive_last(int* cnt, int expected, int* s_flag) {
+  wait_stores();
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const int old = __hip_atomic_fetch_add(cnt, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+    const int last = old == expected - 1;
+    if (last) __hip_atomic_store(cnt, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+    *s_flag = last;
+  }
+  __syncthreads();
+  return *s_flag != 0;
+}
+
 // wave-level reductions (64 lanes)
 __device__ inline float wave_max(float v) {
 #pragma unroll

@@ -87,6 +87,7 @@ def _run_case(S, shape, prompt_len, gamma, seed, n_rounds=1, max_len=None):
         ok, rel = row_tol_ok(got, want, _tol(shape))
         print(f"round {r}: max rel err {rel.max():.2e}", flush=True)
         assert ok.all(), rel
+        print(f"  bf16/f32 logits vs oracle: max rel {rel.max():.2e}, median {np.median(rel):.2e}", flush=True)
         tol_abs = _tol(shape) * np.abs(want).max(-1)
         near = argmax_near_tie(want, tol_abs)
         amg = am[0].cpu().numpy()
@@ -210,3 +211,31 @@ def test_capacity_refusal_and_determinism(S):
     _, _, err = kv.state()
     assert err & 1
     assert (l3 == 7.0).all()
+
+
+@pytest.mark.parametrize("shape", [MID_BF16, MID_GQA128, W.TINY], ids=["hd64-qknorm", "hd128-gqa4", "tiny-f32"])
+def test_block_verify_equals_sequential_decode(S, shape):
+    """Row j of a gamma-row verify must equal a decode step at the same position after committing
+    drafts 1..j one at a time (same cache contents, same arithmetic up to summation order)."""
+    m = _gpu_model(S, shape)
+    gamma, P = 12, 30
+    kv = S.KVCache(m, 2, 64)
+    ws = m.workspace(64)
+    toks = to_dev_i32(W.prompt(11, P, shape.vocab))
+    kv.prefill(0, toks, ws)
+    kv.prefill(1, toks, ws)
+    drafts = W.prompt(12, gamma, shape.vocab)
+    lb = torch.empty((1, gamma + 1, shape.vocab), dtype=torch.float32, device="cuda")
+    kv.verify(to_dev_i32([0]), to_dev_i32(drafts.reshape(1, gamma)), lb, None, ws)
+    l1 = torch.empty((1, 1, shape.vocab), dtype=torch.float32, device="cuda")
+    one, zero = to_dev_i32([1]), to_dev_i32([0])
+    worst = 0.0
+    for j in range(gamma + 1):
+        kv.verify(one, torch.empty((1, 0), dtype=torch.int32, device="cuda"), l1, None, ws)
+        a, b = lb[0, j].cpu().numpy(), l1[0, 0].cpu().numpy()
+        rel = np.abs(a - b).max() / np.abs(a).max()
+        worst = max(worst, rel)
+        if j < gamma:
+            kv.commit(one, zero, to_dev_i32([drafts[j]]))
+    print(f"{shape.dtype} verify-vs-decode max rel diff {worst:.2e}")
+    assert worst == 0.0, worst  # a row's arithmetic does not depend on the other rows of its block
