@@ -48,9 +48,11 @@ struct GemmArgs {
   int n_wg;
   float* part;    // partial tiles [n_wg][2][M][NG*16]
   int* cnt;       // arrival counter per column group
-  int* done;      // groups-finished counter
   const RowInfo* rows;
-  const float* rs;  // RMSNorm row scale of the input (NULL: none)
+  // RMSNorm of the input rows: r_m = 1/sqrt(sum_g ss_in[g][m] / d_in + eps),
+  // from per-column-group sums of squares written by the producer (NULL: none)
+  const float* ss_in;
+  int ss_groups, d_in;
   float eps;
   // EPI_QKV
   char* q_out;
@@ -66,8 +68,7 @@ struct GemmArgs {
   char* xa;
   int d;
   const float* g_next;
-  float* ss_part;
-  float* rs_out;
+  float* ss_part;  // sums of squares of this GEMM's output rows per column group
   // EPI_SWIGLU
   char* ffh;
   int dff;
@@ -76,7 +77,6 @@ struct GemmArgs {
   int V;
   float* amax_v;
   int* amax_i;
-  int* argmax_out;
 };
 
 template <typename T>
@@ -102,7 +102,7 @@ __device__ inline int unit_owner(int64_t x, int64_t U, int n) { return (int)(((x
 __device__ inline int64_t unit_start(int w, int64_t U, int n) { return (int64_t)w * U / n; }
 
 template <typename T, int NG>
-__device__ void epilogue_qkv(const GemmArgs& a, const float* tile, int g, int layer_unused) {
+__device__ void epilogue_qkv(const GemmArgs& a, const float* tile, int g, const float* rsl) {
   constexpr int C = NG * 16;  // == head_dim
   const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
   const int h = g;
@@ -111,7 +111,7 @@ __device__ void epilogue_qkv(const GemmArgs& a, const float* tile, int g, int la
     const int m = a.m0 + mm;
     const RowInfo ri = a.rows[m];
     if (!ri.valid) continue;
-    const float r = a.rs ? a.rs[m] : 1.f;
+    const float r = rsl[mm];
     float y[C / 64 > 0 ? C / 64 : 1];
     if constexpr (C == 128) {
       y[0] = tile[mm * C + lane] * r;
@@ -176,17 +176,17 @@ __device__ void epilogue_resid(const GemmArgs& a, const float* tile, int g) {
       ss += xv * xv;
     }
     ss = wave_sum(ss);
-    if (lane == 0) st_coherent(&a.ss_part[(int64_t)g * a.mp + m], ss);
+    if (lane == 0) a.ss_part[(int64_t)g * a.mp + m] = ss;
   }
 }
 
 template <typename T, int NG>
-__device__ void epilogue_swiglu(const GemmArgs& a, const float* tile, int g) {
+__device__ void epilogue_swiglu(const GemmArgs& a, const float* tile, int g, const float* rsl) {
   constexpr int C = NG * 16, P = NG / 2;
   const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
   for (int mm = wave; mm < a.M; mm += kGemmThreads / kWave) {
     const int m = a.m0 + mm;
-    const float r = a.rs ? a.rs[m] : 1.f;
+    const float r = rsl[mm];
     for (int idx = lane; idx < P * 16; idx += kWave) {
       const int t = idx / 16, j = idx % 16;
       const float gt = tile[mm * C + (2 * t) * 16 + j] * r;
@@ -204,13 +204,13 @@ __device__ inline bool arg_better(float v2, int i2, float v1, int i1) {
 }
 
 template <int NG>
-__device__ void epilogue_logits(const GemmArgs& a, const float* tile, int g) {
+__device__ void epilogue_logits(const GemmArgs& a, const float* tile, int g, const float* rsl) {
   constexpr int C = NG * 16;
   const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
   for (int mm = wave; mm < a.M; mm += kGemmThreads / kWave) {
     const int m = a.m0 + mm;
     const RowInfo ri = a.rows[m];
-    const float r = a.rs ? a.rs[m] : 1.f;
+    const float r = rsl[mm];
     float bv = -INFINITY;
     int bi = -1;
     for (int c = lane; c < C; c += kWave) {
@@ -233,38 +233,40 @@ __device__ void epilogue_logits(const GemmArgs& a, const float* tile, int g) {
       }
     }
     if (lane == 0) {
-      st_coherent(&a.amax_v[(int64_t)g * a.mp + m], bv);
-      st_coherent(&a.amax_i[(int64_t)g * a.mp + m], bi);
+      a.amax_v[(int64_t)g * a.mp + m] = bv;
+      a.amax_i[(int64_t)g * a.mp + m] = bi;
     }
   }
 }
 
-// After every column group of a RESID / LOGITS GEMM pass is final, the last
-// group to finish reduces the per-group row statistics in group order.
-template <int EPI>
-__device__ void finish_rows(const GemmArgs& a) {
-  __shared__ int s_last_done;
-  if (!arrive_last(a.done, a.G, &s_last_done)) return;
-  for (int mm = threadIdx.x; mm < a.M; mm += kGemmThreads) {
-    const int m = a.m0 + mm;
-    if constexpr (EPI == EPI_RESID) {
-      float s = 0.f;
-      for (int g = 0; g < a.G; ++g) s += ld_coherent(&a.ss_part[(int64_t)g * a.mp + m]);
-      a.rs_out[m] = 1.f / sqrtf(s / (float)a.d + a.eps);
-    } else {
-      float bv = -INFINITY;
-      int bi = -1;
-      for (int g = 0; g < a.G; ++g) {
-        const float v = ld_coherent(&a.amax_v[(int64_t)g * a.mp + m]);
-        const int i = ld_coherent(&a.amax_i[(int64_t)g * a.mp + m]);
-        if (arg_better(v, i, bv, bi)) {
-          bv = v;
-          bi = i;
-        }
-      }
-      if (a.argmax_out && a.rows[m].valid) a.argmax_out[m] = bi < 0 ? 0 : bi;
+// Row argmax over the per-column-group maxima of the LM head: one workgroup per
+// row; max value, lowest index among equal maxima (NaN never wins).
+__global__ void __launch_bounds__(256) row_argmax_kernel(const float* amax_v, const int* amax_i, int G, int mp,
+                                                        const RowInfo* rows, int32_t* out) {
+  __shared__ float sv[256];
+  __shared__ int si[256];
+  const int m = blockIdx.x, t = threadIdx.x;
+  float bv = -INFINITY;
+  int bi = -1;
+  for (int g = t; g < G; g += 256) {
+    const float v = amax_v[(int64_t)g * mp + m];
+    const int i = amax_i[(int64_t)g * mp + m];
+    if (arg_better(v, i, bv, bi)) {
+      bv = v;
+      bi = i;
     }
   }
+  sv[t] = bv;
+  si[t] = bi;
+  __syncthreads();
+  for (int o = 128; o > 0; o >>= 1) {
+    if (t < o && arg_better(sv[t + o], si[t + o], sv[t], si[t])) {
+      sv[t] = sv[t + o];
+      si[t] = si[t + o];
+    }
+    __syncthreads();
+  }
+  if (t == 0 && rows[m].valid) out[m] = si[0] < 0 ? 0 : si[0];
 }
 
 template <typename T, int TB, int NG, int EPI>
@@ -276,6 +278,7 @@ __global__ void __launch_bounds__(kGemmThreads, 1) gemm_kernel(GemmArgs a) {
   // reduction buffer for waves 2,3 (later reused as the output tile)
   __shared__ f32x4 red[2][NACC][kWave];
   __shared__ int s_flag;
+  __shared__ float s_rs[kMaxPassRows];
   float* tile = reinterpret_cast<float*>(&red[1][0][0]);
   static_assert(NACC * kWave * 4 >= TB * 16 * C, "tile must fit the reduction buffer");
 
@@ -285,6 +288,27 @@ __global__ void __launch_bounds__(kGemmThreads, 1) gemm_kernel(GemmArgs a) {
   const int64_t u0 = unit_start(w, U, a.n_wg), u1 = unit_start(w + 1, U, a.n_wg);
   const uint4* W = reinterpret_cast<const uint4*>(a.W);
   const int MC = a.M * C;
+  if constexpr (EPI != EPI_RESID) {
+    // RMSNorm row scales of the input rows from the producer's per-group sums
+    // of squares: four threads per row take every fourth group, then the four
+    // partial sums are added in a fixed order.
+    float* part4 = reinterpret_cast<float*>(&red[0][0][0]);  // [4][64]
+    const int ng_in = a.ss_in ? a.ss_groups : 0;
+    const int row = threadIdx.x % kMaxPassRows, q4 = threadIdx.x / kMaxPassRows;
+    float ssum = 0.f;
+    if (row < a.M) {
+#pragma unroll 4
+      for (int gg = q4; gg < ng_in; gg += 4) ssum += a.ss_in[(int64_t)gg * a.mp + a.m0 + row];
+    }
+    part4[q4 * kMaxPassRows + row] = ssum;
+    __syncthreads();
+    if ((int)threadIdx.x < a.M) {
+      const int t = threadIdx.x;
+      const float tot = (part4[t] + part4[kMaxPassRows + t]) + (part4[2 * kMaxPassRows + t] + part4[3 * kMaxPassRows + t]);
+      s_rs[t] = ng_in ? 1.f / sqrtf(tot / (float)a.d_in + a.eps) : 1.f;
+    }
+    __syncthreads();
+  }
 
   for (int64_t u = u0; u < u1;) {
     const int g = (int)(u / a.KT);
@@ -386,17 +410,25 @@ __global__ void __launch_bounds__(kGemmThreads, 1) gemm_kernel(GemmArgs a) {
       float sum[EPT];
 #pragma unroll
       for (int e = 0; e < EPT; ++e) sum[e] = 0.f;
-      for (int ww = wf; ww <= wl; ++ww) {
-        const int wh = (g == (int)(unit_start(ww, U, a.n_wg) / a.KT)) ? 0 : 1;
-        float* src = a.part + ((int64_t)ww * 2 + wh) * MC;
-        float v[EPT];
+      for (int ww = wf; ww <= wl; ww += 2) {
+        // two contributors' loads in flight at once; added in workgroup order
+        const bool two = ww + 1 <= wl;
+        const int wh0 = (g == (int)(unit_start(ww, U, a.n_wg) / a.KT)) ? 0 : 1;
+        const int wh1 = two && (g == (int)(unit_start(ww + 1, U, a.n_wg) / a.KT)) ? 0 : 1;
+        float* src0 = a.part + ((int64_t)ww * 2 + wh0) * MC;
+        float* src1 = a.part + ((int64_t)(two ? ww + 1 : ww) * 2 + (two ? wh1 : wh0)) * MC;
+        float v0[EPT], v1[EPT];
 #pragma unroll
         for (int e = 0; e < EPT; ++e) {
           const int i = threadIdx.x + e * kGemmThreads;
-          v[e] = i < MC ? ld_coherent(&src[i]) : 0.f;
+          v0[e] = i < MC ? ld_coherent(&src0[i]) : 0.f;
+          v1[e] = (i < MC && two) ? ld_coherent(&src1[i]) : 0.f;
         }
 #pragma unroll
-        for (int e = 0; e < EPT; ++e) sum[e] += v[e];
+        for (int e = 0; e < EPT; ++e) {
+          sum[e] += v0[e];
+          if (two) sum[e] += v1[e];
+        }
       }
 #pragma unroll
       for (int e = 0; e < EPT; ++e) {
@@ -407,11 +439,10 @@ __global__ void __launch_bounds__(kGemmThreads, 1) gemm_kernel(GemmArgs a) {
     }
 
     // ---- epilogue on the final tile of column group g ----
-    if constexpr (EPI == EPI_QKV) epilogue_qkv<T, NG>(a, tile, g, 0);
+    if constexpr (EPI == EPI_QKV) epilogue_qkv<T, NG>(a, tile, g, s_rs);
     if constexpr (EPI == EPI_RESID) epilogue_resid<T, NG>(a, tile, g);
-    if constexpr (EPI == EPI_SWIGLU) epilogue_swiglu<T, NG>(a, tile, g);
-    if constexpr (EPI == EPI_LOGITS) epilogue_logits<NG>(a, tile, g);
-    if constexpr (EPI == EPI_RESID || EPI == EPI_LOGITS) finish_rows<EPI>(a);
+    if constexpr (EPI == EPI_SWIGLU) epilogue_swiglu<T, NG>(a, tile, g, s_rs);
+    if constexpr (EPI == EPI_LOGITS) epilogue_logits<NG>(a, tile, g, s_rs);
   }
 }
 
@@ -672,7 +703,7 @@ struct EmbedArgs {
   const float* g; // attention-norm gain of layer 0 (or final norm when there are no layers)
   float* x;
   char* xa;
-  float* rs;
+  float* ss;  // sum of squares of each row (the RMSNorm statistic of layer 0)
   RowInfo* rows;
   int d, V, R, gamma, max_len, max_batch;
   float eps;
@@ -740,7 +771,7 @@ __global__ void __launch_bounds__(256) embed_kernel(EmbedArgs a) {
   ss = wave_sum(ss);
   if (tid % kWave == 0) red[tid / kWave] = ss;
   __syncthreads();
-  if (tid == 0) a.rs[m] = 1.f / sqrtf(((red[0] + red[1]) + (red[2] + red[3])) / (float)a.d + a.eps);
+  if (tid == 0) a.ss[m] = (red[0] + red[1]) + (red[2] + red[3]);  // one column group
 }
 
 __global__ void commit_kernel(int32_t* len, int32_t* pending, int32_t* err, const int32_t* seq_ids, int n,
@@ -797,15 +828,15 @@ __global__ void kv_init_kernel(int32_t* len, int32_t* pending, int32_t* err, int
 
 
 // Counter region at the start of every workspace, sized by the model only, so
-// that it stays at one place whatever the row count of a call: [0, 16) group
-// completion counters, then one arrival counter per GEMM column group.
+// that it stays at one place whatever the row count of a call: one arrival
+// counter per GEMM column group.
 
 static int64_t gemm_counter_count(const sdd_model* m) {
   return ceil_div(m->cfg.vocab, 16) + ceil_div(2 * (int64_t)m->cfg.d_ff, 16) + ceil_div(m->cfg.d_model, 16) + 64;
 }
 
 static size_t counters_bytes(const sdd_model* m) {
-  return align_up((size_t)(16 + gemm_counter_count(m)) * 4, 256);
+  return align_up((size_t)gemm_counter_count(m) * 4, 256);
 }
 
 WsLayout ws_layout(const sdd_model* m, int max_rows) {
@@ -827,7 +858,6 @@ WsLayout ws_layout(const sdd_model* m, int max_rows) {
   L.rowinfo = take((size_t)mp * sizeof(RowInfo));
   L.x = take((size_t)mp * d * 4);
   L.xa = take((size_t)mp * d * es);
-  L.rs = take((size_t)mp * 4);
   L.ss_part = take((size_t)ceil_div(d, 16) * mp * 4);
   L.q = take((size_t)mp * hq * es);
   L.ao = take((size_t)mp * hq * es);
@@ -878,8 +908,7 @@ static int run_gemm(CallCtx& cx, int epi, unsigned prof, size_t w_off, int64_t N
   a.ldx = K;
   a.mp = cx.L.mp;
   a.part = reinterpret_cast<float*>(cx.ws + cx.L.part);
-  a.cnt = reinterpret_cast<int*>(cx.ws + cx.L.cnt) + 16;
-  a.done = reinterpret_cast<int*>(cx.ws + cx.L.cnt);
+  a.cnt = reinterpret_cast<int*>(cx.ws + cx.L.cnt);
   a.rows = reinterpret_cast<const RowInfo*>(cx.ws + cx.L.rowinfo);
   a.eps = m->cfg.rms_eps;
   const int64_t U = (int64_t)a.G * a.KT;
@@ -912,7 +941,7 @@ static int run_gemm(CallCtx& cx, int epi, unsigned prof, size_t w_off, int64_t N
   return SDD_OK;
 }
 
-// Forward of M rows whose RowInfo/x/xa/rs were written by embed_kernel.
+// Forward of M rows whose RowInfo/x/xa/sum of squares were written by embed_kernel.
 static int forward_rows(CallCtx& cx, int nb, int R, float* logits, int32_t* argmax) {
   const int M = nb * R;
   sdd_model* m = cx.m;
@@ -923,14 +952,19 @@ static int forward_rows(CallCtx& cx, int nb, int R, float* logits, int32_t* argm
   const WsLayout& L = cx.L;
   float* x = reinterpret_cast<float*>(ws + L.x);
   char* xa = ws + L.xa;
-  float* rs = reinterpret_cast<float*>(ws + L.rs);
+  float* ss = reinterpret_cast<float*>(ws + L.ss_part);
+  // column groups of the RMSNorm statistic of the current residual stream
+  const int g_resid_o = (int)(d / 16 / m->ng_o), g_resid_down = (int)(d / 16 / m->ng_down);
+  int ss_groups = 1;  // from embed_kernel
   int rc;
   for (int l = 0; l < c.n_layers; ++l) {
     const sdd_model::Layer& Ly = m->layers[l];
     // q/k/v + QK-norm + RoPE + cache append
     {
       GemmArgs a{};
-      a.rs = rs;
+      a.ss_in = ss;
+      a.ss_groups = ss_groups;
+      a.d_in = (int)d;
       a.q_out = ws + L.q;
       a.hq = c.n_q_heads;
       a.hkv = c.n_kv_heads;
@@ -989,19 +1023,19 @@ static int forward_rows(CallCtx& cx, int nb, int R, float* logits, int32_t* argm
     // output projection + residual; next input scaled by the FFN norm gain
     {
       GemmArgs a{};
-      a.rs = nullptr;
       a.x = x;
       a.xa = xa;
       a.d = (int)d;
       a.g_next = reinterpret_cast<const float*>(m->base + Ly.ffn_norm);
-      a.ss_part = reinterpret_cast<float*>(ws + L.ss_part);
-      a.rs_out = rs;
+      a.ss_part = ss;
       if ((rc = run_gemm(cx, EPI_RESID, PROF_GEMM_O, Ly.o, d, (int)hq, ws + L.ao, a, M, m->ng_o))) return rc;
     }
     // gate/up + SwiGLU
     {
       GemmArgs a{};
-      a.rs = rs;
+      a.ss_in = ss;
+      a.ss_groups = g_resid_o;
+      a.d_in = (int)d;
       a.ffh = ws + L.ffh;
       a.dff = c.d_ff;
       if ((rc = run_gemm(cx, EPI_SWIGLU, PROF_GEMM_GU, Ly.gu, 2 * (int64_t)c.d_ff, (int)d, xa, a, M, m->ng_gu)))
@@ -1010,26 +1044,34 @@ static int forward_rows(CallCtx& cx, int nb, int R, float* logits, int32_t* argm
     // down projection + residual; next input scaled by the next norm gain
     {
       GemmArgs a{};
-      a.rs = nullptr;
       a.x = x;
       a.xa = xa;
       a.d = (int)d;
       a.g_next = reinterpret_cast<const float*>(
           m->base + (l + 1 < c.n_layers ? m->layers[l + 1].attn_norm : m->off_final_norm));
-      a.ss_part = reinterpret_cast<float*>(ws + L.ss_part);
-      a.rs_out = rs;
+      a.ss_part = ss;
       if ((rc = run_gemm(cx, EPI_RESID, PROF_GEMM_DOWN, Ly.down, d, c.d_ff, ws + L.ffh, a, M, m->ng_down))) return rc;
+      ss_groups = g_resid_down;
     }
   }
   if (logits) {
     GemmArgs a{};
-    a.rs = rs;
+    a.ss_in = ss;
+    a.ss_groups = ss_groups;
+    a.d_in = (int)d;
     a.logits = logits;
     a.V = c.vocab;
     a.amax_v = reinterpret_cast<float*>(ws + L.amax);
     a.amax_i = reinterpret_cast<int*>(ws + L.amax + (size_t)L.max_groups * L.mp * 4);
-    a.argmax_out = argmax;
     if ((rc = run_gemm(cx, EPI_LOGITS, PROF_GEMM_LM, m->off_lm, c.vocab, (int)d, xa, a, M, m->ng_lm))) return rc;
+    if (argmax) {
+      const int G = (int)(c.vocab / 16 / m->ng_lm);
+      prof_begin(PROF_GEMM_LM, cx.st);
+      hipLaunchKernelGGL(row_argmax_kernel, dim3(M), dim3(256), 0, cx.st, a.amax_v, a.amax_i, G, L.mp,
+                         reinterpret_cast<const RowInfo*>(ws + L.rowinfo), argmax);
+      prof_end(PROF_GEMM_LM, cx.st);
+      if ((rc = check_launch("row_argmax_kernel"))) return rc;
+    }
   }
   return SDD_OK;
 }
@@ -1041,7 +1083,7 @@ static int launch_embed(CallCtx& cx, EmbedArgs e, int M) {
   e.g = reinterpret_cast<const float*>(m->base + (c.n_layers > 0 ? m->layers[0].attn_norm : m->off_final_norm));
   e.x = reinterpret_cast<float*>(cx.ws + cx.L.x);
   e.xa = cx.ws + cx.L.xa;
-  e.rs = reinterpret_cast<float*>(cx.ws + cx.L.rs);
+  e.ss = reinterpret_cast<float*>(cx.ws + cx.L.ss_part);
   e.rows = reinterpret_cast<RowInfo*>(cx.ws + cx.L.rowinfo);
   e.d = c.d_model;
   e.V = c.vocab;

@@ -71,7 +71,7 @@ struct RowInfo {
 
 // Per-call workspace carve-up for up to max_rows rows.
 struct WsLayout {
-  size_t rowinfo, x, xa, rs, ss_part, q, ao, ffh, part, cnt, amax, total;
+  size_t rowinfo, x, xa, ss_part, q, ao, ffh, part, cnt, amax, total;
   int mp;         // padded rows
   int max_groups; // column groups of the widest GEMM
   int n_wg;       // GEMM workgroups

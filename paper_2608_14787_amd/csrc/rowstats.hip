@@ -209,37 +209,50 @@ __device__ inline void thread_stats(const uint4* regs, int nv, int base, float z
   }
 }
 
-// Combines the C chunk records of one row in chunk order.
+// Combined statistics of one row.
 struct RowStats {
   float m, s, qm, qs;
   int arg, cnt, flags;
 };
 
-__device__ inline RowStats combine_row(RowRec* rp, int C) {
+// One wave combines the C <= 64 chunk records of a row: lane c loads record c
+// (all loads in flight together), then a fixed butterfly reduces the lanes, so
+// the result is the same in every lane and on every run.
+__device__ inline RowStats combine_row_wave(RowRec* rp, int C, int lane) {
+  const bool have = lane < C;
+  float m = have ? ld_coherent(&rp[lane].m) : -INFINITY;
+  int arg = have ? ld_coherent(&rp[lane].arg) : -1;
+  float sv = have ? ld_coherent(&rp[lane].s) : 0.f;
+  int cnt = have ? ld_coherent(&rp[lane].cnt) : 0;
+  int fl = have ? ld_coherent(&rp[lane].flags) : 0;
+  float qm = have ? ld_coherent(&rp[lane].qm) : -INFINITY;
+  float qs = have ? ld_coherent(&rp[lane].qs) : 0.f;
   RowStats o;
-  o.m = -INFINITY;
-  o.arg = -1;
-  o.cnt = 0;
-  o.flags = 0;
-  o.qm = -INFINITY;
-  for (int c = 0; c < C; ++c) {
-    const float m = ld_coherent(&rp[c].m);
-    const int arg = ld_coherent(&rp[c].arg);
-    if (better(m, arg, o.m, o.arg)) {
-      o.m = m;
-      o.arg = arg;
+  float M = m, QM = qs > 0.f ? qm : -INFINITY;
+  int A = arg;
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) {
+    const float m2 = __shfl_xor(M, off);
+    const int a2 = __shfl_xor(A, off);
+    if (better(m2, a2, M, A)) {
+      M = m2;
+      A = a2;
     }
-    o.cnt += ld_coherent(&rp[c].cnt);
-    o.flags |= ld_coherent(&rp[c].flags);
-    if (ld_coherent(&rp[c].qs) > 0.f) o.qm = fmaxf(o.qm, ld_coherent(&rp[c].qm));
+    QM = fmaxf(QM, __shfl_xor(QM, off));
+    cnt += __shfl_xor(cnt, off);
+    fl |= __shfl_xor(fl, off);
   }
-  o.s = 0.f;
-  o.qs = 0.f;
-  for (int c = 0; c < C; ++c) {
-    const float s = ld_coherent(&rp[c].s), qs = ld_coherent(&rp[c].qs);
-    if (s > 0.f) o.s += s * __expf(ld_coherent(&rp[c].m) - o.m);
-    if (qs > 0.f) o.qs += qs * __expf(ld_coherent(&rp[c].qm) - o.qm);
-  }
+  float s = sv > 0.f ? sv * __expf(m - M) : 0.f;
+  float q = qs > 0.f ? qs * __expf(qm - QM) : 0.f;
+  s = wave_sum(s);
+  q = wave_sum(q);
+  o.m = M;
+  o.arg = A;
+  o.s = s;
+  o.cnt = cnt;
+  o.flags = fl;
+  o.qm = QM;
+  o.qs = q;
   return o;
 }
 
@@ -312,11 +325,12 @@ __global__ void __launch_bounds__(kThreads) rowstats_kernel(Job job) {
   }
   if (!arrive_last(&job.counters[b], job.rows * job.C, &s_last)) return;
 
-  // ---- last workgroup of sequence b: combine and decide ----
-  const int t = threadIdx.x;
+  // ---- last workgroup of sequence b: combine and decide, one wave per row ----
   RowRec* recs = job.recs + (size_t)b * job.rows * job.C;
-  if (t < job.rows) {
-    const RowStats st = combine_row(recs + t * job.C, job.C);
+  const int wv = threadIdx.x / kWave, ln = threadIdx.x % kWave;
+  for (int t = wv; t < job.rows; t += kThreads / kWave) {
+    const RowStats st = combine_row_wave(recs + t * job.C, job.C, ln);
+    if (ln != 0) continue;
     const bool bad = (st.flags & 1) != 0;
     s_arg[t] = st.arg < 0 ? 0 : st.arg;
     s_flag[t] = bad ? 1 : 0;
@@ -368,7 +382,7 @@ __global__ void __launch_bounds__(kThreads) rowstats_kernel(Job job) {
     }
   }
   __syncthreads();
-  if (t == 0) {
+  if (threadIdx.x == 0) {
     if (KIND == kAccept) {
       int L = job.gamma, fl = 0;
       for (int jj = 0; jj < job.gamma; ++jj) {
@@ -411,12 +425,15 @@ int choose_vec(const void* p, size_t seq_stride, size_t row_stride, int V, int e
   return 1;
 }
 
+// Chunks per row: about 2048 workgroups in total, but no chunk smaller than
+// 8192 elements (a workgroup should stream tens of kilobytes) and none larger
+// than the registers of a workgroup hold.
 int chunks_for(int nrows, int V, int vec) {
   const int per_wg_max = kThreads * vec * kMaxVecPerThread;
-  int c = (int)ceil_div(4096, (int64_t)(nrows > 0 ? nrows : 1));  // ~4096 workgroups in total
-  c = max(c, (int)ceil_div(V, per_wg_max));
-  c = min(c, (int)ceil_div(V, kThreads * vec));  // at least one vector per thread
-  return max(c, (int)ceil_div(V, per_wg_max));
+  int c = (int)ceil_div(2048, (int64_t)(nrows > 0 ? nrows : 1));
+  c = min(c, (int)ceil_div(V, 8192));
+  c = min(c, 64);  // one wave combines a row's chunk records, a lane per chunk
+  return max(1, max(c, (int)ceil_div(V, per_wg_max)));
 }
 
 size_t counters_region(int B) { return ((size_t)B * sizeof(int) + 255) / 256 * 256; }
@@ -462,6 +479,7 @@ static int setup_ws(Job& job, void* ws, size_t ws_bytes, int vec) {
   job.C = chunks_for(job.B * job.rows, job.V, vec);
   job.chunk = (int)ceil_div(ceil_div(job.V, job.C), vec) * vec;
   job.C = (int)ceil_div(job.V, job.chunk);
+  if (job.C > 64) return fail(SDD_EUNSUPPORTED, "vocabulary of %d needs %d chunks per row (at most 64)", job.V, job.C);
   size_t need = rowstats_ws(job.B, job.rows, job.V);
   if (ws == nullptr || ws_bytes < need)
     return fail(SDD_ENOMEM, "rowstats workspace needs %zu bytes, got %zu", need, ws_bytes);
