@@ -97,102 +97,148 @@ __device__ inline void store_t(char* base, int64_t idx, float v) {
   reinterpret_cast<T*>(base)[idx] = Elem<T>::from_f32(v);
 }
 
-// owner of unit x: the workgroup whose share [w*U/n, (w+1)*U/n) contains x
-__device__ inline int unit_owner(int64_t x, int64_t U, int n) { return (int)(((x + 1) * n + U - 1) / U - 1); }
-__device__ inline int64_t unit_start(int w, int64_t U, int n) { return (int64_t)w * U / n; }
+// Stream-K bookkeeping in 32-bit unsigned arithmetic (64-bit division is a
+// long software sequence on this GPU); the host guarantees units x workgroups
+// < 2^31.  Workgroup w owns units [w*U/n, (w+1)*U/n); unit_owner(x) is the
+// workgroup whose share contains unit x.
+__device__ inline int unit_owner(uint32_t x, uint32_t U, uint32_t n) { return (int)(((x + 1) * n + U - 1) / U) - 1; }
+__device__ inline uint32_t unit_start(uint32_t w, uint32_t U, uint32_t n) { return w * U / n; }
 
-template <typename T, int NG>
-__device__ void epilogue_qkv(const GemmArgs& a, const float* tile, int g, const float* rsl) {
+// Epilogues run on the final [rows][C] tile of one column group (LDS, row
+// stride C + 4).  Each wave owns rows wave, wave + 4, ...; a row's reductions
+// run over its columns lane, lane + 64 and then across the wave, in an order
+// that does not depend on the number of rows, so a row's result is the same
+// whatever block it is verified in.  Every global load a wave needs is issued
+// before any of them is used.
+template <typename T, int NG, int R>
+__device__ void epilogue_qkv(const GemmArgs& a, const float* tile, int g, const float* rsl, const RowInfo* ri_s) {
   constexpr int C = NG * 16;  // == head_dim
-  const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
-  const int h = g;
-  const bool is_q = h < a.hq, is_k = !is_q && h < a.hq + a.hkv;
-  for (int mm = wave; mm < a.M; mm += kGemmThreads / kWave) {
-    const int m = a.m0 + mm;
-    const RowInfo ri = a.rows[m];
-    if (!ri.valid) continue;
-    const float r = rsl[mm];
-    float y[C / 64 > 0 ? C / 64 : 1];
-    if constexpr (C == 128) {
-      y[0] = tile[mm * C + lane] * r;
-      y[1] = tile[mm * C + lane + 64] * r;
-    } else {
-      y[0] = tile[mm * C + lane] * r;
-    }
-    if (is_q || is_k) {
+  constexpr int CP = C + 4, RPW = R / 4;
+  if constexpr (C == 64 || C == 128) {
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave), lane = threadIdx.x % kWave;
+    const int h = g;
+    const bool is_q = h < a.hq, is_k = !is_q && h < a.hq + a.hkv, rot = is_q || is_k;
+    float gn0 = 1.f, gn1 = 1.f;
+    float2 cs[RPW];
+    if (rot) {
       if (a.qk_norm) {
-        float ss = (C == 128) ? y[0] * y[0] + y[C == 128 ? 1 : 0] * y[C == 128 ? 1 : 0] : y[0] * y[0];
-        ss = wave_sum(ss);
-        const float inv = 1.f / sqrtf(ss / (float)C + a.eps);
-        const float* gn = is_q ? a.qn : a.kn;
-        y[0] *= inv * gn[lane];
-        if constexpr (C == 128) y[1] *= inv * gn[lane + 64];
+        const float* gp = is_q ? a.qn : a.kn;
+        gn0 = gp[lane];
+        if constexpr (C == 128) gn1 = gp[lane + 64];
       }
-      const float* rp = a.rope + (size_t)ri.pos * (C / 2) * 2;
-      if constexpr (C == 128) {
-        const float c = rp[2 * lane], s = rp[2 * lane + 1];
-        const float y0 = y[0], y1 = y[1];
-        y[0] = y0 * c - y1 * s;
-        y[1] = y1 * c + y0 * s;
-      } else {
-        const int i = lane % 32;
-        const float c = rp[2 * i], s = rp[2 * i + 1];
-        const float other = __shfl_xor(y[0], 32);
-        y[0] = lane < 32 ? y[0] * c - other * s : y[0] * c + other * s;
+      // (cos, sin) of each row's position: table [pos][C/2] of float2
+#pragma unroll
+      for (int j = 0; j < RPW; ++j) {
+        const int mm = wave + 4 * j;
+        cs[j] = make_float2(1.f, 0.f);
+        if (mm < a.M && ri_s[mm].valid)
+          cs[j] = reinterpret_cast<const float2*>(a.rope)[(size_t)ri_s[mm].pos * (C / 2) + (C == 128 ? lane : lane % 32)];
       }
     }
-    if (is_q || is_k) {
-      char* dst;
-      int64_t base;
-      if (is_q) {
-        dst = a.q_out;
-        base = ((int64_t)m * a.hq + h) * C;
-      } else {
-        dst = a.kc;
-        base = (((int64_t)ri.seq * a.hkv + (h - a.hq)) * a.max_len + ri.pos) * C;
+#pragma unroll
+    for (int j = 0; j < RPW; ++j) {
+      const int mm = wave + 4 * j;
+      if (mm >= a.M) break;
+      const RowInfo ri = ri_s[mm];
+      if (!ri.valid) continue;
+      const int m = a.m0 + mm;
+      const float r = rsl[mm];
+      float y0 = tile[mm * CP + lane] * r;
+      float y1 = C == 128 ? tile[mm * CP + (lane + 64) % C] * r : 0.f;
+      if (rot) {
+        if (a.qk_norm) {
+          float ss = (C == 128) ? y0 * y0 + y1 * y1 : y0 * y0;
+          ss = wave_sum_fast(ss);
+          const float inv = 1.f / sqrtf(ss / (float)C + a.eps);
+          y0 *= inv * gn0;
+          if constexpr (C == 128) y1 *= inv * gn1;
+        }
+        const float c = cs[j].x, sn = cs[j].y;
+        if constexpr (C == 128) {
+          const float t0 = y0, t1 = y1;
+          y0 = t0 * c - t1 * sn;
+          y1 = t1 * c + t0 * sn;
+        } else {
+          const float other = __shfl_xor(y0, 32);
+          y0 = lane < 32 ? y0 * c - other * sn : y0 * c + other * sn;
+        }
+        char* dst;
+        int64_t base;
+        if (is_q) {
+          dst = a.q_out;
+          base = ((int64_t)m * a.hq + h) * C;
+        } else {
+          dst = a.kc;
+          base = (((int64_t)ri.seq * a.hkv + (h - a.hq)) * a.max_len + ri.pos) * C;
+        }
+        store_t<T>(dst, base + lane, y0);
+        if constexpr (C == 128) store_t<T>(dst, base + lane + 64, y1);
+      } else {  // V cache is transposed: [seq][kv head][dim][position]
+        const int64_t base = ((int64_t)ri.seq * a.hkv + (h - a.hq - a.hkv)) * C;
+        store_t<T>(a.vc, (base + lane) * a.max_len + ri.pos, y0);
+        if constexpr (C == 128) store_t<T>(a.vc, (base + lane + 64) * a.max_len + ri.pos, y1);
       }
-      store_t<T>(dst, base + lane, y[0]);
-      if constexpr (C == 128) store_t<T>(dst, base + lane + 64, y[1]);
-    } else {  // V cache is transposed: [seq][kv head][dim][position]
-      const int64_t base = ((int64_t)ri.seq * a.hkv + (h - a.hq - a.hkv)) * C;
-      store_t<T>(a.vc, (base + lane) * a.max_len + ri.pos, y[0]);
-      if constexpr (C == 128) store_t<T>(a.vc, (base + lane + 64) * a.max_len + ri.pos, y[1]);
     }
   }
 }
 
-template <typename T, int NG>
+template <typename T, int NG, int R>
 __device__ void epilogue_resid(const GemmArgs& a, const float* tile, int g) {
-  constexpr int C = NG * 16;
-  const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
-  for (int mm = wave; mm < a.M; mm += kGemmThreads / kWave) {
+  constexpr int C = NG * 16, CP = C + 4, RPW = R / 4, NCL = (C + kWave - 1) / kWave;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave), lane = threadIdx.x % kWave;
+  float gv[NCL], xo[RPW][NCL];
+#pragma unroll
+  for (int k = 0; k < NCL; ++k) {
+    const int c = lane + k * kWave;
+    gv[k] = c < C ? a.g_next[(int64_t)g * C + c] : 0.f;
+  }
+#pragma unroll
+  for (int j = 0; j < RPW; ++j) {
+    const int mm = wave + 4 * j;
+#pragma unroll
+    for (int k = 0; k < NCL; ++k) {
+      const int c = lane + k * kWave;
+      xo[j][k] = (mm < a.M && c < C) ? a.x[(int64_t)(a.m0 + mm) * a.d + (int64_t)g * C + c] : 0.f;
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < RPW; ++j) {
+    const int mm = wave + 4 * j;
+    if (mm >= a.M) break;
     const int m = a.m0 + mm;
     float ss = 0.f;
-    for (int c = lane; c < C; c += kWave) {
-      const int64_t n = (int64_t)g * C + c;
-      const float xv = a.x[(int64_t)m * a.d + n] + tile[mm * C + c];
-      a.x[(int64_t)m * a.d + n] = xv;
-      store_t<T>(a.xa, (int64_t)m * a.d + n, xv * a.g_next[n]);
-      ss += xv * xv;
+#pragma unroll
+    for (int k = 0; k < NCL; ++k) {
+      const int c = lane + k * kWave;
+      if (c < C) {
+        const int64_t n = (int64_t)g * C + c;
+        const float xv = xo[j][k] + tile[mm * CP + c];
+        a.x[(int64_t)m * a.d + n] = xv;
+        store_t<T>(a.xa, (int64_t)m * a.d + n, xv * gv[k]);
+        ss += xv * xv;
+      }
     }
-    ss = wave_sum(ss);
+    ss = wave_sum_fast(ss);
     if (lane == 0) a.ss_part[(int64_t)g * a.mp + m] = ss;
   }
 }
 
-template <typename T, int NG>
+template <typename T, int NG, int R>
 __device__ void epilogue_swiglu(const GemmArgs& a, const float* tile, int g, const float* rsl) {
-  constexpr int C = NG * 16, P = NG / 2;
-  const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
-  for (int mm = wave; mm < a.M; mm += kGemmThreads / kWave) {
+  constexpr int C = NG * 16, CP = C + 4, P = NG / 2, RPW = R / 4;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave), lane = threadIdx.x % kWave;
+#pragma unroll
+  for (int j = 0; j < RPW; ++j) {
+    const int mm = wave + 4 * j;
+    if (mm >= a.M) break;
     const int m = a.m0 + mm;
     const float r = rsl[mm];
     for (int idx = lane; idx < P * 16; idx += kWave) {
-      const int t = idx / 16, j = idx % 16;
-      const float gt = tile[mm * C + (2 * t) * 16 + j] * r;
-      const float up = tile[mm * C + (2 * t + 1) * 16 + j] * r;
+      const int t = idx / 16, jj = idx % 16;
+      const float gt = tile[mm * CP + (2 * t) * 16 + jj] * r;
+      const float up = tile[mm * CP + (2 * t + 1) * 16 + jj] * r;
       const float hv = gt / (1.f + expf(-gt)) * up;
-      store_t<T>(a.ffh, (int64_t)m * a.dff + ((int64_t)g * P + t) * 16 + j, hv);
+      store_t<T>(a.ffh, (int64_t)m * a.dff + ((int64_t)g * P + t) * 16 + jj, hv);
     }
   }
 }
@@ -203,35 +249,58 @@ __device__ inline bool arg_better(float v2, int i2, float v1, int i1) {
   return v2 > v1 || (v2 == v1 && i2 < i1);
 }
 
-template <int NG>
-__device__ void epilogue_logits(const GemmArgs& a, const float* tile, int g, const float* rsl) {
-  constexpr int C = NG * 16;
-  const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
-  for (int mm = wave; mm < a.M; mm += kGemmThreads / kWave) {
+// Best (value, lowest index) over a fully active wave.  The combine is
+// associative and commutative, so the order of the steps does not matter.
+__device__ inline void wave_argmax(float& bv, int& bi) {
+  auto step = [&](float v2, int i2) {
+    if (arg_better(v2, i2, bv, bi)) {
+      bv = v2;
+      bi = i2;
+    }
+  };
+  step(dpp_f<kDppXor1>(bv), dpp_i<kDppXor1>(bi));
+  step(dpp_f<kDppXor2>(bv), dpp_i<kDppXor2>(bi));
+  step(dpp_f<kDppHalfMirror>(bv), dpp_i<kDppHalfMirror>(bi));
+  step(dpp_f<kDppMirror>(bv), dpp_i<kDppMirror>(bi));
+  float rv = lane_f(bv, 0);
+  int ri = __builtin_amdgcn_readlane(bi, 0);
+#pragma unroll
+  for (int r = 16; r < 64; r += 16) {
+    const float v2 = lane_f(bv, r);
+    const int i2 = __builtin_amdgcn_readlane(bi, r);
+    if (arg_better(v2, i2, rv, ri)) {
+      rv = v2;
+      ri = i2;
+    }
+  }
+  bv = rv;
+  bi = ri;
+}
+
+template <int NG, int R>
+__device__ void epilogue_logits(const GemmArgs& a, const float* tile, int g, const float* rsl, const RowInfo* ri_s) {
+  constexpr int C = NG * 16, CP = C + 4, RPW = R / 4;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave), lane = threadIdx.x % kWave;
+#pragma unroll
+  for (int j = 0; j < RPW; ++j) {
+    const int mm = wave + 4 * j;
+    if (mm >= a.M) break;
     const int m = a.m0 + mm;
-    const RowInfo ri = a.rows[m];
+    const bool valid = ri_s[mm].valid != 0;
     const float r = rsl[mm];
     float bv = -INFINITY;
     int bi = -1;
     for (int c = lane; c < C; c += kWave) {
       const int n = g * C + c;
       if (n >= a.V) break;
-      const float v = tile[mm * C + c] * r;
-      if (ri.valid) a.logits[(int64_t)m * a.V + n] = v;
+      const float v = tile[mm * CP + c] * r;
+      if (valid) a.logits[(int64_t)m * a.V + n] = v;
       if (arg_better(v, n, bv, bi)) {
         bv = v;
         bi = n;
       }
     }
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) {
-      const float v2 = __shfl_xor(bv, o);
-      const int i2 = __shfl_xor(bi, o);
-      if (arg_better(v2, i2, bv, bi)) {
-        bv = v2;
-        bi = i2;
-      }
-    }
+    wave_argmax(bv, bi);
     if (lane == 0) {
       a.amax_v[(int64_t)g * a.mp + m] = bv;
       a.amax_i[(int64_t)g * a.mp + m] = bi;
@@ -271,178 +340,229 @@ __global__ void __launch_bounds__(256) row_argmax_kernel(const float* amax_v, co
 
 template <typename T, int TB, int NG, int EPI>
 __global__ void __launch_bounds__(kGemmThreads, 1) gemm_kernel(GemmArgs a) {
-  constexpr int C = NG * 16;
-  constexpr int NACC = NG * TB;
+  constexpr int C = NG * 16;       // output columns of a column group
+  constexpr int CP = C + 4;        // LDS row stride of the output tile (16-byte row writes hit distinct banks)
+  constexpr int R = TB * 16;       // padded rows of this pass
+  constexpr int NACC = NG * TB;    // 16x16 accumulator tiles per wave
+  constexpr int IPW = (NACC + 3) / 4;
   constexpr int EPL = 16 / sizeof(T);
   constexpr int KTILE = 4 * EPL;
-  // reduction buffer for waves 2,3 (later reused as the output tile)
-  __shared__ f32x4 red[2][NACC][kWave];
-  __shared__ int s_flag;
+  constexpr int EPT = R * C / kGemmThreads;  // tile elements per thread in the cross-workgroup reduction
+  // each wave's accumulators; after the cross-wave sum the same memory holds the output tile [R][CP]
+  __shared__ f32x4 red[4][NACC][kWave];
+  __shared__ RowInfo s_ri[kMaxPassRows];
   __shared__ float s_rs[kMaxPassRows];
-  float* tile = reinterpret_cast<float*>(&red[1][0][0]);
-  static_assert(NACC * kWave * 4 >= TB * 16 * C, "tile must fit the reduction buffer");
+  __shared__ float s_part4[4][kMaxPassRows];
+  __shared__ int s_flag;
+  float* tile = reinterpret_cast<float*>(&red[0][0][0]);
+  static_assert(4 * NACC * kWave * 4 >= R * CP, "tile must fit the reduction buffer");
+  static_assert(R * C % kGemmThreads == 0, "tile elements split evenly over the threads");
 
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave), lane = threadIdx.x % kWave;
-  const int64_t U = (int64_t)a.G * a.KT;
+  const uint32_t KT = (uint32_t)a.KT, U = (uint32_t)a.G * KT;
   const int w = blockIdx.x;
-  const int64_t u0 = unit_start(w, U, a.n_wg), u1 = unit_start(w + 1, U, a.n_wg);
+  const uint32_t u0 = unit_start(w, U, a.n_wg), u1 = unit_start(w + 1, U, a.n_wg);
+  const int g_first = (int)(u0 / KT);
   const uint4* W = reinterpret_cast<const uint4*>(a.W);
   const int MC = a.M * C;
+  const char* Xl = a.X + ((int64_t)(a.m0 + lane % 16) * a.ldx + (lane / 16) * EPL) * sizeof(T);
+  const int64_t xrow16 = (int64_t)16 * a.ldx * sizeof(T);
+
+  uint4 wa0[NG], wa1[NG], wa2[NG], wa3[NG], xb0[TB], xb1[TB], xb2[TB], xb3[TB];
+  // One k-step of column group g: NG contiguous 1 KiB weight tiles and the
+  // TB activation fragments.  Loads are unconditional (kt is clamped to the
+  // wave's last k-tile, so a tail reloads a tile already read) so that the
+  // compiler can wait for exactly the oldest stage.
+  auto load = [&](int g, int kt, int kz, uint4* wa, uint4* xb) {
+    kt = min(kt, kz - 1);
+    const uint4* Wk = W + ((int64_t)g * a.KT + kt) * NG * kWave + lane;
+#pragma unroll
+    for (int nt = 0; nt < NG; ++nt) wa[nt] = load_nt16(Wk + nt * kWave);
+#pragma unroll
+    for (int tb = 0; tb < TB; ++tb) xb[tb] = load16(Xl + tb * xrow16 + (int64_t)kt * KTILE * sizeof(T));
+    // keep the next stages' loads ahead of this stage's MFMAs
+    __builtin_amdgcn_sched_barrier(0);
+  };
+  // A segment is this workgroup's part of one column group: k-tiles [kb, ke);
+  // wave w streams the quarter [ka, kz).
+  struct Seg {
+    int g, kb, ke, ka, kz;
+  };
+  auto make_seg = [&](uint32_t u) {
+    Seg s;
+    s.g = (int)(u / KT);
+    s.kb = (int)(u - (uint32_t)s.g * KT);
+    s.ke = (int)std::min<uint32_t>(KT, s.kb + (u1 - u));
+    const int S = s.ke - s.kb;
+    s.ka = __builtin_amdgcn_readfirstlane(s.kb + S * wave / 4);
+    s.kz = __builtin_amdgcn_readfirstlane(s.kb + S * (wave + 1) / 4);
+    return s;
+  };
+  // the first three pipeline stages of a segment (weights do not depend on
+  // the activations, so they are issued as early as possible)
+  auto prime = [&](const Seg& s) {
+    if (s.ka < s.kz) {
+      load(s.g, s.ka, s.kz, wa0, xb0);
+      load(s.g, s.ka + 1, s.kz, wa1, xb1);
+      load(s.g, s.ka + 2, s.kz, wa2, xb2);
+    }
+  };
+
+  uint32_t u = u0;
+  Seg s = make_seg(u);
+  prime(s);
+
+  if constexpr (EPI == EPI_QKV || EPI == EPI_LOGITS) {
+    if ((int)threadIdx.x < a.M) s_ri[threadIdx.x] = a.rows[a.m0 + threadIdx.x];
+  }
   if constexpr (EPI != EPI_RESID) {
     // RMSNorm row scales of the input rows from the producer's per-group sums
-    // of squares: four threads per row take every fourth group, then the four
-    // partial sums are added in a fixed order.
-    float* part4 = reinterpret_cast<float*>(&red[0][0][0]);  // [4][64]
+    // of squares: four threads per row take every fourth group (in group
+    // order), then the four partial sums are added in a fixed order.
     const int ng_in = a.ss_in ? a.ss_groups : 0;
     const int row = threadIdx.x % kMaxPassRows, q4 = threadIdx.x / kMaxPassRows;
     float ssum = 0.f;
     if (row < a.M) {
-#pragma unroll 4
-      for (int gg = q4; gg < ng_in; gg += 4) ssum += a.ss_in[(int64_t)gg * a.mp + a.m0 + row];
+      for (int g0 = q4; g0 < ng_in; g0 += 64) {
+        float v[16];
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+          const int gg = g0 + 4 * j;
+          v[j] = gg < ng_in ? a.ss_in[(int64_t)gg * a.mp + a.m0 + row] : 0.f;
+        }
+#pragma unroll
+        for (int j = 0; j < 16; ++j)
+          if (g0 + 4 * j < ng_in) ssum += v[j];
+      }
     }
-    part4[q4 * kMaxPassRows + row] = ssum;
+    s_part4[q4][row] = ssum;
     __syncthreads();
     if ((int)threadIdx.x < a.M) {
       const int t = threadIdx.x;
-      const float tot = (part4[t] + part4[kMaxPassRows + t]) + (part4[2 * kMaxPassRows + t] + part4[3 * kMaxPassRows + t]);
+      const float tot = (s_part4[0][t] + s_part4[1][t]) + (s_part4[2][t] + s_part4[3][t]);
       s_rs[t] = ng_in ? 1.f / sqrtf(tot / (float)a.d_in + a.eps) : 1.f;
     }
-    __syncthreads();
   }
+  __syncthreads();
 
-  for (int64_t u = u0; u < u1;) {
-    const int g = (int)(u / a.KT);
-    const int kb = (int)(u % a.KT);
-    const int ke = (int)std::min<int64_t>(a.KT, kb + (u1 - u));
-    const bool full = kb == 0 && ke == a.KT;
-    const int which = (g == (int)(u0 / a.KT)) ? 0 : 1;
-    u += ke - kb;
-
-    // ---- stream this segment: each wave takes a quarter of the k-tiles ----
-    const int S = ke - kb;
-    const int ka = __builtin_amdgcn_readfirstlane(kb + S * wave / 4);
-    const int kz = __builtin_amdgcn_readfirstlane(kb + S * (wave + 1) / 4);
+  for (;;) {
+    // ---- stream this segment: four register stages, three in flight ----
     f32x4 acc[NACC];
 #pragma unroll
     for (int i = 0; i < NACC; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
-    const uint4* Wg = W + (int64_t)g * NG * a.KT * kWave + lane;  // k-step kt: NG contiguous tiles
-    const char* Xl = a.X + ((int64_t)(a.m0 + lane % 16) * a.ldx + (lane / 16) * EPL) * sizeof(T);
-    const int64_t xrow16 = (int64_t)16 * a.ldx * sizeof(T);
-    uint4 wa0[NG], wa1[NG], wa2[NG], wa3[NG], xb0[TB], xb1[TB], xb2[TB], xb3[TB];
-    // Stage loads are unconditional (the k-tile index is clamped to the last
-    // one, so a tail reloads a tile already read) so that the compiler can wait
-    // for exactly the oldest stage.
-    auto load = [&](int kt, uint4* wa, uint4* xb) {
-      kt = min(kt, kz - 1);
-#pragma unroll
-      for (int nt = 0; nt < NG; ++nt) wa[nt] = load_nt16(Wg + ((int64_t)kt * NG + nt) * kWave);
-#pragma unroll
-      for (int tb = 0; tb < TB; ++tb) xb[tb] = load16(Xl + tb * xrow16 + (int64_t)kt * KTILE * sizeof(T));
-      // keep the next stages' loads ahead of this stage's MFMAs
-      __builtin_amdgcn_sched_barrier(0);
-    };
     auto mma = [&](const uint4* wa, const uint4* xb) {
 #pragma unroll
       for (int nt = 0; nt < NG; ++nt)
 #pragma unroll
         for (int tb = 0; tb < TB; ++tb) mma_tile<T>(wa[nt], xb[tb], acc[nt * TB + tb]);
     };
-    // Four register stages, three in flight while one is consumed.
-    int kt = ka;
-    if (kt < kz) {
-      load(kt, wa0, xb0);
-      load(kt + 1, wa1, xb1);
-      load(kt + 2, wa2, xb2);
-      for (; kt + 4 <= kz; kt += 4) {
-        load(kt + 3, wa3, xb3);
+    int kt = s.ka;
+    if (kt < s.kz) {
+      for (; kt + 4 <= s.kz; kt += 4) {
+        load(s.g, kt + 3, s.kz, wa3, xb3);
         mma(wa0, xb0);
-        load(kt + 4, wa0, xb0);
+        load(s.g, kt + 4, s.kz, wa0, xb0);
         mma(wa1, xb1);
-        load(kt + 5, wa1, xb1);
+        load(s.g, kt + 5, s.kz, wa1, xb1);
         mma(wa2, xb2);
-        load(kt + 6, wa2, xb2);
+        load(s.g, kt + 6, s.kz, wa2, xb2);
         mma(wa3, xb3);
       }
       // 0..3 k-tiles left, already loaded in stages 0..2
-      const int left = kz - kt;
+      const int left = s.kz - kt;
       if (left > 0) mma(wa0, xb0);
       if (left > 1) mma(wa1, xb1);
       if (left > 2) mma(wa2, xb2);
     }
+    const int g = s.g;
+    const bool full = s.kb == 0 && s.ke == a.KT;
+    const int which = g == g_first ? 0 : 1;
+    u += s.ke - s.kb;
+    const bool more = u < u1;
 
-    // ---- reduce the four waves: (w0 + w2) + (w1 + w3), fixed order ----
-    __syncthreads();  // previous segment's tile readers are done
-    if (wave >= 2)
+    // ---- sum the four waves, (w0 + w2) + (w1 + w3) per element ----
+    __syncthreads();  // the previous tile's readers are done
 #pragma unroll
-      for (int i = 0; i < NACC; ++i) red[wave - 2][i][lane] = acc[i];
+    for (int i = 0; i < NACC; ++i) red[wave][i][lane] = acc[i];
     __syncthreads();
-    if (wave < 2)
+    f32x4 rs[IPW];
 #pragma unroll
-      for (int i = 0; i < NACC; ++i) acc[i] += red[wave][i][lane];
-    __syncthreads();
-    if (wave == 1)
+    for (int j = 0; j < IPW; ++j) {
+      const int i = wave + 4 * j;
+      if (i < NACC) rs[j] = (red[0][i][lane] + red[2][i][lane]) + (red[1][i][lane] + red[3][i][lane]);
+    }
+    __syncthreads();  // all reads of red done before the tile overwrites it
+    // accumulator tile i = nt*TB + tb, element e: row tb*16 + lane%16, column nt*16 + 4*(lane/16) + e
 #pragma unroll
-      for (int i = 0; i < NACC; ++i) red[0][i][lane] = acc[i];
-    __syncthreads();
-    if (wave == 0) {
-#pragma unroll
-      for (int i = 0; i < NACC; ++i) acc[i] += red[0][i][lane];
-      // acc[nt*TB+tb] element e: row tb*16 + lane%16, column nt*16 + 4*(lane/16) + e
-#pragma unroll
-      for (int nt = 0; nt < NG; ++nt)
-#pragma unroll
-        for (int tb = 0; tb < TB; ++tb)
-#pragma unroll
-          for (int e = 0; e < 4; ++e) tile[(tb * 16 + lane % 16) * C + nt * 16 + 4 * (lane / 16) + e] = acc[nt * TB + tb][e];
+    for (int j = 0; j < IPW; ++j) {
+      const int i = wave + 4 * j;
+      if (i < NACC)
+        *reinterpret_cast<f32x4*>(&tile[((i % TB) * 16 + lane % 16) * CP + (i / TB) * 16 + 4 * (lane / 16)]) = rs[j];
     }
     __syncthreads();
 
+    bool fin = true;
     if (!full) {
-      // ---- split column group: publish the partial, last contributor reduces ----
+      // ---- split column group: publish the partial, the last contributor reduces ----
       float* my = a.part + ((int64_t)w * 2 + which) * MC;
-      for (int i = threadIdx.x; i < MC; i += kGemmThreads) st_coherent(&my[i], tile[i]);
-      const int wf = unit_owner((int64_t)g * a.KT, U, a.n_wg);
-      const int wl = unit_owner((int64_t)(g + 1) * a.KT - 1, U, a.n_wg);
-      if (!arrive_last(&a.cnt[g], wl - wf + 1, &s_flag)) continue;
-      // sum the contributors in workgroup order; each thread keeps its EPT
-      // elements in registers and issues one contributor's loads together
-      constexpr int EPT = TB * 16 * C / kGemmThreads;
-      float sum[EPT];
-#pragma unroll
-      for (int e = 0; e < EPT; ++e) sum[e] = 0.f;
-      for (int ww = wf; ww <= wl; ww += 2) {
-        // two contributors' loads in flight at once; added in workgroup order
-        const bool two = ww + 1 <= wl;
-        const int wh0 = (g == (int)(unit_start(ww, U, a.n_wg) / a.KT)) ? 0 : 1;
-        const int wh1 = two && (g == (int)(unit_start(ww + 1, U, a.n_wg) / a.KT)) ? 0 : 1;
-        float* src0 = a.part + ((int64_t)ww * 2 + wh0) * MC;
-        float* src1 = a.part + ((int64_t)(two ? ww + 1 : ww) * 2 + (two ? wh1 : wh0)) * MC;
-        float v0[EPT], v1[EPT];
-#pragma unroll
-        for (int e = 0; e < EPT; ++e) {
-          const int i = threadIdx.x + e * kGemmThreads;
-          v0[e] = i < MC ? ld_coherent(&src0[i]) : 0.f;
-          v1[e] = (i < MC && two) ? ld_coherent(&src1[i]) : 0.f;
-        }
-#pragma unroll
-        for (int e = 0; e < EPT; ++e) {
-          sum[e] += v0[e];
-          if (two) sum[e] += v1[e];
-        }
-      }
 #pragma unroll
       for (int e = 0; e < EPT; ++e) {
         const int i = threadIdx.x + e * kGemmThreads;
-        if (i < MC) tile[i] = sum[e];
+        if (i < MC) st_coherent(&my[i], tile[(i / C) * CP + i % C]);
       }
-      __syncthreads();
+      const int wf = unit_owner((uint32_t)g * KT, U, a.n_wg);
+      const int wl = unit_owner((uint32_t)(g + 1) * KT - 1, U, a.n_wg);
+      fin = arrive_last(&a.cnt[g], wl - wf + 1, &s_flag);
+      if (fin) {
+        // contributors added in workgroup order; FB contributors' loads in flight at once
+        constexpr int FB = EPT >= 32 ? 2 : EPT >= 16 ? 4 : 8;
+        float sum[EPT];
+#pragma unroll
+        for (int e = 0; e < EPT; ++e) sum[e] = 0.f;
+        for (int ww = wf; ww <= wl; ww += FB) {
+          float v[FB][EPT];
+#pragma unroll
+          for (int q = 0; q < FB; ++q) {
+            const int wq = std::min(ww + q, wl);
+            const int slot = (g == (int)(unit_start(wq, U, a.n_wg) / KT)) ? 0 : 1;
+            const float* src = a.part + ((int64_t)wq * 2 + slot) * MC;
+#pragma unroll
+            for (int e = 0; e < EPT; ++e) {
+              const int i = threadIdx.x + e * kGemmThreads;
+              v[q][e] = (ww + q <= wl && i < MC) ? ld_coherent(const_cast<float*>(&src[i])) : 0.f;
+            }
+          }
+#pragma unroll
+          for (int q = 0; q < FB; ++q)
+            if (ww + q <= wl)
+#pragma unroll
+              for (int e = 0; e < EPT; ++e) sum[e] += v[q][e];
+        }
+#pragma unroll
+        for (int e = 0; e < EPT; ++e) {
+          const int i = threadIdx.x + e * kGemmThreads;
+          if (i < MC) tile[(i / C) * CP + i % C] = sum[e];
+        }
+        __syncthreads();
+      }
     }
 
+    // the next segment's first loads overlap this one's epilogue (only where
+    // workgroups cover several segments and the registers allow it)
+    constexpr bool kPrimeEarly = (EPI == EPI_SWIGLU || EPI == EPI_LOGITS) && TB <= 3;
+    if (more) {
+      s = make_seg(u);
+      if constexpr (kPrimeEarly) prime(s);
+    }
     // ---- epilogue on the final tile of column group g ----
-    if constexpr (EPI == EPI_QKV) epilogue_qkv<T, NG>(a, tile, g, s_rs);
-    if constexpr (EPI == EPI_RESID) epilogue_resid<T, NG>(a, tile, g);
-    if constexpr (EPI == EPI_SWIGLU) epilogue_swiglu<T, NG>(a, tile, g, s_rs);
-    if constexpr (EPI == EPI_LOGITS) epilogue_logits<NG>(a, tile, g, s_rs);
+    if (fin) {
+      if constexpr (EPI == EPI_QKV) epilogue_qkv<T, NG, R>(a, tile, g, s_rs, s_ri);
+      if constexpr (EPI == EPI_RESID) epilogue_resid<T, NG, R>(a, tile, g);
+      if constexpr (EPI == EPI_SWIGLU) epilogue_swiglu<T, NG, R>(a, tile, g, s_rs);
+      if constexpr (EPI == EPI_LOGITS) epilogue_logits<NG, R>(a, tile, g, s_rs, s_ri);
+    }
+    if (!more) break;
+    if constexpr (!kPrimeEarly) prime(s);
   }
 }
 
@@ -914,6 +1034,8 @@ static int run_gemm(CallCtx& cx, int epi, unsigned prof, size_t w_off, int64_t N
   const int64_t U = (int64_t)a.G * a.KT;
   const int nblocks = (int)std::min<int64_t>(U, cx.L.n_wg);
   a.n_wg = nblocks;
+  if ((U + 1) * nblocks >= (int64_t(1) << 31))
+    return fail(SDD_EUNSUPPORTED, "matrix of %lld weight tiles exceeds the 32-bit stream-K bookkeeping", (long long)U);
   for (int m0 = 0; m0 < M; m0 += kMaxPassRows) {
     a.m0 = m0;
     a.M = std::min(kMaxPassRows, M - m0);

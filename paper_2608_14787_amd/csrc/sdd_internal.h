@@ -122,6 +122,35 @@ __device__ inline bool arrive_last(int* cnt, int expected, int* s_flag) {
   return *s_flag != 0;
 }
 
+// Lane permutations inside rows of 16 lanes by DPP (a VALU operand modifier:
+// no LDS round trip, unlike a general shuffle).  The wave must be fully active.
+constexpr int kDppXor1 = 0xB1;        // quad_perm [1,0,3,2]
+constexpr int kDppXor2 = 0x4E;        // quad_perm [2,3,0,1]
+constexpr int kDppHalfMirror = 0x141; // lane i <- lane 7-i within each 8
+constexpr int kDppMirror = 0x140;     // lane i <- lane 15-i within each 16
+template <int CTRL>
+__device__ inline int dpp_i(int v) {
+  return __builtin_amdgcn_update_dpp(0, v, CTRL, 0xF, 0xF, false);
+}
+template <int CTRL>
+__device__ inline float dpp_f(float v) {
+  return __builtin_bit_cast(float, dpp_i<CTRL>(__builtin_bit_cast(int, v)));
+}
+__device__ inline float lane_f(float v, int l) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), l));
+}
+// Sum over a fully active wave, the same value in every lane.  Fixed order:
+// pairs, quads, eights and sixteens inside each row (each step adds two equal
+// partial sums in either operand order, which IEEE addition treats alike),
+// then the four row sums as (r0 + r1) + (r2 + r3).
+__device__ inline float wave_sum_fast(float v) {
+  v += dpp_f<kDppXor1>(v);
+  v += dpp_f<kDppXor2>(v);
+  v += dpp_f<kDppHalfMirror>(v);
+  v += dpp_f<kDppMirror>(v);
+  return (lane_f(v, 0) + lane_f(v, 16)) + (lane_f(v, 32) + lane_f(v, 48));
+}
+
 // wave-level reductions (64 lanes)
 __device__ inline float wave_max(float v) {
 #pragma unroll
