@@ -357,6 +357,7 @@ __global__ void __launch_bounds__(kGemmThreads, 1) gemm_kernel(GemmArgs a) {
   float* tile = reinterpret_cast<float*>(&red[0][0][0]);
   static_assert(4 * NACC * kWave * 4 >= R * CP, "tile must fit the reduction buffer");
   static_assert(R * C % kGemmThreads == 0, "tile elements split evenly over the threads");
+  touch_kernargs<GemmArgs>();
 
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave), lane = threadIdx.x % kWave;
   const uint32_t KT = (uint32_t)a.KT, U = (uint32_t)a.G * KT;
@@ -368,16 +369,14 @@ __global__ void __launch_bounds__(kGemmThreads, 1) gemm_kernel(GemmArgs a) {
   const char* Xl = a.X + ((int64_t)(a.m0 + lane % 16) * a.ldx + (lane / 16) * EPL) * sizeof(T);
   const int64_t xrow16 = (int64_t)16 * a.ldx * sizeof(T);
 
-  uint4 wa0[NG], wa1[NG], wa2[NG], wa3[NG], xb0[TB], xb1[TB], xb2[TB], xb3[TB];
   // One k-step of column group g: NG contiguous 1 KiB weight tiles and the
   // TB activation fragments.  Loads are unconditional (kt is clamped to the
   // wave's last k-tile, so a tail reloads a tile already read) so that the
   // compiler can wait for exactly the oldest stage.
-  auto load = [&](int g, int kt, int kz, uint4* wa, uint4* xb) {
+  auto load = [&](const uint4* Wg, int kt, int kz, uint4* wa, uint4* xb) {
     kt = min(kt, kz - 1);
-    const uint4* Wk = W + ((int64_t)g * a.KT + kt) * NG * kWave + lane;
 #pragma unroll
-    for (int nt = 0; nt < NG; ++nt) wa[nt] = load_nt16(Wk + nt * kWave);
+    for (int nt = 0; nt < NG; ++nt) wa[nt] = load_nt16(Wg + ((int64_t)kt * NG + nt) * kWave);
 #pragma unroll
     for (int tb = 0; tb < TB; ++tb) xb[tb] = load16(Xl + tb * xrow16 + (int64_t)kt * KTILE * sizeof(T));
     // keep the next stages' loads ahead of this stage's MFMAs
@@ -398,20 +397,8 @@ __global__ void __launch_bounds__(kGemmThreads, 1) gemm_kernel(GemmArgs a) {
     s.kz = __builtin_amdgcn_readfirstlane(s.kb + S * (wave + 1) / 4);
     return s;
   };
-  // the first three pipeline stages of a segment (weights do not depend on
-  // the activations, so they are issued as early as possible)
-  auto prime = [&](const Seg& s) {
-    if (s.ka < s.kz) {
-      load(s.g, s.ka, s.kz, wa0, xb0);
-      load(s.g, s.ka + 1, s.kz, wa1, xb1);
-      load(s.g, s.ka + 2, s.kz, wa2, xb2);
-    }
-  };
-
-  uint32_t u = u0;
-  Seg s = make_seg(u);
-  prime(s);
-
+  // Row info and RMSNorm row scales of this pass, used by the epilogues.
+  auto prologue = [&]() {
   if constexpr (EPI == EPI_QKV || EPI == EPI_LOGITS) {
     if ((int)threadIdx.x < a.M) s_ri[threadIdx.x] = a.rows[a.m0 + threadIdx.x];
   }
@@ -443,10 +430,21 @@ __global__ void __launch_bounds__(kGemmThreads, 1) gemm_kernel(GemmArgs a) {
       s_rs[t] = ng_in ? 1.f / sqrtf(tot / (float)a.d_in + a.eps) : 1.f;
     }
   }
-  __syncthreads();
+  };
 
-  for (;;) {
+  uint32_t u = u0;
+  for (bool first = true;; first = false) {
+    const Seg s = make_seg(u);
     // ---- stream this segment: four register stages, three in flight ----
+    uint4 wa0[NG], wa1[NG], wa2[NG], wa3[NG], xb0[TB], xb1[TB], xb2[TB], xb3[TB];
+    const uint4* Wg = W + (int64_t)s.g * NG * a.KT * kWave + lane;  // k-step kt: NG contiguous tiles
+    if (s.ka < s.kz) {
+      load(Wg, s.ka, s.kz, wa0, xb0);
+      load(Wg, s.ka + 1, s.kz, wa1, xb1);
+      load(Wg, s.ka + 2, s.kz, wa2, xb2);
+    }
+    // the prologue's loads queue behind the first weight loads
+    if (first) prologue();
     f32x4 acc[NACC];
 #pragma unroll
     for (int i = 0; i < NACC; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -459,13 +457,13 @@ __global__ void __launch_bounds__(kGemmThreads, 1) gemm_kernel(GemmArgs a) {
     int kt = s.ka;
     if (kt < s.kz) {
       for (; kt + 4 <= s.kz; kt += 4) {
-        load(s.g, kt + 3, s.kz, wa3, xb3);
+        load(Wg, kt + 3, s.kz, wa3, xb3);
         mma(wa0, xb0);
-        load(s.g, kt + 4, s.kz, wa0, xb0);
+        load(Wg, kt + 4, s.kz, wa0, xb0);
         mma(wa1, xb1);
-        load(s.g, kt + 5, s.kz, wa1, xb1);
+        load(Wg, kt + 5, s.kz, wa1, xb1);
         mma(wa2, xb2);
-        load(s.g, kt + 6, s.kz, wa2, xb2);
+        load(Wg, kt + 6, s.kz, wa2, xb2);
         mma(wa3, xb3);
       }
       // 0..3 k-tiles left, already loaded in stages 0..2
@@ -547,13 +545,6 @@ __global__ void __launch_bounds__(kGemmThreads, 1) gemm_kernel(GemmArgs a) {
       }
     }
 
-    // the next segment's first loads overlap this one's epilogue (only where
-    // workgroups cover several segments and the registers allow it)
-    constexpr bool kPrimeEarly = (EPI == EPI_SWIGLU || EPI == EPI_LOGITS) && TB <= 3;
-    if (more) {
-      s = make_seg(u);
-      if constexpr (kPrimeEarly) prime(s);
-    }
     // ---- epilogue on the final tile of column group g ----
     if (fin) {
       if constexpr (EPI == EPI_QKV) epilogue_qkv<T, NG, R>(a, tile, g, s_rs, s_ri);
@@ -562,7 +553,6 @@ __global__ void __launch_bounds__(kGemmThreads, 1) gemm_kernel(GemmArgs a) {
       if constexpr (EPI == EPI_LOGITS) epilogue_logits<NG, R>(a, tile, g, s_rs, s_ri);
     }
     if (!more) break;
-    if constexpr (!kPrimeEarly) prime(s);
   }
 }
 

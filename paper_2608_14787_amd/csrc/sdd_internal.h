@@ -88,17 +88,17 @@ __host__ __device__ inline int64_t ceil_div(int64_t a, int64_t b) { return (a + 
 // Cross-workgroup hand-off without cache-wide fences.  A device-scope fence on
 // this part writes back and invalidates a whole L2 (one per XCD), which costs
 // far more than the few kilobytes handed over.  Instead the published data and
-// the arrival counters use relaxed system-scope accesses, which go to the
-// memory side (coherent for every XCD) and bypass the L2 and L1; a publisher
-// waits for its stores to complete before it arrives, and the last arriver
-// reads the data back with the same coherent loads.
+// the arrival counters use relaxed device-scope atomic accesses, which the
+// compiler maps to accesses coherent across all XCDs of the device; a
+// publisher waits for its stores to complete before it arrives, and the last
+// arriver reads the data back with the same coherent loads.
 template <typename T>
 __device__ inline void st_coherent(T* p, T v) {
-  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 template <typename T>
 __device__ inline T ld_coherent(T* p) {
-  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 // Waits until every memory operation this thread issued has completed.
 __device__ inline void wait_stores() {
@@ -113,13 +113,28 @@ __device__ inline bool arrive_last(int* cnt, int expected, int* s_flag) {
   wait_stores();
   __syncthreads();
   if (threadIdx.x == 0) {
-    const int old = __hip_atomic_fetch_add(cnt, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+    const int old = __hip_atomic_fetch_add(cnt, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     const int last = old == expected - 1;
-    if (last) __hip_atomic_store(cnt, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+    if (last) __hip_atomic_store(cnt, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     *s_flag = last;
   }
   __syncthreads();
   return *s_flag != 0;
+}
+
+// Kernel arguments are read through the scalar cache on first use; a kernel
+// whose argument block spans several 64-byte lines otherwise pays one memory
+// round trip per line, one after another, as the compiler spreads the reads.
+// Touching every line once at entry overlaps those misses.
+template <typename Args>
+__device__ inline void touch_kernargs() {
+  typedef const __attribute__((address_space(4))) int* kernarg_ptr;
+  const kernarg_ptr kp = (kernarg_ptr)__builtin_amdgcn_kernarg_segment_ptr();
+  constexpr int n = (int)sizeof(Args) / 4;
+  int acc = kp[n - 1];
+#pragma unroll
+  for (int i = 0; i < n; i += 16) acc ^= kp[i];
+  asm volatile("" ::"s"(acc));
 }
 
 // Lane permutations inside rows of 16 lanes by DPP (a VALU operand modifier:
