@@ -214,12 +214,13 @@ int sdd_confidence_prefix(const void* logits, int dtype, size_t seq_stride, int 
 #define SDD_PROF_ACCEPT 128u
 #define SDD_PROF_CONF 256u
 
-/* Starts timing: until sdd_profile_stop, each launch of a class in
- * class_mask is bracketed by two HIP events on its own stream (at most
- * max_launches launches are recorded; events are allocated here, on the
- * host thread, not during the launches).  Not thread-safe: one profiling
- * session per process. */
-int sdd_profile_start(unsigned class_mask, int max_launches);
+/* Starts timing: until sdd_profile_stop, every every-th launch (1: each) of
+ * the classes in class_mask is bracketed by two HIP events on its own stream
+ * (at most max_launches launches are recorded; events are allocated here, on
+ * the host thread, not during the launches).  SDD_EINVAL for max_launches
+ * outside [1, 2^20] or every < 1.  Not thread-safe: one profiling session per
+ * process. */
+int sdd_profile_start(unsigned class_mask, int max_launches, int every);
 /* Waits for the recorded events and returns, over the launches of the
  * classes in cls: count, total, min and max duration in ms (min/max may be
  * NULL). */

@@ -60,7 +60,7 @@ struct GemmArgs {
   const float* qn;
   const float* kn;
   const float* rope;
-  int max_len;
+  int kv_ld;  // position stride of the K / V^T caches
   char* kc;
   char* vc;
   // EPI_RESID
@@ -169,14 +169,14 @@ __device__ void epilogue_qkv(const GemmArgs& a, const float* tile, int g, const 
           base = ((int64_t)m * a.hq + h) * C;
         } else {
           dst = a.kc;
-          base = (((int64_t)ri.seq * a.hkv + (h - a.hq)) * a.max_len + ri.pos) * C;
+          base = (((int64_t)ri.seq * a.hkv + (h - a.hq)) * a.kv_ld + ri.pos) * C;
         }
         store_t<T>(dst, base + lane, y0);
         if constexpr (C == 128) store_t<T>(dst, base + lane + 64, y1);
       } else {  // V cache is transposed: [seq][kv head][dim][position]
         const int64_t base = ((int64_t)ri.seq * a.hkv + (h - a.hq - a.hkv)) * C;
-        store_t<T>(a.vc, (base + lane) * a.max_len + ri.pos, y0);
-        if constexpr (C == 128) store_t<T>(a.vc, (base + lane + 64) * a.max_len + ri.pos, y1);
+        store_t<T>(a.vc, (base + lane) * a.kv_ld + ri.pos, y0);
+        if constexpr (C == 128) store_t<T>(a.vc, (base + lane + 64) * a.kv_ld + ri.pos, y1);
       }
     }
   }
@@ -568,7 +568,7 @@ struct AttnArgs {
   const char* vc;
   char* out;      // [rows][hq*hd]
   const RowInfo* rows;
-  int m0, hq, hkv, hd, max_len;
+  int m0, hq, hkv, hd, ld;  // ld: position stride of the caches
   float scale;
 };
 
@@ -591,7 +591,7 @@ __global__ void __launch_bounds__(256) attention_kernel(AttnArgs a) {
   const T* qp = reinterpret_cast<const T*>(a.q) + ((int64_t)m * a.hq + h) * hd;
   for (int d = tid; d < hd; d += 256) qs[d] = Elem<T>::to_f32(qp[d]) * a.scale;
   __syncthreads();
-  const int64_t hb = ((int64_t)ri.seq * a.hkv + kh) * a.max_len;
+  const int64_t hb = ((int64_t)ri.seq * a.hkv + kh) * a.ld;
   const T* K = reinterpret_cast<const T*>(a.kc) + hb * hd;
   const T* Vp = reinterpret_cast<const T*>(a.vc) + hb * hd;
   const int npos = ri.pos + 1;
@@ -630,7 +630,7 @@ __global__ void __launch_bounds__(256) attention_kernel(AttnArgs a) {
     run_m = new_m;
     acc *= alpha;
     if (dsub < nsub)
-      for (int i = dsub; i < n; i += nsub) acc += sc[i] * Elem<T>::to_f32(Vp[(int64_t)dd * a.max_len + p0 + i]);
+      for (int i = dsub; i < n; i += nsub) acc += sc[i] * Elem<T>::to_f32(Vp[(int64_t)dd * a.ld + p0 + i]);
     __syncthreads();
   }
   if (dsub < nsub) acc2[dsub * hd + dd] = acc;
@@ -648,35 +648,34 @@ __global__ void __launch_bounds__(256) attention_kernel(AttnArgs a) {
 // block's rows times the heads that share it (GQA).  The waves split the cache
 // positions into 32-position steps taken round-robin; per step a wave
 // computes S^T = K Q^T with K rows as the MFMA A operand, so each lane ends up
-// holding 8 scores of its own query column, exactly the P^T fragment that
-// O^T = V^T P^T takes as its B operand; V is cached transposed so the A operand
-// is two contiguous 8-byte reads.  The softmax is online within a wave; the
-// waves' partial (max, sum, O) are combined through LDS in wave order.
+// holding scores of its own query column, which is the P^T fragment that
+// O^T = V^T P^T takes as its B operand.  Inside a step the K rows are fed in
+// the order that leaves lane group g (lane / 16) holding the 8 consecutive
+// positions 8g..8g+7, so the matching V^T operand (V is cached transposed) is
+// one 16-byte read per lane.  Each wave keeps two steps of K/V loads in
+// flight.  The softmax is online within a wave; the waves' partial
+// (max, sum, O) are combined through LDS in wave order.
 constexpr int kAttnWaves = 8;
 
 struct AttnMfmaArgs {
   const uint16_t* q;   // [rows][hq][HD]
-  const uint16_t* kc;  // layer base [seq][hkv][max_len][HD]
-  const uint16_t* vc;  // layer base [seq][hkv][HD][max_len]
+  const uint16_t* kc;  // layer base [seq][hkv][ld][HD]
+  const uint16_t* vc;  // layer base [seq][hkv][HD][ld]
   uint16_t* out;       // [rows][hq*HD]
   const RowInfo* rows;
-  int nb, R, hq, hkv, grp, max_len, qblocks;
+  int nb, R, hq, hkv, grp, ld, qblocks;  // ld: position stride of the caches (multiple of 64)
   float scale;
 };
 
-__device__ inline uint2 load4_bf16(const uint16_t* row, int p, int end) {
-  if (p + 3 < end) return *reinterpret_cast<const uint2*>(row + p);
-  uint16_t t[4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i) t[i] = (p + i < end) ? row[p + i] : (uint16_t)0;
-  return make_uint2((uint32_t)t[0] | ((uint32_t)t[1] << 16), (uint32_t)t[2] | ((uint32_t)t[3] << 16));
-}
+// position (within a 32-position step) of MFMA row rho of K sub-tile b
+__device__ inline int attn_pos(int rho, int b) { return 8 * (rho / 4) + 4 * b + rho % 4; }
 
 template <int HD>
 __global__ void __launch_bounds__(kAttnWaves * 64) attention_mfma_kernel(AttnMfmaArgs a) {
   constexpr int KK = HD / 32, DB = HD / 16;
   __shared__ float s_o[kAttnWaves][16][HD + 1];
-  __shared__ float s_m[kAttnWaves][16], s_l[kAttnWaves][16];
+  __shared__ float s_m[kAttnWaves][16], s_l[kAttnWaves][16], s_f[kAttnWaves][16], s_L[16];
+  touch_kernargs<AttnMfmaArgs>();
   const int qb = blockIdx.x, bk = blockIdx.y;
   if (bk >= a.nb * a.hkv || qb >= a.qblocks) return;  // launch larger than the block set
   const int blk = bk / a.hkv, kvh = bk % a.hkv;
@@ -686,70 +685,79 @@ __global__ void __launch_bounds__(kAttnWaves * 64) attention_mfma_kernel(AttnMfm
   const bool qok = qv < QV;
   const int r = qok ? qv / a.grp : 0, hh = qok ? qv % a.grp : 0;
   const int m = blk * a.R + r;
-  const RowInfo first = a.rows[blk * a.R], last = a.rows[blk * a.R + a.R - 1];
-  // positions this query block can see: up to its last row's position
+  // row info and this lane's query are independent loads, issued together
   const int r_hi = min(a.R - 1, (qb * 16 + 15) / a.grp);
-  const int kv_end = __builtin_amdgcn_readfirstlane(first.valid ? a.rows[blk * a.R + r_hi].pos + 1 : 0);
-  (void)last;
+  const RowInfo first = a.rows[blk * a.R];
+  const int pos_hi = a.rows[blk * a.R + r_hi].pos;
   const int qpos = a.rows[m].pos;
-  const int64_t head = (int64_t)first.seq * a.hkv + kvh;
-  const uint16_t* K = a.kc + head * a.max_len * HD;
-  const uint16_t* Vt = a.vc + head * HD * a.max_len;
-
-  uint4 qf[KK];
+  uint4 qf[KK];  // lanes past the last query vector load row 0's (their scores are masked)
   const uint16_t* Q = a.q + ((int64_t)m * a.hq + kvh * a.grp + hh) * HD;
 #pragma unroll
-  for (int kk = 0; kk < KK; ++kk) qf[kk] = qok ? load16(Q + 32 * kk + 8 * (lane / 16)) : make_uint4(0, 0, 0, 0);
+  for (int kk = 0; kk < KK; ++kk) qf[kk] = load16(Q + 32 * kk + 8 * (lane / 16));
+  // positions this query block can see: up to its last row's position
+  const int kv_end = __builtin_amdgcn_readfirstlane(first.valid ? pos_hi + 1 : 0);
+  const int64_t head = (int64_t)first.seq * a.hkv + kvh;
+  const uint16_t* K = a.kc + head * a.ld * HD;
+  const uint16_t* Vt = a.vc + head * HD * a.ld;
+  const int g8 = 8 * (lane / 16);
+
+  // One step's operands: K rows for the two 16-row sub-tiles and the V^T rows
+  // of the lane's 8 positions.  The loads are unconditional, so that a step's
+  // loads stay in flight together: K rows past kv_end are clamped to the last
+  // one (their scores are masked), and V^T values at positions at or past
+  // kv_end are zeroed after the load (a V^T read starts at a multiple of 8
+  // below kv_end <= ld, a multiple of 64, so it stays inside its row).
+  struct StepRegs {
+    uint4 kf[2][KK];
+    uint4 vf[DB];
+  };
+  auto load_step = [&](int p, StepRegs& st) {
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+      const int kp = min(p + attn_pos(lane % 16, b), kv_end - 1);
+#pragma unroll
+      for (int kk = 0; kk < KK; ++kk) st.kf[b][kk] = load16(K + (int64_t)kp * HD + 32 * kk + g8);
+    }
+    const int vp = p + g8;
+    const int nv = kv_end - vp;  // valid positions of the lane's 8 (may be <= 0 or >= 8)
+    uint32_t mask[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) mask[i] = (2 * i < nv ? 0xFFFFu : 0u) | (2 * i + 1 < nv ? 0xFFFF0000u : 0u);
+#pragma unroll
+    for (int db = 0; db < DB; ++db) {
+      const uint4 v = load16(Vt + (int64_t)(16 * db + lane % 16) * a.ld + vp);
+      st.vf[db] = make_uint4(v.x & mask[0], v.y & mask[1], v.z & mask[2], v.w & mask[3]);
+    }
+  };
 
   f32x4 o[DB];
 #pragma unroll
   for (int db = 0; db < DB; ++db) o[db] = f32x4{0.f, 0.f, 0.f, 0.f};
   float mrun = -INFINITY, lrun = 0.f;
-  const int g4 = 4 * (lane / 16);
-  // Fixed assignment of 32-position steps to waves (step t to wave t % waves),
-  // independent of the other rows of the block: a row's result does not
-  // depend on how rows are batched, so a block verify reproduces decode steps
-  // bit for bit.  Steps past a row's own position are fully masked and leave
-  // its running state unchanged.
-  for (int p = 32 * wave; p < kv_end; p += 32 * kAttnWaves) {
-    uint4 kf[2][KK];
-#pragma unroll
-    for (int b = 0; b < 2; ++b) {
-      const int kp = p + 16 * b + lane % 16;
-#pragma unroll
-      for (int kk = 0; kk < KK; ++kk)
-        kf[b][kk] = kp < kv_end ? load16(K + (int64_t)kp * HD + 32 * kk + 8 * (lane / 16)) : make_uint4(0, 0, 0, 0);
-    }
-    uint4 vf[DB];
-#pragma unroll
-    for (int db = 0; db < DB; ++db) {
-      const uint16_t* vrow = Vt + (int64_t)(16 * db + lane % 16) * a.max_len;
-      const uint2 v0 = load4_bf16(vrow, p + g4, kv_end), v1 = load4_bf16(vrow, p + 16 + g4, kv_end);
-      vf[db] = make_uint4(v0.x, v0.y, v1.x, v1.y);
-    }
+  auto step = [&](int p, const StepRegs& st) {
     f32x4 sacc[2];
 #pragma unroll
     for (int b = 0; b < 2; ++b) {
       sacc[b] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int kk = 0; kk < KK; ++kk)
-        sacc[b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kf[b][kk]),
+        sacc[b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, st.kf[b][kk]),
                                                           __builtin_bit_cast(bf16x8, qf[kk]), sacc[b], 0, 0, 0);
     }
-    // sacc[b][i]: position p + 16 b + g4 + i, query column lane % 16
+    // sacc[b][i]: position p + g8 + 4 b + i, query column lane % 16
     float sv[8];
     float mloc = -INFINITY;
 #pragma unroll
     for (int b = 0; b < 2; ++b)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const int kp = p + 16 * b + g4 + i;
+        const int kp = p + g8 + 4 * b + i;
         const float v = (qok && kp <= qpos && kp < kv_end) ? sacc[b][i] * a.scale : -INFINITY;
         sv[b * 4 + i] = v;
         mloc = fmaxf(mloc, v);
       }
-    mloc = fmaxf(mloc, __shfl_xor(mloc, 16));
-    mloc = fmaxf(mloc, __shfl_xor(mloc, 32));
+    mloc = xor16_op(mloc, [](float x, float y) { return fmaxf(x, y); });
+    mloc = xor32_op(mloc, [](float x, float y) { return fmaxf(x, y); });
     const float mnew = fmaxf(mrun, mloc);
     const float alpha = mrun == -INFINITY ? 0.f : __expf(mrun - mnew);
     float lsum = 0.f;
@@ -767,41 +775,66 @@ __global__ void __launch_bounds__(kAttnWaves * 64) attention_mfma_kernel(AttnMfm
 #pragma unroll
     for (int db = 0; db < DB; ++db) {
       o[db] *= alpha;
-      o[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, vf[db]), __builtin_bit_cast(bf16x8, pf),
+      o[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, st.vf[db]), __builtin_bit_cast(bf16x8, pf),
                                                       o[db], 0, 0, 0);
     }
+  };
+  // Fixed assignment of 32-position steps to waves (step t to wave t % waves),
+  // independent of the other rows of the block: a row's result does not
+  // depend on how rows are batched, so a block verify reproduces decode steps
+  // bit for bit.  Steps past a row's own position are fully masked and leave
+  // its running state unchanged.
+  constexpr int kStride = 32 * kAttnWaves;
+  StepRegs s0, s1;
+  int p = 32 * wave;
+  if (p < kv_end) load_step(p, s0);
+  if (p + kStride < kv_end) load_step(p + kStride, s1);
+  for (; p < kv_end; p += 2 * kStride) {
+    step(p, s0);
+    if (p + 2 * kStride < kv_end) load_step(p + 2 * kStride, s0);
+    if (p + kStride >= kv_end) break;
+    step(p + kStride, s1);
+    if (p + 3 * kStride < kv_end) load_step(p + 3 * kStride, s1);
   }
   // softmax denominator of query lane%16 over this wave's positions
-  float ltot = lrun + __shfl_xor(lrun, 16);
-  ltot += __shfl_xor(ltot, 32);
-  // publish the wave's partial to LDS: o[db][i] is O^T[16 db + g4 + i][query lane%16]
+  float ltot = xor16_op(lrun, [](float x, float y) { return x + y; });
+  ltot = xor32_op(ltot, [](float x, float y) { return x + y; });
+  // publish the wave's partial to LDS: o[db][i] is O^T[16 db + 4 (lane / 16) + i][query lane%16]
 #pragma unroll
   for (int db = 0; db < DB; ++db)
 #pragma unroll
-    for (int i = 0; i < 4; ++i) s_o[wave][lane % 16][16 * db + g4 + i] = o[db][i];
+    for (int i = 0; i < 4; ++i) s_o[wave][lane % 16][16 * db + 4 * (lane / 16) + i] = o[db][i];
   if (lane < 16) {
     s_m[wave][lane] = mrun;
     s_l[wave][lane] = ltot;
   }
   __syncthreads();
-  // combine the waves in wave order
+  // per query: the common max, each wave's rescale factor and the total sum,
+  // all accumulated in wave order
+  if (threadIdx.x < 16) {
+    const int q = threadIdx.x;
+    float M = -INFINITY;
+#pragma unroll
+    for (int w = 0; w < kAttnWaves; ++w) M = fmaxf(M, s_m[w][q]);
+    float L = 0.f;
+#pragma unroll
+    for (int w = 0; w < kAttnWaves; ++w) {
+      const float ms = s_m[w][q];
+      const float f = (M == -INFINITY || ms == -INFINITY) ? 0.f : __expf(ms - M);
+      s_f[w][q] = f;
+      L += s_l[w][q] * f;
+    }
+    s_L[q] = L;
+  }
+  __syncthreads();
   for (int e = threadIdx.x; e < 16 * HD; e += kAttnWaves * 64) {
     const int q = e / HD, dim = e % HD;
     const int qq = qb * 16 + q;
     if (qq >= QV) continue;
-    float M = -INFINITY;
+    float O = 0.f;
 #pragma unroll
-    for (int w = 0; w < kAttnWaves; ++w) M = fmaxf(M, s_m[w][q]);
-    float L = 0.f, O = 0.f;
-    if (M != -INFINITY) {
-#pragma unroll
-      for (int w = 0; w < kAttnWaves; ++w) {
-        const float ms = s_m[w][q];
-        const float f = ms == -INFINITY ? 0.f : __expf(ms - M);
-        L += s_l[w][q] * f;
-        O += s_o[w][q][dim] * f;
-      }
-    }
+    for (int w = 0; w < kAttnWaves; ++w) O += s_o[w][q][dim] * s_f[w][q];
+    const float L = s_L[q];
     const int rr = qq / a.grp, hq2 = kvh * a.grp + qq % a.grp;
     a.out[((int64_t)(blk * a.R + rr) * a.hq + hq2) * HD + dim] = f32_to_bf16(L > 0.f ? O / L : 0.f);
   }
@@ -1085,7 +1118,7 @@ static int forward_rows(CallCtx& cx, int nb, int R, float* logits, int32_t* argm
       a.qn = reinterpret_cast<const float*>(m->base + Ly.q_norm);
       a.kn = reinterpret_cast<const float*>(m->base + Ly.k_norm);
       a.rope = kv->rope;
-      a.max_len = kv->max_len;
+      a.kv_ld = kv->ld;
       a.kc = kv->k + (size_t)l * kv->layer_stride;
       a.vc = kv->v + (size_t)l * kv->layer_stride;
       if ((rc = run_gemm(cx, EPI_QKV, PROF_GEMM_QKV, Ly.qkv, hq + 2 * hk, (int)d, xa, a, M, m->ng_qkv))) return rc;
@@ -1103,7 +1136,7 @@ static int forward_rows(CallCtx& cx, int nb, int R, float* logits, int32_t* argm
       a.hq = c.n_q_heads;
       a.hkv = c.n_kv_heads;
       a.grp = c.n_q_heads / c.n_kv_heads;
-      a.max_len = kv->max_len;
+      a.ld = kv->ld;
       a.qblocks = (int)ceil_div((int64_t)R * a.grp, 16);
       a.scale = 1.f / sqrtf((float)c.head_dim);
       const dim3 grid(a.qblocks, nb * a.hkv);
@@ -1125,7 +1158,7 @@ static int forward_rows(CallCtx& cx, int nb, int R, float* logits, int32_t* argm
       a.hq = c.n_q_heads;
       a.hkv = c.n_kv_heads;
       a.hd = c.head_dim;
-      a.max_len = kv->max_len;
+      a.ld = kv->ld;
       a.scale = 1.f / sqrtf((float)c.head_dim);
       prof_begin(PROF_ATTN, cx.st);
       hipLaunchKernelGGL(attention_kernel<float>, dim3(M, c.n_q_heads), dim3(256), 0, cx.st, a);
@@ -1222,7 +1255,7 @@ extern "C" int sdd_kv_bytes(const sdd_model_config* cfg, int max_batch, int max_
   const int es = cfg->dtype == SDD_BF16 ? 2 : 4;
   size_t hdr = align_up((size_t)(2 * max_batch + 1) * 4, 256);
   size_t rope = align_up((size_t)max_len * cfg->head_dim * 4, 256);
-  size_t per_layer = align_up((size_t)max_batch * cfg->n_kv_heads * max_len * cfg->head_dim * es, 256);
+  size_t per_layer = align_up((size_t)max_batch * cfg->n_kv_heads * kv_ld(max_len) * cfg->head_dim * es, 256);
   *bytes = hdr + rope + 2 * per_layer * (size_t)std::max(1, cfg->n_layers);
   return SDD_OK;
 }
@@ -1249,7 +1282,8 @@ extern "C" int sdd_kv_create(sdd_model* m, int max_batch, int max_len, void* buf
   size_t hdr = align_up((size_t)(2 * max_batch + 1) * 4, 256);
   kv->rope = reinterpret_cast<float*>(kv->base + hdr);
   size_t rope = align_up((size_t)max_len * c.head_dim * 4, 256);
-  kv->layer_stride = align_up((size_t)max_batch * c.n_kv_heads * max_len * c.head_dim * m->es, 256);
+  kv->ld = kv_ld(max_len);
+  kv->layer_stride = align_up((size_t)max_batch * c.n_kv_heads * kv->ld * c.head_dim * m->es, 256);
   kv->k = kv->base + hdr + rope;
   kv->v = kv->k + kv->layer_stride * (size_t)std::max(1, c.n_layers);
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);

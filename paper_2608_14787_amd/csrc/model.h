@@ -34,16 +34,21 @@ struct sdd_model {
 struct sdd_kv {
   sdd_model* m;
   int max_batch, max_len;
+  int ld;            // position stride of the caches: max_len rounded up to 64 (128-byte V^T rows)
   char* base;
   size_t bytes;
   int32_t* len;      // [max_batch]
   int32_t* pending;  // [max_batch]
   int32_t* err;      // sticky error bits
   float* rope;       // [max_len][head_dim/2][2] (cos, sin)
-  char* k;           // [layers][max_batch][n_kv_heads][max_len][head_dim]
-  char* v;               // [layers][max_batch][n_kv_heads][head_dim][max_len] (transposed)
+  char* k;           // [layers][max_batch][n_kv_heads][ld][head_dim]
+  char* v;           // [layers][max_batch][n_kv_heads][head_dim][ld] (transposed)
   size_t layer_stride;  // bytes per layer of k (and of v)
 };
+
+namespace sdd {
+inline int kv_ld(int max_len) { return (max_len + 63) / 64 * 64; }
+}  // namespace sdd
 
 namespace sdd {
 

@@ -1,6 +1,8 @@
-// Launch timing for benchmarks: while enabled, launches of the selected kernel
-// classes are bracketed with HIP events on their own stream.  Single-threaded
-// use; the events are recorded into a fixed pool allocated at start.
+// Launch timing for benchmarks: while enabled, every n-th launch of the
+// selected kernel classes is bracketed with HIP events on its own stream (an
+// event pair costs a few microseconds of stream time, so sampling keeps the
+// timed work close to the untimed one).  Single-threaded use; the events are
+// recorded into a fixed pool allocated at start.
 #include <vector>
 
 #include "sdd_internal.h"
@@ -12,6 +14,8 @@ struct Rec {
   hipEvent_t a, b;
 };
 unsigned g_mask = 0;
+int g_every = 1;
+long long g_seen = 0;
 std::vector<hipEvent_t> g_pool;
 std::vector<Rec> g_recs;
 size_t g_next = 0;
@@ -21,6 +25,7 @@ Rec g_cur;
 
 void prof_begin(unsigned cls, hipStream_t st) {
   if (!(g_mask & cls) || g_next + 2 > g_pool.size()) return;
+  if (g_seen++ % g_every) return;
   g_cur.cls = cls;
   g_cur.a = g_pool[g_next++];
   g_cur.b = g_pool[g_next++];
@@ -38,8 +43,11 @@ void prof_end(unsigned cls, hipStream_t st) {
 
 using namespace sdd;
 
-extern "C" int sdd_profile_start(unsigned class_mask, int max_launches) {
+extern "C" int sdd_profile_start(unsigned class_mask, int max_launches, int every) {
   SDD_REQUIRE(max_launches > 0 && max_launches <= (1 << 20), "bad max_launches");
+  SDD_REQUIRE(every >= 1, "bad sampling interval");
+  g_every = every;
+  g_seen = 0;
   for (hipEvent_t e : g_pool) (void)hipEventDestroy(e);
   g_pool.clear();
   g_recs.clear();

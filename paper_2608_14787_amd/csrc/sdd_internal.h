@@ -154,6 +154,33 @@ __device__ inline float dpp_f(float v) {
 __device__ inline float lane_f(float v, int l) {
   return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), l));
 }
+// op(v[l], v[l ^ 16]) and op(v[l], v[l ^ 32]) in every lane of a fully active
+// wave, by the gfx950 row-swap permutes (no LDS round trip).  With a copy of
+// v in both registers, v_permlane16_swap leaves each lane holding its own
+// row pair's two values (lower row in the first register) and
+// v_permlane32_swap likewise for the two halves, so a commutative op gives
+// the butterfly's value in every lane.  Written as inline assembly with both
+// registers as in/out operands (the compiler's builtins fold the two results
+// into one); the nops cover the permute's VALU read/write hazards.
+__device__ inline void permlane16_swap(unsigned& a, unsigned& b) {
+  asm volatile("s_nop 1\n\tv_permlane16_swap_b32 %0, %1\n\ts_nop 1" : "+v"(a), "+v"(b));
+}
+__device__ inline void permlane32_swap(unsigned& a, unsigned& b) {
+  asm volatile("s_nop 1\n\tv_permlane32_swap_b32 %0, %1\n\ts_nop 1" : "+v"(a), "+v"(b));
+}
+template <typename Op>
+__device__ inline float xor16_op(float v, Op op) {
+  unsigned a = __builtin_bit_cast(unsigned, v), b = a;
+  permlane16_swap(a, b);
+  return op(__builtin_bit_cast(float, a), __builtin_bit_cast(float, b));
+}
+template <typename Op>
+__device__ inline float xor32_op(float v, Op op) {
+  unsigned a = __builtin_bit_cast(unsigned, v), b = a;
+  permlane32_swap(a, b);
+  return op(__builtin_bit_cast(float, a), __builtin_bit_cast(float, b));
+}
+
 // Sum over a fully active wave, the same value in every lane.  Fixed order:
 // pairs, quads, eights and sixteens inside each row (each step adds two equal
 // partial sums in either operand order, which IEEE addition treats alike),

@@ -64,7 +64,7 @@ _SIGS = {
     "sdd_rowstats_workspace_bytes": (I, [I, I, I, P]),
     "sdd_accept": (I, [P, P, I, P, I, SZ, P, I, I, I, I, I, F, P, P, P, P, SZ, P]),
     "sdd_confidence_prefix": (I, [P, I, SZ, I, I, I, F, P, P, P, P, P, SZ, P]),
-    "sdd_profile_start": (I, [C.c_uint, I]),
+    "sdd_profile_start": (I, [C.c_uint, I, I]),
     "sdd_profile_read": (I, [C.c_uint, P, P, P, P]),
     "sdd_profile_stop": (I, []),
 }
@@ -172,9 +172,9 @@ def confidence_prefix(logits: torch.Tensor, gamma: int, tau: float, *, draft=Non
     return sk, (lc[:, :gamma] if lc is not None else None), (lp[:, :gamma] if lp is not None else None)
 
 
-def profile_start(class_mask: int, max_launches: int = 65536):
-    """Brackets launches of the given kernel classes with HIP events until profile_stop()."""
-    _check(lib().sdd_profile_start(class_mask, max_launches))
+def profile_start(class_mask: int, max_launches: int = 65536, every: int = 1):
+    """Brackets every `every`-th launch of the given kernel classes with HIP events until profile_stop()."""
+    _check(lib().sdd_profile_start(class_mask, max_launches, every))
 
 
 def profile_read(cls: int):

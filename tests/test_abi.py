@@ -47,6 +47,17 @@ def test_host_side_argument_errors(S):
     assert L.sdd_weights_bytes(C.byref(bad), C.byref(out)) == S.EUNSUPPORTED
     bad = S.ModelConfig(2, 256, 5, 2, 64, 688, 4096, 1e-6, 1e4, 0, S.F32)
     assert L.sdd_weights_bytes(C.byref(bad), C.byref(out)) == S.EINVAL
+    # KV cache: the position stride is max_len rounded up to 64, so 1..64 positions size alike
+    kv1, kv64, kv65 = C.c_size_t(), C.c_size_t(), C.c_size_t()
+    assert L.sdd_kv_bytes(C.byref(cfg), 1, 1, C.byref(kv1)) == S.OK
+    assert L.sdd_kv_bytes(C.byref(cfg), 1, 64, C.byref(kv64)) == S.OK
+    assert L.sdd_kv_bytes(C.byref(cfg), 1, 65, C.byref(kv65)) == S.OK
+    rope = lambda n: -(-n * 64 * 4 // 256) * 256  # [max_len][head_dim] fp32 (cos, sin) table
+    per_layer64 = 1 * 2 * 64 * 64 * 4  # [batch][kv heads][64 positions][head_dim] fp32, for K and for V
+    assert kv64.value - kv1.value == rope(64) - rope(1)
+    assert kv65.value - kv64.value == rope(65) - rope(64) + 2 * 2 * per_layer64
+    # profiling: the sampling interval must be positive
+    assert L.sdd_profile_start(1, 16, 0) == S.EINVAL
     # accept: NULL required pointers, bad mode parameters, bad shapes
     P = C.c_void_p(16)
     args = lambda **kw: [kw.get("draft", P), kw.get("p", P), S.BF16, None, S.BF16, 0, None, kw.get("B", 2),
