@@ -34,6 +34,33 @@ HBM_PEAK_GBS = 8000.0  # MI355X HBM3E
 TAU = 0.7
 
 
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gateup_gemm_qwen32b_hbm_traffic.txt")
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2608_14787_amd", "csrc", f) for f in ("decoder.hip", "sdd_internal.h", "model.h")]
+
+
+def measured_traffic():
+    """HBM bytes per launch of the gate/up kernel at 33 rows from the committed rocprofv3 counter summary,
+    or None when the kernel sources have changed since the counters were taken."""
+    import hashlib
+    try:
+        text = open(TRAFFIC_FILE).read()
+    except OSError:
+        return None
+    vals = {}
+    for line in text.splitlines():
+        parts = line.split()
+        if len(parts) == 3 and parts[0] == "traffic_bytes_per_launch":
+            vals[parts[1]] = float(parts[2])
+        elif len(parts) == 2 and parts[0] == "kernel_source_sha256":
+            vals["sha256"] = parts[1]
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        h.update(open(f, "rb").read())
+    if vals.get("sha256") != h.hexdigest():
+        return None
+    return vals.get("gateup_33rows")
+
+
 def parse():
     p = argparse.ArgumentParser()
     p.add_argument("--gpus", type=int, default=1)
@@ -43,6 +70,9 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--drafts", default="greedy", choices=["greedy", "random"])
     p.add_argument("--all-kernels", action="store_true", help="report every kernel class (extra pass)")
+    p.add_argument("--copy-calibration", action="store_true",
+                   help="only run a plain 1 GiB device copy: the reference kernel whose rocprofv3 FETCH_SIZE / "
+                        "WRITE_SIZE readings scale the verify kernels' counters to bytes")
     return p.parse_args()
 
 
@@ -97,6 +127,15 @@ def main():
         raise SystemExit("libsdd.so is not built: run `python __graft_entry__.py` first")
     torch.cuda.set_device(0)
     assert sdd.device_ok(), "needs a gfx950 GPU"
+    if a.copy_calibration:
+        n = 1 << 30
+        src = torch.ones(n // 4, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes_read": n, "copy_bytes_written": n, "launches": 3}))
+        return
 
     shape, P, gamma = SHAPES[a.workload]
     V = shape.vocab
@@ -218,7 +257,8 @@ def main():
         "call_bytes": call_bytes,
         "roofline": {"bound": "hbm", "kernel": "gemm_kernel gate/up (SwiGLU epilogue)",
                      "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
-                     "traffic": None, "bytes_per_launch": gu_bytes, "launches": n_dom,
+                     "traffic": measured_traffic() if a.workload == "qwen32b" else None,
+                     "traffic_source": os.path.relpath(TRAFFIC_FILE, ROOT), "bytes_per_launch": gu_bytes, "launches": n_dom,
                      "avg_ms": dom_ms, "min_ms": mn_dom, "max_ms": mx_dom},
     }
     if a.all_kernels:
