@@ -24,6 +24,7 @@
 // K-range is split between workgroups is reduced by its last-arriving
 // contributor, which sums the partials in a fixed order (deterministic).
 #include <algorithm>
+#include <type_traits>
 #include <cmath>
 #include <new>
 
@@ -110,73 +111,102 @@ __device__ inline uint32_t unit_start(uint32_t w, uint32_t U, uint32_t n) { retu
 // that does not depend on the number of rows, so a row's result is the same
 // whatever block it is verified in.  Every global load a wave needs is issued
 // before any of them is used.
+// Epilogues run on the final [rows][C] tile of one column group (LDS, row
+// stride C + 4).  Each wave owns rows wave, wave + 4, ... (R / 4 of them, the
+// padded ones included: their results are computed and not stored), so the
+// rows' work is straight-line code that the compiler interleaves.  A row's
+// reductions run over its columns lane, lane + 64 and then across the wave,
+// in an order that does not depend on the number of rows, so a row's result
+// is the same whatever block it is verified in (floating-point contraction is
+// off here, so that the compiler cannot fuse a row's operations differently in
+// instantiations for different row counts).  Every global load a wave needs is
+// issued before any of them is used.
 template <typename T, int NG, int R>
 __device__ void epilogue_qkv(const GemmArgs& a, const float* tile, int g, const float* rsl, const RowInfo* ri_s) {
+  // no contraction: every instantiation (row count) must round each row alike
+#pragma clang fp contract(off)
   constexpr int C = NG * 16;  // == head_dim
   constexpr int CP = C + 4, RPW = R / 4;
   if constexpr (C == 64 || C == 128) {
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave), lane = threadIdx.x % kWave;
     const int h = g;
-    const bool is_q = h < a.hq, is_k = !is_q && h < a.hq + a.hkv, rot = is_q || is_k;
-    float gn0 = 1.f, gn1 = 1.f;
-    float2 cs[RPW];
-    if (rot) {
-      if (a.qk_norm) {
-        const float* gp = is_q ? a.qn : a.kn;
-        gn0 = gp[lane];
-        if constexpr (C == 128) gn1 = gp[lane + 64];
+    const bool is_q = h < a.hq, is_k = !is_q && h < a.hq + a.hkv;
+    if (!is_q && !is_k) {
+      // V head: lane = row, so that each cached dimension's consecutive
+      // positions are written together (V is cached transposed)
+      const int mm = lane;
+      const bool ok = mm < a.M && ri_s[mm < a.M ? mm : 0].valid;
+      const RowInfo ri = ri_s[mm < a.M ? mm : 0];
+      const float r = rsl[mm < a.M ? mm : 0];
+      const int64_t base = ((int64_t)ri.seq * a.hkv + (h - a.hq - a.hkv)) * C;
+      constexpr int DPW = C / 4;  // dimensions per wave
+#pragma unroll 8
+      for (int dd = 0; dd < DPW; ++dd) {
+        const int dim = wave * DPW + dd;
+        const float y = tile[(mm < R ? mm : 0) * CP + dim] * r;
+        if (ok) store_t<T>(a.vc, (base + dim) * a.kv_ld + ri.pos, y);
       }
-      // (cos, sin) of each row's position: table [pos][C/2] of float2
+      return;
+    }
+    float gn0 = 1.f, gn1 = 1.f;
+    if (a.qk_norm) {
+      const float* gp = is_q ? a.qn : a.kn;
+      gn0 = gp[lane];
+      if constexpr (C == 128) gn1 = gp[lane + 64];
+    }
+    // (cos, sin) of each row's position: table [pos][C/2] of float2
+    float2 cs[RPW];
+    float y0[RPW], y1[RPW];
+#pragma unroll
+    for (int j = 0; j < RPW; ++j) {
+      const int mm = wave + 4 * j;
+      const int mc = mm < a.M ? mm : 0;
+      const RowInfo ri = ri_s[mc];
+      cs[j] = reinterpret_cast<const float2*>(a.rope)[(size_t)(ri.valid ? ri.pos : 0) * (C / 2) + (C == 128 ? lane : lane % 32)];
+      const float r = rsl[mc];
+      y0[j] = tile[mm * CP + lane] * r;
+      y1[j] = C == 128 ? tile[mm * CP + (lane + 64) % C] * r : 0.f;
+    }
+    if (a.qk_norm) {
+      float ss[RPW];
+#pragma unroll
+      for (int j = 0; j < RPW; ++j) ss[j] = (C == 128) ? y0[j] * y0[j] + y1[j] * y1[j] : y0[j] * y0[j];
+      wave_sum_fast_n(ss);
 #pragma unroll
       for (int j = 0; j < RPW; ++j) {
-        const int mm = wave + 4 * j;
-        cs[j] = make_float2(1.f, 0.f);
-        if (mm < a.M && ri_s[mm].valid)
-          cs[j] = reinterpret_cast<const float2*>(a.rope)[(size_t)ri_s[mm].pos * (C / 2) + (C == 128 ? lane : lane % 32)];
+        const float inv = 1.f / sqrtf(ss[j] / (float)C + a.eps);
+        y0[j] *= inv * gn0;
+        if constexpr (C == 128) y1[j] *= inv * gn1;
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < RPW; ++j) {
+      const float c = cs[j].x, sn = cs[j].y;
+      if constexpr (C == 128) {
+        const float t0 = y0[j], t1 = y1[j];
+        y0[j] = t0 * c - t1 * sn;
+        y1[j] = t1 * c + t0 * sn;
+      } else {
+        const float other = __shfl_xor(y0[j], 32);
+        y0[j] = lane < 32 ? y0[j] * c - other * sn : y0[j] * c + other * sn;
       }
     }
 #pragma unroll
     for (int j = 0; j < RPW; ++j) {
       const int mm = wave + 4 * j;
-      if (mm >= a.M) break;
-      const RowInfo ri = ri_s[mm];
-      if (!ri.valid) continue;
-      const int m = a.m0 + mm;
-      const float r = rsl[mm];
-      float y0 = tile[mm * CP + lane] * r;
-      float y1 = C == 128 ? tile[mm * CP + (lane + 64) % C] * r : 0.f;
-      if (rot) {
-        if (a.qk_norm) {
-          float ss = (C == 128) ? y0 * y0 + y1 * y1 : y0 * y0;
-          ss = wave_sum_fast(ss);
-          const float inv = 1.f / sqrtf(ss / (float)C + a.eps);
-          y0 *= inv * gn0;
-          if constexpr (C == 128) y1 *= inv * gn1;
-        }
-        const float c = cs[j].x, sn = cs[j].y;
-        if constexpr (C == 128) {
-          const float t0 = y0, t1 = y1;
-          y0 = t0 * c - t1 * sn;
-          y1 = t1 * c + t0 * sn;
-        } else {
-          const float other = __shfl_xor(y0, 32);
-          y0 = lane < 32 ? y0 * c - other * sn : y0 * c + other * sn;
-        }
+      if (mm < a.M && ri_s[mm].valid) {
+        const RowInfo ri = ri_s[mm];
         char* dst;
         int64_t base;
         if (is_q) {
           dst = a.q_out;
-          base = ((int64_t)m * a.hq + h) * C;
+          base = ((int64_t)(a.m0 + mm) * a.hq + h) * C;
         } else {
           dst = a.kc;
           base = (((int64_t)ri.seq * a.hkv + (h - a.hq)) * a.kv_ld + ri.pos) * C;
         }
-        store_t<T>(dst, base + lane, y0);
-        if constexpr (C == 128) store_t<T>(dst, base + lane + 64, y1);
-      } else {  // V cache is transposed: [seq][kv head][dim][position]
-        const int64_t base = ((int64_t)ri.seq * a.hkv + (h - a.hq - a.hkv)) * C;
-        store_t<T>(a.vc, (base + lane) * a.kv_ld + ri.pos, y0);
-        if constexpr (C == 128) store_t<T>(a.vc, (base + lane + 64) * a.kv_ld + ri.pos, y1);
+        store_t<T>(dst, base + lane, y0[j]);
+        if constexpr (C == 128) store_t<T>(dst, base + lane + 64, y1[j]);
       }
     }
   }
@@ -184,9 +214,11 @@ __device__ void epilogue_qkv(const GemmArgs& a, const float* tile, int g, const 
 
 template <typename T, int NG, int R>
 __device__ void epilogue_resid(const GemmArgs& a, const float* tile, int g) {
+  // no contraction: every instantiation (row count) must round each row alike
+#pragma clang fp contract(off)
   constexpr int C = NG * 16, CP = C + 4, RPW = R / 4, NCL = (C + kWave - 1) / kWave;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave), lane = threadIdx.x % kWave;
-  float gv[NCL], xo[RPW][NCL];
+  float gv[NCL], xv[RPW][NCL], ss[RPW];
 #pragma unroll
   for (int k = 0; k < NCL; ++k) {
     const int c = lane + k * kWave;
@@ -198,47 +230,66 @@ __device__ void epilogue_resid(const GemmArgs& a, const float* tile, int g) {
 #pragma unroll
     for (int k = 0; k < NCL; ++k) {
       const int c = lane + k * kWave;
-      xo[j][k] = (mm < a.M && c < C) ? a.x[(int64_t)(a.m0 + mm) * a.d + (int64_t)g * C + c] : 0.f;
+      xv[j][k] = (mm < a.M && c < C) ? a.x[(int64_t)(a.m0 + mm) * a.d + (int64_t)g * C + c] : 0.f;
     }
   }
 #pragma unroll
   for (int j = 0; j < RPW; ++j) {
     const int mm = wave + 4 * j;
-    if (mm >= a.M) break;
-    const int m = a.m0 + mm;
-    float ss = 0.f;
+    ss[j] = 0.f;
 #pragma unroll
     for (int k = 0; k < NCL; ++k) {
       const int c = lane + k * kWave;
       if (c < C) {
-        const int64_t n = (int64_t)g * C + c;
-        const float xv = xo[j][k] + tile[mm * CP + c];
-        a.x[(int64_t)m * a.d + n] = xv;
-        store_t<T>(a.xa, (int64_t)m * a.d + n, xv * gv[k]);
-        ss += xv * xv;
+        xv[j][k] += tile[mm * CP + c];
+        ss[j] += xv[j][k] * xv[j][k];
       }
     }
-    ss = wave_sum_fast(ss);
-    if (lane == 0) a.ss_part[(int64_t)g * a.mp + m] = ss;
+  }
+  wave_sum_fast_n(ss);
+#pragma unroll
+  for (int j = 0; j < RPW; ++j) {
+    const int mm = wave + 4 * j;
+    if (mm < a.M) {
+      const int m = a.m0 + mm;
+#pragma unroll
+      for (int k = 0; k < NCL; ++k) {
+        const int c = lane + k * kWave;
+        if (c < C) {
+          const int64_t n = (int64_t)g * C + c;
+          a.x[(int64_t)m * a.d + n] = xv[j][k];
+          store_t<T>(a.xa, (int64_t)m * a.d + n, xv[j][k] * gv[k]);
+        }
+      }
+      if (lane == 0) a.ss_part[(int64_t)g * a.mp + m] = ss[j];
+    }
   }
 }
 
 template <typename T, int NG, int R>
 __device__ void epilogue_swiglu(const GemmArgs& a, const float* tile, int g, const float* rsl) {
+  // no contraction: every instantiation (row count) must round each row alike
+#pragma clang fp contract(off)
   constexpr int C = NG * 16, CP = C + 4, P = NG / 2, RPW = R / 4;
+  constexpr int NI = (P * 16 + kWave - 1) / kWave;  // gate/up pairs per lane and row
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave), lane = threadIdx.x % kWave;
 #pragma unroll
   for (int j = 0; j < RPW; ++j) {
     const int mm = wave + 4 * j;
-    if (mm >= a.M) break;
-    const int m = a.m0 + mm;
-    const float r = rsl[mm];
-    for (int idx = lane; idx < P * 16; idx += kWave) {
-      const int t = idx / 16, jj = idx % 16;
-      const float gt = tile[mm * CP + (2 * t) * 16 + jj] * r;
-      const float up = tile[mm * CP + (2 * t + 1) * 16 + jj] * r;
-      const float hv = gt / (1.f + expf(-gt)) * up;
-      store_t<T>(a.ffh, (int64_t)m * a.dff + ((int64_t)g * P + t) * 16 + jj, hv);
+    if (mm < a.M) {
+      const int m = a.m0 + mm;
+      const float r = rsl[mm];
+#pragma unroll
+      for (int i = 0; i < NI; ++i) {
+        const int idx = lane + i * kWave;
+        if (idx < P * 16) {
+          const int t = idx / 16, jj = idx % 16;
+          const float gt = tile[mm * CP + (2 * t) * 16 + jj] * r;
+          const float up = tile[mm * CP + (2 * t + 1) * 16 + jj] * r;
+          const float hv = gt / (1.f + expf(-gt)) * up;
+          store_t<T>(a.ffh, (int64_t)m * a.dff + ((int64_t)g * P + t) * 16 + jj, hv);
+        }
+      }
     }
   }
 }
@@ -277,33 +328,86 @@ __device__ inline void wave_argmax(float& bv, int& bi) {
   bi = ri;
 }
 
+// wave_argmax of N independent (value, index) pairs at once
+template <int N>
+__device__ inline void wave_argmax_n(float (&bv)[N], int (&bi)[N]) {
+  auto step = [&](auto ctrl) {
+    constexpr int CTRL = decltype(ctrl)::value;
+#pragma unroll
+    for (int j = 0; j < N; ++j) {
+      const float v2 = dpp_f<CTRL>(bv[j]);
+      const int i2 = dpp_i<CTRL>(bi[j]);
+      if (arg_better(v2, i2, bv[j], bi[j])) {
+        bv[j] = v2;
+        bi[j] = i2;
+      }
+    }
+  };
+  step(std::integral_constant<int, kDppXor1>{});
+  step(std::integral_constant<int, kDppXor2>{});
+  step(std::integral_constant<int, kDppHalfMirror>{});
+  step(std::integral_constant<int, kDppMirror>{});
+#pragma unroll
+  for (int j = 0; j < N; ++j) {
+    float rv = lane_f(bv[j], 0);
+    int ri = __builtin_amdgcn_readlane(bi[j], 0);
+#pragma unroll
+    for (int r = 16; r < 64; r += 16) {
+      const float v2 = lane_f(bv[j], r);
+      const int i2 = __builtin_amdgcn_readlane(bi[j], r);
+      if (arg_better(v2, i2, rv, ri)) {
+        rv = v2;
+        ri = i2;
+      }
+    }
+    bv[j] = rv;
+    bi[j] = ri;
+  }
+}
+
 template <int NG, int R>
 __device__ void epilogue_logits(const GemmArgs& a, const float* tile, int g, const float* rsl, const RowInfo* ri_s) {
-  constexpr int C = NG * 16, CP = C + 4, RPW = R / 4;
+  // no contraction: every instantiation (row count) must round each row alike
+#pragma clang fp contract(off)
+  constexpr int C = NG * 16, CP = C + 4, RPW = R / 4, NCL = (C + kWave - 1) / kWave;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave), lane = threadIdx.x % kWave;
+  float v[RPW][NCL], bv[RPW];
+  int bi[RPW];
 #pragma unroll
   for (int j = 0; j < RPW; ++j) {
     const int mm = wave + 4 * j;
-    if (mm >= a.M) break;
-    const int m = a.m0 + mm;
-    const bool valid = ri_s[mm].valid != 0;
-    const float r = rsl[mm];
-    float bv = -INFINITY;
-    int bi = -1;
-    for (int c = lane; c < C; c += kWave) {
-      const int n = g * C + c;
-      if (n >= a.V) break;
-      const float v = tile[mm * CP + c] * r;
-      if (valid) a.logits[(int64_t)m * a.V + n] = v;
-      if (arg_better(v, n, bv, bi)) {
-        bv = v;
-        bi = n;
+    const float r = rsl[mm < a.M ? mm : 0];
+    bv[j] = -INFINITY;
+    bi[j] = -1;
+#pragma unroll
+    for (int k = 0; k < NCL; ++k) {
+      const int c = lane + k * kWave, n = g * C + c;
+      v[j][k] = c < C ? tile[mm * CP + c] * r : 0.f;
+      if (c < C && n < a.V && arg_better(v[j][k], n, bv[j], bi[j])) {
+        bv[j] = v[j][k];
+        bi[j] = n;
       }
     }
-    wave_argmax(bv, bi);
-    if (lane == 0) {
-      a.amax_v[(int64_t)g * a.mp + m] = bv;
-      a.amax_i[(int64_t)g * a.mp + m] = bi;
+  }
+#pragma unroll
+  for (int j = 0; j < RPW; ++j) {
+    const int mm = wave + 4 * j;
+    if (mm < a.M && ri_s[mm].valid) {
+      const int64_t row = (int64_t)(a.m0 + mm) * a.V;
+#pragma unroll
+      for (int k = 0; k < NCL; ++k) {
+        const int c = lane + k * kWave, n = g * C + c;
+        if (c < C && n < a.V) a.logits[row + n] = v[j][k];
+      }
+    }
+  }
+  wave_argmax_n(bv, bi);
+#pragma unroll
+  for (int j = 0; j < RPW; ++j) {
+    const int mm = wave + 4 * j;
+    if (mm < a.M && lane == 0) {
+      a.amax_v[(int64_t)g * a.mp + a.m0 + mm] = bv[j];
+      a.amax_i[(int64_t)g * a.mp + a.m0 + mm] = bi[j];
     }
   }
 }
@@ -347,7 +451,7 @@ __global__ void __launch_bounds__(kGemmThreads, 1) gemm_kernel(GemmArgs a) {
   constexpr int IPW = (NACC + 3) / 4;
   constexpr int EPL = 16 / sizeof(T);
   constexpr int KTILE = 4 * EPL;
-  constexpr int EPT = R * C / kGemmThreads;  // tile elements per thread in the cross-workgroup reduction
+  constexpr int EPT4 = (R * C / 4 + kGemmThreads - 1) / kGemmThreads;  // tile float4s per thread (cross-workgroup reduction)
   // each wave's accumulators; after the cross-wave sum the same memory holds the output tile [R][CP]
   __shared__ f32x4 red[4][NACC][kWave];
   __shared__ RowInfo s_ri[kMaxPassRows];
@@ -356,7 +460,6 @@ __global__ void __launch_bounds__(kGemmThreads, 1) gemm_kernel(GemmArgs a) {
   __shared__ int s_flag;
   float* tile = reinterpret_cast<float*>(&red[0][0][0]);
   static_assert(4 * NACC * kWave * 4 >= R * CP, "tile must fit the reduction buffer");
-  static_assert(R * C % kGemmThreads == 0, "tile elements split evenly over the threads");
   touch_kernargs<GemmArgs>();
 
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave), lane = threadIdx.x % kWave;
@@ -502,44 +605,56 @@ __global__ void __launch_bounds__(kGemmThreads, 1) gemm_kernel(GemmArgs a) {
     bool fin = true;
     if (!full) {
       // ---- split column group: publish the partial, the last contributor reduces ----
-      float* my = a.part + ((int64_t)w * 2 + which) * MC;
+      // Partials move as 16-byte device-coherent (sc1) buffer accesses: thread t
+      // owns the float4s t, t + 256, ... of the [M][C] partial (C is a multiple of
+      // 4, so a float4 never straddles a row).
+      const __amdgpu_buffer_rsrc_t prs = __builtin_amdgcn_make_buffer_rsrc(a.part, 0, 0x7fffffff, kBufferRsrcWord3);
+      const int my_off = ((w * 2 + which) * MC) * 4;  // byte offset of this partial (< 2^31: the buffer is 16 MiB)
+      f32x4 pv[EPT4];  // all tile reads first: the stores would otherwise wait on each
 #pragma unroll
-      for (int e = 0; e < EPT; ++e) {
-        const int i = threadIdx.x + e * kGemmThreads;
-        if (i < MC) st_coherent(&my[i], tile[(i / C) * CP + i % C]);
+      for (int e = 0; e < EPT4; ++e) {
+        const int i = 4 * (threadIdx.x + e * kGemmThreads);
+        pv[e] = i < R * C ? *reinterpret_cast<const f32x4*>(&tile[(i / C) * CP + i % C]) : f32x4{0.f, 0.f, 0.f, 0.f};
+      }
+#pragma unroll
+      for (int e = 0; e < EPT4; ++e) {
+        const int i = 4 * (threadIdx.x + e * kGemmThreads);
+        if (i < MC) __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, pv[e]), prs, my_off + 4 * i, 0, kCoherentCpol);
       }
       const int wf = unit_owner((uint32_t)g * KT, U, a.n_wg);
       const int wl = unit_owner((uint32_t)(g + 1) * KT - 1, U, a.n_wg);
       fin = arrive_last(&a.cnt[g], wl - wf + 1, &s_flag);
       if (fin) {
         // contributors added in workgroup order; FB contributors' loads in flight at once
-        constexpr int FB = EPT >= 32 ? 2 : EPT >= 16 ? 4 : 8;
-        float sum[EPT];
+        constexpr int FB = EPT4 >= 8 ? 2 : EPT4 >= 4 ? 4 : 8;
+        f32x4 sum[EPT4];
 #pragma unroll
-        for (int e = 0; e < EPT; ++e) sum[e] = 0.f;
+        for (int e = 0; e < EPT4; ++e) sum[e] = f32x4{0.f, 0.f, 0.f, 0.f};
         for (int ww = wf; ww <= wl; ww += FB) {
-          float v[FB][EPT];
+          f32x4 v[FB][EPT4];
 #pragma unroll
           for (int q = 0; q < FB; ++q) {
             const int wq = std::min(ww + q, wl);
             const int slot = (g == (int)(unit_start(wq, U, a.n_wg) / KT)) ? 0 : 1;
-            const float* src = a.part + ((int64_t)wq * 2 + slot) * MC;
+            const int src_off = ((wq * 2 + slot) * MC) * 4;
 #pragma unroll
-            for (int e = 0; e < EPT; ++e) {
-              const int i = threadIdx.x + e * kGemmThreads;
-              v[q][e] = (ww + q <= wl && i < MC) ? ld_coherent(const_cast<float*>(&src[i])) : 0.f;
+            for (int e = 0; e < EPT4; ++e) {
+              const int i = 4 * (threadIdx.x + e * kGemmThreads);
+              v[q][e] = (ww + q <= wl && i < MC)
+                            ? __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(prs, src_off + 4 * i, 0, kCoherentCpol))
+                            : f32x4{0.f, 0.f, 0.f, 0.f};
             }
           }
 #pragma unroll
           for (int q = 0; q < FB; ++q)
             if (ww + q <= wl)
 #pragma unroll
-              for (int e = 0; e < EPT; ++e) sum[e] += v[q][e];
+              for (int e = 0; e < EPT4; ++e) sum[e] += v[q][e];
         }
 #pragma unroll
-        for (int e = 0; e < EPT; ++e) {
-          const int i = threadIdx.x + e * kGemmThreads;
-          if (i < MC) tile[(i / C) * CP + i % C] = sum[e];
+        for (int e = 0; e < EPT4; ++e) {
+          const int i = 4 * (threadIdx.x + e * kGemmThreads);
+          if (i < MC) *reinterpret_cast<f32x4*>(&tile[(i / C) * CP + i % C]) = sum[e];
         }
         __syncthreads();
       }

@@ -100,6 +100,12 @@ template <typename T>
 __device__ inline T ld_coherent(T* p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
+// Raw buffer accesses with the device-coherent cache policy (sc1, the bits the
+// compiler uses for device-scope atomic loads and stores): 16 bytes at a time
+// where the relaxed atomics above move 4.  Descriptor word 3 of an untyped
+// buffer on this GPU family.
+constexpr int kBufferRsrcWord3 = 0x00020000;
+constexpr int kCoherentCpol = 16;  // sc1
 // Waits until every memory operation this thread issued has completed.
 __device__ inline void wait_stores() {
   __atomic_signal_fence(__ATOMIC_SEQ_CST);
@@ -191,6 +197,22 @@ __device__ inline float wave_sum_fast(float v) {
   v += dpp_f<kDppHalfMirror>(v);
   v += dpp_f<kDppMirror>(v);
   return (lane_f(v, 0) + lane_f(v, 16)) + (lane_f(v, 32) + lane_f(v, 48));
+}
+
+// wave_sum_fast of N independent values at once (the DPP steps of the N sums
+// interleave); each result is bit-identical to wave_sum_fast of that value.
+template <int N>
+__device__ inline void wave_sum_fast_n(float (&v)[N]) {
+#pragma unroll
+  for (int j = 0; j < N; ++j) v[j] += dpp_f<kDppXor1>(v[j]);
+#pragma unroll
+  for (int j = 0; j < N; ++j) v[j] += dpp_f<kDppXor2>(v[j]);
+#pragma unroll
+  for (int j = 0; j < N; ++j) v[j] += dpp_f<kDppHalfMirror>(v[j]);
+#pragma unroll
+  for (int j = 0; j < N; ++j) v[j] += dpp_f<kDppMirror>(v[j]);
+#pragma unroll
+  for (int j = 0; j < N; ++j) v[j] = (lane_f(v[j], 0) + lane_f(v[j], 16)) + (lane_f(v[j], 32) + lane_f(v[j], 48));
 }
 
 // wave-level reductions (64 lanes)
