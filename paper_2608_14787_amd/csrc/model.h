@@ -54,11 +54,11 @@ namespace sdd {
 
 __host__ __device__ inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
-// Row tiles per column group: the largest of 8, 4, 2 dividing the tile count
-// (even for the gate/up interleave, which pairs tiles).
-inline int pick_ng(int64_t ntiles, bool pairs) {
+// Row tiles per column group: the largest of 8, 4, 2 (at most max_ng) dividing
+// the tile count (even for the gate/up interleave, which pairs tiles).
+inline int pick_ng(int64_t ntiles, bool pairs, int max_ng = 8) {
   for (int ng : {8, 4, 2})
-    if (ntiles % ng == 0 && (!pairs || ng % 2 == 0)) return ng;
+    if (ng <= max_ng && ntiles % ng == 0 && (!pairs || ng % 2 == 0)) return ng;
   return pairs ? 2 : 1;
 }
 

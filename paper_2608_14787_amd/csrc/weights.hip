@@ -151,7 +151,12 @@ static size_t plan_weights(const sdd_model_config* c, sdd_model* m) {
     m->off_lm = lm;
     m->off_final_norm = fn;
     m->ng_qkv = (int)(hd / 16);
-    m->ng_o = pick_ng(d / 16, false);
+    // o_proj has few output columns and a long K, so 128-column groups would
+    // each be split over ~6 workgroups' equal shares; 64-column groups halve
+    // the contributors a split group's last workgroup reduces.  (down_proj
+    // streams 3x the bytes and keeps 128-column groups: their 8 KiB k-steps
+    // keep more bytes in flight per wave.)
+    m->ng_o = pick_ng(d / 16, false, 4);
     m->ng_gu = pick_ng(2 * (int64_t)c->d_ff / 16, true);
     m->ng_down = pick_ng(d / 16, false);
     m->ng_lm = pick_ng(c->vocab / 16, false);
