@@ -771,6 +771,7 @@ __global__ void __launch_bounds__(256) attention_kernel(AttnArgs a) {
 // flight.  The softmax is online within a wave; the waves' partial
 // (max, sum, O) are combined through LDS in wave order.
 constexpr int kAttnWaves = 8;
+constexpr int kXcds = 8;  // XCDs of the MI355X (32 CUs each)
 
 struct AttnMfmaArgs {
   const uint16_t* q;   // [rows][hq][HD]
@@ -791,8 +792,12 @@ __global__ void __launch_bounds__(kAttnWaves * 64) attention_mfma_kernel(AttnMfm
   __shared__ float s_o[kAttnWaves][16][HD + 1];
   __shared__ float s_m[kAttnWaves][16], s_l[kAttnWaves][16], s_f[kAttnWaves][16], s_L[16];
   touch_kernargs<AttnMfmaArgs>();
-  const int qb = blockIdx.x, bk = blockIdx.y;
-  if (bk >= a.nb * a.hkv || qb >= a.qblocks) return;  // launch larger than the block set
+  // Workgroups are dispatched to the XCDs round-robin by linear id; all query
+  // blocks of one (sequence, KV head) get ids of one residue mod kXcds, so they
+  // run on one XCD and share its L2 copy of that head's K/V.
+  const int xcd = blockIdx.x % kXcds, slot = blockIdx.x / kXcds;
+  const int bk = xcd + kXcds * (slot / a.qblocks), qb = slot % a.qblocks;
+  if (bk >= a.nb * a.hkv) return;  // launch larger than the block set
   const int blk = bk / a.hkv, kvh = bk % a.hkv;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave), lane = threadIdx.x % kWave;
   const int QV = a.R * a.grp;
@@ -1254,7 +1259,7 @@ static int forward_rows(CallCtx& cx, int nb, int R, float* logits, int32_t* argm
       a.ld = kv->ld;
       a.qblocks = (int)ceil_div((int64_t)R * a.grp, 16);
       a.scale = 1.f / sqrtf((float)c.head_dim);
-      const dim3 grid(a.qblocks, nb * a.hkv);
+      const dim3 grid(kXcds * a.qblocks * (int)ceil_div((int64_t)nb * a.hkv, kXcds));
       prof_begin(PROF_ATTN, cx.st);
       if (c.head_dim == 128)
         hipLaunchKernelGGL(attention_mfma_kernel<128>, grid, dim3(kAttnWaves * 64), 0, cx.st, a);
