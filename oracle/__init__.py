@@ -61,6 +61,8 @@ def lib():
                                  C.c_int, C.c_double, P, P, P, P, P]
         L.orc_confidence_prefix.argtypes = [P, C.c_size_t, C.c_int, C.c_int, C.c_int, C.c_double,
                                             P, P, P, P]
+        L.orc_schedule.argtypes = [P, P, C.c_int, C.c_int, C.c_int, C.c_double, C.c_double, C.c_int, C.c_int,
+                                   C.c_int, P, C.c_int, C.c_int, P, P, P, P]
         _lib = L
     return _lib
 
@@ -229,3 +231,28 @@ def confidence_prefix(logits, gamma: int, tau: float, draft=None):
     if lp is not None:
         out["log_p_draft"] = lp[:, :gamma]
     return out
+
+
+# skip scheduler (Sec. 4.1 - 4.2)
+SIG_RAW, SIG_MARGINAL, SIG_CONDITIONAL = 0, 1, 2
+R_SKIP, R_STALE, R_NO_CANDIDATE, R_SHORT, R_SHORT_BLOCK, R_SPECIAL, R_REPEAT = range(7)
+
+
+def schedule(log_q, D, signal: int, eta_b: float, eta_c: float, k_min: int = 0, s_max: int = 1 << 30,
+             block_len=None, draft=None, special=(), rep_max: int = 0):
+    """Two-gate skip decision per sequence.  log_q [B, gamma] fp32 position log-scores; D [B] unverified
+    tokens since the last verifier call (returned updated).  Returns dict K, K_hat, reason, D."""
+    lq = np.ascontiguousarray(log_q, np.float32)
+    B, gamma = lq.shape
+    d = np.ascontiguousarray(np.asarray(D, np.int32).reshape(B)).copy()
+    K = np.empty(B, np.int32)
+    Kh = np.empty(B, np.int32)
+    rs = np.empty(B, np.int32)
+    dr = None if draft is None else np.ascontiguousarray(np.asarray(draft, np.int32).reshape(B, gamma))
+    sp = np.ascontiguousarray(np.asarray(special, np.int32).reshape(-1)) if len(special) else None
+    rc = lib().orc_schedule(_p(lq), _p(dr), B, gamma, int(signal), float(eta_b), float(eta_c), int(k_min),
+                            int(s_max), gamma if block_len is None else int(block_len), _p(sp),
+                            0 if sp is None else sp.size, int(rep_max), _p(d), _p(K), _p(Kh), _p(rs))
+    if rc != 0:
+        raise ValueError("invalid schedule arguments")
+    return dict(K=K, K_hat=Kh, reason=rs, D=d)

@@ -22,6 +22,9 @@
  *   - raw confidence q_j = max softmax and the local gate B_k = min_{j<=k} q_j
  *     with K = max{k : B_k >= tau} (Sec. 4.1 candidate skip length, Sec. 4.2
  *     raw confidence).
+ *   - the two-gate skip scheduler with its three confidence signals, the
+ *     guards and the staleness counter D (Sec. 4.1 candidate skip length and
+ *     commit rule, Sec. 4.2 signals, Appendix "Baselines and Sweep Settings").
  */
 #include "sdd_oracle.h"
 
@@ -706,6 +709,61 @@ int orc_confidence_prefix(const float* logits, size_t seq_stride, int B, int gam
       if (K == gamma && !((float)lc >= log_tau32)) K = j;
     }
     skip_len[b] = K;
+  }
+  return 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Skip scheduler (Sec. 4.1 - 4.2) */
+
+static float log_threshold(double eta) { return eta > 0.0 ? (float)log(eta) : -INFINITY; }
+
+int orc_schedule(const float* log_q, const int32_t* draft, int B, int gamma, int signal, double eta_b,
+                 double eta_c, int k_min, int s_max, int block_len, const int32_t* special, int n_special,
+                 int rep_max, int32_t* D, int32_t* K, int32_t* K_hat, int32_t* reason) {
+  if (!log_q || !D || !K || B <= 0 || gamma < 0 || gamma > 64 || signal < 0 || signal > 2 || isnan(eta_b) ||
+      isnan(eta_c) || n_special < 0 || (n_special > 0 && !special) || ((n_special > 0 || rep_max >= 2) && !draft))
+    return -1;
+  const float lb = log_threshold(eta_b), lc = log_threshold(eta_c);
+  for (int b = 0; b < B; ++b) {
+    const float* lq = log_q + (size_t)b * gamma;
+    /* Eq. (candidate skip length): the largest k whose prefix passes both gates */
+    int khat = 0;
+    float Bk = INFINITY, S = 0.0f;
+    for (int k = 1; k <= gamma; ++k) {
+      const float x = lq[k - 1];
+      if (isnan(x) || x == INFINITY) break; /* invalid score: no longer prefix passes */
+      Bk = x < Bk ? x : Bk;
+      S = S + x;
+      float C;
+      if (signal == ORC_SIG_RAW) C = S / (float)k;
+      else if (signal == ORC_SIG_MARGINAL) C = Bk;
+      else C = S;
+      if (Bk >= lb && C >= lc) khat = k;
+    }
+    int r;
+    if (D[b] >= s_max) r = ORC_R_STALE;
+    else if (khat == 0) r = ORC_R_NO_CANDIDATE;
+    else if (khat < k_min) r = ORC_R_SHORT;
+    else if (block_len < gamma) r = ORC_R_SHORT_BLOCK;
+    else {
+      r = ORC_R_SKIP;
+      const int32_t* x = draft ? draft + (size_t)b * gamma : NULL;
+      for (int j = 0; j < khat && r == ORC_R_SKIP && n_special > 0; ++j)
+        for (int s = 0; s < n_special; ++s)
+          if (x[j] == special[s]) r = ORC_R_SPECIAL;
+      if (r == ORC_R_SKIP && rep_max >= 2) {
+        int run = 1;
+        for (int j = 1; j < khat; ++j) {
+          run = x[j] == x[j - 1] ? run + 1 : 1;
+          if (run >= rep_max) { r = ORC_R_REPEAT; break; }
+        }
+      }
+    }
+    K[b] = r == ORC_R_SKIP ? khat : 0;
+    if (K_hat) K_hat[b] = khat;
+    if (reason) reason[b] = r;
+    D[b] = K[b] > 0 ? D[b] + K[b] : 0;
   }
   return 0;
 }
