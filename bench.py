@@ -2,7 +2,9 @@
 """Benchmark of the verify hot path on one MI355X.
 
 One step = one pass of the whole hot path over one block: the pre-call
-confidence prefix on the drafter's logits, the gamma = 32 block verification
+confidence prefix on the drafter's logits and the skip decision (two-gate
+scheduler, raw signal; the drafter logits are unconfident noise, so every
+round is strict and the verifier runs), the gamma = 32 block verification
 (causal decoder forward of gamma + 1 rows against the KV cache, fp32 logits),
 the acceptance test and the commit.  Default workload: the Qwen3-32B-shaped
 target (64 layers, d 5120, 64/8 heads x 128, QK-norm, FFN 25600, V 151936,
@@ -32,6 +34,8 @@ import workloads as W  # noqa: E402
 METRIC = "verify-call ms & tokens verified/s at γ=32, Qwen3-32B shape; % HBM peak"
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E
 TAU = 0.7
+# skip scheduler at the paper's main raw-confidence setting: (eta_b, eta_c) = (0.90, 0.93), K_min 6, S_max 64
+ETA_B, ETA_C, K_MIN, S_MAX = 0.90, 0.93, 6, 64
 
 
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gateup_gemm_qwen32b_hbm_traffic.txt")
@@ -196,13 +200,20 @@ def main():
     conf_ws = sdd.rowstats_workspace(1, gamma, V)
     outs = tuple(torch.empty(1, dtype=torch.int32, device="cuda") for _ in range(3))
     skip = torch.empty(1, dtype=torch.int32, device="cuda")
+    log_conf = torch.empty((1, gamma), dtype=torch.float32, device="cuda")
+    stale = torch.zeros(1, dtype=torch.int32, device="cuda")
+    sched_out = tuple(torch.empty(1, dtype=torch.int32, device="cuda") for _ in range(3))
+    skips = torch.zeros(rounds, dtype=torch.int32, device="cuda")
     accepted = torch.zeros(rounds, dtype=torch.int32, device="cuda")
 
     def step(r):
         # drafter stand-in: the next gamma continuation tokens after the cache, 20% replaced
         idx = (kv_len[0] + 1 - P + ar).clamp_(0, max(n_cont - 1, 0)).long()
         torch.where(mask[r], repl[r], cont[idx], out=drafts[0])
-        sdd.confidence_prefix(drafter[r], gamma, TAU, ws=conf_ws, out=skip)
+        sdd.confidence_prefix(drafter[r], gamma, TAU, ws=conf_ws, out=skip, log_conf=log_conf)
+        K, _, _ = sdd.schedule(log_conf, stale, sdd.SIG_RAW, ETA_B, ETA_C, k_min=K_MIN, s_max=S_MAX,
+                               draft=drafts, out=sched_out)
+        skips[r] = K[0]
         kv.verify(seq0, drafts, logits, am, ws)
         L, nxt, _ = sdd.accept(drafts, logits, sdd.GREEDY, ws=acc_ws, out=outs)
         kv.commit(seq0, L, nxt)
@@ -227,6 +238,7 @@ def main():
     n_dom, tot_dom, mn_dom, mx_dom = sdd.profile_read(dom)
     sdd.profile_stop()
     acc_l = accepted[a.warmup:].cpu().numpy()
+    assert int(skips.sum()) == 0, "a round was scheduled as a skip: the step would not call the verifier"
     final_len = int(kv.state()[0][0])
     log(f"timed {a.steps} steps: {ms:.3f} ms/step (wall {wall * 1e3 / a.steps:.3f}), "
         f"accepted lengths {acc_l.tolist()}, final len {final_len}")
@@ -252,7 +264,8 @@ def main():
         "config": {"workload": f"{a.workload}-verify-gamma{gamma}", "layers": shape.n_layers,
                    "d_model": d, "heads": f"{shape.n_q_heads}/{shape.n_kv_heads}x{shape.head_dim}",
                    "d_ff": dff, "vocab": V, "prompt": P, "gamma": gamma, "batch": 1,
-                   "rounds": a.steps, "drafts": a.drafts, "tau": TAU},
+                   "rounds": a.steps, "drafts": a.drafts, "tau": TAU,
+                   "scheduler": {"signal": "raw", "eta_b": ETA_B, "eta_c": ETA_C, "k_min": K_MIN, "s_max": S_MAX}},
         "verify_calls_per_s": 1e3 / ms,
         "accepted_tokens_per_s": float((acc_l + 1).sum()) * 1e3 / (ms * a.steps),
         "call_hbm_frac": call_bytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
@@ -264,11 +277,11 @@ def main():
                      "avg_ms": dom_ms, "min_ms": mn_dom, "max_ms": mx_dom},
     }
     if a.all_kernels:
-        sdd.profile_start(0x1FF, 4096)
+        sdd.profile_start(0x3FF, 4096)
         step(rounds - 1)
         torch.cuda.synchronize()
         names = {"embed": 1, "qkv": 2, "attention": 4, "o_proj": 8, "gate_up": 16, "down": 32, "lm_head": 64,
-                 "accept": 128, "confidence": 256}
+                 "accept": 128, "confidence": 256, "schedule": 512}
         result["kernels_ms_per_step"] = {k: sdd.profile_read(v)[1] for k, v in names.items()}
         sdd.profile_stop()
     if not a.no_cpu_baseline:

@@ -201,6 +201,52 @@ int sdd_confidence_prefix(const void* logits, int dtype, size_t seq_stride, int 
                           const int32_t* draft, float* log_p_draft, void* ws, size_t ws_bytes,
                           sdd_stream_t stream);
 
+/* ---- skip scheduler ------------------------------------------------------ */
+
+/* confidence signals for the prefix gate (Sec. 4.2) */
+#define SDD_SIG_RAW 0         /* C_k = geometric mean of q_1..q_k (raw confidence) */
+#define SDD_SIG_MARGINAL 1    /* C_k = min_{j<=k} a_j (marginal survival; both gates become eta_m) */
+#define SDD_SIG_CONDITIONAL 2 /* C_k = prod_{j<=k} s_j (conditional survival, chain rule) */
+
+/* why a round is a skip (K > 0) or strict (K = 0) */
+#define SDD_SKIP_OK 0           /* all conditions hold: K = K_hat tokens are committed unverified */
+#define SDD_SKIP_STALE 1        /* D >= s_max: staleness forces a strict round */
+#define SDD_SKIP_NO_CANDIDATE 2 /* K_hat = 0 */
+#define SDD_SKIP_SHORT 3        /* K_hat < k_min */
+#define SDD_SKIP_SHORT_BLOCK 4  /* the block is a shortened final block */
+#define SDD_SKIP_SPECIAL 5      /* a special (e.g. end-of-sequence) token in x^_1..x^_K_hat */
+#define SDD_SKIP_REPEAT 6       /* rep_max equal consecutive drafts in x^_1..x^_K_hat */
+
+/* Skip decision for B sequences (Sec. 4.1 candidate skip length, commit rule
+ * and staleness; Sec. 4.2 signals; Appendix "Baselines and Sweep Settings"
+ * guard list).  Device inputs:
+ *   log_q      fp32 [B][gamma]: log of the position score of draft j (raw
+ *              confidence, marginal survival a_j or conditional survival s_j;
+ *              sdd_confidence_prefix's log_conf is the raw one)
+ *   draft      int32 [B][gamma]; needed when n_special > 0 or rep_max >= 2
+ *   block_len  int32 [B] drafted block length (< gamma: shortened final
+ *              block); NULL = every block is whole
+ *   special    int32 [n_special] tokens a skipped prefix may not contain
+ *   D          int32 [B] unverified tokens committed since the last verifier
+ *              call; read and updated in place
+ * For a prefix of length k the local gate is B_k = min_{j<=k} log q_j >=
+ * log eta_b and the prefix gate is C_k >= log eta_c (C_k per signal, in log
+ * space; the raw mean is S_k / k with S_k = S_{k-1} + log q_k summed in
+ * position order in fp32).  Thresholds are rounded to fp32 as
+ * (float)log(eta) (eta <= 0: -inf) and every comparison is an fp32 >=.
+ * K_hat = the largest k passing both gates (0 if none); a NaN or +inf score
+ * ends the search.  Guards in order: D >= s_max, K_hat = 0, K_hat < k_min,
+ * block_len < gamma, special token, repetition; the first that applies sets
+ * reason and K = 0, otherwise K = K_hat.  D becomes D + K after a skip and 0
+ * after a strict round.  Outputs (device int32 [B]): K, and optionally K_hat
+ * and reason (may be NULL).
+ * Errors: SDD_EINVAL for NULL required pointers, B <= 0, gamma outside
+ * [0, 64], a bad signal, a NaN threshold, n_special outside [0, 256]. */
+int sdd_schedule(const float* log_q, const int32_t* draft, const int32_t* block_len, int B, int gamma,
+                 int signal, double eta_b, double eta_c, int k_min, int s_max, const int32_t* special,
+                 int n_special, int rep_max, int32_t* D, int32_t* K, int32_t* K_hat, int32_t* reason,
+                 sdd_stream_t stream);
+
 /* ---- launch timing (benchmarks) ----------------------------------------- */
 
 /* Kernel classes */
@@ -213,6 +259,7 @@ int sdd_confidence_prefix(const void* logits, int dtype, size_t seq_stride, int 
 #define SDD_PROF_GEMM_LM 64u
 #define SDD_PROF_ACCEPT 128u
 #define SDD_PROF_CONF 256u
+#define SDD_PROF_SCHED 512u
 
 /* Starts timing: until sdd_profile_stop, every every-th launch (1: each) of
  * the classes in class_mask is bracketed by two HIP events on its own stream

@@ -62,7 +62,7 @@ def lib():
         L.orc_confidence_prefix.argtypes = [P, C.c_size_t, C.c_int, C.c_int, C.c_int, C.c_double,
                                             P, P, P, P]
         L.orc_schedule.argtypes = [P, P, C.c_int, C.c_int, C.c_int, C.c_double, C.c_double, C.c_int, C.c_int,
-                                   C.c_int, P, C.c_int, C.c_int, P, P, P, P]
+                                   P, P, C.c_int, C.c_int, P, P, P, P]
         _lib = L
     return _lib
 
@@ -250,8 +250,9 @@ def schedule(log_q, D, signal: int, eta_b: float, eta_c: float, k_min: int = 0, 
     rs = np.empty(B, np.int32)
     dr = None if draft is None else np.ascontiguousarray(np.asarray(draft, np.int32).reshape(B, gamma))
     sp = np.ascontiguousarray(np.asarray(special, np.int32).reshape(-1)) if len(special) else None
+    bl = None if block_len is None else np.ascontiguousarray(np.broadcast_to(np.asarray(block_len, np.int32), (B,)))
     rc = lib().orc_schedule(_p(lq), _p(dr), B, gamma, int(signal), float(eta_b), float(eta_c), int(k_min),
-                            int(s_max), gamma if block_len is None else int(block_len), _p(sp),
+                            int(s_max), _p(bl), _p(sp),
                             0 if sp is None else sp.size, int(rep_max), _p(d), _p(K), _p(Kh), _p(rs))
     if rc != 0:
         raise ValueError("invalid schedule arguments")

@@ -719,8 +719,8 @@ int orc_confidence_prefix(const float* logits, size_t seq_stride, int B, int gam
 static float log_threshold(double eta) { return eta > 0.0 ? (float)log(eta) : -INFINITY; }
 
 int orc_schedule(const float* log_q, const int32_t* draft, int B, int gamma, int signal, double eta_b,
-                 double eta_c, int k_min, int s_max, int block_len, const int32_t* special, int n_special,
-                 int rep_max, int32_t* D, int32_t* K, int32_t* K_hat, int32_t* reason) {
+                 double eta_c, int k_min, int s_max, const int32_t* block_len, const int32_t* special,
+                 int n_special, int rep_max, int32_t* D, int32_t* K, int32_t* K_hat, int32_t* reason) {
   if (!log_q || !D || !K || B <= 0 || gamma < 0 || gamma > 64 || signal < 0 || signal > 2 || isnan(eta_b) ||
       isnan(eta_c) || n_special < 0 || (n_special > 0 && !special) || ((n_special > 0 || rep_max >= 2) && !draft))
     return -1;
@@ -745,7 +745,7 @@ int orc_schedule(const float* log_q, const int32_t* draft, int B, int gamma, int
     if (D[b] >= s_max) r = ORC_R_STALE;
     else if (khat == 0) r = ORC_R_NO_CANDIDATE;
     else if (khat < k_min) r = ORC_R_SHORT;
-    else if (block_len < gamma) r = ORC_R_SHORT_BLOCK;
+    else if (block_len && block_len[b] < gamma) r = ORC_R_SHORT_BLOCK;
     else {
       r = ORC_R_SKIP;
       const int32_t* x = draft ? draft + (size_t)b * gamma : NULL;

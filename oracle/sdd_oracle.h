@@ -118,7 +118,8 @@ int orc_confidence_prefix(const float* logits, size_t seq_stride, int B, int gam
  * K_hat = max{k in 1..gamma : both gates}, 0 if none; a non-finite score
  * (NaN, +inf) is invalid and no prefix reaching it passes.  Guards, in order
  * (reason code when the round is strict): D >= s_max (STALE); K_hat = 0
- * (NO_CANDIDATE); K_hat < k_min (SHORT); block_len < gamma (SHORT_BLOCK);
+ * (NO_CANDIDATE); K_hat < k_min (SHORT); block_len[b] < gamma (SHORT_BLOCK;
+ * block_len may be NULL: every block is whole);
  * a draft in x_1..x_{K_hat} in special[] (SPECIAL); rep_max >= 2 and
  * rep_max equal consecutive drafts in x_1..x_{K_hat} (REPEAT).  Otherwise
  * K = K_hat (SKIP).  Then D += K if K > 0, else D = 0 (a strict round calls
@@ -127,8 +128,8 @@ enum { ORC_SIG_RAW = 0, ORC_SIG_MARGINAL = 1, ORC_SIG_CONDITIONAL = 2 };
 enum { ORC_R_SKIP = 0, ORC_R_STALE = 1, ORC_R_NO_CANDIDATE = 2, ORC_R_SHORT = 3, ORC_R_SHORT_BLOCK = 4,
        ORC_R_SPECIAL = 5, ORC_R_REPEAT = 6 };
 int orc_schedule(const float* log_q, const int32_t* draft, int B, int gamma, int signal, double eta_b,
-                 double eta_c, int k_min, int s_max, int block_len, const int32_t* special, int n_special,
-                 int rep_max, int32_t* D, int32_t* K, int32_t* K_hat, int32_t* reason);
+                 double eta_c, int k_min, int s_max, const int32_t* block_len, const int32_t* special,
+                 int n_special, int rep_max, int32_t* D, int32_t* K, int32_t* K_hat, int32_t* reason);
 
 #ifdef __cplusplus
 }

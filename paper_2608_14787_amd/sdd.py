@@ -64,6 +64,7 @@ _SIGS = {
     "sdd_rowstats_workspace_bytes": (I, [I, I, I, P]),
     "sdd_accept": (I, [P, P, I, P, I, SZ, P, I, I, I, I, I, F, P, P, P, P, SZ, P]),
     "sdd_confidence_prefix": (I, [P, I, SZ, I, I, I, F, P, P, P, P, P, SZ, P]),
+    "sdd_schedule": (I, [P, P, P, I, I, I, C.c_double, C.c_double, I, I, P, I, I, P, P, P, P, P]),
     "sdd_profile_start": (I, [C.c_uint, I, I]),
     "sdd_profile_read": (I, [C.c_uint, P, P, P, P]),
     "sdd_profile_stop": (I, []),
@@ -71,6 +72,10 @@ _SIGS = {
 
 PROF_EMBED, PROF_GEMM_QKV, PROF_ATTN, PROF_GEMM_O = 1, 2, 4, 8
 PROF_GEMM_GATEUP, PROF_GEMM_DOWN, PROF_GEMM_LM, PROF_ACCEPT, PROF_CONF = 16, 32, 64, 128, 256
+PROF_SCHED = 512
+SIG_RAW, SIG_MARGINAL, SIG_CONDITIONAL = 0, 1, 2
+(SKIP_OK, SKIP_STALE, SKIP_NO_CANDIDATE, SKIP_SHORT, SKIP_SHORT_BLOCK, SKIP_SPECIAL,
+ SKIP_REPEAT) = range(7)
 
 
 def lib() -> C.CDLL:
@@ -154,22 +159,45 @@ def accept(draft: torch.Tensor, p: torch.Tensor, mode: int, *, q: torch.Tensor |
 
 
 def confidence_prefix(logits: torch.Tensor, gamma: int, tau: float, *, draft=None,
-                      log_conf: bool = False, ws: torch.Tensor | None = None, out=None, stream=None):
+                      log_conf=False, ws: torch.Tensor | None = None, out=None, stream=None):
     """sdd_confidence_prefix over drafter rows logits[B, >=gamma, V].
 
+    log_conf: False, True (allocate) or a contiguous fp32 [B, gamma] tensor to write into.
     Returns skip_len int32 [B] (and log_conf, log_p_draft fp32 [B, gamma] when requested)."""
     B, R, V = logits.shape
     if ws is None:
         ws = rowstats_workspace(B, gamma, V, logits.device)
     sk = out if out is not None else torch.empty(B, dtype=torch.int32, device=logits.device)
-    lc = torch.empty((B, max(gamma, 1)), dtype=torch.float32, device=logits.device) if log_conf else None
+    if isinstance(log_conf, torch.Tensor):
+        assert log_conf.dtype == torch.float32 and log_conf.is_contiguous() and log_conf.numel() >= B * gamma
+        lc = log_conf
+    else:
+        lc = torch.empty((B, max(gamma, 1)), dtype=torch.float32, device=logits.device) if log_conf else None
     lp = torch.empty((B, max(gamma, 1)), dtype=torch.float32, device=logits.device) if draft is not None else None
     _check(lib().sdd_confidence_prefix(_ptr(logits), _dtype_code(logits), logits.stride(0), B, gamma,
                                        V, tau, _ptr(sk), _ptr(lc), _ptr(draft), _ptr(lp), _ptr(ws),
                                        ws.numel(), _stream(stream)))
-    if not log_conf and draft is None:
+    if lc is None and draft is None:
         return sk
     return sk, (lc[:, :gamma] if lc is not None else None), (lp[:, :gamma] if lp is not None else None)
+
+
+def schedule(log_q: torch.Tensor, D: torch.Tensor, signal: int, eta_b: float, eta_c: float, *,
+             k_min: int = 0, s_max: int = 1 << 30, draft=None, block_len=None, special=None,
+             rep_max: int = 0, out=None, stream=None):
+    """sdd_schedule: two-gate skip decision for log_q fp32 [B, gamma]; D int32 [B] is updated in place.
+
+    Returns (K, K_hat, reason), int32 [B] each."""
+    B, gamma = log_q.shape
+    dev = log_q.device
+    if out is None:
+        out = tuple(torch.empty(B, dtype=torch.int32, device=dev) for _ in range(3))
+    K, Kh, rs = out
+    n_special = 0 if special is None else special.numel()
+    _check(lib().sdd_schedule(_ptr(log_q), _ptr(draft), _ptr(block_len), B, gamma, signal, float(eta_b),
+                              float(eta_c), k_min, s_max, _ptr(special), n_special, rep_max, _ptr(D),
+                              _ptr(K), _ptr(Kh), _ptr(rs), _stream(stream)))
+    return K, Kh, rs
 
 
 def profile_start(class_mask: int, max_launches: int = 65536, every: int = 1):

@@ -71,3 +71,17 @@ def test_host_side_argument_errors(S):
     assert L.sdd_accept(*args(mode=S.RATIO)) == S.EINVAL  # ratio needs q and uniforms
     assert L.sdd_confidence_prefix(P, S.BF16, 400, 2, 4, 100, float("nan"), P, None, None, None, P, 1 << 20, None) == S.EINVAL
     assert L.sdd_confidence_prefix(P, S.BF16, 10, 2, 4, 100, 0.5, P, None, None, None, P, 1 << 20, None) == S.EINVAL
+
+    def sched(lq=P, draft=None, B=4, gamma=8, signal=S.SIG_RAW, eb=0.9, ec=0.93, special=None, n_special=0,
+              rep_max=0, D=P, K=P):
+        return L.sdd_schedule(lq, draft, None, B, gamma, signal, eb, ec, 6, 64, special, n_special, rep_max, D, K,
+                              None, None, None)
+    assert sched(lq=None) == S.EINVAL
+    assert sched(D=None) == S.EINVAL and sched(K=None) == S.EINVAL
+    assert sched(B=0) == S.EINVAL and sched(gamma=65) == S.EINVAL and sched(gamma=-1) == S.EINVAL
+    assert sched(signal=3) == S.EINVAL and sched(signal=-1) == S.EINVAL
+    assert sched(eb=float("nan")) == S.EINVAL and sched(ec=float("nan")) == S.EINVAL
+    assert sched(special=P, n_special=257, draft=P) == S.EINVAL
+    assert sched(special=None, n_special=1, draft=P) == S.EINVAL
+    assert sched(special=P, n_special=1, draft=None) == S.EINVAL  # the special-token guard reads drafts
+    assert sched(rep_max=2, draft=None) == S.EINVAL

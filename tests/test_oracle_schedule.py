@@ -223,3 +223,36 @@ def test_gate_comparisons_are_inclusive():
         assert oracle.schedule(lq, [0], MARG, eta, eta)["K_hat"][0] == 5
         assert oracle.schedule(lq, [0], MARG, 0.0, eta)["K_hat"][0] == 5
         assert oracle.schedule(lq, [0], COND, eta, 0.0)["K_hat"][0] == 5
+
+
+def test_block_len_per_sequence():
+    """Appendix guard list: a shortened final block refuses the skip for that sequence only."""
+    lq = np.log(np.full((3, 8), 0.99)).astype(np.float32)
+    r = oracle.schedule(lq, [0, 0, 0], RAW, 0.9, 0.9, block_len=[8, 5, 8])
+    assert list(r["reason"]) == [oracle.R_SKIP, oracle.R_SHORT_BLOCK, oracle.R_SKIP]
+    assert list(r["K"]) == [8, 0, 8] and list(r["D"]) == [8, 0, 8]
+
+
+def test_prefix_frequency_construction_monte_carlo():
+    """Prop. 1 (construction of its proof, Appendix "Proof"): two score processes with identical positionwise
+    joint laws of (q_j, 1{L >= j}) whose local-gate prefixes of length K occur with probabilities
+    Pr(L >= K) rho and Pr(L >= K) rho^K.  Monte-Carlo through the scheduler's local gate (K_hat >= K iff
+    min_{j<=K} q_j >= tau), each frequency within 5 binomial standard deviations."""
+    rng = np.random.default_rng(11)
+    n, gamma, K, rho, tau, q_lo, q_hi = 40000, 8, 4, 0.7, 0.8, 0.3, 0.95
+    L = np.minimum(rng.geometric(0.15, size=n) - 1, gamma)  # any law with Pr(L >= K) > 0
+    Y = (L[:, None] >= np.arange(1, gamma + 1)[None]).astype(np.float64)
+    Z = (rng.random((n, 1)) < rho).astype(np.float64)
+    Zj = (rng.random((n, gamma)) < rho).astype(np.float64)
+    q = q_lo + (q_hi - q_lo) * Y * Z
+    q2 = q_lo + (q_hi - q_lo) * Y * Zj
+    D = np.zeros(n, np.int32)
+    kh = oracle.schedule(np.log(q).astype(np.float32), D, MARG, tau, 0.0)["K_hat"]
+    kh2 = oracle.schedule(np.log(q2).astype(np.float32), D, MARG, tau, 0.0)["K_hat"]
+    pL = float(np.mean(L >= K))
+    for got, p in ((np.mean(kh >= K), pL * rho), (np.mean(kh2 >= K), pL * rho ** K)):
+        assert abs(got - p) <= 5 * math.sqrt(p * (1 - p) / n), (got, p)
+    # identical positionwise joint law: per position, Pr(q_j = q_hi, Y_j = 1) agree within sampling error
+    hi1 = ((q == q_hi) & (Y == 1)).mean(0)
+    hi2 = ((q2 == q_hi) & (Y == 1)).mean(0)
+    assert np.all(np.abs(hi1 - hi2) <= 5 * np.sqrt(2 * hi1 * (1 - hi1) / n) + 1e-12)

@@ -14,6 +14,7 @@ code-prompt length and random-weight decoders of the named shapes):
   qwen7b   28 layers, d 3584, 28/4 heads x 128, FFN 18944, V 152064, 512-token prompt
   qwen32b  64 layers, d 5120, 64/8 heads x 128, QK-norm, FFN 25600, V 151936, 1024-token prompt
   batch8   qwen32b shape, 8 sequences with KV lengths U[256, 4096]
+  schedule log scores [64, 32] from log(1 - e), e ~ Exp(lam), lam log-uniform per sequence
 """
 from __future__ import annotations
 
@@ -151,3 +152,35 @@ def accept_inputs(seed: int, B: int = 16, gamma: int = 32, vocab: int = 151936,
 def batch8_lengths(seed: int, n: int = 8, lo: int = 256, hi: int = 4096) -> np.ndarray:
     """Ragged prompt lengths U[lo, hi]."""
     return rng(seed).integers(lo, hi + 1, size=n, dtype=np.int64).astype(np.int32)
+
+
+@dataclass
+class ScheduleInputs:
+    log_q: np.ndarray      # fp32 [B, gamma] log position scores
+    draft: np.ndarray      # int32 [B, gamma]
+    D: np.ndarray          # int32 [B] unverified tokens since the last verifier call
+    block_len: np.ndarray  # int32 [B] (gamma, or shorter for a truncated final block)
+
+
+def schedule_inputs(seed: int, B: int = 64, gamma: int = 32, vocab: int = 151936,
+                    p_short: float = 0.1, p_repeat: float = 0.2, d_max: int = 80) -> ScheduleInputs:
+    """Skip-scheduler workload: per-position failure probability e ~ Exp(mean lam) clipped to 0.999,
+    with lam log-uniform in [1e-3, 0.3] per sequence (confident and unsure sequences in one batch),
+    log score = log(1 - e) in fp32; drafts uniform tokens with a run of one repeated token inserted
+    w.p. p_repeat; D uniform in [0, d_max]; a shortened block (length U[1, gamma-1]) w.p. p_short."""
+    g = rng(seed)
+    lam = np.exp(g.uniform(np.log(1e-3), np.log(0.3), size=(B, 1)))
+    e = np.minimum(g.exponential(1.0, size=(B, gamma)) * lam, 0.999)
+    log_q = np.log1p(-e).astype(np.float32)
+    draft = g.integers(0, vocab, size=(B, gamma), dtype=np.int64).astype(np.int32)
+    if gamma >= 2:
+        for b in np.nonzero(g.random(B) < p_repeat)[0]:
+            n = int(g.integers(2, min(gamma, 6) + 1))
+            s = int(g.integers(0, gamma - n + 1))
+            draft[b, s:s + n] = draft[b, s]
+    D = g.integers(0, d_max + 1, size=B, dtype=np.int64).astype(np.int32)
+    block_len = np.full(B, gamma, np.int32)
+    if gamma >= 2:
+        short = g.random(B) < p_short
+        block_len[short] = g.integers(1, gamma, size=int(short.sum()), dtype=np.int64)
+    return ScheduleInputs(log_q, draft, D, block_len)
