@@ -16,7 +16,7 @@ import numpy as np
 
 from . import build as _build
 
-GREEDY, RATIO, TOPK, LENIENT = 0, 1, 2, 3
+GREEDY, RATIO, TOPK, LENIENT, RATIO_SAMPLE = 0, 1, 2, 3, 4
 (EMBED, LM_HEAD, FINAL_NORM, WQ, WK, WV, WO, WGATE, WUP, WDOWN,
  ATTN_NORM, FFN_NORM, Q_NORM, K_NORM) = range(14)
 
@@ -58,7 +58,7 @@ def lib():
         L.orc_verify.argtypes = [P, P, C.c_int, P]
         L.orc_commit.argtypes = [P, C.c_int, C.c_int]
         L.orc_accept.argtypes = [C.c_int, P, P, P, C.c_size_t, P, C.c_int, C.c_int, C.c_int,
-                                 C.c_int, C.c_double, P, P, P, P, P]
+                                 C.c_int, C.c_double, P, P, P, P, P, P]
         L.orc_confidence_prefix.argtypes = [P, C.c_size_t, C.c_int, C.c_int, C.c_int, C.c_double,
                                             P, P, P, P]
         L.orc_schedule.argtypes = [P, P, C.c_int, C.c_int, C.c_int, C.c_double, C.c_double, C.c_int, C.c_int,
@@ -188,8 +188,9 @@ def accept(mode: int, draft, p, q=None, u=None, k: int = 1, lenience: float = 1.
            margins: bool = True):
     """Acceptance test over target rows p [B, gamma+1, V] (fp32 values).
 
-    Returns dict(accepted_len, next_token, dec_margin, argmax_gap, flags).
-    q: drafter rows [B, >=gamma, V] (ratio mode), u: uniforms [B, gamma]."""
+    Returns dict(accepted_len, next_token, dec_margin, argmax_gap, flags, sample_margin).
+    q: drafter rows [B, >=gamma, V] (ratio modes), u: uniforms [B, gamma] (RATIO) or
+    [B, gamma+1] (RATIO_SAMPLE: column gamma draws the next token)."""
     p = np.ascontiguousarray(p, np.float32)
     B, R, V = p.shape
     gamma = R - 1
@@ -199,18 +200,19 @@ def accept(mode: int, draft, p, q=None, u=None, k: int = 1, lenience: float = 1.
         q = np.ascontiguousarray(q, np.float32)
         qs = q.shape[1] * V
     if u is not None:
-        u = np.ascontiguousarray(u, np.float32).reshape(B, gamma)
+        u = np.ascontiguousarray(u, np.float32).reshape(B, gamma + (mode == RATIO_SAMPLE))
     L = np.empty(B, np.int32)
     nxt = np.empty(B, np.int32)
     fl = np.empty(B, np.int32)
     dm = np.empty((B, max(gamma, 1)), np.float64) if margins else None
     gap = np.empty((B, gamma + 1), np.float64) if margins else None
+    sm = np.empty(B, np.float64)
     rc = lib().orc_accept(mode, _p(draft), _p(p), _p(q), qs, _p(u), B, gamma, V, int(k),
-                          float(lenience), _p(L), _p(nxt), _p(dm), _p(gap), _p(fl))
+                          float(lenience), _p(L), _p(nxt), _p(dm), _p(gap), _p(fl), _p(sm))
     if rc != 0:
         raise ValueError("invalid accept arguments")
     return dict(accepted_len=L, next_token=nxt, dec_margin=None if dm is None else dm[:, :gamma],
-                argmax_gap=gap, flags=fl)
+                argmax_gap=gap, flags=fl, sample_margin=sm)
 
 
 def confidence_prefix(logits, gamma: int, tau: float, draft=None):

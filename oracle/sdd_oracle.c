@@ -608,16 +608,53 @@ static double kth_excluding(const float* z, int V, int x, int k) {
   return r;
 }
 
+/* Residual draw of the distribution-preserving ratio rule: weights
+ * r(v) = max(0, p(v) - q(v)) (q = NULL: r = p), total R, target t = u R; the
+ * draw is the first v with r(v) > 0 whose cumulative weight exceeds t.  R <= 0
+ * (p and q equal to rounding) draws from p.  *margin = distance of t from the
+ * drawn interval's edges over R. */
+static int residual_draw(const float* zp, const float* zq, int V, double u, double* margin) {
+  const double lp = row_lse(zp, V), lq = zq ? row_lse(zq, V) : 0.0;
+  double R = 0.0;
+  for (int v = 0; v < V; ++v) {
+    const double r = exp((double)zp[v] - lp) - (zq ? exp((double)zq[v] - lq) : 0.0);
+    if (r > 0.0) R += r;
+  }
+  if (!(R > 0.0)) {
+    zq = NULL;
+    R = 0.0;
+    for (int v = 0; v < V; ++v) R += exp((double)zp[v] - lp);
+  }
+  const double t = u * R;
+  double c = 0.0;
+  int last = -1;
+  for (int v = 0; v < V; ++v) {
+    const double r = exp((double)zp[v] - lp) - (zq ? exp((double)zq[v] - lq) : 0.0);
+    if (!(r > 0.0)) continue;
+    last = v;
+    if (c + r > t) {
+      const double lo = t - c, hi = c + r - t;
+      *margin = (lo < hi ? lo : hi) / R;
+      return v;
+    }
+    c += r;
+  }
+  *margin = 0.0; /* t at or beyond the total: rounding; the last positive weight */
+  return last;
+}
+
 int orc_accept(int mode, const int32_t* draft, const float* p, const float* q,
                size_t q_seq_stride, const float* u, int B, int gamma, int V, int k,
                double lenience, int32_t* accepted_len, int32_t* next_token,
-               double* dec_margin, double* argmax_gap, int32_t* flags) {
+               double* dec_margin, double* argmax_gap, int32_t* flags, double* sample_margin) {
   if (!p || !accepted_len || !next_token || B <= 0 || gamma < 0 || V <= 0) return -1;
   if (gamma > 0 && !draft) return -1;
   if (mode == ORC_TOPK && k < 1) return -1;
   if (mode == ORC_LENIENT && !(lenience > 0.0 && lenience <= 1.0)) return -1;
-  if (mode == ORC_RATIO && (!q || !u)) return -1;
-  if (mode < ORC_GREEDY || mode > ORC_LENIENT) return -1;
+  const int ratio = mode == ORC_RATIO || mode == ORC_RATIO_SAMPLE;
+  if (ratio && (!q || !u)) return -1;
+  if (mode < ORC_GREEDY || mode > ORC_RATIO_SAMPLE) return -1;
+  const int u_stride = mode == ORC_RATIO_SAMPLE ? gamma + 1 : gamma;
   const float log_len32 = (float)log(lenience);
   for (int b = 0; b < B; ++b) {
     int L = gamma, fl = 0;
@@ -630,7 +667,7 @@ int orc_accept(int mode, const int32_t* draft, const float* p, const float* q,
         pass = 0;
         fl |= 2;
       } else if (!row_finite(z, V) ||
-                 (mode == ORC_RATIO && !row_finite(q + (size_t)b * q_seq_stride + (size_t)j * V, V))) {
+                 (ratio && !row_finite(q + (size_t)b * q_seq_stride + (size_t)j * V, V))) {
         pass = 0;
         fl |= 1;
       } else if (mode == ORC_GREEDY || (mode == ORC_LENIENT && lenience == 1.0)) {
@@ -655,7 +692,7 @@ int orc_accept(int mode, const int32_t* draft, const float* p, const float* q,
         const float* zq = q + (size_t)b * q_seq_stride + (size_t)j * V;
         double lp = (double)z[x] - row_lse(z, V);
         double lq = (double)zq[x] - row_lse(zq, V);
-        double uu = u[(size_t)b * gamma + j];
+        double uu = u[(size_t)b * u_stride + j];
         double lu = uu > 0.0 ? log(uu) : -INFINITY;
         pass = lu < lp - lq;
         margin = fabs(lu - (lp - lq));
@@ -672,6 +709,12 @@ int orc_accept(int mode, const int32_t* draft, const float* p, const float* q,
     if (!row_finite(zL, V)) fl |= 1;
     accepted_len[b] = L;
     next_token[b] = row_argmax(zL, V);
+    double sm = INFINITY;
+    if (mode == ORC_RATIO_SAMPLE && row_finite(zL, V)) {
+      const float* zqL = L < gamma ? q + (size_t)b * q_seq_stride + (size_t)L * V : NULL;
+      if (!zqL || row_finite(zqL, V)) next_token[b] = residual_draw(zL, zqL, V, u[(size_t)b * u_stride + gamma], &sm);
+    }
+    if (sample_margin) sample_margin[b] = sm;
     if (flags) flags[b] = fl;
     if (argmax_gap)
       for (int j = 0; j <= gamma; ++j) {

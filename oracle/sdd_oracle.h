@@ -43,7 +43,7 @@ enum {
 };
 
 /* Acceptance modes (Appendix "Baselines and Sweep Settings"; Sec. 3.1). */
-enum { ORC_GREEDY = 0, ORC_RATIO = 1, ORC_TOPK = 2, ORC_LENIENT = 3 };
+enum { ORC_GREEDY = 0, ORC_RATIO = 1, ORC_TOPK = 2, ORC_LENIENT = 3, ORC_RATIO_SAMPLE = 4 };
 
 /* Threads the oracle's parallel loops use. */
 int orc_num_threads(void);
@@ -85,17 +85,27 @@ int orc_verify(orc_kv* kv, const int32_t* drafts, int gamma, double* logits);
 int orc_commit(orc_kv* kv, int accepted_len, int next_token);
 
 /* Acceptance test over target rows p[B][gamma+1][V] (fp32 values).
- * Ratio mode also reads drafter rows q (row j of sequence b at
- * q + b*q_seq_stride + j*V) and uniforms u[B][gamma].
+ * Ratio modes also read drafter rows q (row j of sequence b at
+ * q + b*q_seq_stride + j*V) and uniforms: u[B][gamma] (RATIO) or
+ * u[B][gamma+1] (RATIO_SAMPLE, column gamma is the draw of the next token).
+ * RATIO_SAMPLE is the distribution-preserving rule of the min(1, p/q) test
+ * that Sec. 3.1 cites: after the first rejection at row L the next token is
+ * drawn from norm(max(0, p_L - q_L)), after a fully accepted block from
+ * p_gamma, by inverse CDF in vocabulary order (first v whose cumulative
+ * weight exceeds u * R, R the total weight; R <= 0 draws from p_L); p and q
+ * are softmax of the rows, in fp64.  The other modes take next = argmax of
+ * row L (lowest index), as does RATIO_SAMPLE when row L is non-finite.
  * Outputs accepted_len[B], next_token[B]; optional margins:
  *   dec_margin[B][gamma]   distance of each decision from its threshold
  *   argmax_gap[B][gamma+1] top-1 minus top-2 value of each target row
  *   flags[B]               bit0: a non-finite value was seen in a decisive row
- *                          bit1: a draft token outside [0, V) */
+ *                          bit1: a draft token outside [0, V)
+ *   sample_margin[B]       RATIO_SAMPLE: distance of u * R from the edges of
+ *                          the drawn token's interval, divided by R */
 int orc_accept(int mode, const int32_t* draft, const float* p, const float* q,
                size_t q_seq_stride, const float* u, int B, int gamma, int V, int k,
                double lenience, int32_t* accepted_len, int32_t* next_token,
-               double* dec_margin, double* argmax_gap, int32_t* flags);
+               double* dec_margin, double* argmax_gap, int32_t* flags, double* sample_margin);
 
 /* Raw-confidence prefix (Sec. 4.1-4.2): log conf_j = max_v z_j - LSE(z_j);
  * skip_len = first j with conf_j < tau (gamma if none).  Rows of sequence b
