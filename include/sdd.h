@@ -50,6 +50,7 @@ typedef struct ihipStream_t* sdd_stream_t; /* a hipStream_t; NULL = default stre
 #define SDD_RATIO 1   /* accept iff u_j < p(x^_j)/q(x^_j) (min(1, p/q) test of [Leviathan 2023]) */
 #define SDD_TOPK 2    /* accept iff x^_j is among the k largest target logits */
 #define SDD_LENIENT 3 /* accept iff z(x^_j) - max_v z(v) >= log(lenience); lenience 1 = greedy */
+#define SDD_RATIO_SAMPLE 4 /* RATIO, and the next token is drawn (distribution-preserving rule, below) */
 
 /* tensor kinds for sdd_model_load_tensor (row-major, PyTorch Linear [out][in]) */
 #define SDD_T_EMBED 0      /* [vocab][d_model] */
@@ -165,23 +166,34 @@ int sdd_kv_commit(sdd_kv* kv, const int32_t* seq_ids, int n_seq, const int32_t* 
                   const int32_t* next_token, sdd_stream_t stream);
 /* ---- acceptance and confidence ---------------------------------------- */
 
-/* Workspace bytes for sdd_accept / sdd_confidence_prefix at these shapes. */
+/* Workspace bytes for sdd_accept / sdd_confidence_prefix at these shapes
+ * (zeroed once by sdd_workspace_init; the calls leave it reusable). */
 int sdd_rowstats_workspace_bytes(int B, int gamma, int V, size_t* bytes);
 
 /* Acceptance test (Sec. 3.1; lenience equation and top-k rule, Appendix
  * "Baselines and Sweep Settings").  Device inputs:
  *   draft     int32 [B][gamma]
  *   p_logits  target logits [B][gamma+1][V], dtype p_dtype, contiguous
- *   q_logits  drafter logits, RATIO only: row j of sequence b at
+ *   q_logits  drafter logits, ratio modes only: row j of sequence b at
  *             q_logits + b*q_seq_stride + j*V elements (dtype q_dtype)
- *   uniforms  fp32 [B][gamma] in [0,1), RATIO only
+ *   uniforms  fp32 in [0,1): [B][gamma] (RATIO) or [B][gamma+1]
+ *             (RATIO_SAMPLE; column gamma draws the next token)
  * For j < gamma, row j decides draft j; L = first failing j (gamma if none);
- * next_token = argmax of target row L (lowest index on ties).  A non-finite
+ * next_token = argmax of target row L (lowest index on ties).  RATIO_SAMPLE
+ * (the distribution-preserving form of the min(1, p/q) rule that Sec. 3.1
+ * cites) instead draws next_token from norm(max(0, p_L - q_L)) when L <
+ * gamma and from p_gamma when every draft passed, p and q being the softmax
+ * of the rows: inverse CDF in vocabulary order, the first v whose running
+ * weight exceeds u * W (W the total weight), with fp32 weights summed in one
+ * fixed order (bit-reproducible); if the residual total is not positive the
+ * draw is from p_L; a non-finite row L keeps the argmax.  A non-finite
  * value in a deciding row, or a draft token outside [0,V), fails that
  * position.  Outputs (device int32 [B]): accepted_len, next_token, and flags
  * (may be NULL; bit0 non-finite value seen, bit1 draft token out of range).
- * Errors: SDD_EINVAL for NULL required pointers, B <= 0, gamma < 0 or > 64,
- * V <= 0, k < 1 (TOPK), lenience not in (0,1] (LENIENT). */
+ * Errors: SDD_EINVAL for NULL required pointers (uniforms in the ratio
+ * modes, drafter logits in the ratio modes when gamma > 0), B <= 0, gamma < 0
+ * or > 64, V <= 0, k < 1 (TOPK), lenience not in (0,1] (LENIENT), drafter and
+ * target logits of different dtypes (ratio modes). */
 int sdd_accept(const int32_t* draft, const void* p_logits, int p_dtype, const void* q_logits,
                int q_dtype, size_t q_seq_stride, const float* uniforms, int B, int gamma, int V,
                int mode, int k, float lenience, int32_t* accepted_len, int32_t* next_token,

@@ -652,7 +652,7 @@ int orc_accept(int mode, const int32_t* draft, const float* p, const float* q,
   if (mode == ORC_TOPK && k < 1) return -1;
   if (mode == ORC_LENIENT && !(lenience > 0.0 && lenience <= 1.0)) return -1;
   const int ratio = mode == ORC_RATIO || mode == ORC_RATIO_SAMPLE;
-  if (ratio && (!q || !u)) return -1;
+  if (ratio && (!u || (gamma > 0 && !q))) return -1; /* no drafter row is read when gamma = 0 */
   if (mode < ORC_GREEDY || mode > ORC_RATIO_SAMPLE) return -1;
   const int u_stride = mode == ORC_RATIO_SAMPLE ? gamma + 1 : gamma;
   const float log_len32 = (float)log(lenience);

@@ -3,7 +3,10 @@
 //
 // Acceptance (Sec. 3.1; lenience equation and top-k rule in Appendix
 // "Baselines and Sweep Settings"): for every target row j < gamma decide
-// whether draft j passes; L = first failure; next token = argmax of row L.
+// whether draft j passes; L = first failure; next token = argmax of row L,
+// or, in the distribution-preserving ratio mode (the min(1, p/q) rule that
+// Sec. 3.1 cites), a draw from norm(max(0, p_L - q_L)) after a rejection and
+// from p_gamma after a full block (second kernel, resample_kernel).
 // Confidence (Sec. 4.1 local gate, Sec. 4.2 raw confidence): q_j = max softmax
 // of drafter row j; skip length = first j with q_j < tau.
 //
@@ -35,6 +38,20 @@ struct RowRec {
   int pad;
 };
 
+// Row-L statistics that the acceptance pass hands to the residual draw.
+struct SeqRec {
+  int L;
+  int bad;  // row L of p (or of q, L < gamma) holds a non-finite value: no draw, next = argmax
+  float m, s, qm, qs;
+  int pad[2];
+};
+
+// Per-chunk weight totals of the residual draw: residual max(0, p - q), and p alone (fallback when the
+// residual total is not positive).
+struct ResRec {
+  float r, p;
+};
+
 struct Job {
   const void* p;  // rows to reduce
   size_t p_seq_stride, p_row_stride;
@@ -44,6 +61,12 @@ struct Job {
   const float* u;
   int B, gamma, V, rows, C, chunk;
   int mode, k;
+  int sample;     // ratio mode with the residual draw
+  int u_stride;   // uniforms per sequence: gamma, or gamma + 1 with the draw
+  int C2, seg;    // residual draw: chunks per row, elements per thread (C2 = ceil(V / (256 seg)))
+  SeqRec* seqs;
+  ResRec* rrecs;
+  int* counters2;
   float log_len;  // fp32 log(lenience)
   float log_tau;  // fp32 log(tau)
   RowRec* recs;
@@ -263,6 +286,8 @@ __global__ void __launch_bounds__(kThreads) rowstats_kernel(Job job) {
   __shared__ int s_pass[72];
   __shared__ int s_arg[72];
   __shared__ int s_flag[72];
+  __shared__ int s_bad[72];
+  __shared__ float s_st[72][4];
 
   const int c = blockIdx.x % job.C;
   const int rowid = blockIdx.x / job.C;  // b * rows + j
@@ -334,6 +359,13 @@ __global__ void __launch_bounds__(kThreads) rowstats_kernel(Job job) {
     const bool bad = (st.flags & 1) != 0;
     s_arg[t] = st.arg < 0 ? 0 : st.arg;
     s_flag[t] = bad ? 1 : 0;
+    if (KIND == kAccept && job.sample) {
+      s_bad[t] = bad || (kQ && (st.flags & 4)) ? 1 : 0;
+      s_st[t][0] = st.m;
+      s_st[t][1] = st.s;
+      s_st[t][2] = st.qm;
+      s_st[t][3] = st.qs;
+    }
     if (KIND == kAccept) {
       int pass = 0;
       if (t < job.gamma) {
@@ -359,7 +391,7 @@ __global__ void __launch_bounds__(kThreads) rowstats_kernel(Job job) {
             const float zq = Elem<TQ>::to_f32(qr[xx]);
             const float lp = z - (st.m + logf(st.s));
             const float lq = zq - (st.qm + logf(st.qs));
-            const float uu = job.u[(size_t)b * job.gamma + t];
+            const float uu = job.u[(size_t)b * job.u_stride + t];
             const float lu = uu > 0.f ? logf(uu) : -INFINITY;
             pass = lu < lp - lq;
           }
@@ -397,6 +429,17 @@ __global__ void __launch_bounds__(kThreads) rowstats_kernel(Job job) {
       job.out_len[b] = L;
       job.out_next[b] = s_arg[L];
       if (job.out_flags) job.out_flags[b] = fl;
+      if (job.sample) {
+        SeqRec r;
+        r.L = L;
+        r.bad = s_bad[L];
+        r.m = s_st[L][0];
+        r.s = s_st[L][1];
+        r.qm = s_st[L][2];
+        r.qs = s_st[L][3];
+        r.pad[0] = r.pad[1] = 0;
+        job.seqs[b] = r;  // read by the next launch on the stream
+      }
     } else {
       int K = job.gamma;
       for (int jj = 0; jj < job.gamma; ++jj)
@@ -408,6 +451,218 @@ __global__ void __launch_bounds__(kThreads) rowstats_kernel(Job job) {
     }
   }
 }
+
+// ---- residual draw of the distribution-preserving ratio rule ---------------
+//
+// After the acceptance pass has fixed L and the statistics of row L, the next
+// token is drawn by inverse CDF in vocabulary order: weights w(v) = max(0,
+// p(v) - q(v)) (p alone at the bonus row), target t = u W with W the total,
+// draw = the first v whose running weight exceeds t.  The CDF is defined by
+// one fixed summation tree: each thread sums its own contiguous segment of
+// `seg` elements in index order; a wave sums 4 consecutive thread sums and
+// takes an inclusive scan over its 64 lanes (one chunk); the last workgroup
+// scans the chunk totals over lanes.  The search re-walks the same tree from
+// the top (chunk, lane, thread, element) with the same arithmetic, so every
+// partial sum it compares is bit-identical to the one that defined the total.
+// If rounding leaves t at or beyond a level's total, the last positive weight
+// of that level is taken.
+#pragma clang fp contract(off)
+template <typename T, int VEC>
+__device__ inline void load_vals(const T* ptr, float* v) {
+  static_assert(VEC == 1 || VEC * sizeof(T) == 16, "one element or one 16-byte load");
+  if constexpr (VEC > 1) {
+    unpack16(load16(ptr), v, T());
+  } else {
+    v[0] = Elem<T>::to_f32(*ptr);
+  }
+}
+
+struct DrawRow {
+  const void* p;
+  const void* q;  // nullptr: weights are p alone
+  float m, inv_s, qm, inv_qs;
+  int use_p;  // residual total not positive: draw from p
+};
+
+template <typename T>
+__device__ inline float draw_weight(const DrawRow& d, float zp, float zq) {
+  const float pv = __expf(zp - d.m) * d.inv_s;
+  if (d.use_p || d.q == nullptr) return pv;
+  const float diff = pv - __expf(zq - d.qm) * d.inv_qs;
+  return diff > 0.f ? diff : 0.f;
+}
+
+// Sum of the weights of elements [lo, hi) in index order (both the residual and p alone).
+template <typename T, int VEC>
+__device__ inline void segment_sums(const DrawRow& d, int lo, int hi, float& wr, float& wp) {
+  const T* pr = reinterpret_cast<const T*>(d.p);
+  const T* qr = reinterpret_cast<const T*>(d.q);
+  wr = 0.f;
+  wp = 0.f;
+  for (int e = lo; e < hi; e += VEC) {
+    float zp[VEC], zq[VEC];
+    load_vals<T, VEC>(pr + e, zp);
+    if (qr) load_vals<T, VEC>(qr + e, zq);
+#pragma unroll
+    for (int t = 0; t < VEC; ++t) {
+      const float pv = __expf(zp[t] - d.m) * d.inv_s;
+      float r = pv;
+      if (qr) {
+        const float diff = pv - __expf(zq[t] - d.qm) * d.inv_qs;
+        r = diff > 0.f ? diff : 0.f;
+      }
+      wr += r;
+      wp += pv;
+    }
+  }
+}
+
+// First element of [lo, hi) whose running weight exceeds t (same order and arithmetic as segment_sums);
+// the last positive one if none does.
+template <typename T, int VEC>
+__device__ inline int segment_find(const DrawRow& d, int lo, int hi, float t) {
+  const T* pr = reinterpret_cast<const T*>(d.p);
+  const T* qr = reinterpret_cast<const T*>(d.q);
+  float c = 0.f;
+  int last = lo;
+  for (int e = lo; e < hi; e += VEC) {
+    float zp[VEC], zq[VEC];
+    load_vals<T, VEC>(pr + e, zp);
+    if (qr && !d.use_p) load_vals<T, VEC>(qr + e, zq);
+#pragma unroll
+    for (int k = 0; k < VEC; ++k) {
+      const float w = draw_weight<T>(d, zp[k], (qr && !d.use_p) ? zq[k] : 0.f);
+      if (w > 0.f) {
+        if (c + w > t) return e + k;
+        last = e + k;
+      }
+      c += w;
+    }
+  }
+  return last;
+}
+
+// Wave 0: lane l combines thread sums 4l..4l+3 in order, then an inclusive scan over the lanes.
+__device__ inline float lane_sum4(const float* w, int lane) {
+  return ((w[4 * lane] + w[4 * lane + 1]) + w[4 * lane + 2]) + w[4 * lane + 3];
+}
+__device__ inline float wave_incl_scan(float v, int lane) {
+#pragma unroll
+  for (int o = 1; o < kWave; o <<= 1) {
+    const float y = __shfl_up(v, o);
+    if (lane >= o) v += y;
+  }
+  return v;
+}
+// Index of the first lane whose inclusive sum exceeds t and the remainder of t past the lanes before it;
+// with none, the last lane of positive weight and t = +inf (take the last positive weight below).
+__device__ inline int lane_select(float incl, float w, float t, int lane, float& t_rest) {
+  const uint64_t hit = __ballot(incl > t);
+  const float excl = __shfl_up(incl, 1);
+  if (hit) {
+    const int l = __builtin_ctzll(hit);
+    const float e = __shfl(excl, l);
+    t_rest = l == 0 ? t : t - e;
+    return l;
+  }
+  const uint64_t pos = __ballot(w > 0.f);
+  t_rest = INFINITY;
+  return pos ? 63 - __builtin_clzll(pos) : 0;
+}
+
+template <typename T, int VEC>
+__global__ void __launch_bounds__(kThreads) resample_kernel(Job job) {
+  __shared__ float s_wr[kThreads], s_wp[kThreads];
+  __shared__ int s_last, s_sel;
+  __shared__ float s_t;
+  const int c = blockIdx.x % job.C2, b = blockIdx.x / job.C2;
+  const SeqRec r = job.seqs[b];
+  if (r.bad) return;  // every workgroup of b returns: nobody arrives, next stays the argmax
+  DrawRow d;
+  d.p = reinterpret_cast<const T*>(job.p) + (size_t)b * job.p_seq_stride + (size_t)r.L * job.p_row_stride;
+  d.q = r.L < job.gamma ? reinterpret_cast<const T*>(job.q) + (size_t)b * job.q_seq_stride + (size_t)r.L * job.V
+                        : nullptr;
+  d.m = r.m;
+  d.inv_s = 1.f / r.s;
+  d.qm = r.qm;
+  d.inv_qs = d.q ? 1.f / r.qs : 0.f;
+  d.use_p = 0;
+  const int tid = threadIdx.x, lane = tid % kWave;
+  const int chunk2 = kThreads * job.seg;
+
+  {  // this chunk's totals
+    const int lo = min(job.V, c * chunk2 + tid * job.seg), hi = min(job.V, lo + job.seg);
+    float wr, wp;
+    segment_sums<T, VEC>(d, lo, hi, wr, wp);
+    s_wr[tid] = wr;
+    s_wp[tid] = wp;
+    __syncthreads();
+    if (tid < kWave) {
+      const float tr = __shfl(wave_incl_scan(lane_sum4(s_wr, lane), lane), kWave - 1);
+      const float tp = __shfl(wave_incl_scan(lane_sum4(s_wp, lane), lane), kWave - 1);
+      if (tid == 0) {
+        st_coherent(&job.rrecs[(size_t)b * 64 + c].r, tr);
+        st_coherent(&job.rrecs[(size_t)b * 64 + c].p, tp);
+      }
+    }
+  }
+  if (!arrive_last(&job.counters2[b], job.C2, &s_last)) return;
+
+  // ---- last workgroup of sequence b: select the chunk, then the lane, thread and element ----
+  if (tid < kWave) {
+    const bool have = lane < job.C2;
+    const float wr = have ? ld_coherent(&job.rrecs[(size_t)b * 64 + lane].r) : 0.f;
+    const float wp = have ? ld_coherent(&job.rrecs[(size_t)b * 64 + lane].p) : 0.f;
+    const float ir = wave_incl_scan(wr, lane), ip = wave_incl_scan(wp, lane);
+    const float R = __shfl(ir, kWave - 1);
+    const int use_p = !(R > 0.f);
+    const float W = use_p ? __shfl(ip, kWave - 1) : R;
+    const float t = job.u[(size_t)b * job.u_stride + job.gamma] * W;
+    float t_rest;
+    const int cs = lane_select(use_p ? ip : ir, use_p ? wp : wr, t, lane, t_rest);
+    if (tid == 0) {
+      s_sel = cs | (use_p << 16);
+      s_t = t_rest;
+    }
+  }
+  __syncthreads();
+  const int cs = s_sel & 0xffff;
+  d.use_p = s_sel >> 16;
+  float t = s_t;
+  const int lo = min(job.V, cs * chunk2 + tid * job.seg), hi = min(job.V, lo + job.seg);
+  {
+    float wr, wp;
+    segment_sums<T, VEC>(d, lo, hi, wr, wp);
+    s_wr[tid] = d.use_p ? wp : wr;
+  }
+  __syncthreads();
+  if (tid < kWave) {
+    const float ls = lane_sum4(s_wr, lane);
+    float t_rest;
+    const int l = lane_select(wave_incl_scan(ls, lane), ls, t, lane, t_rest);
+    if (tid == 0) {
+      // the thread within lane l's four, in the lane sum's order
+      int pick = -1, lastpos = 4 * l;
+      float run = 0.f, t_thr = INFINITY;
+      for (int i = 0; i < 4; ++i) {
+        const float w = s_wr[4 * l + i];
+        if (w > 0.f) {
+          if (pick < 0 && run + w > t_rest) {
+            pick = 4 * l + i;
+            t_thr = t_rest - run;
+          }
+          lastpos = 4 * l + i;
+        }
+        run += w;
+      }
+      s_sel = pick >= 0 ? pick : lastpos;
+      s_t = pick >= 0 ? t_thr : INFINITY;
+    }
+  }
+  __syncthreads();
+  if (tid == s_sel) job.out_next[b] = segment_find<T, VEC>(d, lo, hi, s_t);
+}
+#pragma clang fp contract(on)
 
 __global__ void fill_i32_kernel(int32_t* p, int n, int v) {
   int i = blockIdx.x * blockDim.x + threadIdx.x;
@@ -437,7 +692,10 @@ int chunks_for(int nrows, int V, int vec) {
 }
 
 size_t counters_region(int B) { return ((size_t)B * sizeof(int) + 255) / 256 * 256; }
+// Residual draw records: per sequence the row-L statistics and up to 64 chunk totals.
+size_t draw_region(int B) { return (size_t)B * (sizeof(SeqRec) + 64 * sizeof(ResRec)); }
 
+// Workspace: [acceptance counters][draw counters][SeqRec x B][ResRec x B x 64][RowRec records]
 size_t rowstats_ws(int B, int rows, int V) {
   size_t best = 0;
   for (int vec : {1, 4, 8}) {
@@ -445,20 +703,38 @@ size_t rowstats_ws(int B, int rows, int V) {
     size_t need = (size_t)B * rows * C * sizeof(RowRec);
     best = best > need ? best : need;
   }
-  return counters_region(B) + best;
+  return 2 * counters_region(B) + draw_region(B) + best;
+}
+
+// Elements per thread of the residual draw: at least 16, and few enough chunks (<= 64) for one wave.
+int draw_seg(int V) {
+  const int need = (int)ceil_div(ceil_div(V, 64), kThreads);
+  return need <= 16 ? 16 : (int)ceil_div(need, 16) * 16;
+}
+
+template <typename T>
+int launch_draw(Job& job, int vec, hipStream_t st) {
+  const int blocks = job.B * job.C2;
+  constexpr int kVec = 16 / sizeof(T);  // one 16-byte load (choose_vec returns this or 1)
+  prof_begin(PROF_ACCEPT, st);
+  if (vec == kVec)
+    hipLaunchKernelGGL((resample_kernel<T, kVec>), dim3(blocks), dim3(kThreads), 0, st, job);
+  else
+    hipLaunchKernelGGL((resample_kernel<T, 1>), dim3(blocks), dim3(kThreads), 0, st, job);
+  prof_end(PROF_ACCEPT, st);
+  return check_launch("resample_kernel");
 }
 
 template <int KIND, bool kSum, bool kCount, bool kQ, typename T, typename TQ>
 int launch_t(Job& job, int vec, hipStream_t st) {
   const int blocks = job.B * job.rows * job.C;
   const unsigned prof = KIND == kAccept ? PROF_ACCEPT : PROF_CONF;
+  constexpr int kVec = 16 / sizeof(T);  // one 16-byte load (choose_vec returns this or 1)
   prof_begin(prof, st);
-  if (vec == 1)
-    hipLaunchKernelGGL((rowstats_kernel<T, TQ, 1, KIND, kSum, kCount, kQ>), dim3(blocks), dim3(kThreads), 0, st, job);
-  else if (vec == 4)
-    hipLaunchKernelGGL((rowstats_kernel<T, TQ, 4, KIND, kSum, kCount, kQ>), dim3(blocks), dim3(kThreads), 0, st, job);
+  if (vec == kVec)
+    hipLaunchKernelGGL((rowstats_kernel<T, TQ, kVec, KIND, kSum, kCount, kQ>), dim3(blocks), dim3(kThreads), 0, st, job);
   else
-    hipLaunchKernelGGL((rowstats_kernel<T, TQ, 8, KIND, kSum, kCount, kQ>), dim3(blocks), dim3(kThreads), 0, st, job);
+    hipLaunchKernelGGL((rowstats_kernel<T, TQ, 1, KIND, kSum, kCount, kQ>), dim3(blocks), dim3(kThreads), 0, st, job);
   prof_end(prof, st);
   return check_launch("rowstats_kernel");
 }
@@ -484,8 +760,12 @@ static int setup_ws(Job& job, void* ws, size_t ws_bytes, int vec) {
   if (ws == nullptr || ws_bytes < need)
     return fail(SDD_ENOMEM, "rowstats workspace needs %zu bytes, got %zu", need, ws_bytes);
   if ((uintptr_t)ws % 16) return fail(SDD_EINVAL, "workspace must be 16-byte aligned");
-  job.counters = reinterpret_cast<int*>(ws);
-  job.recs = reinterpret_cast<RowRec*>(reinterpret_cast<char*>(ws) + counters_region(job.B));
+  char* w = reinterpret_cast<char*>(ws);
+  job.counters = reinterpret_cast<int*>(w);
+  job.counters2 = reinterpret_cast<int*>(w + counters_region(job.B));
+  job.seqs = reinterpret_cast<SeqRec*>(w + 2 * counters_region(job.B));
+  job.rrecs = reinterpret_cast<ResRec*>(w + 2 * counters_region(job.B) + (size_t)job.B * sizeof(SeqRec));
+  job.recs = reinterpret_cast<RowRec*>(w + 2 * counters_region(job.B) + draw_region(job.B));
   return SDD_OK;
 }
 
@@ -496,11 +776,13 @@ extern "C" int sdd_accept(const int32_t* draft, const void* p_logits, int p_dtyp
   SDD_REQUIRE(p_logits && accepted_len && next_token, "NULL required pointer");
   SDD_REQUIRE(B > 0 && gamma >= 0 && gamma <= 64 && V > 0, "bad shape B=%d gamma=%d V=%d", B, gamma, V);
   SDD_REQUIRE(gamma == 0 || draft, "draft is NULL");
-  SDD_REQUIRE(mode >= SDD_GREEDY && mode <= SDD_LENIENT, "bad mode %d", mode);
+  SDD_REQUIRE(mode >= SDD_GREEDY && mode <= SDD_RATIO_SAMPLE, "bad mode %d", mode);
   SDD_REQUIRE(mode != SDD_TOPK || k >= 1, "top-k needs k >= 1 (k=%d)", k);
   SDD_REQUIRE(mode != SDD_LENIENT || (lenience > 0.f && lenience <= 1.f), "lenience must be in (0,1]");
   SDD_REQUIRE(p_dtype == SDD_F32 || p_dtype == SDD_BF16, "bad p dtype");
-  const bool ratio = mode == SDD_RATIO && gamma > 0;
+  const bool sample = mode == SDD_RATIO_SAMPLE;
+  if (sample) SDD_REQUIRE(uniforms, "the residual draw needs uniforms [B][gamma+1]");
+  const bool ratio = (mode == SDD_RATIO || sample) && gamma > 0;
   if (ratio) {
     SDD_REQUIRE(q_logits && uniforms, "ratio mode needs drafter logits and uniforms");
     SDD_REQUIRE(q_dtype == p_dtype, "ratio mode needs drafter and target logits of one dtype");
@@ -518,7 +800,12 @@ extern "C" int sdd_accept(const int32_t* draft, const void* p_logits, int p_dtyp
   job.gamma = gamma;
   job.V = V;
   job.rows = gamma + 1;
-  job.mode = (mode == SDD_LENIENT && lenience == 1.f) ? SDD_GREEDY : mode;
+  job.mode = (mode == SDD_LENIENT && lenience == 1.f) ? SDD_GREEDY : sample ? SDD_RATIO : mode;
+  job.sample = sample ? 1 : 0;
+  job.u_stride = sample ? gamma + 1 : gamma;
+  job.seg = draw_seg(V);
+  job.C2 = (int)ceil_div(V, (int64_t)kThreads * job.seg);
+  if (job.C2 > 64) return fail(SDD_EUNSUPPORTED, "vocabulary of %d needs %d draw chunks (at most 64)", V, job.C2);
   job.k = k;
   job.log_len = (float)std::log((double)lenience);
   job.out_len = accepted_len;
@@ -530,6 +817,12 @@ extern "C" int sdd_accept(const int32_t* draft, const void* p_logits, int p_dtyp
   if (rc) return rc;
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
   const bool bf = p_dtype == SDD_BF16;
+  if (sample) {  // acceptance pass (ratio test, every row's statistics), then the draw from row L
+    rc = bf ? launch_t<kAccept, true, false, true, uint16_t, uint16_t>(job, vec, st)
+            : launch_t<kAccept, true, false, true, float, float>(job, vec, st);
+    if (rc) return rc;
+    return bf ? launch_draw<uint16_t>(job, vec, st) : launch_draw<float>(job, vec, st);
+  }
   switch (job.mode) {
     case SDD_GREEDY:
     case SDD_LENIENT:

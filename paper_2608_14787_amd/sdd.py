@@ -16,7 +16,7 @@ LIB_PATH = os.path.join(HERE, "libsdd.so")
 
 OK, EINVAL, ENOMEM, EHIP, ECAPACITY, EUNSUPPORTED = 0, -1, -2, -3, -4, -5
 F32, BF16 = 0, 1
-GREEDY, RATIO, TOPK, LENIENT = 0, 1, 2, 3
+GREEDY, RATIO, TOPK, LENIENT, RATIO_SAMPLE = 0, 1, 2, 3, 4
 (T_EMBED, T_LM_HEAD, T_FINAL_NORM, T_WQ, T_WK, T_WV, T_WO, T_WGATE, T_WUP, T_WDOWN,
  T_ATTN_NORM, T_FFN_NORM, T_Q_NORM, T_K_NORM) = range(14)
 
