@@ -63,6 +63,8 @@ def lib():
                                             P, P, P, P]
         L.orc_schedule.argtypes = [P, P, C.c_int, C.c_int, C.c_int, C.c_double, C.c_double, C.c_int, C.c_int,
                                    P, P, C.c_int, C.c_int, P, P, P, P]
+        L.orc_survival_mlp.argtypes = [P, P, C.c_int, C.c_int, C.c_int, C.c_int, P, P, P, P, P, P, P, P, P,
+                                       C.c_float, P, P]
         _lib = L
     return _lib
 
@@ -259,3 +261,22 @@ def schedule(log_q, D, signal: int, eta_b: float, eta_c: float, k_min: int = 0, 
     if rc != 0:
         raise ValueError("invalid schedule arguments")
     return dict(K=K, K_hat=Kh, reason=rs, D=d)
+
+
+def survival_mlp(hidden_bits, scalars, mu, sigma, W1, b1, W2, b2, W3, b3, w4, b4):
+    """Survival predictor: hidden_bits uint16 bf16 [n, d_hid], scalars fp32 [n, n_sc], normalization
+    mu/sigma [d_in], Linear weights [out][in] fp32.  Returns (log_score, logit) fp64 [n]."""
+    h = np.ascontiguousarray(hidden_bits, np.uint16)
+    n, d_hid = h.shape
+    sc = np.ascontiguousarray(scalars, np.float32).reshape(n, -1)
+    n_sc = sc.shape[1]
+    H = np.asarray(b1).shape[0]
+    f = lambda a: np.ascontiguousarray(a, np.float32)
+    ls = np.empty(max(n, 1), np.float64)
+    lg = np.empty(max(n, 1), np.float64)
+    rc = lib().orc_survival_mlp(_p(h), _p(sc) if n_sc else None, n, d_hid, n_sc, H, _p(f(mu)), _p(f(sigma)),
+                                _p(f(W1)), _p(f(b1)), _p(f(W2)), _p(f(b2)), _p(f(W3)), _p(f(b3)), _p(f(w4)),
+                                float(b4), _p(ls), _p(lg))
+    if rc != 0:
+        raise ValueError("invalid survival_mlp arguments")
+    return ls[:n], lg[:n]

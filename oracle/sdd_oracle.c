@@ -22,6 +22,8 @@
  *   - raw confidence q_j = max softmax and the local gate B_k = min_{j<=k} q_j
  *     with K = max{k : B_k >= tau} (Sec. 4.1 candidate skip length, Sec. 4.2
  *     raw confidence).
+ *   - the survival predictor MLP (Appendix "Predictor Details") whose sigmoid
+ *     output is the marginal or conditional survival score (Sec. 4.2).
  *   - the two-gate skip scheduler with its three confidence signals, the
  *     guards and the staleness counter D (Sec. 4.1 candidate skip length and
  *     commit rule, Sec. 4.2 signals, Appendix "Baselines and Sweep Settings").
@@ -809,4 +811,59 @@ int orc_schedule(const float* log_q, const int32_t* draft, int B, int gamma, int
     D[b] = K[b] > 0 ? D[b] + K[b] : 0;
   }
   return 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Survival predictor MLP */
+
+static double gelu_erf(double x) { return 0.5 * x * (1.0 + erf(x / sqrt(2.0))); }
+
+static double bf16_bits_value(uint16_t b) {
+  const uint32_t u = (uint32_t)b << 16;
+  float f;
+  memcpy(&f, &u, sizeof f);
+  return (double)f;
+}
+
+/* log sigmoid(z) = -log(1 + exp(-z)), evaluated without overflow */
+static double log_sigmoid(double z) { return z >= 0.0 ? -log1p(exp(-z)) : z - log1p(exp(z)); }
+
+static void dense(const double* x, int din, const float* W, const float* b, int dout, double* y, int act) {
+  for (int o = 0; o < dout; ++o) {
+    double acc = b ? (double)b[o] : 0.0;
+    for (int i = 0; i < din; ++i) acc += (double)W[(size_t)o * din + i] * x[i];
+    y[o] = act ? gelu_erf(acc) : acc;
+  }
+}
+
+int orc_survival_mlp(const uint16_t* hidden, const float* scalars, int n, int d_hid, int n_sc, int H,
+                     const float* mu, const float* sigma, const float* W1, const float* b1, const float* W2,
+                     const float* b2, const float* W3, const float* b3, const float* w4, float b4,
+                     double* log_score, double* logit) {
+  if (!hidden || (n_sc > 0 && !scalars) || !mu || !sigma || !W1 || !W2 || !W3 || !w4 || !log_score || n < 0 ||
+      d_hid < 0 || n_sc < 0 || d_hid + n_sc <= 0 || H <= 0)
+    return -1;
+  const int din = d_hid + n_sc;
+  int rc = 0;
+#pragma omp parallel for schedule(static) reduction(| : rc)
+  for (int r = 0; r < n; ++r) {
+    double* x = (double*)malloc(sizeof(double) * (size_t)(din + 3 * H));
+    if (!x) { rc |= 1; continue; }
+    double *h1 = x + din, *h2 = h1 + H, *h3 = h2 + H;
+    for (int i = 0; i < din; ++i) {
+      const double raw = i < d_hid ? bf16_bits_value(hidden[(size_t)r * d_hid + i])
+                                   : (double)scalars[(size_t)r * n_sc + (i - d_hid)];
+      x[i] = (raw - (double)mu[i]) / (double)sigma[i];
+    }
+    dense(x, din, W1, b1, H, h1, 1);
+    dense(h1, H, W2, b2, H, h2, 1);
+    dense(h2, H, W3, b3, H, h3, 1);
+    double z;
+    dense(h3, H, w4, NULL, 1, &z, 0);
+    z += (double)b4;
+    log_score[r] = log_sigmoid(z);
+    if (logit) logit[r] = z;
+    free(x);
+  }
+  return rc ? -1 : 0;
 }

@@ -141,6 +141,21 @@ int orc_schedule(const float* log_q, const int32_t* draft, int B, int gamma, int
                  double eta_c, int k_min, int s_max, const int32_t* block_len, const int32_t* special,
                  int n_special, int rep_max, int32_t* D, int32_t* K, int32_t* K_hat, int32_t* reason);
 
+/* Survival predictor (Appendix "Predictor Details"): per draft position, the
+ * drafter's LM-head input h (d_hid values, bf16 bits) and n_sc scalar
+ * features form x = [h, s] (d_in = d_hid + n_sc); x is normalized as
+ * (x - mu) / sigma; then an MLP d_in -> H -> H -> H -> 1 with GELU (erf
+ * form) after each hidden layer (dropout is off at inference):
+ *   h1 = GELU(W1 x~ + b1), h2 = GELU(W2 h1 + b2), h3 = GELU(W3 h2 + b3),
+ *   z = w4 . h3 + b4,  log score = log sigmoid(z)
+ * (the marginal a_j or conditional s_j survival estimate, Sec. 4.2).  Weights
+ * are PyTorch Linear layouts [out][in], fp32.  Everything in fp64.
+ * Outputs log_score[n] and (optional) logit[n]. */
+int orc_survival_mlp(const uint16_t* hidden, const float* scalars, int n, int d_hid, int n_sc, int H,
+                     const float* mu, const float* sigma, const float* W1, const float* b1, const float* W2,
+                     const float* b2, const float* W3, const float* b3, const float* w4, float b4,
+                     double* log_score, double* logit);
+
 #ifdef __cplusplus
 }
 #endif

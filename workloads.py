@@ -15,6 +15,7 @@ code-prompt length and random-weight decoders of the named shapes):
   qwen32b  64 layers, d 5120, 64/8 heads x 128, QK-norm, FFN 25600, V 151936, 1024-token prompt
   batch8   qwen32b shape, 8 sequences with KV lengths U[256, 4096]
   schedule log scores [64, 32] from log(1 - e), e ~ Exp(lam), lam log-uniform per sequence
+  survival 32 positions x (3584 bf16 hidden + 19 scalar features), MLP 3603 -> 256 -> 256 -> 256 -> 1
 """
 from __future__ import annotations
 
@@ -184,3 +185,59 @@ def schedule_inputs(seed: int, B: int = 64, gamma: int = 32, vocab: int = 151936
         short = g.random(B) < p_short
         block_len[short] = g.integers(1, gamma, size=int(short.sum()), dtype=np.int64)
     return ScheduleInputs(log_q, draft, D, block_len)
+
+
+@dataclass
+class SurvivalInputs:
+    hidden_bits: np.ndarray  # uint16 bf16 [n, d_hid]: the drafter's LM-head input per draft position
+    scalars: np.ndarray      # fp32 [n, n_sc]
+    mu: np.ndarray           # fp32 [d_in] normalization mean
+    sigma: np.ndarray        # fp32 [d_in] normalization scale (> 0)
+    W1: np.ndarray           # fp32 [H, d_in]
+    b1: np.ndarray
+    W2: np.ndarray           # fp32 [H, H]
+    b2: np.ndarray
+    W3: np.ndarray           # fp32 [H, H]
+    b3: np.ndarray
+    w4: np.ndarray           # fp32 [1, H]
+    b4: float
+
+
+def survival_inputs(seed: int, n: int = 32, d_hid: int = 3584, n_sc: int = 19, H: int = 256) -> SurvivalInputs:
+    """Survival-predictor workload (Appendix "Predictor Details" shape: 3584 + 19 -> 256 -> 256 -> 256 -> 1).
+
+    Hidden states bf16 N(0, 1.5^2); the 19 scalars in the ranges of the listed features (reveal step,
+    rank, parallelism, late flag, top-1 probability and its log, entropy and its negative, margin, top-5
+    mass, step-0 values and changes, block position, generated length, segment position, two dataset
+    flags); normalization statistics from a separate draw of the same distribution (dataset flags: mean
+    the constant, scale 1); weights U(-1/sqrt(fan_in), 1/sqrt(fan_in)) as a freshly initialized Linear."""
+    g = rng(seed)
+    hidden = to_bf16_bits((g.standard_normal((n, d_hid)) * 1.5).astype(np.float32))
+
+    def feats(m):
+        p1 = g.uniform(0.05, 1.0, m)
+        ent = g.uniform(0.0, 3.0, m)
+        p1_0 = g.uniform(0.05, 1.0, m)
+        ent0 = g.uniform(0.0, 3.0, m)
+        cols = [g.integers(0, 2, m), g.uniform(0, 1, m), g.integers(1, 33, m), g.integers(0, 2, m), p1, np.log(p1),
+                ent, -ent, g.uniform(0, 1, m) * p1, np.minimum(1.0, p1 + g.uniform(0, 0.5, m)), p1_0, -ent0,
+                p1 - p1_0, ent0 - ent, g.integers(0, 32, m), g.integers(0, 513, m), g.uniform(0, 1, m),
+                np.ones(m), np.zeros(m)]
+        return np.stack(cols, 1)[:, :n_sc].astype(np.float32)
+
+    scalars = feats(n)
+    ref = feats(4096)
+    mu = np.concatenate([np.zeros(d_hid), ref.mean(0)]).astype(np.float32)
+    sd = ref.std(0)
+    sigma = np.concatenate([np.full(d_hid, 1.5), np.where(sd > 1e-6, sd, 1.0)]).astype(np.float32)
+    d_in = d_hid + n_sc
+
+    def lin(o, i):
+        bound = 1.0 / np.sqrt(i)
+        return (g.uniform(-bound, bound, (o, i)).astype(np.float32), g.uniform(-bound, bound, o).astype(np.float32))
+
+    W1, b1 = lin(H, d_in)
+    W2, b2 = lin(H, H)
+    W3, b3 = lin(H, H)
+    w4, b4 = lin(1, H)
+    return SurvivalInputs(hidden, scalars, mu, sigma, W1, b1, W2, b2, W3, b3, w4, float(b4[0]))
