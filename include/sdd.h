@@ -259,6 +259,37 @@ int sdd_schedule(const float* log_q, const int32_t* draft, const int32_t* block_
                  int n_special, int rep_max, int32_t* D, int32_t* K, int32_t* K_hat, int32_t* reason,
                  sdd_stream_t stream);
 
+/* ---- survival predictor ------------------------------------------------- */
+
+/* Weights of the learned survival predictor (Appendix "Predictor Details"):
+ * inputs x = [h, s], h the drafter's LM-head input (d_hid values, bf16), s
+ * the n_sc scalar features (fp32), normalized as (x - mu) / sigma; MLP
+ * d_in -> H -> H -> H -> 1 (d_in = d_hid + n_sc; the paper: 3584 + 19 = 3603
+ * and H = 256) with GELU (erf form) after each hidden layer.  Device fp32
+ * tensors in PyTorch Linear layout [out][in]: W1 [H][d_in], W2 and W3 [H][H],
+ * w4 [H]; biases b1..b3 [H]; mu, sigma [d_in].  Caller-owned; read only. */
+typedef struct {
+  int d_hid, n_sc, H; /* H a multiple of 16, at most 256 */
+  const float *mu, *sigma, *W1, *b1, *W2, *b2, *W3, *b3, *w4;
+  float b4;
+} sdd_mlp;
+
+/* Workspace bytes for sdd_survival_mlp over n positions. */
+int sdd_survival_workspace_bytes(const sdd_mlp* m, int n, size_t* bytes);
+
+/* Survival scores of n draft positions (Sec. 4.2: the marginal a_j or the
+ * conditional s_j estimate, depending on which targets the weights were
+ * trained on): log_score[i] = log sigmoid(z_i) fp32 [n] (device), the log
+ * position score that sdd_schedule takes (SDD_SIG_MARGINAL or
+ * SDD_SIG_CONDITIONAL); logit (may be NULL) receives z_i.  Inputs (device):
+ * hidden bf16 [n][d_hid], scalars fp32 [n][n_sc].  Sums run in a fixed order
+ * in fp32 (MFMA), so results are bit-reproducible.  The workspace (zeroed
+ * once by sdd_workspace_init, 256-byte aligned) is left reusable.
+ * Errors: SDD_EINVAL for a bad shape or NULL pointer, SDD_ENOMEM for a small
+ * workspace. */
+int sdd_survival_mlp(const sdd_mlp* m, const uint16_t* hidden, const float* scalars, int n, float* log_score,
+                     float* logit, void* ws, size_t ws_bytes, sdd_stream_t stream);
+
 /* ---- launch timing (benchmarks) ----------------------------------------- */
 
 /* Kernel classes */
@@ -272,6 +303,7 @@ int sdd_schedule(const float* log_q, const int32_t* draft, const int32_t* block_
 #define SDD_PROF_ACCEPT 128u
 #define SDD_PROF_CONF 256u
 #define SDD_PROF_SCHED 512u
+#define SDD_PROF_MLP 1024u
 
 /* Starts timing: until sdd_profile_stop, every every-th launch (1: each) of
  * the classes in class_mask is bracketed by two HIP events on its own stream

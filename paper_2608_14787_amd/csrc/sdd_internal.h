@@ -234,7 +234,7 @@ namespace sdd {
 enum ProfClass : unsigned {
   PROF_EMBED = 1u, PROF_GEMM_QKV = 2u, PROF_ATTN = 4u, PROF_GEMM_O = 8u, PROF_GEMM_GU = 16u,
   PROF_GEMM_DOWN = 32u, PROF_GEMM_LM = 64u, PROF_ACCEPT = 128u, PROF_CONF = 256u,
-  PROF_SCHED = 512u
+  PROF_SCHED = 512u, PROF_MLP = 1024u
 };
 // Bracket a launch with events on its stream when timing of cls is enabled.
 void prof_begin(unsigned cls, hipStream_t st);

@@ -1,0 +1,263 @@
+// Survival predictor inference (Appendix "Predictor Details"; its sigmoid output is the marginal or
+// conditional survival score of Sec. 4.2): per draft position x = [h, s] (the drafter's LM-head input and
+// the scalar features), normalized as (x - mu) / sigma, then d_in -> H -> H -> H -> 1 with GELU (erf form)
+// after each hidden layer; the output is log sigmoid(z), the log position score the skip scheduler reads.
+//
+// Three launches, every contraction on fp32 MFMA (v_mfma_f32_16x16x4_f32, weights as the A operand so a
+// wave's accumulators hold 16 output columns x 16 positions):
+//   layer1_kernel: (16-column tile, k-split, 64-row tile) per workgroup; the input slice is normalized while
+//                  it is staged into LDS; partial tiles are published with device-coherent 16-byte stores
+//                  and the last arriving split of a tile adds them in split order, adds the bias, applies
+//                  GELU and writes h1.
+//   dense_kernel:  (16-column tile, 64-row tile) per workgroup over K = H, bias + GELU (layers 2 and 3);
+//                  the layer-3 launch also forms each tile's share of w4 . h3, and the last tile of a row
+//                  tile adds the shares in tile order, adds b4 and writes log sigmoid(z).
+// The k-order of every sum is fixed, so results are bit-reproducible.
+#include "sdd_internal.h"
+
+namespace sdd {
+namespace {
+
+constexpr int kMlpThreads = 256;
+constexpr int kRowTile = 64;   // positions per workgroup (4 waves x 16)
+constexpr int kKc = 128;       // k-chunk staged in LDS by layer 1
+constexpr int kMaxH = 256;
+
+struct MlpArgs {
+  const uint16_t* hidden;  // [n][d_hid] bf16
+  const float* scalars;    // [n][n_sc]
+  const float *mu, *sigma, *W1, *b1, *W2, *b2, *W3, *b3, *w4;
+  float b4;
+  int n, d_hid, n_sc, d_in, H;
+  int S, kc_split;  // layer-1 k-splits and k per split (a multiple of kKc)
+  float* part;      // layer-1 partial tiles [rt][ct][S][64][16]
+  float* h1;        // [rt*64][H]
+  float* h2;
+  float* zpart;     // [rt][ct][64]
+  int* cnt1;        // [rt][ct]
+  int* cnt3;        // [rt]
+  float* log_score;
+  float* logit;
+};
+
+#pragma clang fp contract(off)
+__device__ inline float gelu_erf(float x) { return 0.5f * x * (1.f + erff(x * 0.70710678118654752f)); }
+__device__ inline float log_sigmoid(float z) { return z >= 0.f ? -log1pf(__expf(-z)) : z - log1pf(__expf(z)); }
+// h . w over 4 consecutive columns, added left to right
+__device__ inline float dot4(const float* h, const float* w) { return ((h[0] * w[0] + h[1] * w[1]) + h[2] * w[2]) + h[3] * w[3]; }
+#pragma clang fp contract(on)
+
+__device__ inline f32x4 mfma4(float a, float b, f32x4 c) { return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0); }
+
+__global__ void __launch_bounds__(kMlpThreads) layer1_kernel(MlpArgs a) {
+  __shared__ float sW[16][kKc + 1];
+  __shared__ float sX[kRowTile][kKc + 1];
+  __shared__ int s_last;
+  const int CT = a.H / 16;
+  const int ct = blockIdx.x % CT, s = (blockIdx.x / CT) % a.S, rt = blockIdx.x / (CT * a.S);
+  const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
+  const int c0 = ct * 16, r0 = rt * kRowTile;
+  const int kb = s * a.kc_split, ke = min(a.d_in, kb + a.kc_split);
+  f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int k0 = kb; k0 < ke; k0 += kKc) {
+    // stage W1[c0..c0+16)[k0..k0+kKc) and the normalized inputs of 64 rows (zeros past d_in and n)
+    for (int i = tid; i < 16 * kKc; i += kMlpThreads) {
+      const int c = i / kKc, k = k0 + i % kKc;
+      sW[c][i % kKc] = k < ke ? a.W1[(int64_t)(c0 + c) * a.d_in + k] : 0.f;
+    }
+    for (int i = tid; i < kRowTile * kKc; i += kMlpThreads) {
+      const int r = i / kKc, k = k0 + i % kKc, row = r0 + r;
+      float v = 0.f;
+      if (row < a.n && k < ke) {
+        const float raw = k < a.d_hid ? bf16_to_f32(a.hidden[(int64_t)row * a.d_hid + k])
+                                      : a.scalars[(int64_t)row * a.n_sc + (k - a.d_hid)];
+        v = (raw - a.mu[k]) / a.sigma[k];
+      }
+      sX[r][i % kKc] = v;
+    }
+    __syncthreads();
+#pragma unroll 8
+    for (int kk = 0; kk < kKc; kk += 4)
+      acc = mfma4(sW[lane % 16][kk + lane / 16], sX[wave * 16 + lane % 16][kk + lane / 16], acc);
+    __syncthreads();
+  }
+  // acc[t]: column c0 + 4 (lane / 16) + t, row r0 + 16 wave + lane % 16
+  const __amdgpu_buffer_rsrc_t prs = __builtin_amdgcn_make_buffer_rsrc(a.part, 0, 0x7fffffff, kBufferRsrcWord3);
+  const int tile = rt * CT + ct;
+  const int row_l = wave * 16 + lane % 16, col4 = 4 * (lane / 16);
+  const int off = (((tile * a.S + s) * kRowTile + row_l) * 16 + col4) * 4;  // bytes (< 2^31: checked on the host)
+  __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, acc), prs, off, 0, kCoherentCpol);
+  if (!arrive_last(&a.cnt1[tile], a.S, &s_last)) return;
+  // last split of this tile: sum the splits in order, bias, GELU
+  f32x4 sum = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int ss = 0; ss < a.S; ++ss) {
+    const int o = (((tile * a.S + ss) * kRowTile + row_l) * 16 + col4) * 4;
+    sum += __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(prs, o, 0, kCoherentCpol));
+  }
+  const int row = r0 + row_l;
+  if (row < a.n) {
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      const int c = c0 + col4 + t;
+      a.h1[(int64_t)row * a.H + c] = gelu_erf(sum[t] + a.b1[c]);
+    }
+  }
+}
+
+template <bool LAST>
+__global__ void __launch_bounds__(kMlpThreads) dense_kernel(MlpArgs a, const float* hin, const float* W, const float* b,
+                                                            float* hout) {
+  __shared__ float sW[16][kMaxH + 1];
+  __shared__ float sX[kRowTile][kMaxH + 1];
+  __shared__ int s_last;
+  const int CT = a.H / 16;
+  const int ct = blockIdx.x % CT, rt = blockIdx.x / CT;
+  const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
+  const int c0 = ct * 16, r0 = rt * kRowTile, H = a.H;
+  for (int i = tid; i < 16 * H; i += kMlpThreads) sW[i / H][i % H] = W[(int64_t)(c0 + i / H) * H + i % H];
+  for (int i = tid; i < kRowTile * H; i += kMlpThreads) {
+    const int r = i / H, row = r0 + r;
+    sX[r][i % H] = row < a.n ? hin[(int64_t)row * H + i % H] : 0.f;
+  }
+  __syncthreads();
+  f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int kk = 0; kk < H; kk += 4) acc = mfma4(sW[lane % 16][kk + lane / 16], sX[wave * 16 + lane % 16][kk + lane / 16], acc);
+  const int row_l = wave * 16 + lane % 16, col4 = 4 * (lane / 16), row = r0 + row_l;
+  float hv[4];
+#pragma unroll
+  for (int t = 0; t < 4; ++t) hv[t] = gelu_erf(acc[t] + b[c0 + col4 + t]);
+  if constexpr (!LAST) {
+    if (row < a.n)
+#pragma unroll
+      for (int t = 0; t < 4; ++t) hout[(int64_t)row * H + c0 + col4 + t] = hv[t];
+  } else {
+    // this tile's share of w4 . h3 for the row: the lane's 4 columns in order, then the 4 lane groups in order
+    const float zs = dot4(hv, a.w4 + c0 + col4);
+    const float z1 = __shfl(zs, lane % 16 + 16), z2 = __shfl(zs, lane % 16 + 32), z3 = __shfl(zs, lane % 16 + 48);
+    const float tz = ((zs + z1) + z2) + z3;  // lanes 0..15: rows 16 wave + lane
+    const __amdgpu_buffer_rsrc_t zrs = __builtin_amdgcn_make_buffer_rsrc(a.zpart, 0, 0x7fffffff, kBufferRsrcWord3);
+    if (lane < 16)
+      __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, tz), zrs, ((rt * CT + ct) * kRowTile + row_l) * 4,
+                                            0, kCoherentCpol);
+    if (!arrive_last(&a.cnt3[rt], CT, &s_last)) return;
+    if (tid < kRowTile && r0 + tid < a.n) {
+      float z = 0.f;
+      for (int t = 0; t < CT; ++t)
+        z += __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(zrs, ((rt * CT + t) * kRowTile + tid) * 4, 0,
+                                                                            kCoherentCpol));
+      z += a.b4;
+      a.log_score[r0 + tid] = log_sigmoid(z);
+      if (a.logit) a.logit[r0 + tid] = z;
+    }
+  }
+}
+
+struct MlpWs {
+  size_t part, h1, h2, zpart, cnt1, cnt3, total;
+};
+
+MlpWs mlp_ws(int n, int H, int S) {
+  const int RT = (int)ceil_div(n > 0 ? n : 1, kRowTile), CT = H / 16;
+  MlpWs w{};
+  size_t o = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = o;
+    o += (bytes + 255) / 256 * 256;
+    return at;
+  };
+  w.cnt1 = take((size_t)RT * CT * sizeof(int));
+  w.cnt3 = take((size_t)RT * sizeof(int));
+  w.part = take((size_t)RT * CT * S * kRowTile * 16 * sizeof(float));
+  w.h1 = take((size_t)RT * kRowTile * H * sizeof(float));
+  w.h2 = take((size_t)RT * kRowTile * H * sizeof(float));
+  w.zpart = take((size_t)RT * CT * kRowTile * sizeof(float));
+  w.total = o;
+  return w;
+}
+
+// k-splits of layer 1: about 256 workgroups in all, each split a whole number of LDS chunks
+void layer1_splits(int n, int H, int d_in, int& S, int& kc_split) {
+  const int RT = (int)ceil_div(n > 0 ? n : 1, kRowTile), CT = H / 16;
+  int want = std::max(1, 256 / (RT * CT));
+  kc_split = (int)ceil_div(ceil_div(d_in, want), kKc) * kKc;
+  S = (int)ceil_div(d_in, kc_split);
+}
+
+int check_mlp(const sdd_mlp* m) {
+  SDD_REQUIRE(m != nullptr, "NULL predictor");
+  SDD_REQUIRE(m->d_hid >= 0 && m->n_sc >= 0 && m->d_hid + m->n_sc > 0, "bad input width %d + %d", m->d_hid, m->n_sc);
+  SDD_REQUIRE(m->H >= 16 && m->H <= kMaxH && m->H % 16 == 0, "hidden width %d: a multiple of 16 in [16, %d]", m->H, kMaxH);
+  SDD_REQUIRE(m->mu && m->sigma && m->W1 && m->b1 && m->W2 && m->b2 && m->W3 && m->b3 && m->w4, "NULL predictor tensor");
+  return SDD_OK;
+}
+
+}  // namespace
+}  // namespace sdd
+
+using namespace sdd;
+
+extern "C" int sdd_survival_workspace_bytes(const sdd_mlp* m, int n, size_t* bytes) {
+  int rc = check_mlp(m);
+  if (rc) return rc;
+  SDD_REQUIRE(bytes != nullptr && n >= 0, "bad arguments");
+  int S, kc;
+  layer1_splits(n, m->H, m->d_hid + m->n_sc, S, kc);
+  *bytes = mlp_ws(n, m->H, S).total;
+  return SDD_OK;
+}
+
+extern "C" int sdd_survival_mlp(const sdd_mlp* m, const uint16_t* hidden, const float* scalars, int n,
+                                float* log_score, float* logit, void* ws, size_t ws_bytes, sdd_stream_t stream) {
+  int rc = check_mlp(m);
+  if (rc) return rc;
+  SDD_REQUIRE(n >= 0, "n = %d", n);
+  if (n == 0) return SDD_OK;
+  SDD_REQUIRE(log_score && (m->d_hid == 0 || hidden) && (m->n_sc == 0 || scalars), "NULL input or output");
+  MlpArgs a{};
+  a.hidden = hidden;
+  a.scalars = scalars;
+  a.mu = m->mu;
+  a.sigma = m->sigma;
+  a.W1 = m->W1;
+  a.b1 = m->b1;
+  a.W2 = m->W2;
+  a.b2 = m->b2;
+  a.W3 = m->W3;
+  a.b3 = m->b3;
+  a.w4 = m->w4;
+  a.b4 = m->b4;
+  a.n = n;
+  a.d_hid = m->d_hid;
+  a.n_sc = m->n_sc;
+  a.d_in = m->d_hid + m->n_sc;
+  a.H = m->H;
+  layer1_splits(n, a.H, a.d_in, a.S, a.kc_split);
+  const MlpWs L = mlp_ws(n, a.H, a.S);
+  SDD_REQUIRE(ws != nullptr && ws_bytes >= L.total, "predictor workspace needs %zu bytes, got %zu", L.total, ws_bytes);
+  SDD_REQUIRE((uintptr_t)ws % 256 == 0, "workspace must be 256-byte aligned");
+  const int RT = (int)ceil_div(n, kRowTile), CT = a.H / 16;
+  if ((int64_t)RT * CT * a.S * kRowTile * 16 * 4 >= (int64_t(1) << 31))
+    return fail(SDD_EUNSUPPORTED, "%d positions exceed the 32-bit partial offsets", n);
+  char* w = reinterpret_cast<char*>(ws);
+  a.part = reinterpret_cast<float*>(w + L.part);
+  a.h1 = reinterpret_cast<float*>(w + L.h1);
+  a.h2 = reinterpret_cast<float*>(w + L.h2);
+  a.zpart = reinterpret_cast<float*>(w + L.zpart);
+  a.cnt1 = reinterpret_cast<int*>(w + L.cnt1);
+  a.cnt3 = reinterpret_cast<int*>(w + L.cnt3);
+  a.log_score = log_score;
+  a.logit = logit;
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  prof_begin(PROF_MLP, st);
+  hipLaunchKernelGGL(layer1_kernel, dim3(RT * CT * a.S), dim3(kMlpThreads), 0, st, a);
+  prof_end(PROF_MLP, st);
+  if ((rc = check_launch("layer1_kernel"))) return rc;
+  prof_begin(PROF_MLP, st);
+  hipLaunchKernelGGL(dense_kernel<false>, dim3(RT * CT), dim3(kMlpThreads), 0, st, a, a.h1, a.W2, a.b2, a.h2);
+  prof_end(PROF_MLP, st);
+  if ((rc = check_launch("dense_kernel"))) return rc;
+  prof_begin(PROF_MLP, st);
+  hipLaunchKernelGGL(dense_kernel<true>, dim3(RT * CT), dim3(kMlpThreads), 0, st, a, a.h2, a.W3, a.b3, nullptr);
+  prof_end(PROF_MLP, st);
+  return check_launch("dense_kernel");
+}

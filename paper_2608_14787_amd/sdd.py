@@ -65,6 +65,8 @@ _SIGS = {
     "sdd_accept": (I, [P, P, I, P, I, SZ, P, I, I, I, I, I, F, P, P, P, P, SZ, P]),
     "sdd_confidence_prefix": (I, [P, I, SZ, I, I, I, F, P, P, P, P, P, SZ, P]),
     "sdd_schedule": (I, [P, P, P, I, I, I, C.c_double, C.c_double, I, I, P, I, I, P, P, P, P, P]),
+    "sdd_survival_workspace_bytes": (I, [P, I, P]),
+    "sdd_survival_mlp": (I, [P, P, P, I, P, P, P, SZ, P]),
     "sdd_profile_start": (I, [C.c_uint, I, I]),
     "sdd_profile_read": (I, [C.c_uint, P, P, P, P]),
     "sdd_profile_stop": (I, []),
@@ -72,7 +74,7 @@ _SIGS = {
 
 PROF_EMBED, PROF_GEMM_QKV, PROF_ATTN, PROF_GEMM_O = 1, 2, 4, 8
 PROF_GEMM_GATEUP, PROF_GEMM_DOWN, PROF_GEMM_LM, PROF_ACCEPT, PROF_CONF = 16, 32, 64, 128, 256
-PROF_SCHED = 512
+PROF_SCHED, PROF_MLP = 512, 1024
 SIG_RAW, SIG_MARGINAL, SIG_CONDITIONAL = 0, 1, 2
 (SKIP_OK, SKIP_STALE, SKIP_NO_CANDIDATE, SKIP_SHORT, SKIP_SHORT_BLOCK, SKIP_SPECIAL,
  SKIP_REPEAT) = range(7)
@@ -198,6 +200,41 @@ def schedule(log_q: torch.Tensor, D: torch.Tensor, signal: int, eta_b: float, et
                               float(eta_c), k_min, s_max, _ptr(special), n_special, rep_max, _ptr(D),
                               _ptr(K), _ptr(Kh), _ptr(rs), _stream(stream)))
     return K, Kh, rs
+
+
+class MlpDesc(C.Structure):
+    _fields_ = [("d_hid", C.c_int), ("n_sc", C.c_int), ("H", C.c_int), ("mu", P), ("sigma", P), ("W1", P),
+                ("b1", P), ("W2", P), ("b2", P), ("W3", P), ("b3", P), ("w4", P), ("b4", C.c_float)]
+
+
+class SurvivalMLP:
+    """Survival-predictor weights as device fp32 tensors (torch-owned) and their sdd_mlp descriptor."""
+
+    def __init__(self, mu, sigma, W1, b1, W2, b2, W3, b3, w4, b4: float, d_hid: int, device="cuda"):
+        t = lambda a: torch.as_tensor(a, dtype=torch.float32).contiguous().to(device)
+        self.tensors = [t(x) for x in (mu, sigma, W1, b1, W2, b2, W3, b3, w4)]
+        H = self.tensors[3].numel()
+        d_in = self.tensors[0].numel()
+        self.desc = MlpDesc(d_hid, d_in - d_hid, H, *[C.c_void_p(x.data_ptr()) for x in self.tensors], float(b4))
+        self.device = device
+
+    def workspace(self, n: int) -> torch.Tensor:
+        out = C.c_size_t()
+        _check(lib().sdd_survival_workspace_bytes(C.byref(self.desc), n, C.byref(out)))
+        ws = torch.empty(max(int(out.value), 256), dtype=torch.uint8, device=self.device)
+        workspace_init(ws)
+        return ws
+
+    def __call__(self, hidden: torch.Tensor, scalars: torch.Tensor | None, *, ws=None, out=None, logit=None,
+                 stream=None) -> torch.Tensor:
+        """log sigmoid scores fp32 [n] for hidden bf16 [n, d_hid] and scalars fp32 [n, n_sc]."""
+        n = hidden.shape[0]
+        if ws is None:
+            ws = self.workspace(n)
+        ls = out if out is not None else torch.empty(n, dtype=torch.float32, device=hidden.device)
+        _check(lib().sdd_survival_mlp(C.byref(self.desc), _ptr(hidden), _ptr(scalars), n, _ptr(ls), _ptr(logit),
+                                      _ptr(ws), ws.numel(), _stream(stream)))
+        return ls
 
 
 def profile_start(class_mask: int, max_launches: int = 65536, every: int = 1):
