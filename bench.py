@@ -72,6 +72,8 @@ def parse():
     p.add_argument("--warmup", type=int, default=2)
     p.add_argument("--workload", default="qwen32b", choices=["qwen32b", "qwen7b", "tiny"])
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--no-next-rows", action="store_true", help="skip the timing of the scheduler, residual draw and "
+                                                               "survival predictor workloads")
     p.add_argument("--drafts", default="greedy", choices=["greedy", "random"])
     p.add_argument("--all-kernels", action="store_true", help="report every kernel class (extra pass)")
     p.add_argument("--copy-calibration", action="store_true",
@@ -117,6 +119,75 @@ def cpu_baseline(shape: W.ModelShape, gamma: int) -> dict:
             "sample": (f"{n_calls} gamma={gamma} verify calls ({gamma + 1} rows) through 1 of {shape.n_layers} layers "
                        f"plus the LM head, 16-token cache, fp64 oracle: {t:.2f} s per call, scaled by the MAC ratio "
                        f"{scale:.1f} to {call_s:.1f} s per full call")}
+
+
+def next_rows(sdd, torch, reps: int = 20) -> dict:
+    """Timing of the rows beyond the verify call, each on its own workload (the workloads follow the input
+    recipes of the parity tests).  Each figure is the average over `reps` back-to-back calls bracketed by
+    one pair of events on the calls' stream."""
+    out = {}
+
+    def timed(fn):
+        for i in range(3):
+            fn(i)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for i in range(reps):
+            fn(i)
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps * 1e3  # us per call
+
+    dev = "cuda"
+    # residual draw (RATIO_SAMPLE) vs plain RATIO on the acceptance workload [16, 33, 151936] bf16;
+    # four input sets (1.3 GB) rotate so that the 256 MB Infinity Cache does not serve the reads
+    B, gamma, V = 16, 32, 151936
+    g = torch.Generator(device=dev)
+    g.manual_seed(5)
+    sets = []
+    for _ in range(4):
+        p = (torch.randn((B, gamma + 1, V), generator=g, device=dev) * 4).to(torch.bfloat16)
+        q = (p[:, :gamma].float() + torch.randn((B, gamma, V), generator=g, device=dev) * 0.7).to(torch.bfloat16)
+        sets.append((p, q.contiguous()))
+    draft = torch.randint(0, V, (B, gamma), generator=g, device=dev, dtype=torch.int32)
+    u = torch.rand((B, gamma + 1), generator=g, device=dev)
+    ws = sdd.rowstats_workspace(B, gamma, V)
+    outs = tuple(torch.empty(B, dtype=torch.int32, device=dev) for _ in range(3))
+    row_bytes = V * 2
+    for name, mode in (("greedy", sdd.GREEDY), ("ratio", sdd.RATIO), ("ratio_sample", sdd.RATIO_SAMPLE)):
+        us = timed(lambda i: sdd.accept(draft, sets[i % 4][0], mode, q=sets[i % 4][1], uniforms=u, ws=ws, out=outs))
+        L = outs[0].cpu().numpy()
+        # bytes: target rows up to the first rejection and the drafter rows they compare (the kernel reads every
+        # row: one pass over [B][33][V] target + [B][32][V] drafter), plus the draw's row L of p and q
+        nbytes = B * (gamma + 1) * row_bytes + (B * gamma * row_bytes if mode != sdd.GREEDY else 0)
+        if mode == sdd.RATIO_SAMPLE:
+            nbytes += int(sum(2 * row_bytes if l < gamma else row_bytes for l in L))
+        out[f"accept_{name}"] = {"workload": f"accept-{B}x{gamma + 1}x{V}-bf16", "us": us, "bytes": nbytes,
+                                 "GB/s": nbytes / (us * 1e-6) / 1e9, "frac_hbm": nbytes / (us * 1e-6) / 1e9 / HBM_PEAK_GBS}
+    del sets
+    # survival predictor, 32 positions of the paper's shape
+    x = W.survival_inputs(seed=1, n=32)
+    mlp = sdd.SurvivalMLP(x.mu, x.sigma, x.W1, x.b1, x.W2, x.b2, x.W3, x.b3, x.w4, x.b4, d_hid=x.hidden_bits.shape[1])
+    hid = torch.from_numpy(x.hidden_bits.view(np.int16)).to(dev).view(torch.bfloat16)
+    sc = torch.from_numpy(x.scalars).to(dev)
+    mws = mlp.workspace(32)
+    ls = torch.empty(32, dtype=torch.float32, device=dev)
+    us = timed(lambda i: mlp(hid, sc, ws=mws, out=ls))
+    H, d_in = x.W1.shape
+    mbytes = 4 * (H * d_in + 2 * H * H + 4 * H + 2 * d_in) + 32 * (x.hidden_bits.shape[1] * 2 + x.scalars.shape[1] * 4)
+    out["survival_mlp"] = {"workload": f"32x{d_in}->{H}->{H}->{H}->1", "us": us, "launches_per_call": 3,
+                           "bytes": mbytes, "GB/s": mbytes / (us * 1e-6) / 1e9, "bound": "latency",
+                           "mfma_flops": 2 * 32 * (H * d_in + 2 * H * H + H)}
+    # skip scheduler, 64 sequences x 32 positions
+    si = W.schedule_inputs(seed=3)
+    lq = torch.from_numpy(si.log_q).to(dev)
+    dr = torch.from_numpy(si.draft).to(dev)
+    D = torch.from_numpy(si.D).to(dev)
+    so = tuple(torch.empty(64, dtype=torch.int32, device=dev) for _ in range(3))
+    us = timed(lambda i: sdd.schedule(lq, D, sdd.SIG_RAW, ETA_B, ETA_C, k_min=K_MIN, s_max=S_MAX, draft=dr, out=so))
+    out["schedule"] = {"workload": "64x32 raw signal", "us": us, "bound": "latency"}
+    return out
 
 
 def main():
@@ -284,8 +355,12 @@ def main():
                  "accept": 128, "confidence": 256, "schedule": 512}
         result["kernels_ms_per_step"] = {k: sdd.profile_read(v)[1] for k, v in names.items()}
         sdd.profile_stop()
+    if not a.no_next_rows:
+        del drafter
+        torch.cuda.empty_cache()
+        result["next_rows"] = next_rows(sdd, torch)
     if not a.no_cpu_baseline:
-        del model, kv, ws, drafter
+        del model, kv, ws
         torch.cuda.empty_cache()
         result["cpu_baseline"] = cpu_baseline(shape, gamma)
     print(json.dumps(result), flush=True)

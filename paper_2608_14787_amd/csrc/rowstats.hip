@@ -100,7 +100,7 @@ struct BlockRed {
 };
 
 template <bool kSum>
-__device__ void block_reduce(float& m, int& a, float& s, int& cnt, int& fl, BlockRed* red) {
+__device__ __attribute__((always_inline)) void block_reduce(float& m, int& a, float& s, int& cnt, int& fl, BlockRed* red) {
   // wave level
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) {
@@ -164,7 +164,7 @@ __device__ void block_reduce(float& m, int& a, float& s, int& cnt, int& fl, Bloc
 
 // Loads this thread's share of a chunk into registers.
 template <typename T, int VEC>
-__device__ inline int load_chunk(const T* row, int base, int n, uint4* regs) {
+__device__ __attribute__((always_inline)) inline int load_chunk(const T* row, int base, int n, uint4* regs) {
   int nv = 0;
 #pragma unroll
   for (int i = 0; i < kMaxVecPerThread; ++i) {
@@ -193,7 +193,7 @@ __device__ inline void unpack(const uint4& r, float* v) {
 // Per-thread statistics over the registers: max, first argmax, non-finite flag,
 // sum exp relative to the thread max, rank count against (zx, x).
 template <typename T, int VEC, bool kSum, bool kCount>
-__device__ inline void thread_stats(const uint4* regs, int nv, int base, float zx, int x, float& m,
+__device__ __attribute__((always_inline)) inline void thread_stats(const uint4* regs, int nv, int base, float zx, int x, float& m,
                                     int& a, float& s, int& cnt, int& fl) {
   m = -INFINITY;
   a = -1;
@@ -241,7 +241,7 @@ struct RowStats {
 // One wave combines the C <= 64 chunk records of a row: lane c loads record c
 // (all loads in flight together), then a fixed butterfly reduces the lanes, so
 // the result is the same in every lane and on every run.
-__device__ inline RowStats combine_row_wave(RowRec* rp, int C, int lane) {
+__device__ __attribute__((always_inline)) inline RowStats combine_row_wave(RowRec* rp, int C, int lane) {
   const bool have = lane < C;
   float m = have ? ld_coherent(&rp[lane].m) : -INFINITY;
   int arg = have ? ld_coherent(&rp[lane].arg) : -1;

@@ -38,10 +38,26 @@ __global__ __launch_bounds__(kSchedThreads) void schedule_kernel(SchedArgs a) {
   const int nb = min(kSchedThreads, a.B - b0);
   const int n = nb * a.gamma;
   const bool need_draft = a.n_special > 0 || a.rep_max >= 2;
-  for (int i = threadIdx.x; i < n; i += kSchedThreads) {
-    const int r = i / a.gamma, c = i - r * a.gamma;
-    s_lq[r * kPad + c] = a.log_q[(size_t)b0 * a.gamma + i];
-    if (need_draft) s_x[r * kPad + c] = a.draft[(size_t)b0 * a.gamma + i];
+  // batches of kU loads per thread issued before any is used (n <= 64 x 64)
+  constexpr int kU = 16;
+  for (int i0 = 0; i0 < n; i0 += kSchedThreads * kU) {
+    float v[kU];
+    int32_t x[kU];
+#pragma unroll
+    for (int u = 0; u < kU; ++u) {
+      const int i = i0 + u * kSchedThreads + (int)threadIdx.x;
+      v[u] = i < n ? a.log_q[(size_t)b0 * a.gamma + i] : 0.f;
+      x[u] = (need_draft && i < n) ? a.draft[(size_t)b0 * a.gamma + i] : 0;
+    }
+#pragma unroll
+    for (int u = 0; u < kU; ++u) {
+      const int i = i0 + u * kSchedThreads + (int)threadIdx.x;
+      if (i < n) {
+        const int r = i / a.gamma, c = i - r * a.gamma;
+        s_lq[r * kPad + c] = v[u];
+        s_x[r * kPad + c] = x[u];
+      }
+    }
   }
   for (int i = threadIdx.x; i < a.n_special; i += kSchedThreads) s_special[i] = a.special[i];
   __syncthreads();

@@ -60,20 +60,30 @@ __global__ void __launch_bounds__(kMlpThreads) layer1_kernel(MlpArgs a) {
   const int kb = s * a.kc_split, ke = min(a.d_in, kb + a.kc_split);
   f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
   for (int k0 = kb; k0 < ke; k0 += kKc) {
-    // stage W1[c0..c0+16)[k0..k0+kKc) and the normalized inputs of 64 rows (zeros past d_in and n)
-    for (int i = tid; i < 16 * kKc; i += kMlpThreads) {
-      const int c = i / kKc, k = k0 + i % kKc;
-      sW[c][i % kKc] = k < ke ? a.W1[(int64_t)(c0 + c) * a.d_in + k] : 0.f;
+    // stage W1[c0..c0+16)[k0..k0+kKc) and the normalized inputs of 64 rows (zeros past d_in and n).
+    // Thread t always takes column k = k0 + t % kKc, rows (or weight columns) t / kKc + 2 u: every load of
+    // the chunk is issued before any is used.
+    const int kl = tid % kKc, k = k0 + kl, rsub = tid / kKc;
+    const bool kin = k < ke;
+    float wv[16 / 2], xv[kRowTile / 2];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) wv[u] = kin ? a.W1[(int64_t)(c0 + rsub + 2 * u) * a.d_in + k] : 0.f;
+    const bool hid = k < a.d_hid;
+#pragma unroll
+    for (int u = 0; u < kRowTile / 2; ++u) {
+      const int row = r0 + rsub + 2 * u;
+      float raw = 0.f;
+      if (kin && row < a.n)
+        raw = hid ? bf16_to_f32(a.hidden[(int64_t)row * a.d_hid + k]) : a.scalars[(int64_t)row * a.n_sc + (k - a.d_hid)];
+      xv[u] = raw;
     }
-    for (int i = tid; i < kRowTile * kKc; i += kMlpThreads) {
-      const int r = i / kKc, k = k0 + i % kKc, row = r0 + r;
-      float v = 0.f;
-      if (row < a.n && k < ke) {
-        const float raw = k < a.d_hid ? bf16_to_f32(a.hidden[(int64_t)row * a.d_hid + k])
-                                      : a.scalars[(int64_t)row * a.n_sc + (k - a.d_hid)];
-        v = (raw - a.mu[k]) / a.sigma[k];
-      }
-      sX[r][i % kKc] = v;
+    const float mu = kin ? a.mu[k] : 0.f, sg = kin ? a.sigma[k] : 1.f;
+#pragma unroll
+    for (int u = 0; u < 8; ++u) sW[rsub + 2 * u][kl] = wv[u];
+#pragma unroll
+    for (int u = 0; u < kRowTile / 2; ++u) {
+      const int row = r0 + rsub + 2 * u;
+      sX[rsub + 2 * u][kl] = (kin && row < a.n) ? (xv[u] - mu) / sg : 0.f;
     }
     __syncthreads();
 #pragma unroll 8
@@ -114,10 +124,34 @@ __global__ void __launch_bounds__(kMlpThreads) dense_kernel(MlpArgs a, const flo
   const int ct = blockIdx.x % CT, rt = blockIdx.x / CT;
   const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
   const int c0 = ct * 16, r0 = rt * kRowTile, H = a.H;
-  for (int i = tid; i < 16 * H; i += kMlpThreads) sW[i / H][i % H] = W[(int64_t)(c0 + i / H) * H + i % H];
-  for (int i = tid; i < kRowTile * H; i += kMlpThreads) {
-    const int r = i / H, row = r0 + r;
-    sX[r][i % H] = row < a.n ? hin[(int64_t)row * H + i % H] : 0.f;
+  // stage the weight slice [16][H] and the input rows [64][H] with 16-byte loads, all issued before use
+  // (H is a multiple of 16: a row is H / 4 float4s)
+  const int H4 = H / 4;
+  f32x4 wv[kMaxH / 64], xv[kMaxH / 4];
+#pragma unroll
+  for (int u = 0; u < kMaxH / 64; ++u) {
+    const int i = tid + kMlpThreads * u;
+    wv[u] = i < 16 * H4 ? *reinterpret_cast<const f32x4*>(W + (int64_t)(c0 + i / H4) * H + 4 * (i % H4)) : f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+#pragma unroll
+  for (int u = 0; u < kMaxH / 4; ++u) {
+    const int i = tid + kMlpThreads * u, r = i / H4;
+    xv[u] = (i < kRowTile * H4 && r0 + r < a.n) ? *reinterpret_cast<const f32x4*>(hin + (int64_t)(r0 + r) * H + 4 * (i % H4))
+                                                 : f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+#pragma unroll
+  for (int u = 0; u < kMaxH / 64; ++u) {
+    const int i = tid + kMlpThreads * u;
+    if (i < 16 * H4)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) sW[i / H4][4 * (i % H4) + e] = wv[u][e];
+  }
+#pragma unroll
+  for (int u = 0; u < kMaxH / 4; ++u) {
+    const int i = tid + kMlpThreads * u;
+    if (i < kRowTile * H4)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) sX[i / H4][4 * (i % H4) + e] = xv[u][e];
   }
   __syncthreads();
   f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
