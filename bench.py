@@ -123,18 +123,23 @@ def cpu_baseline(shape: W.ModelShape, gamma: int) -> dict:
 
 def next_rows(sdd, torch, reps: int = 20) -> dict:
     """Timing of the rows beyond the verify call, each on its own workload (the workloads follow the input
-    recipes of the parity tests).  Each figure is the average over `reps` back-to-back calls bracketed by
-    one pair of events on the calls' stream."""
+    recipes of the parity tests).  Each figure is the average over `reps` back-to-back calls captured in one
+    HIP graph (so that host launch overhead does not separate them), replayed between two events."""
     out = {}
 
     def timed(fn):
         for i in range(3):
             fn(i)
         torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            for i in range(reps):
+                fn(i)
+        graph.replay()
+        torch.cuda.synchronize()
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record()
-        for i in range(reps):
-            fn(i)
+        graph.replay()
         e1.record()
         torch.cuda.synchronize()
         return e0.elapsed_time(e1) / reps * 1e3  # us per call

@@ -11,10 +11,11 @@
 // of drafter row j; skip length = first j with q_j < tau.
 //
 // Both are HBM-bound streams over [B][rows][V] logits.  Each row is split into
-// C equal chunks; one 256-thread workgroup loads its chunk into registers with
-// 16-byte loads (one pass over HBM), reduces max / first-argmax / sum-exp /
-// rank counts in registers, then across the wave with shuffles and across the
-// four waves through LDS, and writes one record.  The last workgroup of a
+// C equal chunks; one 256-thread workgroup streams its chunk with 16-byte
+// loads, four in flight per thread and row (one pass over HBM), keeping running
+// max / first-argmax / online sum-exp / rank counts in registers, reduces them
+// across the wave with shuffles and across the four waves through LDS, and
+// writes one record.  The last workgroup of a
 // sequence to finish (arrival counter) combines that sequence's records in a
 // fixed order, so results are bit-reproducible, and takes the decisions; it
 // resets the counter so the workspace can be reused.
@@ -25,7 +26,7 @@ namespace sdd {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kMaxVecPerThread = 24;
+constexpr int kRecBatch = 512;  // chunk records staged in LDS at a time by the finishing workgroup (16 KB)
 
 struct RowRec {
   float m;    // row max over the chunk (NaN ignored)
@@ -99,29 +100,50 @@ struct BlockRed {
   int f[kThreads / kWave];
 };
 
+// Combines (m2, a2, s2, c2, f2) into (m, a, s, cnt, fl): max with the first argmax, sums relative to the
+// larger max (finite maxima only), counts, flags.  Commutative, so both lanes of a butterfly agree.
+template <bool kSum>
+__device__ __attribute__((always_inline)) inline void stat_combine(float& m, int& a, float& s, int& cnt, int& fl, float m2,
+                                                                   int a2, float s2, int c2, int f2) {
+  if (kSum) {
+    const float mm = fmaxf(m, m2);
+    const float sa = (s > 0.f) ? s * __expf(m - mm) : 0.f;
+    const float sb = (s2 > 0.f) ? s2 * __expf(m2 - mm) : 0.f;
+    s = sa + sb;
+  }
+  const bool bt = better(m2, a2, m, a);
+  m = bt ? m2 : m;
+  a = bt ? a2 : a;
+  cnt += c2;
+  fl |= f2;
+}
+
+template <int CTRL, bool kSum>
+__device__ __attribute__((always_inline)) inline void stat_dpp_step(float& m, int& a, float& s, int& cnt, int& fl) {
+  const float m2 = dpp_f<CTRL>(m), s2 = kSum ? dpp_f<CTRL>(s) : 0.f;
+  const int a2 = dpp_i<CTRL>(a), c2 = dpp_i<CTRL>(cnt), f2 = dpp_i<CTRL>(fl);
+  stat_combine<kSum>(m, a, s, cnt, fl, m2, a2, s2, c2, f2);
+}
+
 template <bool kSum>
 __device__ __attribute__((always_inline)) void block_reduce(float& m, int& a, float& s, int& cnt, int& fl, BlockRed* red) {
-  // wave level
+  // wave level: DPP within rows of 16 (pairs, quads, eights, sixteens), then the four rows in order
+  stat_dpp_step<kDppXor1, kSum>(m, a, s, cnt, fl);
+  stat_dpp_step<kDppXor2, kSum>(m, a, s, cnt, fl);
+  stat_dpp_step<kDppHalfMirror, kSum>(m, a, s, cnt, fl);
+  stat_dpp_step<kDppMirror, kSum>(m, a, s, cnt, fl);
+  {
+    float wm = lane_f(m, 0), ws = lane_f(s, 0);
+    int wa = __builtin_amdgcn_readlane(a, 0), wc = __builtin_amdgcn_readlane(cnt, 0), wf = __builtin_amdgcn_readlane(fl, 0);
 #pragma unroll
-  for (int o = 32; o > 0; o >>= 1) {
-    float m2 = __shfl_xor(m, o);
-    int a2 = __shfl_xor(a, o);
-    int c2 = __shfl_xor(cnt, o);
-    int f2 = __shfl_xor(fl, o);
-    if (kSum) {
-      float s2 = __shfl_xor(s, o);
-      // combine sums relative to the larger max (finite maxima only)
-      float mm = fmaxf(m, m2);
-      float sa = (s > 0.f) ? s * __expf(m - mm) : 0.f;
-      float sb = (s2 > 0.f) ? s2 * __expf(m2 - mm) : 0.f;
-      s = sa + sb;
-    }
-    if (better(m2, a2, m, a)) {
-      m = m2;
-      a = a2;
-    }
-    cnt += c2;
-    fl |= f2;
+    for (int r = 16; r < kWave; r += 16)
+      stat_combine<kSum>(wm, wa, ws, wc, wf, lane_f(m, r), __builtin_amdgcn_readlane(a, r), lane_f(s, r),
+                         __builtin_amdgcn_readlane(cnt, r), __builtin_amdgcn_readlane(fl, r));
+    m = wm;
+    a = wa;
+    s = ws;
+    cnt = wc;
+    fl = wf;
   }
   const int w = threadIdx.x / kWave, lane = threadIdx.x % kWave;
   if (lane == 0) {
@@ -162,25 +184,6 @@ __device__ __attribute__((always_inline)) void block_reduce(float& m, int& a, fl
   }
 }
 
-// Loads this thread's share of a chunk into registers.
-template <typename T, int VEC>
-__device__ __attribute__((always_inline)) inline int load_chunk(const T* row, int base, int n, uint4* regs) {
-  int nv = 0;
-#pragma unroll
-  for (int i = 0; i < kMaxVecPerThread; ++i) {
-    int e = (i * kThreads + (int)threadIdx.x) * VEC;
-    if (e < n) {
-      if constexpr (VEC > 1) {
-        regs[i] = load_nt16(row + base + e);
-      } else {
-        regs[i].x = __builtin_bit_cast(uint32_t, Elem<T>::to_f32(row[base + e]));
-      }
-      nv = i + 1;
-    }
-  }
-  return nv;
-}
-
 template <typename T, int VEC>
 __device__ inline void unpack(const uint4& r, float* v) {
   if constexpr (VEC > 1) {
@@ -190,46 +193,107 @@ __device__ inline void unpack(const uint4& r, float* v) {
   }
 }
 
-// Per-thread statistics over the registers: max, first argmax, non-finite flag,
-// sum exp relative to the thread max, rank count against (zx, x).
-template <typename T, int VEC, bool kSum, bool kCount>
-__device__ __attribute__((always_inline)) inline void thread_stats(const uint4* regs, int nv, int base, float zx, int x, float& m,
-                                    int& a, float& s, int& cnt, int& fl) {
-  m = -INFINITY;
-  a = -1;
-  fl = 0;
-  cnt = 0;
-#pragma unroll
-  for (int i = 0; i < kMaxVecPerThread; ++i) {
-    if (i < nv) {
-      float v[VEC];
-      unpack<T, VEC>(regs[i], v);
-      const int e0 = base + (i * kThreads + (int)threadIdx.x) * VEC;
-#pragma unroll
-      for (int t = 0; t < VEC; ++t) {
-        float z = v[t];
-        if (!__builtin_isfinite(z)) fl = 1;
-        if (!__builtin_isnan(z) && (a < 0 || z > m)) {
-          m = z;
-          a = e0 + t;
-        }
-        if (kCount) cnt += (z > zx || (z == zx && e0 + t < x)) ? 1 : 0;
-      }
-    }
+// One vector of a row: a 16-byte streaming load, or one element (rows that are not 16-byte aligned).
+template <typename T, int VEC>
+__device__ inline uint4 load_vec(const T* row, int e) {
+  if constexpr (VEC > 1) {
+    return load_nt16(row + e);
+  } else {
+    uint4 r;
+    r.x = __builtin_bit_cast(uint32_t, Elem<T>::to_f32(row[e]));
+    return r;
   }
-  s = 0.f;
-  if (kSum && a >= 0 && __builtin_isfinite(m)) {
+}
+
+// Running statistics of the elements a thread has seen, in increasing index order: max and first index of
+// the max over non-NaN values (m, a); sum over finite values of exp(z - mf), mf their max (online: the sum
+// is rescaled when mf grows); rank count against (zx, x); non-finite flag.
+struct ThreadStats {
+  float m, mf, s;
+  int a, cnt, fl;
+};
+
+__device__ inline ThreadStats stats_init() { return ThreadStats{-INFINITY, -INFINITY, 0.f, -1, 0, 0}; }
+
+template <int VEC, bool kSum, bool kCount>
+__device__ __attribute__((always_inline)) inline void stats_update(ThreadStats& st, const float* v, bool valid, int e0,
+                                                                   float zx, int x) {
+  // branch-free: every element takes the same instructions (selects; an invalid vector changes nothing), so
+  // the streaming loop has no divergent blocks and its loads stay in flight
+  float vm = -INFINITY;
 #pragma unroll
-    for (int i = 0; i < kMaxVecPerThread; ++i) {
-      if (i < nv) {
-        float v[VEC];
-        unpack<T, VEC>(regs[i], v);
-#pragma unroll
-        for (int t = 0; t < VEC; ++t)
-          if (__builtin_isfinite(v[t])) s += exp_shift(v[t], m);
-      }
-    }
+  for (int t = 0; t < VEC; ++t) {
+    const float z = v[t];
+    const bool fin = __builtin_isfinite(z);
+    st.fl |= (valid && !fin) ? 1 : 0;
+    vm = (valid && fin) ? fmaxf(vm, z) : vm;
+    const bool take = valid && !__builtin_isnan(z) && (st.a < 0 || z > st.m);
+    st.m = take ? z : st.m;
+    st.a = take ? e0 + t : st.a;
+    if (kCount) st.cnt += (valid && (z > zx || (z == zx && e0 + t < x))) ? 1 : 0;
   }
+  if (kSum) {
+    const float mn = fmaxf(st.mf, vm);  // -inf while no finite value has been seen
+    float add = 0.f;
+#pragma unroll
+    for (int t = 0; t < VEC; ++t) add += (valid && __builtin_isfinite(v[t])) ? exp_shift(v[t], mn) : 0.f;
+    const float scale = st.mf > -INFINITY ? exp_shift(st.mf, mn) : 0.f;
+    st.s = mn > -INFINITY ? st.s * scale + add : st.s;
+    st.mf = mn;
+  }
+}
+
+// Streams this thread's vectors of [base, base + n) of a row (and of the drafter row) with kDepth to
+// 2 kDepth 16-byte loads of each in flight, updating the running statistics.  Vector i of the thread starts
+// at element base + (i * kThreads + threadIdx.x) * VEC.  The loads are unconditional (an index past the
+// thread's last vector re-reads that vector, an L2 hit, and its values are not used) and the trip count is
+// uniform over the workgroup, so the compiler can wait for exactly the older group.
+template <typename T, typename TQ, int VEC, bool kSum, bool kCount, bool kQ>
+__device__ __attribute__((always_inline)) inline void stream_stats(const T* row, const TQ* qrow, int base, int n, float zx,
+                                                                   int x, ThreadStats& st, ThreadStats& qst) {
+  constexpr int kDepth = kQ ? 2 : 4;  // two rows streamed in the ratio mode: fewer registers, more workgroups
+  const int nvec = n / VEC;  // n is a multiple of VEC (VEC > 1 only when V is); n > 0
+  // trip count uniform over the workgroup; a thread's vectors past its last one re-read that one (valid = 0)
+  const int nvt = nvec > (int)threadIdx.x ? (nvec - (int)threadIdx.x + kThreads - 1) / kThreads : 0;
+  const int nvmax = (nvec + kThreads - 1) / kThreads;
+  const int last = max(nvt - 1, 0);
+  const int tofs = nvt > 0 ? (int)threadIdx.x : 0;  // a thread with no vector reads the chunk's first one
+  auto elem = [&](int i) { return base + (min(i, last) * kThreads + tofs) * VEC; };
+  const bool hq = kQ && qrow != nullptr;
+  // two register buffers of kDepth vectors: the next group's loads are issued (and kept ahead of the
+  // arithmetic by a scheduling barrier) before the current group is consumed
+  uint4 pa[kDepth], pb[kDepth], qa[kQ ? kDepth : 1], qb[kQ ? kDepth : 1];
+  auto load_group = [&](int i, uint4* pv, uint4* qv) {
+#pragma unroll
+    for (int d = 0; d < kDepth; ++d) {
+      pv[d] = load_vec<T, VEC>(row, elem(i + d));
+      if (kQ) qv[d] = hq ? load_vec<TQ, VEC>(qrow, elem(i + d)) : uint4{0, 0, 0, 0};
+    }
+    __builtin_amdgcn_sched_barrier(0);
+  };
+  auto use_group = [&](int i, const uint4* pv, const uint4* qv) {
+#pragma unroll
+    for (int d = 0; d < kDepth; ++d) {
+      float v[VEC], w[VEC];
+      unpack<T, VEC>(pv[d], v);
+      if (kQ) unpack<TQ, VEC>(qv[d], w);
+      const int e = base + ((i + d) * kThreads + (int)threadIdx.x) * VEC;
+      const bool valid = i + d < nvt;
+      stats_update<VEC, kSum, kCount>(st, v, valid, e, zx, x);
+      if (kQ) stats_update<VEC, true, false>(qst, w, valid && hq, e, 0.f, -1);
+    }
+  };
+  load_group(0, pa, qa);
+  for (int i = 0; i < nvmax; i += 2 * kDepth) {
+    load_group(i + kDepth, pb, qb);
+    use_group(i, pa, qa);
+    if (i + kDepth >= nvmax) break;
+    load_group(i + 2 * kDepth, pa, qa);
+    use_group(i + kDepth, pb, qb);
+  }
+  // the block reduction takes the sum relative to m: they differ only when the row holds +inf (flagged)
+  if (st.m != st.mf) st.s = 0.f;
+  if (kQ && qst.m != qst.mf) qst.s = 0.f;
 }
 
 // Combined statistics of one row.
@@ -238,44 +302,37 @@ struct RowStats {
   int arg, cnt, flags;
 };
 
-// One wave combines the C <= 64 chunk records of a row: lane c loads record c
-// (all loads in flight together), then a fixed butterfly reduces the lanes, so
-// the result is the same in every lane and on every run.
-__device__ __attribute__((always_inline)) inline RowStats combine_row_wave(RowRec* rp, int C, int lane) {
-  const bool have = lane < C;
-  float m = have ? ld_coherent(&rp[lane].m) : -INFINITY;
-  int arg = have ? ld_coherent(&rp[lane].arg) : -1;
-  float sv = have ? ld_coherent(&rp[lane].s) : 0.f;
-  int cnt = have ? ld_coherent(&rp[lane].cnt) : 0;
-  int fl = have ? ld_coherent(&rp[lane].flags) : 0;
-  float qm = have ? ld_coherent(&rp[lane].qm) : -INFINITY;
-  float qs = have ? ld_coherent(&rp[lane].qs) : 0.f;
-  RowStats o;
-  float M = m, QM = qs > 0.f ? qm : -INFINITY;
-  int A = arg;
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) {
-    const float m2 = __shfl_xor(M, off);
-    const int a2 = __shfl_xor(A, off);
-    if (better(m2, a2, M, A)) {
-      M = m2;
-      A = a2;
+// One thread folds the C chunk records of its row (staged in LDS) in chunk order: the max and first argmax,
+// the sums rescaled to the running max, counts and flags.  A fixed order, so results are bit-reproducible.
+__device__ __attribute__((always_inline)) inline RowStats fold_row(const RowRec* rp, int C) {
+  float M = -INFINITY, S = 0.f, QM = -INFINITY, QS = 0.f;
+  int A = -1, cnt = 0, fl = 0;
+  for (int c = 0; c < C; ++c) {
+    const RowRec r = rp[c];
+    if (better(r.m, r.arg, M, A)) {
+      // rescale the running sum to the new max (sums are kept relative to the max of finite values)
+      if (r.s > 0.f) S = (S > 0.f ? S * __expf(M - r.m) : 0.f) + r.s;
+      M = r.m;
+      A = r.arg;
+    } else if (r.s > 0.f) {
+      S += r.s * __expf(r.m - M);
     }
-    QM = fmaxf(QM, __shfl_xor(QM, off));
-    cnt += __shfl_xor(cnt, off);
-    fl |= __shfl_xor(fl, off);
+    if (r.qs > 0.f) {
+      const float qn = fmaxf(QM, r.qm);
+      QS = (QS > 0.f ? QS * __expf(QM - qn) : 0.f) + r.qs * __expf(r.qm - qn);
+      QM = qn;
+    }
+    cnt += r.cnt;
+    fl |= r.flags;
   }
-  float s = sv > 0.f ? sv * __expf(m - M) : 0.f;
-  float q = qs > 0.f ? qs * __expf(qm - QM) : 0.f;
-  s = wave_sum(s);
-  q = wave_sum(q);
+  RowStats o;
   o.m = M;
   o.arg = A;
-  o.s = s;
+  o.s = S;
   o.cnt = cnt;
   o.flags = fl;
   o.qm = QM;
-  o.qs = q;
+  o.qs = QS;
   return o;
 }
 
@@ -288,6 +345,9 @@ __global__ void __launch_bounds__(kThreads) rowstats_kernel(Job job) {
   __shared__ int s_flag[72];
   __shared__ int s_bad[72];
   __shared__ float s_st[72][4];
+  __shared__ int s_x[72];
+  __shared__ float s_zp[72], s_zq[72], s_u[72];
+  __shared__ RowRec s_rec[kRecBatch];
 
   const int c = blockIdx.x % job.C;
   const int rowid = blockIdx.x / job.C;  // b * rows + j
@@ -296,27 +356,21 @@ __global__ void __launch_bounds__(kThreads) rowstats_kernel(Job job) {
   const int n = min(job.chunk, job.V - base);
 
   const T* row = reinterpret_cast<const T*>(job.p) + (size_t)b * job.p_seq_stride + (size_t)j * job.p_row_stride;
+  // the draft token and its value are needed in the stream only by the rank count (top-k)
   int x = -1;
   float zx = 0.f;
-  if (job.draft != nullptr && j < job.gamma) {
+  if (kCount && job.draft != nullptr && j < job.gamma) {
     x = job.draft[(size_t)b * job.gamma + j];
     if (x >= 0 && x < job.V) zx = Elem<T>::to_f32(row[x]);
   }
 
-  uint4 regs[kMaxVecPerThread];
-  int nv = load_chunk<T, VEC>(row, base, n, regs);
-  uint4 qregs[kQ ? kMaxVecPerThread : 1];
-  int qnv = 0;
   const bool has_q = kQ && j < job.gamma;
-  const TQ* qrow = nullptr;
-  if (kQ && has_q) {
-    qrow = reinterpret_cast<const TQ*>(job.q) + (size_t)b * job.q_seq_stride + (size_t)j * job.V;
-    qnv = load_chunk<TQ, VEC>(qrow, base, n, qregs);
-  }
+  const TQ* qrow = has_q ? reinterpret_cast<const TQ*>(job.q) + (size_t)b * job.q_seq_stride + (size_t)j * job.V : nullptr;
+  ThreadStats st = stats_init(), qst = stats_init();
+  stream_stats<T, TQ, VEC, kSum, kCount, kQ>(row, qrow, base, n, zx, x, st, qst);
 
-  float m, s;
-  int a, cnt, fl;
-  thread_stats<T, VEC, kSum, kCount>(regs, nv, base, zx, x, m, a, s, cnt, fl);
+  float m = st.m, s = st.s;
+  int a = st.a, cnt = st.cnt, fl = st.fl;
   block_reduce<kSum>(m, a, s, cnt, fl, &red);
   RowRec rec;
   rec.m = m;
@@ -329,9 +383,8 @@ __global__ void __launch_bounds__(kThreads) rowstats_kernel(Job job) {
   rec.pad = 0;
   if (kQ) {
     __syncthreads();
-    float qm = -INFINITY, qs = 0.f;
-    int qa = -1, qc = 0, qf = 0;
-    if (has_q) thread_stats<TQ, VEC, true, false>(qregs, qnv, base, 0.f, -1, qm, qa, qs, qc, qf);
+    float qm = qst.m, qs = qst.s;
+    int qa = qst.a, qc = 0, qf = qst.fl;
     block_reduce<true>(qm, qa, qs, qc, qf, &red);
     rec.qm = qm;
     rec.qs = qs;
@@ -350,66 +403,93 @@ __global__ void __launch_bounds__(kThreads) rowstats_kernel(Job job) {
   }
   if (!arrive_last(&job.counters[b], job.rows * job.C, &s_last)) return;
 
-  // ---- last workgroup of sequence b: combine and decide, one wave per row ----
-  RowRec* recs = job.recs + (size_t)b * job.rows * job.C;
-  const int wv = threadIdx.x / kWave, ln = threadIdx.x % kWave;
-  for (int t = wv; t < job.rows; t += kThreads / kWave) {
-    const RowStats st = combine_row_wave(recs + t * job.C, job.C, ln);
-    if (ln != 0) continue;
-    const bool bad = (st.flags & 1) != 0;
-    s_arg[t] = st.arg < 0 ? 0 : st.arg;
-    s_flag[t] = bad ? 1 : 0;
-    if (KIND == kAccept && job.sample) {
-      s_bad[t] = bad || (kQ && (st.flags & 4)) ? 1 : 0;
-      s_st[t][0] = st.m;
-      s_st[t][1] = st.s;
-      s_st[t][2] = st.qm;
-      s_st[t][3] = st.qs;
+  // ---- last workgroup of sequence b: combine and decide ----
+  // (1) every row's decision inputs at once (thread t: row t): draft token, uniform, and the target and
+  //     drafter values at the draft token (these two wait only for the token)
+  const int tid = threadIdx.x;
+  const bool need_z = KIND == kAccept ? (job.mode != SDD_GREEDY && job.mode != SDD_TOPK) : job.out_log_pdraft != nullptr;
+  if (tid < job.rows) {
+    int xx = -1;
+    float zp = 0.f, zq = 0.f, uu = 1.f;
+    if (tid < job.gamma && job.draft) {
+      xx = job.draft[(size_t)b * job.gamma + tid];
+      if (KIND == kAccept && kQ) uu = job.u[(size_t)b * job.u_stride + tid];
+      if (xx >= 0 && xx < job.V && need_z) {
+        zp = Elem<T>::to_f32(reinterpret_cast<const T*>(job.p)[(size_t)b * job.p_seq_stride + (size_t)tid * job.p_row_stride + xx]);
+        if (KIND == kAccept && kQ)
+          zq = Elem<TQ>::to_f32(reinterpret_cast<const TQ*>(job.q)[(size_t)b * job.q_seq_stride + (size_t)tid * job.V + xx]);
+      }
     }
-    if (KIND == kAccept) {
-      int pass = 0;
-      if (t < job.gamma) {
-        const int xx = job.draft[(size_t)b * job.gamma + t];
-        if (xx < 0 || xx >= job.V) {
-          pass = 0;
-          s_flag[t] |= 2;
-        } else if (bad || (kQ && (st.flags & 4))) {
-          pass = 0;
-          s_flag[t] |= 1;
-        } else {
-          const T* rr = reinterpret_cast<const T*>(job.p) + (size_t)b * job.p_seq_stride + (size_t)t * job.p_row_stride;
-          const float z = Elem<T>::to_f32(rr[xx]);
-          if (job.mode == SDD_GREEDY) {
-            pass = st.arg == xx;
-          } else if (job.mode == SDD_TOPK) {
-            pass = st.cnt < job.k;
-          } else if (job.mode == SDD_LENIENT) {
-            const float diff = z - st.m;
-            pass = diff >= job.log_len;
-          } else {  // SDD_RATIO: log u < (z - LSE_p) - (zq - LSE_q)
-            const TQ* qr = reinterpret_cast<const TQ*>(job.q) + (size_t)b * job.q_seq_stride + (size_t)t * job.V;
-            const float zq = Elem<TQ>::to_f32(qr[xx]);
-            const float lp = z - (st.m + logf(st.s));
-            const float lq = zq - (st.qm + logf(st.qs));
-            const float uu = job.u[(size_t)b * job.u_stride + t];
-            const float lu = uu > 0.f ? logf(uu) : -INFINITY;
-            pass = lu < lp - lq;
+    s_x[tid] = xx;
+    s_zp[tid] = zp;
+    s_zq[tid] = zq;
+    s_u[tid] = uu;
+  }
+  // (2) chunk records staged into LDS in batches of whole rows (16-byte device-coherent loads, all in
+  //     flight together), then one thread per row folds its records and decides
+  const RowRec* recs = job.recs + (size_t)b * job.rows * job.C;
+  const __amdgpu_buffer_rsrc_t rrs = __builtin_amdgcn_make_buffer_rsrc(const_cast<RowRec*>(recs), 0, 0x7fffffff, kBufferRsrcWord3);
+  const int rows_per_batch = kRecBatch / job.C;  // >= 1: C <= 64 < kRecBatch
+  for (int r0 = 0; r0 < job.rows; r0 += rows_per_batch) {
+    const int r1 = min(job.rows, r0 + rows_per_batch);
+    const int nrec = (r1 - r0) * job.C;
+    __syncthreads();  // the previous batch's readers are done
+    for (int h = tid; h < 2 * nrec; h += kThreads) {
+      const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(rrs, (r0 * job.C) * (int)sizeof(RowRec) + 16 * h, 0, kCoherentCpol);
+      reinterpret_cast<u32x4*>(s_rec)[h] = v;
+    }
+    __syncthreads();
+    const int t = r0 + tid;
+    if (t < r1) {
+      const RowStats st = fold_row(s_rec + tid * job.C, job.C);
+      const bool bad = (st.flags & 1) != 0;
+      s_arg[t] = st.arg < 0 ? 0 : st.arg;
+      s_flag[t] = bad ? 1 : 0;
+      if (KIND == kAccept && job.sample) {
+        s_bad[t] = bad || (kQ && (st.flags & 4)) ? 1 : 0;
+        s_st[t][0] = st.m;
+        s_st[t][1] = st.s;
+        s_st[t][2] = st.qm;
+        s_st[t][3] = st.qs;
+      }
+      const int xx = s_x[t];
+      if (KIND == kAccept) {
+        int pass = 0;
+        if (t < job.gamma) {
+          if (xx < 0 || xx >= job.V) {
+            pass = 0;
+            s_flag[t] |= 2;
+          } else if (bad || (kQ && (st.flags & 4))) {
+            pass = 0;
+            s_flag[t] |= 1;
+          } else {
+            const float z = s_zp[t];
+            if (job.mode == SDD_GREEDY) {
+              pass = st.arg == xx;
+            } else if (job.mode == SDD_TOPK) {
+              pass = st.cnt < job.k;
+            } else if (job.mode == SDD_LENIENT) {
+              const float diff = z - st.m;
+              pass = diff >= job.log_len;
+            } else {  // SDD_RATIO: log u < (z - LSE_p) - (zq - LSE_q)
+              const float lp = z - (st.m + logf(st.s));
+              const float lq = s_zq[t] - (st.qm + logf(st.qs));
+              const float uu = s_u[t];
+              const float lu = uu > 0.f ? logf(uu) : -INFINITY;
+              pass = lu < lp - lq;
+            }
           }
         }
-      }
-      s_pass[t] = pass;
-    } else {
-      const float lc = bad ? __builtin_nanf("") : -logf(st.s);
-      s_pass[t] = (lc >= job.log_tau) ? 1 : 0;
-      if (job.out_log_conf) job.out_log_conf[(size_t)b * job.gamma + t] = lc;
-      if (job.out_log_pdraft && job.draft) {
-        const int xx = job.draft[(size_t)b * job.gamma + t];
-        float lp = __builtin_nanf("");
-        if (!bad && xx >= 0 && xx < job.V) {
-          const T* rr = reinterpret_cast<const T*>(job.p) + (size_t)b * job.p_seq_stride + (size_t)t * job.p_row_stride;
-          lp = Elem<T>::to_f32(rr[xx]) - st.m - logf(st.s);
+        s_pass[t] = pass;
+      } else {
+        const float lc = bad ? __builtin_nanf("") : -logf(st.s);
+        s_pass[t] = (lc >= job.log_tau) ? 1 : 0;
+        if (job.out_log_conf) job.out_log_conf[(size_t)b * job.gamma + t] = lc;
+        if (job.out_log_pdraft && job.draft) {
+          float lp = __builtin_nanf("");
+          if (!bad && xx >= 0 && xx < job.V) lp = s_zp[t] - st.m - logf(st.s);
+          job.out_log_pdraft[(size_t)b * job.gamma + t] = lp;
         }
-        job.out_log_pdraft[(size_t)b * job.gamma + t] = lp;
       }
     }
   }
@@ -680,15 +760,14 @@ int choose_vec(const void* p, size_t seq_stride, size_t row_stride, int V, int e
   return 1;
 }
 
-// Chunks per row: about 2048 workgroups in total, but no chunk smaller than
-// 8192 elements (a workgroup should stream tens of kilobytes) and none larger
-// than the registers of a workgroup hold.
-int chunks_for(int nrows, int V, int vec) {
-  const int per_wg_max = kThreads * vec * kMaxVecPerThread;
-  int c = (int)ceil_div(2048, (int64_t)(nrows > 0 ? nrows : 1));
+// Chunks per row: as many workgroups as can be resident at once (one round: a second, partly empty
+// round would cost a whole workgroup's time), no chunk under 8192 elements, at most 64 (one finishing
+// thread folds a row's records).  resident <= 2048 (8 workgroups on each of 256 CUs) bounds the workspace.
+int chunks_for(int nrows, int V, int resident = 2048) {
+  int c = resident / (nrows > 0 ? nrows : 1);
   c = min(c, (int)ceil_div(V, 8192));
-  c = min(c, 64);  // one wave combines a row's chunk records, a lane per chunk
-  return max(1, max(c, (int)ceil_div(V, per_wg_max)));
+  c = min(c, 64);
+  return max(1, c);
 }
 
 size_t counters_region(int B) { return ((size_t)B * sizeof(int) + 255) / 256 * 256; }
@@ -698,10 +777,11 @@ size_t draw_region(int B) { return (size_t)B * (sizeof(SeqRec) + 64 * sizeof(Res
 // Workspace: [acceptance counters][draw counters][SeqRec x B][ResRec x B x 64][RowRec records]
 size_t rowstats_ws(int B, int rows, int V) {
   size_t best = 0;
-  for (int vec : {1, 4, 8}) {
-    int C = chunks_for(B * rows, V, vec);
-    size_t need = (size_t)B * rows * C * sizeof(RowRec);
-    best = best > need ? best : need;
+  {
+    // rows x chunks <= max(rows, 2048) for any row count (chunks_for gives 1 or at most 2048 / rows), so the
+    // same bound serves the gamma confidence rows and the gamma + 1 acceptance rows
+    const size_t nrec = std::max<size_t>((size_t)B * rows, 2048);
+    best = nrec * sizeof(RowRec);
   }
   return 2 * counters_region(B) + draw_region(B) + best;
 }
@@ -725,11 +805,38 @@ int launch_draw(Job& job, int vec, hipStream_t st) {
   return check_launch("resample_kernel");
 }
 
+// Resident workgroups of one kernel instantiation on the whole device (occupancy x compute units), queried
+// once per instantiation.
+template <typename T, typename TQ, int VEC, int KIND, bool kSum, bool kCount, bool kQ>
+int resident_wgs() {
+  static int cached = 0;
+  if (cached == 0) {
+    int occ = 0, cus = 0, dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, rowstats_kernel<T, TQ, VEC, KIND, kSum, kCount, kQ>, kThreads,
+                                                     0) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || occ < 1 || cus < 1)
+      return 2048;
+    cached = occ * cus;
+  }
+  return cached;
+}
+
+// Chunks per row for this kernel's occupancy; never more than the workspace was sized for.
+inline void fit_chunks(Job& job, int vec, int resident) {
+  const int nrows = job.B * job.rows;
+  const int c = std::min(job.C, chunks_for(nrows, job.V, std::min(resident, 2048)));
+  job.chunk = (int)ceil_div(ceil_div(job.V, c), vec) * vec;
+  job.C = (int)ceil_div(job.V, job.chunk);
+}
+
 template <int KIND, bool kSum, bool kCount, bool kQ, typename T, typename TQ>
 int launch_t(Job& job, int vec, hipStream_t st) {
+  constexpr int kVec = 16 / sizeof(T);
+  fit_chunks(job, vec, vec == kVec ? resident_wgs<T, TQ, kVec, KIND, kSum, kCount, kQ>()
+                                    : resident_wgs<T, TQ, 1, KIND, kSum, kCount, kQ>());
   const int blocks = job.B * job.rows * job.C;
   const unsigned prof = KIND == kAccept ? PROF_ACCEPT : PROF_CONF;
-  constexpr int kVec = 16 / sizeof(T);  // one 16-byte load (choose_vec returns this or 1)
   prof_begin(prof, st);
   if (vec == kVec)
     hipLaunchKernelGGL((rowstats_kernel<T, TQ, kVec, KIND, kSum, kCount, kQ>), dim3(blocks), dim3(kThreads), 0, st, job);
@@ -752,7 +859,7 @@ extern "C" int sdd_rowstats_workspace_bytes(int B, int gamma, int V, size_t* byt
 }
 
 static int setup_ws(Job& job, void* ws, size_t ws_bytes, int vec) {
-  job.C = chunks_for(job.B * job.rows, job.V, vec);
+  job.C = chunks_for(job.B * job.rows, job.V);  // the workspace bound; launch_t fits it to the kernel
   job.chunk = (int)ceil_div(ceil_div(job.V, job.C), vec) * vec;
   job.C = (int)ceil_div(job.V, job.chunk);
   if (job.C > 64) return fail(SDD_EUNSUPPORTED, "vocabulary of %d needs %d chunks per row (at most 64)", job.V, job.C);
