@@ -65,6 +65,7 @@ def lib():
                                    P, P, C.c_int, C.c_int, P, P, P, P]
         L.orc_survival_mlp.argtypes = [P, P, C.c_int, C.c_int, C.c_int, C.c_int, P, P, P, P, P, P, P, P, P,
                                        C.c_float, P, P]
+        L.orc_audit_accumulate.argtypes = [P, P, C.c_int, P]
         _lib = L
     return _lib
 
@@ -280,3 +281,19 @@ def survival_mlp(hidden_bits, scalars, mu, sigma, W1, b1, W2, b2, W3, b3, w4, b4
     if rc != 0:
         raise ValueError("invalid survival_mlp arguments")
     return ls[:n], lg[:n]
+
+
+def audit_accumulate(K, L, acc=None):
+    """Adds the rounds with K > 0 to acc = int64 [4] (|A|, sum K, sum min(K, L), count K <= L); returns acc."""
+    k = np.ascontiguousarray(np.asarray(K, np.int32).reshape(-1))
+    l = np.ascontiguousarray(np.asarray(L, np.int32).reshape(-1))
+    a = np.zeros(4, np.int64) if acc is None else acc
+    if lib().orc_audit_accumulate(_p(k), _p(l), k.size, _p(a)) != 0:
+        raise ValueError("invalid audit arguments")
+    return a
+
+
+def agreement(acc):
+    """(StrictToken, FullPrefix) from accumulated counters; 1.0 when no round skipped (Strict SDD)."""
+    n, sk, smin, full = (int(x) for x in acc)
+    return (smin / sk if sk else 1.0), (full / n if n else 1.0)

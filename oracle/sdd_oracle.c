@@ -24,6 +24,8 @@
  *     raw confidence).
  *   - the survival predictor MLP (Appendix "Predictor Details") whose sigmoid
  *     output is the marginal or conditional survival score (Sec. 4.2).
+ *   - agreement with strict verification, StrictToken and FullPrefix over
+ *     the rounds that commit an unverified prefix (Sec. 3.2).
  *   - the two-gate skip scheduler with its three confidence signals, the
  *     guards and the staleness counter D (Sec. 4.1 candidate skip length and
  *     commit rule, Sec. 4.2 signals, Appendix "Baselines and Sweep Settings").
@@ -866,4 +868,19 @@ int orc_survival_mlp(const uint16_t* hidden, const float* scalars, int n, int d_
     free(x);
   }
   return rc ? -1 : 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Agreement accounting */
+
+int orc_audit_accumulate(const int32_t* K, const int32_t* L, int B, int64_t* acc) {
+  if (!K || !L || !acc || B < 0) return -1;
+  for (int b = 0; b < B; ++b) {
+    if (K[b] <= 0) continue; /* strict round: not in A */
+    acc[0] += 1;
+    acc[1] += K[b];
+    acc[2] += K[b] < L[b] ? K[b] : L[b];
+    acc[3] += K[b] <= L[b] ? 1 : 0;
+  }
+  return 0;
 }

@@ -156,6 +156,14 @@ int orc_survival_mlp(const uint16_t* hidden, const float* scalars, int n, int d_
                      const float* b2, const float* W3, const float* b3, const float* w4, float b4,
                      double* log_score, double* logit);
 
+/* Agreement with strict verification (Sec. 3.2, strict token agreement and
+ * full prefix acceptance equations): over the rounds b with K_b > 0 (the set
+ * A of rounds that commit a nonempty unverified prefix), accumulate
+ * acc[0] += |A|, acc[1] += sum K_b, acc[2] += sum min(K_b, L_b),
+ * acc[3] += sum 1{K_b <= L_b}.  StrictToken = acc[2] / acc[1],
+ * FullPrefix = acc[3] / acc[0] (both 1 when A is empty, as for Strict SDD). */
+int orc_audit_accumulate(const int32_t* K, const int32_t* L, int B, int64_t* acc);
+
 #ifdef __cplusplus
 }
 #endif
