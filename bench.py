@@ -195,6 +195,31 @@ def next_rows(sdd, torch, reps: int = 20) -> dict:
     return out
 
 
+def full_recompute(sdd, torch, model, shape: W.ModelShape, P: int, gamma: int, ws, reps: int = 2) -> dict:
+    """The verifier the paper measures: a forward over the whole sequence (P context tokens + gamma drafts) with
+    no verifier cache, on the verify workload's model; MFMA-bound (prefill-shaped)."""
+    n = P + gamma
+    scratch = sdd.KVCache(model, 1, n + 8)
+    toks = torch.from_numpy(np.concatenate([W.prompt(1, P, shape.vocab), W.prompt(41, gamma, shape.vocab)])).cuda()
+    lg = torch.empty((1, gamma + 1, shape.vocab), dtype=torch.float32, device="cuda")
+    scratch.verify_full(toks, gamma, lg, None, ws)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        scratch.verify_full(toks, gamma, lg, None, ws)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    d, L, hd = shape.d_model, shape.n_layers, shape.head_dim
+    flops = 2.0 * n * layer_params(shape) * L + 2.0 * (gamma + 1) * shape.vocab * d
+    flops += L * shape.n_q_heads * hd * 2.0 * 2.0 * (n * (n + 1) / 2)  # causal QK^T and PV
+    del scratch
+    return {"workload": f"{n} tokens ({P} context + {gamma} drafts), no verifier cache", "ms_per_call": ms,
+            "flops": flops, "TFLOP/s": flops / (ms * 1e-3) / 1e12, "bound": "mfma",
+            "frac_mfma_bf16": flops / (ms * 1e-3) / 2.5e15}
+
+
 def main():
     a = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -364,6 +389,8 @@ def main():
         del drafter
         torch.cuda.empty_cache()
         result["next_rows"] = next_rows(sdd, torch)
+        if a.workload != "tiny":
+            result["next_rows"]["full_recompute_verify"] = full_recompute(sdd, torch, model, shape, P, gamma, ws)
     if not a.no_cpu_baseline:
         del model, kv, ws
         torch.cuda.empty_cache()

@@ -160,6 +160,21 @@ int sdd_verify_block(sdd_model* m, sdd_kv* kv, const int32_t* seq_ids, int n_seq
                      const int32_t* drafts, int gamma, float* logits, int32_t* argmax,
                      void* ws, size_t ws_bytes, sdd_stream_t stream);
 
+/* Full-recompute verification (the verifier the paper measures: no verifier
+ * KV cache, Appendix "Evaluation and Throughput"; rows as in Sec. 3.1).
+ * tokens (device int32 [n]) is one sequence's context followed by its gamma
+ * drafts; every position's K/V is recomputed from scratch into slot 0 of the
+ * caller's scratch cache (max_len >= n; its slot-0 contents are overwritten,
+ * other slots untouched).  Outputs as sdd_verify_block for that one sequence:
+ * logits fp32 [gamma+1][vocab] of positions n-gamma-1 .. n-1 (row j < gamma
+ * scores draft j, row gamma is the bonus position), argmax int32 [gamma+1]
+ * (may be NULL).  The same kernels as the cached call, so the logits equal
+ * those of sdd_verify_block on a cache prefilled with the context.
+ * Errors: SDD_EINVAL (NULL pointer, gamma outside [0, 64], n < gamma + 1),
+ * SDD_ECAPACITY (n > max_len, small workspace). */
+int sdd_verify_full(sdd_model* m, sdd_kv* scratch, const int32_t* tokens, int n, int gamma, float* logits,
+                    int32_t* argmax, void* ws, size_t ws_bytes, sdd_stream_t stream);
+
 /* Commit after acceptance (device int32 arrays): len += accepted_len + 1,
  * pending = next_token (the target's correction or bonus token). */
 int sdd_kv_commit(sdd_kv* kv, const int32_t* seq_ids, int n_seq, const int32_t* accepted_len,
@@ -258,6 +273,15 @@ int sdd_schedule(const float* log_q, const int32_t* draft, const int32_t* block_
                  int signal, double eta_b, double eta_c, int k_min, int s_max, const int32_t* special,
                  int n_special, int rep_max, int32_t* D, int32_t* K, int32_t* K_hat, int32_t* reason,
                  sdd_stream_t stream);
+
+/* Agreement with strict verification (Sec. 3.2, strict token agreement and
+ * full prefix acceptance): for the rounds b with K[b] > 0, acc (device int64
+ * [4], caller-zeroed, accumulated across calls) gains |A| += 1, acc[1] += K,
+ * acc[2] += min(K, L), acc[3] += [K <= L]; K is the committed skip length and
+ * L what strict verification accepts from the same block (a shadow verifier
+ * call).  StrictToken = acc[2] / acc[1], FullPrefix = acc[3] / acc[0].
+ * Errors: SDD_EINVAL for NULL pointers or B < 0. */
+int sdd_audit_accumulate(const int32_t* K, const int32_t* L, int B, int64_t* acc, sdd_stream_t stream);
 
 /* ---- survival predictor ------------------------------------------------- */
 

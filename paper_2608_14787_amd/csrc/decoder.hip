@@ -995,7 +995,7 @@ __global__ void __launch_bounds__(256) embed_kernel(EmbedArgs a) {
       valid = pos < a.max_len;
     } else {
       const int s = m / a.R, r = m % a.R;
-      seq = a.seq_ids[s];
+      seq = a.seq_ids ? a.seq_ids[s] : s;  // no id list: block s is sequence s
       if (seq < 0 || seq >= a.max_batch) {  // refused: no cache slot to read or write
         if (r == 0) atomicOr(a.err, 4);
         seq = 0;
@@ -1519,6 +1519,30 @@ extern "C" int sdd_verify_block(sdd_model* m, sdd_kv* kv, const int32_t* seq_ids
   e.gamma = gamma;
   if ((rc = launch_embed(cx, e, M))) return rc;
   return forward_rows(cx, n_seq, R, logits, argmax);
+}
+
+extern "C" int sdd_verify_full(sdd_model* m, sdd_kv* scratch, const int32_t* tokens, int n, int gamma, float* logits,
+                               int32_t* argmax, void* ws, size_t ws_bytes, sdd_stream_t stream) {
+  SDD_REQUIRE(m && scratch && tokens && logits, "NULL pointer");
+  SDD_REQUIRE(gamma >= 0 && gamma <= 64, "gamma must be in [0, 64]");
+  SDD_REQUIRE(n >= gamma + 1, "%d tokens cannot hold a block of gamma = %d drafts after a context token", n, gamma);
+  if (n > scratch->max_len) return fail(SDD_ECAPACITY, "%d tokens exceed the scratch cache's max_len %d", n, scratch->max_len);
+  // every position's K/V is recomputed into slot 0 of the scratch cache: the context first (prefill caches
+  // positions 0..n-gamma-2 and leaves token n-gamma-1 pending), then the gamma + 1 verify rows
+  int rc = sdd_kv_prefill(m, scratch, 0, tokens, n - gamma, ws, ws_bytes, stream);
+  if (rc) return rc;
+  CallCtx cx;
+  if ((rc = make_ctx(cx, m, scratch, ws, ws_bytes, gamma + 1, reinterpret_cast<hipStream_t>(stream)))) return rc;
+  EmbedArgs e{};
+  e.prefill = 0;
+  e.seq_ids = nullptr;  // block 0 is slot 0
+  e.drafts = gamma > 0 ? tokens + (n - gamma) : nullptr;
+  e.kv_len = scratch->len;
+  e.pending = scratch->pending;
+  e.R = gamma + 1;
+  e.gamma = gamma;
+  if ((rc = launch_embed(cx, e, gamma + 1))) return rc;
+  return forward_rows(cx, 1, gamma + 1, logits, argmax);
 }
 
 extern "C" int sdd_kv_commit(sdd_kv* kv, const int32_t* seq_ids, int n_seq, const int32_t* accepted_len,

@@ -112,6 +112,19 @@ __global__ __launch_bounds__(kSchedThreads) void schedule_kernel(SchedArgs a) {
 
 float log_threshold(double eta) { return eta > 0.0 ? (float)std::log(eta) : -INFINITY; }
 
+// Agreement counters over the rounds that commit an unverified prefix (K > 0): |A|, sum K, sum min(K, L),
+// count K <= L.  Integer atomics: the totals do not depend on the order of the additions.
+__global__ void audit_kernel(const int32_t* K, const int32_t* L, int B, unsigned long long* acc) {
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  if (b >= B) return;
+  const int k = K[b], l = L[b];
+  if (k <= 0) return;
+  atomicAdd(&acc[0], 1ull);
+  atomicAdd(&acc[1], (unsigned long long)k);
+  atomicAdd(&acc[2], (unsigned long long)(k < l ? k : (l > 0 ? l : 0)));
+  if (k <= l) atomicAdd(&acc[3], 1ull);
+}
+
 }  // namespace
 }  // namespace sdd
 
@@ -151,4 +164,13 @@ extern "C" int sdd_schedule(const float* log_q, const int32_t* draft, const int3
   hipLaunchKernelGGL(schedule_kernel, dim3((B + kSchedThreads - 1) / kSchedThreads), dim3(kSchedThreads), 0, st, a);
   prof_end(PROF_SCHED, st);
   return check_launch("schedule_kernel");
+}
+
+extern "C" int sdd_audit_accumulate(const int32_t* K, const int32_t* L, int B, int64_t* acc, sdd_stream_t stream) {
+  SDD_REQUIRE(K && L && acc, "NULL pointer");
+  SDD_REQUIRE(B >= 0, "B = %d", B);
+  if (B == 0) return SDD_OK;
+  hipLaunchKernelGGL(audit_kernel, dim3((B + 255) / 256), dim3(256), 0, reinterpret_cast<hipStream_t>(stream), K, L, B,
+                     reinterpret_cast<unsigned long long*>(acc));
+  return check_launch("audit_kernel");
 }

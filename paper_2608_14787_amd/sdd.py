@@ -65,6 +65,8 @@ _SIGS = {
     "sdd_accept": (I, [P, P, I, P, I, SZ, P, I, I, I, I, I, F, P, P, P, P, SZ, P]),
     "sdd_confidence_prefix": (I, [P, I, SZ, I, I, I, F, P, P, P, P, P, SZ, P]),
     "sdd_schedule": (I, [P, P, P, I, I, I, C.c_double, C.c_double, I, I, P, I, I, P, P, P, P, P]),
+    "sdd_verify_full": (I, [P, P, P, I, I, P, P, P, SZ, P]),
+    "sdd_audit_accumulate": (I, [P, P, I, P, P]),
     "sdd_survival_workspace_bytes": (I, [P, I, P]),
     "sdd_survival_mlp": (I, [P, P, P, I, P, P, P, SZ, P]),
     "sdd_profile_start": (I, [C.c_uint, I, I]),
@@ -237,6 +239,11 @@ class SurvivalMLP:
         return ls
 
 
+def audit_accumulate(K: torch.Tensor, L: torch.Tensor, acc: torch.Tensor, stream=None):
+    """sdd_audit_accumulate into acc (int64 [4] device, zero it once)."""
+    _check(lib().sdd_audit_accumulate(_ptr(K), _ptr(L), K.numel(), _ptr(acc), _stream(stream)))
+
+
 def profile_start(class_mask: int, max_launches: int = 65536, every: int = 1):
     """Brackets every `every`-th launch of the given kernel classes with HIP events until profile_stop()."""
     _check(lib().sdd_profile_start(class_mask, max_launches, every))
@@ -331,6 +338,12 @@ class KVCache:
         _check(lib().sdd_verify_block(self.model.handle, self.handle, _ptr(seq_ids), n_seq,
                                       _ptr(drafts) if gamma else None, gamma, _ptr(logits), _ptr(argmax),
                                       _ptr(ws), ws.numel(), _stream(stream)))
+
+    def verify_full(self, tokens: torch.Tensor, gamma: int, logits: torch.Tensor, argmax: torch.Tensor | None,
+                    ws: torch.Tensor, stream=None):
+        """sdd_verify_full: this cache is the scratch (slot 0 overwritten); tokens int32 [n] = context + drafts."""
+        _check(lib().sdd_verify_full(self.model.handle, self.handle, _ptr(tokens), tokens.numel(), gamma, _ptr(logits),
+                                     _ptr(argmax), _ptr(ws), ws.numel(), _stream(stream)))
 
     def commit(self, seq_ids: torch.Tensor, accepted_len: torch.Tensor, next_token: torch.Tensor, stream=None):
         _check(lib().sdd_kv_commit(self.handle, _ptr(seq_ids), seq_ids.numel(), _ptr(accepted_len),
