@@ -469,19 +469,36 @@ __global__ void __launch_bounds__(kGemmThreads, 1) gemm_kernel(GemmArgs a) {
   const int g_first = (int)(u0 / KT);
   const uint4* W = reinterpret_cast<const uint4*>(a.W);
   const int MC = a.M * C;
-  const char* Xl = a.X + ((int64_t)(a.m0 + lane % 16) * a.ldx + (lane / 16) * EPL) * sizeof(T);
-  const int64_t xrow16 = (int64_t)16 * a.ldx * sizeof(T);
+  // activation fragments by buffer loads: descriptor in scalars, the lane's byte offset in one 32-bit register,
+  // the k-step as a scalar offset, so that no address registers are recomputed in the stream (a recomputed
+  // address register can alias an in-flight load's destination and force a full wait)
+  const __amdgpu_buffer_rsrc_t xrs = __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(a.X), 0, 0x7fffffff, kBufferRsrcWord3);
+  const int xlane = ((a.m0 + lane % 16) * a.ldx + (lane / 16) * EPL) * (int)sizeof(T);  // < 2^31: checked on the host
+  const int xrow16 = 16 * a.ldx * (int)sizeof(T);
+  const __amdgpu_buffer_rsrc_t wrs = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint4*>(W), 0, 0x7fffffff, kBufferRsrcWord3);
+  const int wlane = lane * 16;
 
   // One k-step of column group g: NG contiguous 1 KiB weight tiles and the
   // TB activation fragments.  Loads are unconditional (kt is clamped to the
   // wave's last k-tile, so a tail reloads a tile already read) so that the
   // compiler can wait for exactly the oldest stage.
-  auto load = [&](const uint4* Wg, int kt, int kz, uint4* wa, uint4* xb) {
+  auto load = [&](const uint4* Wg, int woff, int kt, int kz, uint4* wa, uint4* xb) {
     kt = min(kt, kz - 1);
 #pragma unroll
-    for (int nt = 0; nt < NG; ++nt) wa[nt] = load_nt16(Wg + ((int64_t)kt * NG + nt) * kWave);
+    for (int nt = 0; nt < NG; ++nt) {
+      if constexpr (NG == 4) {
+        // buffer loads for this group width: the compiler otherwise reuses a load's address registers as its
+        // destination and must then wait for every load before the next k-step's address
+        wa[nt] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(wrs, wlane, woff + (kt * NG + nt) * kWave * 16,
+                                                                                   kNtCpol));
+      } else {
+        wa[nt] = load_nt16(Wg + ((int64_t)kt * NG + nt) * kWave);
+      }
+    }
 #pragma unroll
-    for (int tb = 0; tb < TB; ++tb) xb[tb] = load16(Xl + tb * xrow16 + (int64_t)kt * KTILE * sizeof(T));
+    for (int tb = 0; tb < TB; ++tb)
+      xb[tb] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(xrs, xlane + tb * xrow16,
+                                                                                 kt * KTILE * (int)sizeof(T), 0));
     // keep the next stages' loads ahead of this stage's MFMAs
     __builtin_amdgcn_sched_barrier(0);
   };
@@ -535,19 +552,35 @@ __global__ void __launch_bounds__(kGemmThreads, 1) gemm_kernel(GemmArgs a) {
   }
   };
 
-  uint32_t u = u0;
-  for (bool first = true;; first = false) {
-    const Seg s = make_seg(u);
-    // ---- stream this segment: four register stages, three in flight ----
-    uint4 wa0[NG], wa1[NG], wa2[NG], wa3[NG], xb0[TB], xb1[TB], xb2[TB], xb3[TB];
-    const uint4* Wg = W + (int64_t)s.g * NG * a.KT * kWave + lane;  // k-step kt: NG contiguous tiles
-    if (s.ka < s.kz) {
-      load(Wg, s.ka, s.kz, wa0, xb0);
-      load(Wg, s.ka + 1, s.kz, wa1, xb1);
-      load(Wg, s.ka + 2, s.kz, wa2, xb2);
+  // Epilogues that read nothing from global memory let the next segment's first loads go out before them,
+  // so that their stores do not stall the next stream (loads and stores complete in order).
+  constexpr bool kEarly = EPI == EPI_SWIGLU || EPI == EPI_LOGITS;
+  uint4 wa0[NG], wa1[NG], wa2[NG], wa3[NG], xb0[TB], xb1[TB], xb2[TB], xb3[TB];
+  auto seg_base = [&](const Seg& sg) { return W + (int64_t)sg.g * NG * a.KT * kWave + lane; };  // k-step kt: NG tiles
+  // the segment's byte offset in the matrix (buffer loads; < 2^31: checked on the host)
+  auto seg_off = [&](const Seg& sg) { return sg.g * NG * a.KT * kWave * 16; };
+  auto issue = [&](const Seg& sg, const uint4* Wsg) {
+    if (sg.ka < sg.kz) {
+      const int wo = seg_off(sg);
+      load(Wsg, wo, sg.ka, sg.kz, wa0, xb0);
+      load(Wsg, wo, sg.ka + 1, sg.kz, wa1, xb1);
+      load(Wsg, wo, sg.ka + 2, sg.kz, wa2, xb2);
     }
-    // the prologue's loads queue behind the first weight loads
-    if (first) prologue();
+  };
+  uint32_t u = u0;
+  Seg s = make_seg(u);  // carried across segments: uniform values only (the lane's pointer is recomputed)
+  if constexpr (kEarly) {
+    issue(s, seg_base(s));
+    prologue();  // the prologue's loads queue behind the first weight loads
+  }
+  for (bool first = true;; first = false) {
+    const uint4* Wg = seg_base(s);
+    const int wo = seg_off(s);
+    // ---- stream this segment: four register stages, three in flight ----
+    if constexpr (!kEarly) {
+      issue(s, Wg);
+      if (first) prologue();
+    }
     f32x4 acc[NACC];
 #pragma unroll
     for (int i = 0; i < NACC; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -560,13 +593,13 @@ __global__ void __launch_bounds__(kGemmThreads, 1) gemm_kernel(GemmArgs a) {
     int kt = s.ka;
     if (kt < s.kz) {
       for (; kt + 4 <= s.kz; kt += 4) {
-        load(Wg, kt + 3, s.kz, wa3, xb3);
+        load(Wg, wo, kt + 3, s.kz, wa3, xb3);
         mma(wa0, xb0);
-        load(Wg, kt + 4, s.kz, wa0, xb0);
+        load(Wg, wo, kt + 4, s.kz, wa0, xb0);
         mma(wa1, xb1);
-        load(Wg, kt + 5, s.kz, wa1, xb1);
+        load(Wg, wo, kt + 5, s.kz, wa1, xb1);
         mma(wa2, xb2);
-        load(Wg, kt + 6, s.kz, wa2, xb2);
+        load(Wg, wo, kt + 6, s.kz, wa2, xb2);
         mma(wa3, xb3);
       }
       // 0..3 k-tiles left, already loaded in stages 0..2
@@ -660,6 +693,11 @@ __global__ void __launch_bounds__(kGemmThreads, 1) gemm_kernel(GemmArgs a) {
       }
     }
 
+    Seg sn = s;
+    if (more) {
+      sn = make_seg(u);
+      if constexpr (kEarly) issue(sn, seg_base(sn));
+    }
     // ---- epilogue on the final tile of column group g ----
     if (fin) {
       if constexpr (EPI == EPI_QKV) epilogue_qkv<T, NG, R>(a, tile, g, s_rs, s_ri);
@@ -668,6 +706,7 @@ __global__ void __launch_bounds__(kGemmThreads, 1) gemm_kernel(GemmArgs a) {
       if constexpr (EPI == EPI_LOGITS) epilogue_logits<NG, R>(a, tile, g, s_rs, s_ri);
     }
     if (!more) break;
+    s = sn;
   }
 }
 
@@ -1179,6 +1218,10 @@ static int run_gemm(CallCtx& cx, int epi, unsigned prof, size_t w_off, int64_t N
   a.n_wg = nblocks;
   if ((U + 1) * nblocks >= (int64_t(1) << 31))
     return fail(SDD_EUNSUPPORTED, "matrix of %lld weight tiles exceeds the 32-bit stream-K bookkeeping", (long long)U);
+  if (ng == 4 && ntiles * 16 * K * (int64_t)m->es >= (int64_t(1) << 31))
+    return fail(SDD_EUNSUPPORTED, "matrix of %lld x %d exceeds the 32-bit buffer offsets", (long long)N, K);
+  if ((int64_t)(M + 64) * K * m->es >= (int64_t(1) << 31))
+    return fail(SDD_EUNSUPPORTED, "activations of %d rows x %d exceed the 32-bit buffer offsets", M, K);
   for (int m0 = 0; m0 < M; m0 += kMaxPassRows) {
     a.m0 = m0;
     a.M = std::min(kMaxPassRows, M - m0);

@@ -106,6 +106,7 @@ __device__ inline T ld_coherent(T* p) {
 // buffer on this GPU family.
 constexpr int kBufferRsrcWord3 = 0x00020000;
 constexpr int kCoherentCpol = 16;  // sc1
+constexpr int kNtCpol = 2;         // nt: streamed once, no cache residency
 // Waits until every memory operation this thread issued has completed.
 __device__ inline void wait_stores() {
   __atomic_signal_fence(__ATOMIC_SEQ_CST);
