@@ -93,6 +93,24 @@ __device__ inline void mma_tile(const uint4& a, const uint4& b, f32x4& acc) {
   }
 }
 
+// bf16 K / V caches, fragment-major.  Per (sequence, KV head) a cache holds ld positions (a multiple of
+// 64) as 32-position steps of 32 x HD elements.  A step is the list of 1 KB blocks that one attention step
+// loads, one block per 16-byte-per-lane load, lane-major (lane l holds elements 8 l .. 8 l + 7), so every
+// load reads whole cache lines:
+//   K block b * HD/32 + kk, lane 16 g + rho: K[32 s + kv_row(rho, b)][32 kk + 8 g + e],  e = 0..7
+//   V block db,             lane 16 g + rho: V[32 s + 8 g + e][16 db + rho],             e = 0..7
+// kv_row(rho, b) is the position that K sub-tile b feeds to MFMA row rho; it leaves the scores of lane
+// group g on positions 8 g .. 8 g + 7 of the step, the positions of that lane's V block entries.
+__device__ inline int kv_row(int rho, int b) { return 8 * (rho / 4) + 4 * b + rho % 4; }
+__device__ inline int64_t kfrag_index(int p, int d, int HD) {
+  const int i = p % 32, rho = 4 * (i / 8) + i % 4, b = (i / 4) % 2;
+  return (int64_t)(p / 32) * 32 * HD + (b * (HD / 32) + d / 32) * 512 + (16 * ((d % 32) / 8) + rho) * 8 + d % 8;
+}
+__device__ inline int64_t vfrag_index(int p, int d, int HD) {
+  const int i = p % 32;
+  return (int64_t)(p / 32) * 32 * HD + (d / 16) * 512 + (16 * (i / 8) + d % 16) * 8 + i % 8;
+}
+
 template <typename T>
 __device__ inline void store_t(char* base, int64_t idx, float v) {
   reinterpret_cast<T*>(base)[idx] = Elem<T>::from_f32(v);
@@ -132,19 +150,24 @@ __device__ void epilogue_qkv(const GemmArgs& a, const float* tile, int g, const 
     const int h = g;
     const bool is_q = h < a.hq, is_k = !is_q && h < a.hq + a.hkv;
     if (!is_q && !is_k) {
-      // V head: lane = row, so that each cached dimension's consecutive
-      // positions are written together (V is cached transposed)
+      // V head: lane = row, so that consecutive positions of a cached
+      // dimension are written together (adjacent in both cache layouts)
       const int mm = lane;
       const bool ok = mm < a.M && ri_s[mm < a.M ? mm : 0].valid;
       const RowInfo ri = ri_s[mm < a.M ? mm : 0];
       const float r = rsl[mm < a.M ? mm : 0];
-      const int64_t base = ((int64_t)ri.seq * a.hkv + (h - a.hq - a.hkv)) * C;
+      const int64_t head = (int64_t)ri.seq * a.hkv + (h - a.hq - a.hkv);
       constexpr int DPW = C / 4;  // dimensions per wave
 #pragma unroll 8
       for (int dd = 0; dd < DPW; ++dd) {
         const int dim = wave * DPW + dd;
         const float y = tile[(mm < R ? mm : 0) * CP + dim] * r;
-        if (ok) store_t<T>(a.vc, (base + dim) * a.kv_ld + ri.pos, y);
+        if (ok) {
+          if constexpr (sizeof(T) == 2)
+            store_t<T>(a.vc, head * a.kv_ld * C + vfrag_index(ri.pos, dim, C), y);
+          else
+            store_t<T>(a.vc, (head * C + dim) * a.kv_ld + ri.pos, y);  // fp32: V^T rows
+        }
       }
       return;
     }
@@ -196,17 +219,19 @@ __device__ void epilogue_qkv(const GemmArgs& a, const float* tile, int g, const 
       const int mm = wave + 4 * j;
       if (mm < a.M && ri_s[mm].valid) {
         const RowInfo ri = ri_s[mm];
-        char* dst;
-        int64_t base;
         if (is_q) {
-          dst = a.q_out;
-          base = ((int64_t)(a.m0 + mm) * a.hq + h) * C;
+          const int64_t base = ((int64_t)(a.m0 + mm) * a.hq + h) * C;
+          store_t<T>(a.q_out, base + lane, y0[j]);
+          if constexpr (C == 128) store_t<T>(a.q_out, base + lane + 64, y1[j]);
+        } else if constexpr (sizeof(T) == 2) {
+          const int64_t base = ((int64_t)ri.seq * a.hkv + (h - a.hq)) * a.kv_ld * C;
+          store_t<T>(a.kc, base + kfrag_index(ri.pos, lane, C), y0[j]);
+          if constexpr (C == 128) store_t<T>(a.kc, base + kfrag_index(ri.pos, lane + 64, C), y1[j]);
         } else {
-          dst = a.kc;
-          base = (((int64_t)ri.seq * a.hkv + (h - a.hq)) * a.kv_ld + ri.pos) * C;
+          const int64_t base = (((int64_t)ri.seq * a.hkv + (h - a.hq)) * a.kv_ld + ri.pos) * C;  // fp32: [pos][hd]
+          store_t<T>(a.kc, base + lane, y0[j]);
+          if constexpr (C == 128) store_t<T>(a.kc, base + lane + 64, y1[j]);
         }
-        store_t<T>(dst, base + lane, y0[j]);
-        if constexpr (C == 128) store_t<T>(dst, base + lane + 64, y1[j]);
       }
     }
   }
@@ -805,25 +830,23 @@ __global__ void __launch_bounds__(256) attention_kernel(AttnArgs a) {
 // holding scores of its own query column, which is the P^T fragment that
 // O^T = V^T P^T takes as its B operand.  Inside a step the K rows are fed in
 // the order that leaves lane group g (lane / 16) holding the 8 consecutive
-// positions 8g..8g+7, so the matching V^T operand (V is cached transposed) is
-// one 16-byte read per lane.  Each wave keeps two steps of K/V loads in
-// flight.  The softmax is online within a wave; the waves' partial
+// positions 8g..8g+7, which are the positions of the lane's V^T operand.  The
+// caches are stored in these fragments' order (kfrag_index, vfrag_index), so
+// every operand load is a contiguous 1 KB block.  Each wave keeps two steps of
+// K/V loads in flight.  The softmax is online within a wave; the waves' partial
 // (max, sum, O) are combined through LDS in wave order.
 constexpr int kAttnWaves = 8;
 constexpr int kXcds = 8;  // XCDs of the MI355X (32 CUs each)
 
 struct AttnMfmaArgs {
   const uint16_t* q;   // [rows][hq][HD]
-  const uint16_t* kc;  // layer base [seq][hkv][ld][HD]
-  const uint16_t* vc;  // layer base [seq][hkv][HD][ld]
+  const uint16_t* kc;  // layer base, per (seq, hkv) ld x HD elements, fragment-major
+  const uint16_t* vc;  // layer base, per (seq, hkv) ld x HD elements, fragment-major
   uint16_t* out;       // [rows][hq*HD]
   const RowInfo* rows;
   int nb, R, hq, hkv, grp, ld, qblocks;  // ld: position stride of the caches (multiple of 64)
   float scale;
 };
-
-// position (within a 32-position step) of MFMA row rho of K sub-tile b
-__device__ inline int attn_pos(int rho, int b) { return 8 * (rho / 4) + 4 * b + rho % 4; }
 
 template <int HD>
 __global__ void __launch_bounds__(kAttnWaves * 64) attention_mfma_kernel(AttnMfmaArgs a) {
@@ -857,34 +880,33 @@ __global__ void __launch_bounds__(kAttnWaves * 64) attention_mfma_kernel(AttnMfm
   const int kv_end = __builtin_amdgcn_readfirstlane(first.valid ? pos_hi + 1 : 0);
   const int64_t head = (int64_t)first.seq * a.hkv + kvh;
   const uint16_t* K = a.kc + head * a.ld * HD;
-  const uint16_t* Vt = a.vc + head * HD * a.ld;
+  const uint16_t* Vt = a.vc + head * a.ld * HD;
   const int g8 = 8 * (lane / 16);
 
-  // One step's operands: K rows for the two 16-row sub-tiles and the V^T rows
-  // of the lane's 8 positions.  The loads are unconditional, so that a step's
-  // loads stay in flight together: K rows past kv_end are clamped to the last
-  // one (their scores are masked), and V^T values at positions at or past
-  // kv_end are zeroed after the load (a V^T read starts at a multiple of 8
-  // below kv_end <= ld, a multiple of 64, so it stays inside its row).
+  // One step's operands: the K fragments of the two 16-row sub-tiles and the
+  // V fragments of the lane's 8 positions, each load one contiguous 1 KB block
+  // of the fragment-major caches.  A step starts below kv_end <= ld and ld is a
+  // multiple of 64, so its blocks lie inside the head's cache.  Entries at
+  // positions at or past kv_end hold stale values: their scores are masked,
+  // and their V values are zeroed after the load (P is 0 there, and 0 times a
+  // stale non-finite value would not be).
   struct StepRegs {
     uint4 kf[2][KK];
     uint4 vf[DB];
   };
   auto load_step = [&](int p, StepRegs& st) {
+    const int64_t so = (int64_t)(p / 32) * 32 * HD + lane * 8;
 #pragma unroll
-    for (int b = 0; b < 2; ++b) {
-      const int kp = min(p + attn_pos(lane % 16, b), kv_end - 1);
+    for (int b = 0; b < 2; ++b)
 #pragma unroll
-      for (int kk = 0; kk < KK; ++kk) st.kf[b][kk] = load16(K + (int64_t)kp * HD + 32 * kk + g8);
-    }
-    const int vp = p + g8;
-    const int nv = kv_end - vp;  // valid positions of the lane's 8 (may be <= 0 or >= 8)
+      for (int kk = 0; kk < KK; ++kk) st.kf[b][kk] = load16(K + so + (b * KK + kk) * 512);
+    const int nv = kv_end - (p + g8);  // valid positions of the lane's 8 (may be <= 0 or >= 8)
     uint32_t mask[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) mask[i] = (2 * i < nv ? 0xFFFFu : 0u) | (2 * i + 1 < nv ? 0xFFFF0000u : 0u);
 #pragma unroll
     for (int db = 0; db < DB; ++db) {
-      const uint4 v = load16(Vt + (int64_t)(16 * db + lane % 16) * a.ld + vp);
+      const uint4 v = load16(Vt + so + db * 512);
       st.vf[db] = make_uint4(v.x & mask[0], v.y & mask[1], v.z & mask[2], v.w & mask[3]);
     }
   };
