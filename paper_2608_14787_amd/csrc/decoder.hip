@@ -249,13 +249,14 @@ __device__ void epilogue_resid(const GemmArgs& a, const float* tile, int g) {
     const int c = lane + k * kWave;
     gv[k] = c < C ? a.g_next[(int64_t)g * C + c] : 0.f;
   }
+  // unconditional loads (padded rows read row 0, columns past C the group's last), all in flight together
 #pragma unroll
   for (int j = 0; j < RPW; ++j) {
     const int mm = wave + 4 * j;
 #pragma unroll
     for (int k = 0; k < NCL; ++k) {
-      const int c = lane + k * kWave;
-      xv[j][k] = (mm < a.M && c < C) ? a.x[(int64_t)(a.m0 + mm) * a.d + (int64_t)g * C + c] : 0.f;
+      const int c = min(lane + k * kWave, C - 1);
+      xv[j][k] = a.x[(int64_t)(a.m0 + (mm < a.M ? mm : 0)) * a.d + (int64_t)g * C + c];
     }
   }
 #pragma unroll
@@ -298,22 +299,30 @@ __device__ void epilogue_swiglu(const GemmArgs& a, const float* tile, int g, con
   constexpr int C = NG * 16, CP = C + 4, P = NG / 2, RPW = R / 4;
   constexpr int NI = (P * 16 + kWave - 1) / kWave;  // gate/up pairs per lane and row
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave), lane = threadIdx.x % kWave;
+  // every row of the padded tile is computed (straight-line code, LDS reads batched); only real rows are stored
+  float hv[RPW][NI];
+#pragma unroll
+  for (int j = 0; j < RPW; ++j) {
+    const int mm = wave + 4 * j;
+    const float r = rsl[mm];
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+      const int idx = min(lane + i * kWave, P * 16 - 1);
+      const int t = idx / 16, jj = idx % 16;
+      const float gt = tile[mm * CP + (2 * t) * 16 + jj] * r;
+      const float up = tile[mm * CP + (2 * t + 1) * 16 + jj] * r;
+      hv[j][i] = gt / (1.f + expf(-gt)) * up;
+    }
+  }
 #pragma unroll
   for (int j = 0; j < RPW; ++j) {
     const int mm = wave + 4 * j;
     if (mm < a.M) {
-      const int m = a.m0 + mm;
-      const float r = rsl[mm];
+      const int64_t row = (int64_t)(a.m0 + mm) * a.dff + (int64_t)g * P * 16;
 #pragma unroll
       for (int i = 0; i < NI; ++i) {
         const int idx = lane + i * kWave;
-        if (idx < P * 16) {
-          const int t = idx / 16, jj = idx % 16;
-          const float gt = tile[mm * CP + (2 * t) * 16 + jj] * r;
-          const float up = tile[mm * CP + (2 * t + 1) * 16 + jj] * r;
-          const float hv = gt / (1.f + expf(-gt)) * up;
-          store_t<T>(a.ffh, (int64_t)m * a.dff + ((int64_t)g * P + t) * 16 + jj, hv);
-        }
+        if (idx < P * 16) store_t<T>(a.ffh, row + idx, hv[j][i]);
       }
     }
   }
@@ -542,39 +551,69 @@ __global__ void __launch_bounds__(kGemmThreads, 1) gemm_kernel(GemmArgs a) {
     s.kz = __builtin_amdgcn_readfirstlane(s.kb + S * (wave + 1) / 4);
     return s;
   };
-  // Row info and RMSNorm row scales of this pass, used by the epilogues.
-  auto prologue = [&]() {
-  if constexpr (EPI == EPI_QKV || EPI == EPI_LOGITS) {
-    if ((int)threadIdx.x < a.M) s_ri[threadIdx.x] = a.rows[a.m0 + threadIdx.x];
-  }
-  if constexpr (EPI != EPI_RESID) {
-    // RMSNorm row scales of the input rows from the producer's per-group sums
-    // of squares: four threads per row take every fourth group (in group
-    // order), then the four partial sums are added in a fixed order.
-    const int ng_in = a.ss_in ? a.ss_groups : 0;
-    const int row = threadIdx.x % kMaxPassRows, q4 = threadIdx.x / kMaxPassRows;
-    float ssum = 0.f;
-    if (row < a.M) {
-      for (int g0 = q4; g0 < ng_in; g0 += 64) {
-        float v[16];
+  // Row info and RMSNorm row scales of this pass, used only by the epilogues.
+  // The scales come from the producer's per-group sums of squares: four
+  // threads per row take every fourth group (in group order), then the four
+  // partial sums are added in a fixed order.  Where registers allow (kPreSS
+  // groups per thread), the loads go out with the first weight loads and are
+  // summed after the first segment's stream, so that the stream does not wait
+  // for them; groups beyond kPreSS are loaded when summed.
+  // (the gate/up GEMM reads the o_proj's narrower groups: more of them)
+  constexpr int kPreSS = (EPI == EPI_RESID || TB > 3) ? 0 : EPI == EPI_SWIGLU ? 20 : 12;
+  float pre_ss[kPreSS > 0 ? kPreSS : 1];
+  int4 pre_ri = {0, 0, 0, 0};  // RowInfo as one 16-byte load
+  static_assert(sizeof(RowInfo) == sizeof(int4), "RowInfo is loaded as one int4");
+  auto prologue_issue = [&]() {
+    if constexpr (EPI == EPI_QKV || EPI == EPI_LOGITS) {
+      if ((int)threadIdx.x < a.M) pre_ri = reinterpret_cast<const int4*>(a.rows)[a.m0 + threadIdx.x];
+    }
+    if constexpr (kPreSS > 0) {
+      const int ng_in = a.ss_in ? a.ss_groups : 0;
+      if (ng_in > 0) {
+        // unconditional loads (rows past M read row 0, groups past ng_in the last group): one batch in flight
+        const int row = threadIdx.x % kMaxPassRows, q4 = threadIdx.x / kMaxPassRows;
+        const int64_t rr = a.m0 + (row < a.M ? row : 0);
 #pragma unroll
-        for (int j = 0; j < 16; ++j) {
-          const int gg = g0 + 4 * j;
-          v[j] = gg < ng_in ? a.ss_in[(int64_t)gg * a.mp + a.m0 + row] : 0.f;
-        }
-#pragma unroll
-        for (int j = 0; j < 16; ++j)
-          if (g0 + 4 * j < ng_in) ssum += v[j];
+        for (int j = 0; j < kPreSS; ++j) pre_ss[j] = a.ss_in[(int64_t)min(q4 + 4 * j, ng_in - 1) * a.mp + rr];
       }
     }
-    s_part4[q4][row] = ssum;
-    __syncthreads();
-    if ((int)threadIdx.x < a.M) {
-      const int t = threadIdx.x;
-      const float tot = (s_part4[0][t] + s_part4[1][t]) + (s_part4[2][t] + s_part4[3][t]);
-      s_rs[t] = ng_in ? 1.f / sqrtf(tot / (float)a.d_in + a.eps) : 1.f;
+  };
+  auto prologue_finish = [&]() {
+    if constexpr (EPI == EPI_QKV || EPI == EPI_LOGITS) {
+      if ((int)threadIdx.x < a.M) s_ri[threadIdx.x] = RowInfo{pre_ri.x, pre_ri.y, pre_ri.z, pre_ri.w};
     }
-  }
+    if constexpr (EPI != EPI_RESID) {
+      const int ng_in = a.ss_in ? a.ss_groups : 0;
+      const int row = threadIdx.x % kMaxPassRows, q4 = threadIdx.x / kMaxPassRows;
+      float ssum = 0.f;
+      if (row < a.M) {
+#pragma unroll
+        for (int j = 0; j < kPreSS; ++j)
+          if (q4 + 4 * j < ng_in) ssum += pre_ss[j];
+        for (int g0 = q4 + 4 * kPreSS; g0 < ng_in; g0 += 64) {
+          float v[16];
+#pragma unroll
+          for (int j = 0; j < 16; ++j) {
+            const int gg = g0 + 4 * j;
+            v[j] = gg < ng_in ? a.ss_in[(int64_t)gg * a.mp + a.m0 + row] : 0.f;
+          }
+#pragma unroll
+          for (int j = 0; j < 16; ++j)
+            if (g0 + 4 * j < ng_in) ssum += v[j];
+        }
+      }
+      s_part4[q4][row] = ssum;
+      __syncthreads();
+      if ((int)threadIdx.x < a.M) {
+        const int t = threadIdx.x;
+        const float tot = (s_part4[0][t] + s_part4[1][t]) + (s_part4[2][t] + s_part4[3][t]);
+        s_rs[t] = ng_in ? 1.f / sqrtf(tot / (float)a.d_in + a.eps) : 1.f;
+      }
+    }
+  };
+  auto prologue = [&]() {
+    prologue_issue();
+    if constexpr (kPreSS == 0) prologue_finish();
   };
 
   // Epilogues that read nothing from global memory let the next segment's first loads go out before them,
@@ -633,6 +672,8 @@ __global__ void __launch_bounds__(kGemmThreads, 1) gemm_kernel(GemmArgs a) {
       if (left > 1) mma(wa1, xb1);
       if (left > 2) mma(wa2, xb2);
     }
+    if constexpr (kPreSS > 0)
+      if (first) prologue_finish();
     const int g = s.g;
     const bool full = s.kb == 0 && s.ke == a.KT;
     const int which = g == g_first ? 0 : 1;
@@ -718,6 +759,12 @@ __global__ void __launch_bounds__(kGemmThreads, 1) gemm_kernel(GemmArgs a) {
       }
     }
 
+    // Every older load has landed by now (the stream's clamped reloads, the
+    // fix-up's partials); waiting for them here, on every path and before the
+    // next segment's loads, tells the compiler so.  Otherwise an epilogue
+    // register that one of them last wrote makes it wait for every load, the
+    // next segment's too.
+    if constexpr (kEarly) __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
     Seg sn = s;
     if (more) {
       sn = make_seg(u);
@@ -1220,6 +1267,10 @@ static void launch_gemm_ng(int ng, int tb, const GemmArgs& a, int nblocks, hipSt
 }
 
 // Runs one GEMM over rows [0, M) in passes of at most 64 rows.
+// Weight bytes one workgroup streams in the time a segment's tail takes
+// (about 9 us at the ~25 GB/s per CU of a full-chip stream).
+constexpr double kTailStreamBytes = 224.0 * 1024;
+
 static int run_gemm(CallCtx& cx, int epi, unsigned prof, size_t w_off, int64_t N, int K, const char* X, GemmArgs a,
                     int M, int ng) {
   const sdd_model* m = cx.m;
@@ -1236,7 +1287,18 @@ static int run_gemm(CallCtx& cx, int epi, unsigned prof, size_t w_off, int64_t N
   a.rows = reinterpret_cast<const RowInfo*>(cx.ws + cx.L.rowinfo);
   a.eps = m->cfg.rms_eps;
   const int64_t U = (int64_t)a.G * a.KT;
-  const int nblocks = (int)std::min<int64_t>(U, cx.L.n_wg);
+  int nblocks = (int)std::min<int64_t>(U, cx.L.n_wg);
+  // With at most one column group per workgroup, equal shares of the whole
+  // unit range leave about a third of the workgroups straddling two groups,
+  // and such a workgroup pays a second tail (reduction, partial publish,
+  // fix-up, epilogue).  Splitting every group into s equal k-ranges over
+  // G x s workgroups gives each workgroup exactly one segment; it is taken
+  // when the longer share costs less stream time than one tail.
+  if (a.G <= cx.L.n_wg) {
+    const int s = std::min(cx.L.n_wg / a.G, a.KT);
+    const double extra_units = (double)a.KT / s - (double)U / nblocks;
+    if (extra_units * ng * 1024 < kTailStreamBytes) nblocks = a.G * s;
+  }
   a.n_wg = nblocks;
   if ((U + 1) * nblocks >= (int64_t(1) << 31))
     return fail(SDD_EUNSUPPORTED, "matrix of %lld weight tiles exceeds the 32-bit stream-K bookkeeping", (long long)U);

@@ -107,6 +107,9 @@ __device__ inline T ld_coherent(T* p) {
 constexpr int kBufferRsrcWord3 = 0x00020000;
 constexpr int kCoherentCpol = 16;  // sc1
 constexpr int kNtCpol = 2;         // nt: streamed once, no cache residency
+// s_waitcnt operand (gfx9 encoding: vmcnt in bits 3:0 and 15:14, expcnt 6:4, lgkmcnt 11:8) that waits for
+// every vector memory operation and leaves the other counters unconstrained
+constexpr int kWaitVmcnt0 = 0x0F70;
 // Waits until every memory operation this thread issued has completed.
 __device__ inline void wait_stores() {
   __atomic_signal_fence(__ATOMIC_SEQ_CST);
