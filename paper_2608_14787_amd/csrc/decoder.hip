@@ -932,11 +932,11 @@ __global__ void __launch_bounds__(kAttnWaves * 64) attention_mfma_kernel(AttnMfm
 
   // One step's operands: the K fragments of the two 16-row sub-tiles and the
   // V fragments of the lane's 8 positions, each load one contiguous 1 KB block
-  // of the fragment-major caches.  A step starts below kv_end <= ld and ld is a
-  // multiple of 64, so its blocks lie inside the head's cache.  Entries at
-  // positions at or past kv_end hold stale values: their scores are masked,
-  // and their V values are zeroed after the load (P is 0 there, and 0 times a
-  // stale non-finite value would not be).
+  // of the fragment-major caches.  A loaded step starts below kv_end <= ld and
+  // ld is a multiple of 64, so its blocks lie inside the head's cache.
+  // Entries at positions at or past kv_end hold stale values: their scores are
+  // masked, and their V values are zeroed where they are used (P is 0 there,
+  // and 0 times a stale non-finite value would not be).
   struct StepRegs {
     uint4 kf[2][KK];
     uint4 vf[DB];
@@ -947,15 +947,8 @@ __global__ void __launch_bounds__(kAttnWaves * 64) attention_mfma_kernel(AttnMfm
     for (int b = 0; b < 2; ++b)
 #pragma unroll
       for (int kk = 0; kk < KK; ++kk) st.kf[b][kk] = load16(K + so + (b * KK + kk) * 512);
-    const int nv = kv_end - (p + g8);  // valid positions of the lane's 8 (may be <= 0 or >= 8)
-    uint32_t mask[4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) mask[i] = (2 * i < nv ? 0xFFFFu : 0u) | (2 * i + 1 < nv ? 0xFFFF0000u : 0u);
-#pragma unroll
-    for (int db = 0; db < DB; ++db) {
-      const uint4 v = load16(Vt + so + db * 512);
-      st.vf[db] = make_uint4(v.x & mask[0], v.y & mask[1], v.z & mask[2], v.w & mask[3]);
-    }
+    for (int db = 0; db < DB; ++db) st.vf[db] = load16(Vt + so + db * 512);
   };
 
   f32x4 o[DB];
@@ -1000,10 +993,16 @@ __global__ void __launch_bounds__(kAttnWaves * 64) attention_mfma_kernel(AttnMfm
     mrun = mnew;
     const uint4 pf = make_uint4((uint32_t)pb[0] | ((uint32_t)pb[1] << 16), (uint32_t)pb[2] | ((uint32_t)pb[3] << 16),
                                 (uint32_t)pb[4] | ((uint32_t)pb[5] << 16), (uint32_t)pb[6] | ((uint32_t)pb[7] << 16));
+    const int nv = kv_end - (p + g8);  // valid positions of the lane's 8 (may be <= 0 or >= 8)
+    uint32_t mask[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) mask[i] = (2 * i < nv ? 0xFFFFu : 0u) | (2 * i + 1 < nv ? 0xFFFF0000u : 0u);
 #pragma unroll
     for (int db = 0; db < DB; ++db) {
+      const uint4 v = st.vf[db];
+      const uint4 vm = make_uint4(v.x & mask[0], v.y & mask[1], v.z & mask[2], v.w & mask[3]);
       o[db] *= alpha;
-      o[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, st.vf[db]), __builtin_bit_cast(bf16x8, pf),
+      o[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, vm), __builtin_bit_cast(bf16x8, pf),
                                                       o[db], 0, 0, 0);
     }
   };
@@ -1011,18 +1010,24 @@ __global__ void __launch_bounds__(kAttnWaves * 64) attention_mfma_kernel(AttnMfm
   // independent of the other rows of the block: a row's result does not
   // depend on how rows are batched, so a block verify reproduces decode steps
   // bit for bit.  Steps past a row's own position are fully masked and leave
-  // its running state unchanged.
+  // its running state unchanged, exactly (the rescale factor is 1, or the
+  // state is still zero): each wave runs an even number of steps, two per
+  // iteration, and every load is unconditional, its step clamped to the last
+  // one below kv_end, so that the compiler waits for exactly the step in use
+  // while the other one's loads stay in flight.
   constexpr int kStride = 32 * kAttnWaves;
+  const int p_last = kv_end > 0 ? (kv_end - 1) / 32 * 32 : 0;  // start of the last step with positions
+  const int n_steps = kv_end > 32 * wave ? (kv_end - 32 * wave + kStride - 1) / kStride : 0;
+  // The loads sit only inside the loop (a first pass issues them and skips
+  // the compute), so that the compiler sees one load order on every path.
   StepRegs s0, s1;
-  int p = 32 * wave;
-  if (p < kv_end) load_step(p, s0);
-  if (p + kStride < kv_end) load_step(p + kStride, s1);
-  for (; p < kv_end; p += 2 * kStride) {
-    step(p, s0);
-    if (p + 2 * kStride < kv_end) load_step(p + 2 * kStride, s0);
-    if (p + kStride >= kv_end) break;
-    step(p + kStride, s1);
-    if (p + 3 * kStride < kv_end) load_step(p + 3 * kStride, s1);
+  int p = 32 * wave - 2 * kStride;
+  const int t_end = kv_end > 0 ? n_steps : -2;
+  for (int t = -2; t < t_end; t += 2, p += 2 * kStride) {
+    if (t >= 0) step(p, s0);
+    load_step(min(p + 2 * kStride, p_last), s0);
+    if (t >= 0) step(p + kStride, s1);
+    load_step(min(p + 3 * kStride, p_last), s1);
   }
   // softmax denominator of query lane%16 over this wave's positions
   float ltot = xor16_op(lrun, [](float x, float y) { return x + y; });
