@@ -436,13 +436,22 @@ __device__ void epilogue_logits(const GemmArgs& a, const float* tile, int g, con
     }
   }
   wave_argmax_n(bv, bi);
+  // one lane per row, so the rows' candidates take two store instructions, not
+  // two per row: with the next segment's loads in flight, a wave's outstanding
+  // memory operations would otherwise exceed the 63 the counter holds, and
+  // issue would stall until those loads land
+  float av = bv[0];
+  int ai = bi[0];
 #pragma unroll
-  for (int j = 0; j < RPW; ++j) {
-    const int mm = wave + 4 * j;
-    if (mm < a.M && lane == 0) {
-      a.amax_v[(int64_t)g * a.mp + a.m0 + mm] = bv[j];
-      a.amax_i[(int64_t)g * a.mp + a.m0 + mm] = bi[j];
+  for (int j = 1; j < RPW; ++j)
+    if (lane == j) {
+      av = bv[j];
+      ai = bi[j];
     }
+  const int mm = wave + 4 * lane;
+  if (lane < RPW && mm < a.M) {
+    a.amax_v[(int64_t)g * a.mp + a.m0 + mm] = av;
+    a.amax_i[(int64_t)g * a.mp + a.m0 + mm] = ai;
   }
 }
 
