@@ -515,7 +515,11 @@ __global__ void __launch_bounds__(kGemmThreads, 1) gemm_kernel(GemmArgs a) {
   // activation fragments by buffer loads: descriptor in scalars, the lane's byte offset in one 32-bit register,
   // the k-step as a scalar offset, so that no address registers are recomputed in the stream (a recomputed
   // address register can alias an in-flight load's destination and force a full wait)
-  const __amdgpu_buffer_rsrc_t xrs = __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(a.X), 0, 0x7fffffff, kBufferRsrcWord3);
+  // The descriptor's range ends at the pass's last row: fragments of the padded rows (33 rows pad to 48) are
+  // out of range, read as zero without a memory access (a row's offset is at least row x ldx elements and
+  // below (row + 1) x ldx, so every real row is in range and every padded one is not)
+  const __amdgpu_buffer_rsrc_t xrs = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<char*>(a.X), 0, (a.m0 + a.M) * a.ldx * (int)sizeof(T), kBufferRsrcWord3);
   const int xlane = ((a.m0 + lane % 16) * a.ldx + (lane / 16) * EPL) * (int)sizeof(T);  // < 2^31: checked on the host
   const int xrow16 = 16 * a.ldx * (int)sizeof(T);
   const __amdgpu_buffer_rsrc_t wrs = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint4*>(W), 0, 0x7fffffff, kBufferRsrcWord3);
