@@ -525,26 +525,26 @@ __global__ void __launch_bounds__(kGemmThreads, 1) gemm_kernel(GemmArgs a) {
   const __amdgpu_buffer_rsrc_t wrs = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint4*>(W), 0, 0x7fffffff, kBufferRsrcWord3);
   const int wlane = lane * 16;
 
-  // One k-step of column group g: NG contiguous 1 KiB weight tiles and the
-  // TB activation fragments.  Loads are unconditional (kt is clamped to the
-  // wave's last k-tile, so a tail reloads a tile already read) so that the
-  // compiler can wait for exactly the oldest stage.
-  auto load = [&](const uint4* Wg, int woff, int kt, int kz, uint4* wa, uint4* xb) {
-    kt = min(kt, kz - 1);
+  // a descriptor with no range: every load through it returns zero without a memory access
+  const __amdgpu_buffer_rsrc_t nrs = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint4*>(W), 0, 0, kBufferRsrcWord3);
+
+  // One k-step of column group g: NG contiguous 1 KiB weight tiles and the TB
+  // activation fragments, all buffer loads (descriptors in scalars, the lane's
+  // offset in one register, the k-step as a scalar offset: recomputed address
+  // registers could alias an in-flight load's destination and force a wait for
+  // every load).  The loads are unconditional, so that the compiler can wait
+  // for exactly the oldest stage; a k-step past the wave's range (the stream's
+  // last stages) selects the empty descriptor and so costs no memory traffic.
+  auto load = [&](int woff, int kt, int kz, uint4* wa, uint4* xb) {
+    const bool in = kt < kz;
+    const __amdgpu_buffer_rsrc_t wd = in ? wrs : nrs, xd = in ? xrs : nrs;
 #pragma unroll
-    for (int nt = 0; nt < NG; ++nt) {
-      if constexpr (NG == 4) {
-        // buffer loads for this group width: the compiler otherwise reuses a load's address registers as its
-        // destination and must then wait for every load before the next k-step's address
-        wa[nt] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(wrs, wlane, woff + (kt * NG + nt) * kWave * 16,
-                                                                                   kNtCpol));
-      } else {
-        wa[nt] = load_nt16(Wg + ((int64_t)kt * NG + nt) * kWave);
-      }
-    }
+    for (int nt = 0; nt < NG; ++nt)
+      wa[nt] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(wd, wlane, woff + (kt * NG + nt) * kWave * 16,
+                                                                                 kNtCpol));
 #pragma unroll
     for (int tb = 0; tb < TB; ++tb)
-      xb[tb] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(xrs, xlane + tb * xrow16,
+      xb[tb] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(xd, xlane + tb * xrow16,
                                                                                  kt * KTILE * (int)sizeof(T), 0));
     // keep the next stages' loads ahead of this stage's MFMAs
     __builtin_amdgcn_sched_barrier(0);
@@ -633,29 +633,25 @@ __global__ void __launch_bounds__(kGemmThreads, 1) gemm_kernel(GemmArgs a) {
   // so that their stores do not stall the next stream (loads and stores complete in order).
   constexpr bool kEarly = EPI == EPI_SWIGLU || EPI == EPI_LOGITS;
   uint4 wa0[NG], wa1[NG], wa2[NG], wa3[NG], xb0[TB], xb1[TB], xb2[TB], xb3[TB];
-  auto seg_base = [&](const Seg& sg) { return W + (int64_t)sg.g * NG * a.KT * kWave + lane; };  // k-step kt: NG tiles
   // the segment's byte offset in the matrix (buffer loads; < 2^31: checked on the host)
   auto seg_off = [&](const Seg& sg) { return sg.g * NG * a.KT * kWave * 16; };
-  auto issue = [&](const Seg& sg, const uint4* Wsg) {
-    if (sg.ka < sg.kz) {
-      const int wo = seg_off(sg);
-      load(Wsg, wo, sg.ka, sg.kz, wa0, xb0);
-      load(Wsg, wo, sg.ka + 1, sg.kz, wa1, xb1);
-      load(Wsg, wo, sg.ka + 2, sg.kz, wa2, xb2);
-    }
+  auto issue = [&](const Seg& sg) {  // the first three stages (a wave with an empty range loads nothing)
+    const int wo = seg_off(sg);
+    load(wo, sg.ka, sg.kz, wa0, xb0);
+    load(wo, sg.ka + 1, sg.kz, wa1, xb1);
+    load(wo, sg.ka + 2, sg.kz, wa2, xb2);
   };
   uint32_t u = u0;
-  Seg s = make_seg(u);  // carried across segments: uniform values only (the lane's pointer is recomputed)
+  Seg s = make_seg(u);  // carried across segments: uniform values only
   if constexpr (kEarly) {
-    issue(s, seg_base(s));
+    issue(s);
     prologue();  // the prologue's loads queue behind the first weight loads
   }
   for (bool first = true;; first = false) {
-    const uint4* Wg = seg_base(s);
     const int wo = seg_off(s);
     // ---- stream this segment: four register stages, three in flight ----
     if constexpr (!kEarly) {
-      issue(s, Wg);
+      issue(s);
       if (first) prologue();
     }
     f32x4 acc[NACC];
@@ -670,13 +666,13 @@ __global__ void __launch_bounds__(kGemmThreads, 1) gemm_kernel(GemmArgs a) {
     int kt = s.ka;
     if (kt < s.kz) {
       for (; kt + 4 <= s.kz; kt += 4) {
-        load(Wg, wo, kt + 3, s.kz, wa3, xb3);
+        load(wo, kt + 3, s.kz, wa3, xb3);
         mma(wa0, xb0);
-        load(Wg, wo, kt + 4, s.kz, wa0, xb0);
+        load(wo, kt + 4, s.kz, wa0, xb0);
         mma(wa1, xb1);
-        load(Wg, wo, kt + 5, s.kz, wa1, xb1);
+        load(wo, kt + 5, s.kz, wa1, xb1);
         mma(wa2, xb2);
-        load(Wg, wo, kt + 6, s.kz, wa2, xb2);
+        load(wo, kt + 6, s.kz, wa2, xb2);
         mma(wa3, xb3);
       }
       // 0..3 k-tiles left, already loaded in stages 0..2
@@ -781,7 +777,7 @@ __global__ void __launch_bounds__(kGemmThreads, 1) gemm_kernel(GemmArgs a) {
     Seg sn = s;
     if (more) {
       sn = make_seg(u);
-      if constexpr (kEarly) issue(sn, seg_base(sn));
+      if constexpr (kEarly) issue(sn);
     }
     // ---- epilogue on the final tile of column group g ----
     if (fin) {
@@ -1320,7 +1316,8 @@ static int run_gemm(CallCtx& cx, int epi, unsigned prof, size_t w_off, int64_t N
   a.n_wg = nblocks;
   if ((U + 1) * nblocks >= (int64_t(1) << 31))
     return fail(SDD_EUNSUPPORTED, "matrix of %lld weight tiles exceeds the 32-bit stream-K bookkeeping", (long long)U);
-  if (ng == 4 && ntiles * 16 * K * (int64_t)m->es >= (int64_t(1) << 31))
+  // weight buffer offsets, k-steps up to 4 past a wave's range included
+  if ((int64_t)a.G * ng * (a.KT + 4) * 1024 >= (int64_t(1) << 31))
     return fail(SDD_EUNSUPPORTED, "matrix of %lld x %d exceeds the 32-bit buffer offsets", (long long)N, K);
   if ((int64_t)(M + 64) * K * m->es >= (int64_t(1) << 31))
     return fail(SDD_EUNSUPPORTED, "activations of %d rows x %d exceed the 32-bit buffer offsets", M, K);
