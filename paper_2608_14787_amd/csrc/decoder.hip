@@ -909,6 +909,7 @@ __global__ void __launch_bounds__(kAttnWaves * 64) attention_mfma_kernel(AttnMfm
   constexpr int KK = HD / 32, DB = HD / 16;
   __shared__ float s_o[kAttnWaves][16][HD + 1];
   __shared__ float s_m[kAttnWaves][16], s_l[kAttnWaves][16], s_f[kAttnWaves][16], s_L[16];
+  __shared__ int s_keep;
   touch_kernargs<AttnMfmaArgs>();
   // Workgroups are dispatched to the XCDs round-robin by linear id; all query
   // blocks of one (sequence, KV head) get ids of one residue mod kXcds, so they
@@ -1027,6 +1028,28 @@ __global__ void __launch_bounds__(kAttnWaves * 64) attention_mfma_kernel(AttnMfm
   constexpr int kStride = 32 * kAttnWaves;
   const int p_last = kv_end > 0 ? (kv_end - 1) / 32 * 32 : 0;  // start of the last step with positions
   const int n_steps = kv_end > 32 * wave ? (kv_end - 32 * wave + kStride - 1) / kStride : 0;
+  // The head's query blocks all walk the steps in the same order at about the
+  // same time, so they would miss in L2 together.  First each of them loads a
+  // different share of the head's cache (step s goes to query block s mod
+  // qblocks, its 1 KB blocks spread over the waves) so that the later steps
+  // of every query block find it in L2.  Plain (cached) loads whose values
+  // only feed a flag that is never expected to be set; they are issued before
+  // the stream's own loads and land while its first steps wait.
+  constexpr int kPre = 4;  // blocks per wave
+  constexpr int kBlk = 2 * KK + DB;  // 1 KB blocks per step and cache: K then V
+  uint4 pre[kPre];
+  {
+    const int n_steps_all = (kv_end + 31) / 32;
+#pragma unroll
+    for (int i = 0; i < kPre; ++i) {
+      const int j = wave + kAttnWaves * i;         // this workgroup's j-th block
+      const int st = qb + a.qblocks * (j / (2 * kBlk));
+      const int bi = j % (2 * kBlk);
+      const int stc = st < n_steps_all ? st : 0;   // past the end: step 0 again (in range, already wanted)
+      const uint16_t* src = bi < kBlk ? K : Vt;
+      pre[i] = load16(src + (int64_t)stc * 32 * HD + (bi % kBlk) * 512 + lane * 8);  // unconditional (one load order)
+    }
+  }
   // The loads sit only inside the loop (a first pass issues them and skips
   // the compute), so that the compiler sees one load order on every path.
   StepRegs s0, s1;
@@ -1037,6 +1060,12 @@ __global__ void __launch_bounds__(kAttnWaves * 64) attention_mfma_kernel(AttnMfm
     load_step(min(p + 2 * kStride, p_last), s0);
     if (t >= 0) step(p + kStride, s1);
     load_step(min(p + 3 * kStride, p_last), s1);
+  }
+  {
+    uint32_t x = 0;
+#pragma unroll
+    for (int i = 0; i < kPre; ++i) x ^= pre[i].x ^ pre[i].w;
+    if (x == 0x9e3779b9u) s_keep = 1;
   }
   // softmax denominator of query lane%16 over this wave's positions
   float ltot = xor16_op(lrun, [](float x, float y) { return x + y; });
