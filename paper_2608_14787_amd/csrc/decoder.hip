@@ -909,7 +909,6 @@ __global__ void __launch_bounds__(kAttnWaves * 64) attention_mfma_kernel(AttnMfm
   constexpr int KK = HD / 32, DB = HD / 16;
   __shared__ float s_o[kAttnWaves][16][HD + 1];
   __shared__ float s_m[kAttnWaves][16], s_l[kAttnWaves][16], s_f[kAttnWaves][16], s_L[16];
-  __shared__ int s_keep;
   touch_kernargs<AttnMfmaArgs>();
   // Workgroups are dispatched to the XCDs round-robin by linear id; all query
   // blocks of one (sequence, KV head) get ids of one residue mod kXcds, so they
@@ -1033,8 +1032,8 @@ __global__ void __launch_bounds__(kAttnWaves * 64) attention_mfma_kernel(AttnMfm
   // different share of the head's cache (step s goes to query block s mod
   // qblocks, its 1 KB blocks spread over the waves) so that the later steps
   // of every query block find it in L2.  Plain (cached) loads whose values
-  // only feed a flag that is never expected to be set; they are issued before
-  // the stream's own loads and land while its first steps wait.
+  // are only consumed by an empty asm statement; they are issued before the
+  // stream's own loads and land while its first steps wait.
   constexpr int kPre = 4;  // blocks per wave
   constexpr int kBlk = 2 * KK + DB;  // 1 KB blocks per step and cache: K then V
   uint4 pre[kPre];
@@ -1065,7 +1064,7 @@ __global__ void __launch_bounds__(kAttnWaves * 64) attention_mfma_kernel(AttnMfm
     uint32_t x = 0;
 #pragma unroll
     for (int i = 0; i < kPre; ++i) x ^= pre[i].x ^ pre[i].w;
-    if (x == 0x9e3779b9u) s_keep = 1;
+    asm volatile("" ::"v"(x));  // the values are consumed, so the loads stay
   }
   // softmax denominator of query lane%16 over this wave's positions
   float ltot = xor16_op(lrun, [](float x, float y) { return x + y; });
