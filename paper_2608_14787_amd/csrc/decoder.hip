@@ -78,6 +78,10 @@ struct GemmArgs {
   int V;
   float* amax_v;
   int* amax_i;
+  // the forward's next GEMM (NULL: none), whose first k-steps a workgroup that
+  // only contributed a partial loads into L2 before it ends
+  const char* Wn;
+  int KTn, Gn, ngn, nwg_n;
 };
 
 template <typename T>
@@ -122,6 +126,35 @@ __device__ inline void store_t(char* base, int64_t idx, float v) {
 // workgroup whose share contains unit x.
 __device__ inline int unit_owner(uint32_t x, uint32_t U, uint32_t n) { return (int)(((x + 1) * n + U - 1) / U) - 1; }
 __device__ inline uint32_t unit_start(uint32_t w, uint32_t U, uint32_t n) { return w * U / n; }
+
+// Loads into L2 the first three k-steps of the segment that workgroup
+// blockIdx.x of the next GEMM streams first, each wave the quarter that wave
+// streams there.  Workgroup w runs on XCD w mod 8 in both launches, so the
+// lines land in the L2 that serves them.  Plain (cached) loads whose values are
+// consumed by an empty asm statement.
+__device__ inline void prefetch_next(const GemmArgs& a, int wave, int lane) {
+  const uint32_t KTn = (uint32_t)a.KTn, Un = (uint32_t)a.Gn * KTn, n = (uint32_t)a.nwg_n, w = blockIdx.x;
+  const uint32_t v0 = unit_start(w, Un, n), v1 = unit_start(w + 1, Un, n);
+  const uint32_t g = v0 / KTn;
+  const int kb = (int)(v0 - g * KTn);
+  const int ke = (int)std::min<uint32_t>(KTn, kb + (v1 - v0));
+  const int ka = kb + (ke - kb) * wave / 4, kz = kb + (ke - kb) * (wave + 1) / 4;
+  if (ka >= kz) return;
+  const uint4* base = reinterpret_cast<const uint4*>(a.Wn) + (int64_t)g * a.ngn * a.KTn * kWave + lane;
+  uint4 v[3][8];  // unconditional loads (k-step clamped to the wave's last, tile to the group's last)
+#pragma unroll
+  for (int st = 0; st < 3; ++st) {
+    const int kt = min(ka + st, kz - 1);
+#pragma unroll
+    for (int nt = 0; nt < 8; ++nt) v[st][nt] = base[((int64_t)kt * a.ngn + min(nt, a.ngn - 1)) * kWave];
+  }
+  uint32_t x = 0;
+#pragma unroll
+  for (int st = 0; st < 3; ++st)
+#pragma unroll
+    for (int nt = 0; nt < 8; ++nt) x ^= v[st][nt].x ^ v[st][nt].w;
+  asm volatile("" ::"v"(x));
+}
 
 // Epilogues run on the final [rows][C] tile of one column group (LDS, row
 // stride C + 4).  Each wave owns rows wave, wave + 4, ...; a row's reductions
@@ -779,6 +812,10 @@ __global__ void __launch_bounds__(kGemmThreads, 1) gemm_kernel(GemmArgs a) {
       sn = make_seg(u);
       if constexpr (kEarly) issue(sn);
     }
+    // A workgroup whose last segment only contributed a partial is done; it
+    // loads the next GEMM's first k-steps into L2 while the group's last
+    // arriver reduces and runs the epilogue.
+    if (!fin && !more && a.Wn && (int)blockIdx.x < a.nwg_n) prefetch_next(a, wave, lane);
     // ---- epilogue on the final tile of column group g ----
     if (fin) {
       if constexpr (EPI == EPI_QKV) epilogue_qkv<T, NG, R>(a, tile, g, s_rs, s_ri);
@@ -1313,13 +1350,48 @@ static void launch_gemm_ng(int ng, int tb, const GemmArgs& a, int nblocks, hipSt
 // (about 9 us at the ~25 GB/s per CU of a full-chip stream).
 constexpr double kTailStreamBytes = 224.0 * 1024;
 
+// A GEMM of the forward: tiled weights at w_off, N output columns, K inputs,
+// column groups of ng tiles.
+struct GemmRef {
+  size_t w_off;
+  int64_t N;
+  int K, ng;
+};
+
+// Column groups, k-steps and workgroups of a GEMM launch.
+struct GemmPlan {
+  int G, KT, n_wg;
+};
+
+static GemmPlan plan_gemm(const CallCtx& cx, const GemmRef& r) {
+  GemmPlan p;
+  p.KT = (int)ceil_div(r.K, cx.m->ktile);
+  p.G = (int)(ceil_div(r.N, 16) / r.ng);
+  const int64_t U = (int64_t)p.G * p.KT;
+  p.n_wg = (int)std::min<int64_t>(U, cx.L.n_wg);
+  // With at most one column group per workgroup, equal shares of the whole
+  // unit range leave about a third of the workgroups straddling two groups,
+  // and such a workgroup pays a second tail (reduction, partial publish,
+  // fix-up, epilogue).  Splitting every group into s equal k-ranges over
+  // G x s workgroups gives each workgroup exactly one segment; it is taken
+  // when the longer share costs less stream time than one tail.
+  if (p.G <= cx.L.n_wg) {
+    const int s = std::min(cx.L.n_wg / p.G, p.KT);
+    const double extra_units = (double)p.KT / s - (double)U / p.n_wg;
+    if (extra_units * r.ng * 1024 < kTailStreamBytes) p.n_wg = p.G * s;
+  }
+  return p;
+}
+
+// Runs one GEMM over rows [0, M) in passes of at most 64 rows; `next` is the
+// forward's following GEMM, whose first k-steps the last pass loads into L2.
 static int run_gemm(CallCtx& cx, int epi, unsigned prof, size_t w_off, int64_t N, int K, const char* X, GemmArgs a,
-                    int M, int ng) {
+                    int M, int ng, const GemmRef* next = nullptr) {
   const sdd_model* m = cx.m;
+  const GemmPlan plan = plan_gemm(cx, GemmRef{w_off, N, K, ng});
   a.W = m->base + w_off;
-  a.KT = (int)ceil_div(K, m->ktile);
-  const int64_t ntiles = ceil_div(N, 16);
-  a.G = (int)(ntiles / ng);
+  a.KT = plan.KT;
+  a.G = plan.G;
   a.N = (int)N;
   a.X = X;
   a.ldx = K;
@@ -1329,19 +1401,10 @@ static int run_gemm(CallCtx& cx, int epi, unsigned prof, size_t w_off, int64_t N
   a.rows = reinterpret_cast<const RowInfo*>(cx.ws + cx.L.rowinfo);
   a.eps = m->cfg.rms_eps;
   const int64_t U = (int64_t)a.G * a.KT;
-  int nblocks = (int)std::min<int64_t>(U, cx.L.n_wg);
-  // With at most one column group per workgroup, equal shares of the whole
-  // unit range leave about a third of the workgroups straddling two groups,
-  // and such a workgroup pays a second tail (reduction, partial publish,
-  // fix-up, epilogue).  Splitting every group into s equal k-ranges over
-  // G x s workgroups gives each workgroup exactly one segment; it is taken
-  // when the longer share costs less stream time than one tail.
-  if (a.G <= cx.L.n_wg) {
-    const int s = std::min(cx.L.n_wg / a.G, a.KT);
-    const double extra_units = (double)a.KT / s - (double)U / nblocks;
-    if (extra_units * ng * 1024 < kTailStreamBytes) nblocks = a.G * s;
-  }
+  const int nblocks = plan.n_wg;
   a.n_wg = nblocks;
+  GemmPlan np{};
+  if (next) np = plan_gemm(cx, *next);
   if ((U + 1) * nblocks >= (int64_t(1) << 31))
     return fail(SDD_EUNSUPPORTED, "matrix of %lld weight tiles exceeds the 32-bit stream-K bookkeeping", (long long)U);
   // weight buffer offsets, k-steps up to 4 past a wave's range included
@@ -1352,6 +1415,11 @@ static int run_gemm(CallCtx& cx, int epi, unsigned prof, size_t w_off, int64_t N
   for (int m0 = 0; m0 < M; m0 += kMaxPassRows) {
     a.m0 = m0;
     a.M = std::min(kMaxPassRows, M - m0);
+    a.Wn = next && m0 + kMaxPassRows >= M ? m->base + next->w_off : nullptr;  // last pass only
+    a.KTn = np.KT;
+    a.Gn = np.G;
+    a.ngn = next ? next->ng : 1;
+    a.nwg_n = np.n_wg;
     const int tb = (int)ceil_div(a.M, 16);
     prof_begin(prof, cx.st);
     if (m->es == 2) {
@@ -1411,7 +1479,8 @@ static int forward_rows(CallCtx& cx, int nb, int R, float* logits, int32_t* argm
       a.kv_ld = kv->ld;
       a.kc = kv->k + (size_t)l * kv->layer_stride;
       a.vc = kv->v + (size_t)l * kv->layer_stride;
-      if ((rc = run_gemm(cx, EPI_QKV, PROF_GEMM_QKV, Ly.qkv, hq + 2 * hk, (int)d, xa, a, M, m->ng_qkv))) return rc;
+      const GemmRef nx{Ly.o, d, (int)hq, m->ng_o};
+      if ((rc = run_gemm(cx, EPI_QKV, PROF_GEMM_QKV, Ly.qkv, hq + 2 * hk, (int)d, xa, a, M, m->ng_qkv, &nx))) return rc;
     }
     // attention
     if (m->es == 2) {
@@ -1463,7 +1532,8 @@ static int forward_rows(CallCtx& cx, int nb, int R, float* logits, int32_t* argm
       a.d = (int)d;
       a.g_next = reinterpret_cast<const float*>(m->base + Ly.ffn_norm);
       a.ss_part = ss;
-      if ((rc = run_gemm(cx, EPI_RESID, PROF_GEMM_O, Ly.o, d, (int)hq, ws + L.ao, a, M, m->ng_o))) return rc;
+      const GemmRef nx{Ly.gu, 2 * (int64_t)c.d_ff, (int)d, m->ng_gu};
+      if ((rc = run_gemm(cx, EPI_RESID, PROF_GEMM_O, Ly.o, d, (int)hq, ws + L.ao, a, M, m->ng_o, &nx))) return rc;
     }
     // gate/up + SwiGLU
     {
@@ -1473,7 +1543,8 @@ static int forward_rows(CallCtx& cx, int nb, int R, float* logits, int32_t* argm
       a.d_in = (int)d;
       a.ffh = ws + L.ffh;
       a.dff = c.d_ff;
-      if ((rc = run_gemm(cx, EPI_SWIGLU, PROF_GEMM_GU, Ly.gu, 2 * (int64_t)c.d_ff, (int)d, xa, a, M, m->ng_gu)))
+      const GemmRef nx{Ly.down, d, c.d_ff, m->ng_down};
+      if ((rc = run_gemm(cx, EPI_SWIGLU, PROF_GEMM_GU, Ly.gu, 2 * (int64_t)c.d_ff, (int)d, xa, a, M, m->ng_gu, &nx)))
         return rc;
     }
     // down projection + residual; next input scaled by the next norm gain
@@ -1485,7 +1556,11 @@ static int forward_rows(CallCtx& cx, int nb, int R, float* logits, int32_t* argm
       a.g_next = reinterpret_cast<const float*>(
           m->base + (l + 1 < c.n_layers ? m->layers[l + 1].attn_norm : m->off_final_norm));
       a.ss_part = ss;
-      if ((rc = run_gemm(cx, EPI_RESID, PROF_GEMM_DOWN, Ly.down, d, c.d_ff, ws + L.ffh, a, M, m->ng_down))) return rc;
+      // the next layer's qkv, or the LM head after the last layer
+      const GemmRef nq{l + 1 < c.n_layers ? m->layers[l + 1].qkv : 0, hq + 2 * hk, (int)d, m->ng_qkv};
+      const GemmRef nl{m->off_lm, c.vocab, (int)d, m->ng_lm};
+      const GemmRef* nx = l + 1 < c.n_layers ? &nq : logits ? &nl : nullptr;
+      if ((rc = run_gemm(cx, EPI_RESID, PROF_GEMM_DOWN, Ly.down, d, c.d_ff, ws + L.ffh, a, M, m->ng_down, nx))) return rc;
       ss_groups = g_resid_down;
     }
   }
