@@ -127,26 +127,29 @@ __device__ inline void store_t(char* base, int64_t idx, float v) {
 __device__ inline int unit_owner(uint32_t x, uint32_t U, uint32_t n) { return (int)(((x + 1) * n + U - 1) / U) - 1; }
 __device__ inline uint32_t unit_start(uint32_t w, uint32_t U, uint32_t n) { return w * U / n; }
 
-// Loads into L2 the first three k-steps of the segment that workgroup
-// blockIdx.x of the next GEMM streams first, each wave the quarter that wave
-// streams there.  Workgroup w runs on XCD w mod 8 in both launches, so the
-// lines land in the L2 that serves them.  Plain (cached) loads whose values are
-// consumed by an empty asm statement.
-__device__ inline void prefetch_next(const GemmArgs& a, int wave, int lane) {
-  const uint32_t KTn = (uint32_t)a.KTn, Un = (uint32_t)a.Gn * KTn, n = (uint32_t)a.nwg_n, w = blockIdx.x;
+// Loads into L2 the first three k-steps of the segment that workgroup w of a
+// GEMM launch (tiled weights Wn, KTn k-steps, Gn column groups of ngn tiles,
+// nwg workgroups) streams first, wave `wave` (0..3) the quarter that wave
+// streams there.  Called from a workgroup on XCD w mod 8: workgroups are
+// dispatched to the XCDs round-robin, so the lines land in the L2 that serves
+// them.  Plain (cached) loads whose values are consumed by an empty asm
+// statement.
+__device__ inline void prefetch_gemm_start(const char* Wn, int KTn_, int Gn, int ngn, int nwg, int w_, int wave,
+                                           int lane) {
+  const uint32_t KTn = (uint32_t)KTn_, Un = (uint32_t)Gn * KTn, n = (uint32_t)nwg, w = (uint32_t)w_;
   const uint32_t v0 = unit_start(w, Un, n), v1 = unit_start(w + 1, Un, n);
   const uint32_t g = v0 / KTn;
   const int kb = (int)(v0 - g * KTn);
   const int ke = (int)std::min<uint32_t>(KTn, kb + (v1 - v0));
   const int ka = kb + (ke - kb) * wave / 4, kz = kb + (ke - kb) * (wave + 1) / 4;
   if (ka >= kz) return;
-  const uint4* base = reinterpret_cast<const uint4*>(a.Wn) + (int64_t)g * a.ngn * a.KTn * kWave + lane;
+  const uint4* base = reinterpret_cast<const uint4*>(Wn) + (int64_t)g * ngn * KTn_ * kWave + lane;
   uint4 v[3][8];  // unconditional loads (k-step clamped to the wave's last, tile to the group's last)
 #pragma unroll
   for (int st = 0; st < 3; ++st) {
     const int kt = min(ka + st, kz - 1);
 #pragma unroll
-    for (int nt = 0; nt < 8; ++nt) v[st][nt] = base[((int64_t)kt * a.ngn + min(nt, a.ngn - 1)) * kWave];
+    for (int nt = 0; nt < 8; ++nt) v[st][nt] = base[((int64_t)kt * ngn + min(nt, ngn - 1)) * kWave];
   }
   uint32_t x = 0;
 #pragma unroll
@@ -154,6 +157,11 @@ __device__ inline void prefetch_next(const GemmArgs& a, int wave, int lane) {
 #pragma unroll
     for (int nt = 0; nt < 8; ++nt) x ^= v[st][nt].x ^ v[st][nt].w;
   asm volatile("" ::"v"(x));
+}
+
+// the same for the workgroup of the same index of the forward's next GEMM
+__device__ inline void prefetch_next(const GemmArgs& a, int wave, int lane) {
+  prefetch_gemm_start(a.Wn, a.KTn, a.Gn, a.ngn, a.nwg_n, blockIdx.x, wave, lane);
 }
 
 // Epilogues run on the final [rows][C] tile of one column group (LDS, row
@@ -939,6 +947,12 @@ struct AttnMfmaArgs {
   const RowInfo* rows;
   int nb, R, hq, hkv, grp, ld, qblocks;  // ld: position stride of the caches (multiple of 64)
   float scale;
+  // workgroups past the n_attn attention ones (n_attn and n_pref multiples of
+  // 8) only load into L2 the first k-steps of the next GEMM's workgroups p and
+  // p + n_pref (NULL Wn: none)
+  int n_attn, n_pref;
+  const char* Wn;
+  int KTn, Gn, ngn, nwg_n;
 };
 
 template <int HD>
@@ -947,6 +961,15 @@ __global__ void __launch_bounds__(kAttnWaves * 64) attention_mfma_kernel(AttnMfm
   __shared__ float s_o[kAttnWaves][16][HD + 1];
   __shared__ float s_m[kAttnWaves][16], s_l[kAttnWaves][16], s_f[kAttnWaves][16], s_L[16];
   touch_kernargs<AttnMfmaArgs>();
+  if ((int)blockIdx.x >= a.n_attn) {
+    // on a CU the attention leaves idle: the o_proj's first k-steps into L2,
+    // for its workgroups p and p + n_pref (same XCD: n_attn and n_pref are
+    // multiples of 8), one per four waves
+    const int p = blockIdx.x - a.n_attn, wave4 = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+    const int w = p + (wave4 / 4) * a.n_pref;
+    if (a.Wn && w < a.nwg_n) prefetch_gemm_start(a.Wn, a.KTn, a.Gn, a.ngn, a.nwg_n, w, wave4 % 4, threadIdx.x % kWave);
+    return;
+  }
   // Workgroups are dispatched to the XCDs round-robin by linear id; all query
   // blocks of one (sequence, KV head) get ids of one residue mod kXcds, so they
   // run on one XCD and share its L2 copy of that head's K/V.
@@ -1498,7 +1521,17 @@ static int forward_rows(CallCtx& cx, int nb, int R, float* logits, int32_t* argm
       a.ld = kv->ld;
       a.qblocks = (int)ceil_div((int64_t)R * a.grp, 16);
       a.scale = 1.f / sqrtf((float)c.head_dim);
-      const dim3 grid(kXcds * a.qblocks * (int)ceil_div((int64_t)nb * a.hkv, kXcds));
+      a.n_attn = kXcds * a.qblocks * (int)ceil_div((int64_t)nb * a.hkv, kXcds);
+      // the CUs the attention leaves idle load the o_proj's first k-steps into L2
+      const GemmPlan op = plan_gemm(cx, GemmRef{Ly.o, d, (int)hq, m->ng_o});
+      a.n_pref = std::max(0, std::min((m->n_cu - a.n_attn) / kXcds * kXcds, (op.n_wg + 1) / 2 + kXcds));
+      a.n_pref = a.n_pref / kXcds * kXcds;
+      a.Wn = a.n_pref > 0 ? m->base + Ly.o : nullptr;
+      a.KTn = op.KT;
+      a.Gn = op.G;
+      a.ngn = m->ng_o;
+      a.nwg_n = op.n_wg;
+      const dim3 grid(a.n_attn + a.n_pref);
       prof_begin(PROF_ATTN, cx.st);
       if (c.head_dim == 128)
         hipLaunchKernelGGL(attention_mfma_kernel<128>, grid, dim3(kAttnWaves * 64), 0, cx.st, a);
