@@ -35,6 +35,7 @@ namespace sdd {
 enum Epi { EPI_QKV = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_LOGITS = 3 };
 
 constexpr int kGemmThreads = 256;
+constexpr int kXcds = 8;  // XCDs of the MI355X (32 CUs each); workgroups go to them round-robin by linear id
 constexpr int kMaxPassRows = 64;  // rows per GEMM pass (TB <= 4 row tiles of 16)
 
 struct GemmArgs {
@@ -526,7 +527,7 @@ __global__ void __launch_bounds__(256) row_argmax_kernel(const float* amax_v, co
   if (t == 0 && rows[m].valid) out[m] = si[0] < 0 ? 0 : si[0];
 }
 
-template <typename T, int TB, int NG, int EPI>
+template <typename T, int TB, int NG, int EPI, bool MR = false>
 __global__ void __launch_bounds__(kGemmThreads, 1) gemm_kernel(GemmArgs a) {
   constexpr int C = NG * 16;       // output columns of a column group
   constexpr int CP = C + 4;        // LDS row stride of the output tile (16-byte row writes hit distinct banks)
@@ -546,9 +547,24 @@ __global__ void __launch_bounds__(kGemmThreads, 1) gemm_kernel(GemmArgs a) {
   static_assert(4 * NACC * kWave * 4 >= R * CP, "tile must fit the reduction buffer");
   touch_kernargs<GemmArgs>();
 
+  // Many-row launch (prefill chunks, MR): a.M rows from a.m0 in 64-row tiles;
+  // each workgroup takes one column group whole (n_wg = G: one segment, no
+  // partials) for one row tile.  The row tiles of a group are consecutive
+  // workgroups of one XCD, so they stream the group's weights together through
+  // that XCD's L2 and HBM delivers them about once per chunk.
+  int w = blockIdx.x;
+  if constexpr (MR) {
+    const int nrt = (a.M + kMaxPassRows - 1) / kMaxPassRows;
+    const int j = blockIdx.x / kXcds;
+    const int g = (j / nrt) * kXcds + blockIdx.x % kXcds, rt = j % nrt;
+    if (g >= a.G) return;
+    a.m0 += rt * kMaxPassRows;
+    a.M = min(kMaxPassRows, a.M - rt * kMaxPassRows);
+    w = g;
+  }
+  constexpr int kWCpol = MR ? 0 : kNtCpol;  // row tiles re-read the weights from L2
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave), lane = threadIdx.x % kWave;
   const uint32_t KT = (uint32_t)a.KT, U = (uint32_t)a.G * KT;
-  const int w = blockIdx.x;
   const uint32_t u0 = unit_start(w, U, a.n_wg), u1 = unit_start(w + 1, U, a.n_wg);
   const int g_first = (int)(u0 / KT);
   const uint4* W = reinterpret_cast<const uint4*>(a.W);
@@ -582,7 +598,7 @@ __global__ void __launch_bounds__(kGemmThreads, 1) gemm_kernel(GemmArgs a) {
 #pragma unroll
     for (int nt = 0; nt < NG; ++nt)
       wa[nt] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(wd, wlane, woff + (kt * NG + nt) * kWave * 16,
-                                                                                 kNtCpol));
+                                                                                 kWCpol));
 #pragma unroll
     for (int tb = 0; tb < TB; ++tb)
       xb[tb] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(xd, xlane + tb * xrow16,
@@ -937,7 +953,6 @@ __global__ void __launch_bounds__(256) attention_kernel(AttnArgs a) {
 // K/V loads in flight.  The softmax is online within a wave; the waves' partial
 // (max, sum, O) are combined through LDS in wave order.
 constexpr int kAttnWaves = 8;
-constexpr int kXcds = 8;  // XCDs of the MI355X (32 CUs each)
 
 struct AttnMfmaArgs {
   const uint16_t* q;   // [rows][hq][HD]
@@ -1347,6 +1362,7 @@ struct CallCtx {
   char* ws;
   WsLayout L;
   hipStream_t st;
+  bool many_rows = false;  // prefill chunk: GEMMs over more than 64 rows run all row tiles in one launch
 };
 
 template <typename T, int NG, int EPI>
@@ -1356,6 +1372,15 @@ static void launch_gemm_tb(int tb, const GemmArgs& a, int nblocks, hipStream_t s
     case 2: hipLaunchKernelGGL((gemm_kernel<T, 2, NG, EPI>), dim3(nblocks), dim3(kGemmThreads), 0, st, a); break;
     case 3: hipLaunchKernelGGL((gemm_kernel<T, 3, NG, EPI>), dim3(nblocks), dim3(kGemmThreads), 0, st, a); break;
     default: hipLaunchKernelGGL((gemm_kernel<T, 4, NG, EPI>), dim3(nblocks), dim3(kGemmThreads), 0, st, a); break;
+  }
+}
+
+template <typename T, int EPI>
+static void launch_rows_ng(int ng, const GemmArgs& a, int nblocks, hipStream_t st) {
+  switch (ng) {
+    case 8: hipLaunchKernelGGL((gemm_kernel<T, 4, 8, EPI, true>), dim3(nblocks), dim3(kGemmThreads), 0, st, a); break;
+    case 4: hipLaunchKernelGGL((gemm_kernel<T, 4, 4, EPI, true>), dim3(nblocks), dim3(kGemmThreads), 0, st, a); break;
+    default: hipLaunchKernelGGL((gemm_kernel<T, 4, 2, EPI, true>), dim3(nblocks), dim3(kGemmThreads), 0, st, a); break;
   }
 }
 
@@ -1435,6 +1460,30 @@ static int run_gemm(CallCtx& cx, int epi, unsigned prof, size_t w_off, int64_t N
     return fail(SDD_EUNSUPPORTED, "matrix of %lld x %d exceeds the 32-bit buffer offsets", (long long)N, K);
   if ((int64_t)(M + 64) * K * m->es >= (int64_t(1) << 31))
     return fail(SDD_EUNSUPPORTED, "activations of %d rows x %d exceed the 32-bit buffer offsets", M, K);
+  if (cx.many_rows && M > kMaxPassRows && epi != EPI_LOGITS) {
+    // prefill chunk: every (column group, 64-row tile) in one launch, one group per workgroup
+    a.m0 = 0;
+    a.M = M;
+    a.n_wg = a.G;
+    a.Wn = nullptr;
+    const int nb = (int)(ceil_div(a.G, kXcds) * kXcds * ceil_div(M, kMaxPassRows));
+    prof_begin(prof, cx.st);
+    if (m->es == 2) {
+      switch (epi) {
+        case EPI_QKV: launch_rows_ng<uint16_t, EPI_QKV>(ng, a, nb, cx.st); break;
+        case EPI_RESID: launch_rows_ng<uint16_t, EPI_RESID>(ng, a, nb, cx.st); break;
+        default: launch_rows_ng<uint16_t, EPI_SWIGLU>(ng, a, nb, cx.st); break;
+      }
+    } else {
+      switch (epi) {
+        case EPI_QKV: launch_rows_ng<float, EPI_QKV>(ng, a, nb, cx.st); break;
+        case EPI_RESID: launch_rows_ng<float, EPI_RESID>(ng, a, nb, cx.st); break;
+        default: launch_rows_ng<float, EPI_SWIGLU>(ng, a, nb, cx.st); break;
+      }
+    }
+    prof_end(prof, cx.st);
+    return check_launch("gemm_kernel (row tiles)");
+  }
   for (int m0 = 0; m0 < M; m0 += kMaxPassRows) {
     a.m0 = m0;
     a.M = std::min(kMaxPassRows, M - m0);
@@ -1761,6 +1810,7 @@ extern "C" int sdd_kv_prefill(sdd_model* m, sdd_kv* kv, int seq, const int32_t* 
     CallCtx cx;
     int rc = make_ctx(cx, m, kv, ws, ws_bytes, chunk, st);
     if (rc) return rc;
+    cx.many_rows = true;
     EmbedArgs e{};
     e.prefill = 1;
     e.seq = seq;

@@ -62,13 +62,13 @@ def test_weight_generator_bit_identical(S):
     assert np.array_equal(lm, want)
 
 
-def _run_case(S, shape, prompt_len, gamma, seed, n_rounds=1, max_len=None):
+def _run_case(S, shape, prompt_len, gamma, seed, n_rounds=1, max_len=None, ws_rows=64):
     """Prefill + verify rounds on the GPU and the oracle's cached route; returns per-round results."""
-    print(f"case {shape} prompt={prompt_len} gamma={gamma} seed={seed}", flush=True)
+    print(f"case {shape} prompt={prompt_len} gamma={gamma} seed={seed} ws_rows={ws_rows}", flush=True)
     m = _gpu_model(S, shape)
     max_len = max_len or prompt_len + n_rounds * (gamma + 1) + 8
     kv = S.KVCache(m, 1, max_len)
-    ws = m.workspace(max(64, gamma + 1))
+    ws = m.workspace(max(ws_rows, gamma + 1))
     om = oracle.Model(shape)
     okv = oracle.KV(om, max_len)
     toks = W.prompt(seed, prompt_len, shape.vocab)
@@ -119,6 +119,14 @@ def test_small_bf16(S, shape):
 def test_gamma_zero_and_long_prefill_chunks(S):
     # prompt longer than one prefill chunk, gamma = 0 decode step
     _run_case(S, MID_GQA128, 300, 0, seed=3, n_rounds=2)
+
+
+@pytest.mark.parametrize("shape,prompt_len", [(MID_GQA128, 400), (MID_BF16, 101), (W.TINY, 200)],
+                         ids=["hd128-chunks-256+143", "hd64-qknorm-chunk-100", "tiny-f32-chunk-199"])
+def test_many_row_prefill_chunks(S, shape, prompt_len):
+    """Prefill chunks of more than 64 rows (workspace for 256) run the 128-row-tile GEMM: full and ragged
+    tiles, one and two tiles per chunk; the cache it writes must give the oracle's verify logits."""
+    _run_case(S, shape, prompt_len, 16, seed=4, n_rounds=2, ws_rows=256)
 
 
 def test_tiny_config_full_pipeline(S):

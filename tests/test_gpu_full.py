@@ -25,12 +25,13 @@ def S():
     return sdd
 
 
-@pytest.mark.parametrize("shape,n,gamma", [(W.TINY, 72, 8), (W.TINY, 300, 32), (MID_BF16, 140, 16), (W.TINY, 9, 0)])
-def test_full_recompute_matches_oracle_and_cached_call(S, shape, n, gamma):
-    print(f"full recompute {shape.dtype} n={n} gamma={gamma}", flush=True)
+@pytest.mark.parametrize("shape,n,gamma,ws_rows", [(W.TINY, 72, 8, 64), (W.TINY, 300, 32, 64), (MID_BF16, 140, 16, 64),
+                                                  (W.TINY, 9, 0, 64), (W.TINY, 300, 32, 256), (MID_BF16, 240, 16, 256)])
+def test_full_recompute_matches_oracle_and_cached_call(S, shape, n, gamma, ws_rows):
+    print(f"full recompute {shape.dtype} n={n} gamma={gamma} ws_rows={ws_rows}", flush=True)
     m = S.Model(shape)
     m.init_random(0, 0.02)
-    ws = m.workspace(64)
+    ws = m.workspace(ws_rows)
     toks = W.prompt(n + 3, n, shape.vocab)
     scratch = S.KVCache(m, 1, n + 4)
     lf = torch.empty((1, gamma + 1, shape.vocab), dtype=torch.float32, device="cuda")
