@@ -3,6 +3,7 @@
 * 1-layer models of the exact widths (d 5120 / 3584, 64/8 and 28/4 heads x 128, FFN 25600 / 18944,
   V 151936 / 152064) against the oracle: logits within 2e-2 of the logit scale, argmax bit-exact
   outside near-ties.  Every kernel of a layer runs at its real shape; depth does not change them.
+* 256- and 149-row prefill chunks at the 32B width (the many-row GEMM launches) against the oracle.
 * The full 64-layer 32B model: block verification equals sequential decode steps bit for bit (a
   property that holds at any size: a row's arithmetic does not depend on how rows are batched), and
   repeated calls are bit-identical.
@@ -16,6 +17,16 @@ import workloads as W
 from gpu_helpers import argmax_near_tie, row_tol_ok, to_dev_i32
 
 pytestmark = pytest.mark.gpu
+
+
+_ORACLE_MODELS = {}
+
+
+def _oracle_model(shape):
+    """One oracle model per shape for the whole module (building one at full width takes ~15 s)."""
+    if shape not in _ORACLE_MODELS:
+        _ORACLE_MODELS[shape] = oracle.Model(shape, W.WEIGHT_SEED, W.WEIGHT_SIGMA)
+    return _ORACLE_MODELS[shape]
 
 
 @pytest.fixture(scope="module")
@@ -35,7 +46,7 @@ def test_one_layer_full_width_vs_oracle(S, shape):
     ws = m.workspace(64)
     toks = W.prompt(31, P, shape.vocab)
     kv.prefill(0, to_dev_i32(toks), ws)
-    om = oracle.Model(shape, W.WEIGHT_SEED, W.WEIGHT_SIGMA)
+    om = _oracle_model(shape)
     okv = oracle.KV(om, P + 2 * (gamma + 1) + 8)
     okv.prefill(toks)
     for r in range(2):
@@ -57,6 +68,37 @@ def test_one_layer_full_width_vs_oracle(S, shape):
         L, nxt = int(ref["accepted_len"][0]), int(ref["next_token"][0])
         kv.commit(to_dev_i32([0]), to_dev_i32([L]), to_dev_i32([nxt]))
         okv.commit(L, nxt)
+
+
+@pytest.mark.parametrize("P", [300, 150], ids=["chunks-256+43", "chunk-149"])
+def test_one_layer_full_width_long_prefill_vs_oracle(S, P):
+    """Prefill chunks of 256 and 149 rows at the full 32B width (workspace for 256-row chunks): every GEMM
+    runs all its 64-row tiles in one launch (4 full tiles; 2 full tiles and a ragged one); the verify logits
+    on the cache they wrote must match the oracle's."""
+    shape = W.QWEN32B.with_layers(1)
+    print(f"full-width 1-layer long prefill P={P}", flush=True)
+    m = S.Model(shape)
+    m.init_random(W.WEIGHT_SEED, W.WEIGHT_SIGMA)
+    gamma = 16
+    kv = S.KVCache(m, 1, P + gamma + 8)
+    ws = m.workspace(256)
+    toks = W.prompt(35, P, shape.vocab)
+    kv.prefill(0, to_dev_i32(toks), ws)
+    om = _oracle_model(shape)
+    okv = oracle.KV(om, P + gamma + 8)
+    okv.prefill(toks)
+    drafts = W.prompt(36, gamma, shape.vocab)
+    logits = torch.empty((1, gamma + 1, shape.vocab), dtype=torch.float32, device="cuda")
+    am = torch.empty((1, gamma + 1), dtype=torch.int32, device="cuda")
+    kv.verify(to_dev_i32([0]), to_dev_i32(drafts.reshape(1, gamma)), logits, am, ws)
+    want = okv.verify(drafts)
+    got = logits[0].cpu().numpy()
+    ok, rel = row_tol_ok(got, want, 2e-2)
+    print(f"  logits max rel {rel.max():.2e} median {np.median(rel):.2e}", flush=True)
+    assert ok.all()
+    near = argmax_near_tie(want, 2e-2 * np.abs(want).max(-1))
+    amg = am[0].cpu().numpy()
+    assert (amg[~near] == want.argmax(-1)[~near]).all()
 
 
 def test_qwen32b_verify_equals_decode_and_is_bit_stable(S):
