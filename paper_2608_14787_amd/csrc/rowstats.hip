@@ -215,28 +215,44 @@ struct ThreadStats {
 
 __device__ inline ThreadStats stats_init() { return ThreadStats{-INFINITY, -INFINITY, 0.f, -1, 0, 0}; }
 
-template <int VEC, bool kSum, bool kCount>
+template <int VEC, bool kSum, bool kCount, bool kIdx = true>
 __device__ __attribute__((always_inline)) inline void stats_update(ThreadStats& st, const float* v, bool valid, int e0,
                                                                    float zx, int x) {
   // branch-free: every element takes the same instructions (selects; an invalid vector changes nothing), so
-  // the streaming loop has no divergent blocks and its loads stay in flight
-  float vm = -INFINITY;
+  // the streaming loop has no divergent blocks and its loads stay in flight.  The max and first argmax are
+  // taken per vector: vx = the vector's max over non-NaN values (fmaxf skips NaN); it replaces the running
+  // max when greater (or when none is held yet), at the vector's first element equal to it -- the same
+  // result as visiting the elements one by one in index order.  kIdx = false (drafter rows, whose argmax is
+  // never used) records index 0 instead of searching.
+  float vm = -INFINITY;  // max over finite values (reference of the sum)
+  float vx = -INFINITY;  // max over non-NaN values (comparisons with NaN are false)
+  float zf[VEC];         // the finite values of a valid vector, -inf elsewhere (exp(-inf - m) adds exactly 0)
+  bool nonfin = false, has = false;
 #pragma unroll
   for (int t = 0; t < VEC; ++t) {
     const float z = v[t];
     const bool fin = __builtin_isfinite(z);
-    st.fl |= (valid && !fin) ? 1 : 0;
-    vm = (valid && fin) ? fmaxf(vm, z) : vm;
-    const bool take = valid && !__builtin_isnan(z) && (st.a < 0 || z > st.m);
-    st.m = take ? z : st.m;
-    st.a = take ? e0 + t : st.a;
+    nonfin |= !fin;
+    has |= !__builtin_isnan(z);
+    zf[t] = (valid && fin) ? z : -INFINITY;
+    vm = fmaxf(vm, zf[t]);
+    vx = z > vx ? z : vx;
     if (kCount) st.cnt += (valid && (z > zx || (z == zx && e0 + t < x))) ? 1 : 0;
   }
+  st.fl |= (valid && nonfin) ? 1 : 0;
+  const bool take = valid && has && (st.a < 0 || vx > st.m);
+  int idx = 0;
+  if (kIdx) {
+#pragma unroll
+    for (int t = VEC - 1; t >= 0; --t) idx = v[t] == vx ? t : idx;
+  }
+  st.m = take ? vx : st.m;
+  st.a = take ? e0 + idx : st.a;
   if (kSum) {
     const float mn = fmaxf(st.mf, vm);  // -inf while no finite value has been seen
-    float add = 0.f;
+    float add = 0.f;  // (mn = -inf: no finite value yet, the sum is left unchanged below)
 #pragma unroll
-    for (int t = 0; t < VEC; ++t) add += (valid && __builtin_isfinite(v[t])) ? exp_shift(v[t], mn) : 0.f;
+    for (int t = 0; t < VEC; ++t) add += exp_shift(zf[t], mn);
     const float scale = st.mf > -INFINITY ? exp_shift(st.mf, mn) : 0.f;
     st.s = mn > -INFINITY ? st.s * scale + add : st.s;
     st.mf = mn;
@@ -280,7 +296,7 @@ __device__ __attribute__((always_inline)) inline void stream_stats(const T* row,
       const int e = base + ((i + d) * kThreads + (int)threadIdx.x) * VEC;
       const bool valid = i + d < nvt;
       stats_update<VEC, kSum, kCount>(st, v, valid, e, zx, x);
-      if (kQ) stats_update<VEC, true, false>(qst, w, valid && hq, e, 0.f, -1);
+      if (kQ) stats_update<VEC, true, false, false>(qst, w, valid && hq, e, 0.f, -1);
     }
   };
   load_group(0, pa, qa);
