@@ -130,8 +130,8 @@ __device__ inline uint32_t unit_start(uint32_t w, uint32_t U, uint32_t n) { retu
 
 // Loads into L2 the first three k-steps of the segment that workgroup w of a
 // GEMM launch (tiled weights Wn, KTn k-steps, Gn column groups of ngn tiles,
-// nwg workgroups) streams first, wave `wave` (0..3) the quarter that wave
-// streams there.  Called from a workgroup on XCD w mod 8: workgroups are
+// nwg workgroups) streams first, wave `wave` (0..3) the k-steps that wave
+// streams there (every fourth from the segment's start + wave).  Called from a workgroup on XCD w mod 8: workgroups are
 // dispatched to the XCDs round-robin, so the lines land in the L2 that serves
 // them.  Plain (cached) loads whose values are consumed by an empty asm
 // statement.
@@ -142,15 +142,16 @@ __device__ inline void prefetch_gemm_start(const char* Wn, int KTn_, int Gn, int
   const uint32_t g = v0 / KTn;
   const int kb = (int)(v0 - g * KTn);
   const int ke = (int)std::min<uint32_t>(KTn, kb + (v1 - v0));
-  const int ka = kb + (ke - kb) * wave / 4, kz = kb + (ke - kb) * (wave + 1) / 4;
-  if (ka >= kz) return;
-  const uint4* base = reinterpret_cast<const uint4*>(Wn) + (int64_t)g * ngn * KTn_ * kWave + lane;
+  const int nk = ke - kb > wave ? (ke - kb - wave + 3) / 4 : 0;  // this wave's k-steps
+  if (nk == 0) return;
+  const int64_t ntn = (int64_t)Gn * ngn;  // tiles per k-step
+  const uint4* base = reinterpret_cast<const uint4*>(Wn) + (int64_t)g * ngn * kWave + lane;
   uint4 v[3][8];  // unconditional loads (k-step clamped to the wave's last, tile to the group's last)
 #pragma unroll
   for (int st = 0; st < 3; ++st) {
-    const int kt = min(ka + st, kz - 1);
+    const int kt = kb + wave + 4 * min(st, nk - 1);
 #pragma unroll
-    for (int nt = 0; nt < 8; ++nt) v[st][nt] = base[((int64_t)kt * ngn + min(nt, ngn - 1)) * kWave];
+    for (int nt = 0; nt < 8; ++nt) v[st][nt] = base[((int64_t)kt * ntn + min(nt, ngn - 1)) * kWave];
   }
   uint32_t x = 0;
 #pragma unroll
@@ -579,37 +580,48 @@ __global__ void __launch_bounds__(kGemmThreads, 1) gemm_kernel(GemmArgs a) {
       const_cast<char*>(a.X), 0, (a.m0 + a.M) * a.ldx * (int)sizeof(T), kBufferRsrcWord3);
   const int xlane = ((a.m0 + lane % 16) * a.ldx + (lane / 16) * EPL) * (int)sizeof(T);  // < 2^31: checked on the host
   const int xrow16 = 16 * a.ldx * (int)sizeof(T);
-  const __amdgpu_buffer_rsrc_t wrs = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint4*>(W), 0, 0x7fffffff, kBufferRsrcWord3);
+  // the whole matrix: k-step kt of every column group is one contiguous run of G x NG tiles
+  const __amdgpu_buffer_rsrc_t wrs =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint4*>(W), 0, (int)(KT * a.G * NG * kWave * 16), kBufferRsrcWord3);
+  const uint32_t kstep4w = 4u * a.G * NG * kWave * 16;    // bytes between a wave's consecutive k-steps
+  const uint32_t kstep4x = 4u * KTILE * (uint32_t)sizeof(T);
   const int wlane = lane * 16;
 
   // a descriptor with no range: every load through it returns zero without a memory access
   const __amdgpu_buffer_rsrc_t nrs = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint4*>(W), 0, 0, kBufferRsrcWord3);
 
-  // One k-step of column group g: NG contiguous 1 KiB weight tiles and the TB
-  // activation fragments, all buffer loads (descriptors in scalars, the lane's
-  // offset in one register, the k-step as a scalar offset: recomputed address
-  // registers could alias an in-flight load's destination and force a wait for
-  // every load).  The loads are unconditional, so that the compiler can wait
-  // for exactly the oldest stage; a k-step past the wave's range (the stream's
-  // last stages) selects the empty descriptor and so costs no memory traffic.
-  auto load = [&](int woff, int kt, int kz, uint4* wa, uint4* xb) {
+  // Local k-step kt of this wave in its segment: the NG contiguous 1 KiB
+  // weight tiles of its column group and the TB activation fragments, all
+  // buffer loads (descriptors in scalars, the lane's offset in one register,
+  // the k-step as a scalar offset: recomputed address registers could alias an
+  // in-flight load's destination and force a wait for every load).  The loads
+  // are unconditional, so that the compiler can wait for exactly the oldest
+  // stage; a k-step past the wave's range (the stream's last stages) selects
+  // the empty descriptor and so costs no memory traffic (its offset is not
+  // used, and unsigned arithmetic keeps it defined).
+  auto load = [&](uint32_t wo, uint32_t xo, int kt, int kz, uint4* wa, uint4* xb) {
     const bool in = kt < kz;
     const __amdgpu_buffer_rsrc_t wd = in ? wrs : nrs, xd = in ? xrs : nrs;
 #pragma unroll
     for (int nt = 0; nt < NG; ++nt)
-      wa[nt] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(wd, wlane, woff + (kt * NG + nt) * kWave * 16,
-                                                                                 kWCpol));
+      wa[nt] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(
+                                             wd, wlane, (int)(wo + (uint32_t)kt * kstep4w + (uint32_t)nt * kWave * 16), kWCpol));
 #pragma unroll
     for (int tb = 0; tb < TB; ++tb)
       xb[tb] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(xd, xlane + tb * xrow16,
-                                                                                 kt * KTILE * (int)sizeof(T), 0));
+                                                                                 (int)(xo + (uint32_t)kt * kstep4x), 0));
     // keep the next stages' loads ahead of this stage's MFMAs
     __builtin_amdgcn_sched_barrier(0);
   };
   // A segment is this workgroup's part of one column group: k-tiles [kb, ke);
-  // wave w streams the quarter [ka, kz).
+  // wave w streams k-tiles kb + w, kb + w + 4, ... (kz of them), so that at any
+  // time the four waves read adjacent k-steps and, the matrix being stored
+  // k-step by k-step, the launch reads few long runs of memory.  wo and xo are
+  // the byte offsets of the wave's first k-step in the weights and in an
+  // activation row.
   struct Seg {
     int g, kb, ke, ka, kz;
+    uint32_t wo, xo;
   };
   auto make_seg = [&](uint32_t u) {
     Seg s;
@@ -617,8 +629,11 @@ __global__ void __launch_bounds__(kGemmThreads, 1) gemm_kernel(GemmArgs a) {
     s.kb = (int)(u - (uint32_t)s.g * KT);
     s.ke = (int)std::min<uint32_t>(KT, s.kb + (u1 - u));
     const int S = s.ke - s.kb;
-    s.ka = __builtin_amdgcn_readfirstlane(s.kb + S * wave / 4);
-    s.kz = __builtin_amdgcn_readfirstlane(s.kb + S * (wave + 1) / 4);
+    s.ka = 0;
+    s.kz = __builtin_amdgcn_readfirstlane(S > wave ? (S - wave + 3) / 4 : 0);
+    const uint32_t k0 = (uint32_t)(s.kb + wave);
+    s.wo = __builtin_amdgcn_readfirstlane(k0 * (kstep4w / 4) + (uint32_t)s.g * NG * kWave * 16);
+    s.xo = __builtin_amdgcn_readfirstlane(k0 * KTILE * (uint32_t)sizeof(T));
     return s;
   };
   // Row info and RMSNorm row scales of this pass, used only by the epilogues.
@@ -690,13 +705,10 @@ __global__ void __launch_bounds__(kGemmThreads, 1) gemm_kernel(GemmArgs a) {
   // so that their stores do not stall the next stream (loads and stores complete in order).
   constexpr bool kEarly = EPI == EPI_SWIGLU || EPI == EPI_LOGITS;
   uint4 wa0[NG], wa1[NG], wa2[NG], wa3[NG], xb0[TB], xb1[TB], xb2[TB], xb3[TB];
-  // the segment's byte offset in the matrix (buffer loads; < 2^31: checked on the host)
-  auto seg_off = [&](const Seg& sg) { return sg.g * NG * a.KT * kWave * 16; };
   auto issue = [&](const Seg& sg) {  // the first three stages (a wave with an empty range loads nothing)
-    const int wo = seg_off(sg);
-    load(wo, sg.ka, sg.kz, wa0, xb0);
-    load(wo, sg.ka + 1, sg.kz, wa1, xb1);
-    load(wo, sg.ka + 2, sg.kz, wa2, xb2);
+    load(sg.wo, sg.xo, 0, sg.kz, wa0, xb0);
+    load(sg.wo, sg.xo, 1, sg.kz, wa1, xb1);
+    load(sg.wo, sg.xo, 2, sg.kz, wa2, xb2);
   };
   uint32_t u = u0;
   Seg s = make_seg(u);  // carried across segments: uniform values only
@@ -705,7 +717,7 @@ __global__ void __launch_bounds__(kGemmThreads, 1) gemm_kernel(GemmArgs a) {
     prologue();  // the prologue's loads queue behind the first weight loads
   }
   for (bool first = true;; first = false) {
-    const int wo = seg_off(s);
+    const uint32_t wo = s.wo, xo = s.xo;
     // ---- stream this segment: four register stages, three in flight ----
     if constexpr (!kEarly) {
       issue(s);
@@ -723,13 +735,13 @@ __global__ void __launch_bounds__(kGemmThreads, 1) gemm_kernel(GemmArgs a) {
     int kt = s.ka;
     if (kt < s.kz) {
       for (; kt + 4 <= s.kz; kt += 4) {
-        load(wo, kt + 3, s.kz, wa3, xb3);
+        load(wo, xo, kt + 3, s.kz, wa3, xb3);
         mma(wa0, xb0);
-        load(wo, kt + 4, s.kz, wa0, xb0);
+        load(wo, xo, kt + 4, s.kz, wa0, xb0);
         mma(wa1, xb1);
-        load(wo, kt + 5, s.kz, wa1, xb1);
+        load(wo, xo, kt + 5, s.kz, wa1, xb1);
         mma(wa2, xb2);
-        load(wo, kt + 6, s.kz, wa2, xb2);
+        load(wo, xo, kt + 6, s.kz, wa2, xb2);
         mma(wa3, xb3);
       }
       // 0..3 k-tiles left, already loaded in stages 0..2

@@ -70,12 +70,11 @@ __global__ void fill_tiled_kernel(char* dst, TiledSrc s, int only_part) {
   const int64_t slices = ceil_div(s.N, 16) * (int64_t)s.KT * 64;
   for (int64_t id = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; id < slices;
        id += (int64_t)gridDim.x * blockDim.x) {
-    const int64_t tile = id / 64;  // physical: ((nt / ng) * KT + kt) * ng + nt % ng
+    const int64_t tile = id / 64;  // physical: kt * NT + nt (k-step major, NT = ceil(N / 16) row tiles)
     const int lane = (int)(id % 64);
-    const int64_t grp = tile / ((int64_t)s.KT * s.ng);
-    const int64_t rem = tile % ((int64_t)s.KT * s.ng);
-    const int kt = (int)(rem / s.ng);
-    const int64_t nt = grp * s.ng + rem % s.ng;
+    const int64_t NT = ceil_div(s.N, 16);
+    const int kt = (int)(tile / NT);
+    const int64_t nt = tile % NT;
     const int64_t row = nt * 16 + lane % 16;
     const int k0 = kt * s.ktile + (lane / 16) * EPL;
     int part = 0;

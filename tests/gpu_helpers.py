@@ -5,30 +5,21 @@ import torch
 import workloads as W
 
 
-def group_size(ntiles: int) -> int:
-    """Row tiles per column group: the largest of 8, 4, 2 dividing the tile count."""
-    for ng in (8, 4, 2):
-        if ntiles % ng == 0:
-            return ng
-    return 1
-
-
 def untile(buf: np.ndarray, rows: int, cols: int, dtype: str) -> np.ndarray:
     """Decodes libsdd's documented tiled weight layout back to a row-major [rows][cols] matrix.
 
     Tiles of 16 rows x ktile columns (ktile 32 for bf16, 16 for fp32), 1 KiB each; tile (nt, kt) at
-    index ((nt // NG) * KT + kt) * NG + nt % NG; lane l of a tile holds row l%16 and
+    index kt * NT + nt (k-step major, NT = ceil(rows / 16)); lane l of a tile holds row l%16 and
     EPL = 16/sizeof(elem) columns from (l//16)*EPL."""
     es = 2 if dtype == "bf16" else 4
     epl = 16 // es
     kt = 4 * epl
     NT, KT = -(-rows // 16), -(-cols // kt)
-    NG = group_size(NT)
     if dtype == "bf16":
         vals = W.bf16_bits_to_f32(buf[: NT * KT * 1024].view(np.uint16))
     else:
         vals = buf[: NT * KT * 1024].view(np.float32)
-    a = vals.reshape(NT // NG, KT, NG, 4, 16, epl).transpose(0, 2, 4, 1, 3, 5).reshape(NT * 16, KT * kt)
+    a = vals.reshape(KT, NT, 4, 16, epl).transpose(1, 3, 0, 2, 4).reshape(NT * 16, KT * kt)
     return a[:rows, :cols]
 
 
