@@ -9,10 +9,10 @@
 // reads 16 contiguous bytes holding row (l % 16) and the EPL = 16/sizeof(T)
 // consecutive columns starting at (l / 16) * EPL: exactly one MFMA A-operand
 // fragment per lane, so a wave streams a tile with one coalesced 16-byte load
-// per lane.  Row tiles are grouped NG at a time (NG in {8, 4, 2}, per matrix);
-// tile (nt, kt) sits at index ((nt / NG) * KT + kt) * NG + nt % NG, so one
-// k-step of a column group is NG KiB of contiguous memory and a group's whole
-// K-run is contiguous.  Q, K and V projections are fused into one
+// per lane.  Tiles are stored k-step by k-step: tile (nt, kt) sits at index
+// kt * NT + nt (NT = N / 16 row tiles), so one k-step of a column group (NG
+// consecutive row tiles, NG in {8, 4, 2} per matrix) is NG KiB of contiguous
+// memory and one k-step of the whole matrix is one contiguous run.  Q, K and V projections are fused into one
 // matrix (rows [Wq; Wk; Wv]); gate and up projections are fused and
 // interleaved per 16-row tile (tile 2t = gate rows 16t.., tile 2t+1 = up rows
 // 16t..), so that one column group holds matching gate/up outputs.
