@@ -1260,13 +1260,45 @@ __global__ void __launch_bounds__(256) embed_kernel(EmbedArgs a) {
     s_tok = tok;
   }
   __syncthreads();
+  // 16-byte vectors of the embedding row and the gains (d is a multiple of 32, rows 16-byte aligned),
+  // a round's loads all issued before any is used
+  constexpr int EPL = 16 / sizeof(T), kRound = 4;
   const T* e = reinterpret_cast<const T*>(a.E) + (int64_t)s_tok * a.d;
+  float* xrow = a.x + (int64_t)m * a.d;
+  T* xarow = reinterpret_cast<T*>(a.xa) + (int64_t)m * a.d;
+  const int nv = a.d / EPL;
   float ss = 0.f;
-  for (int i = tid; i < a.d; i += 256) {
-    const float v = Elem<T>::to_f32(e[i]);
-    a.x[(int64_t)m * a.d + i] = v;
-    store_t<T>(a.xa, (int64_t)m * a.d + i, v * a.g[i]);
-    ss += v * v;
+  for (int base = 0; base < nv; base += 256 * kRound) {
+    uint4 ev[kRound];
+    f32x4 gv[kRound][EPL / 4];
+#pragma unroll
+    for (int j = 0; j < kRound; ++j) {
+      const int iv = min(base + j * 256 + tid, nv - 1);
+      ev[j] = *reinterpret_cast<const uint4*>(e + iv * EPL);
+#pragma unroll
+      for (int q = 0; q < EPL / 4; ++q) gv[j][q] = *reinterpret_cast<const f32x4*>(a.g + iv * EPL + 4 * q);
+    }
+#pragma unroll
+    for (int j = 0; j < kRound; ++j) {
+      const int iv = base + j * 256 + tid;
+      if (iv < nv) {
+        const T* ve = reinterpret_cast<const T*>(&ev[j]);
+        T xa_out[EPL];
+#pragma unroll
+        for (int q = 0; q < EPL / 4; ++q) {
+          f32x4 xo;
+#pragma unroll
+          for (int t = 0; t < 4; ++t) {
+            const float v = Elem<T>::to_f32(ve[4 * q + t]);
+            xo[t] = v;
+            xa_out[4 * q + t] = Elem<T>::from_f32(v * gv[j][q][t]);
+            ss += v * v;
+          }
+          *reinterpret_cast<f32x4*>(xrow + iv * EPL + 4 * q) = xo;
+        }
+        *reinterpret_cast<uint4*>(xarow + iv * EPL) = *reinterpret_cast<const uint4*>(xa_out);
+      }
+    }
   }
   ss = wave_sum(ss);
   if (tid % kWave == 0) red[tid / kWave] = ss;
