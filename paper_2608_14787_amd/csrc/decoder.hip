@@ -131,9 +131,9 @@ __device__ inline uint32_t unit_start(uint32_t w, uint32_t U, uint32_t n) { retu
 // Loads into L2 the first three k-steps of the segment that workgroup w of a
 // GEMM launch (tiled weights Wn, KTn k-steps, Gn column groups of ngn tiles,
 // nwg workgroups) streams first, wave `wave` (0..3) the k-steps that wave
-// streams there (every fourth from the segment's start + wave).  Called from a workgroup on XCD w mod 8: workgroups are
-// dispatched to the XCDs round-robin, so the lines land in the L2 that serves
-// them.  Plain (cached) loads whose values are consumed by an empty asm
+// streams there (every fourth from the segment's start + wave).  Called from
+// a workgroup on XCD w mod 8: workgroups are dispatched to the XCDs
+// round-robin, so the lines land in the L2 that serves them.  Plain (cached) loads whose values are consumed by an empty asm
 // statement.
 __device__ inline void prefetch_gemm_start(const char* Wn, int KTn_, int Gn, int ngn, int nwg, int w_, int wave,
                                            int lane) {
