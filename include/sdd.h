@@ -142,7 +142,16 @@ int sdd_workspace_init(void* ws, size_t bytes, sdd_stream_t stream);
 
 /* Prefill of sequence seq with tokens[0..n) (device int32): caches positions
  * 0..n-2, sets len = n-1 and pending = tokens[n-1].  The prompt is processed
- * in row chunks of at most max_rows of the workspace. */
+ * in row chunks of at most max_rows of the workspace.
+ * The verifier KV cache is this library's reading of the verify call: the
+ * paper's own verifier keeps no cache and recomputes the whole sequence every
+ * call (Appendix "Evaluation and Throughput"; sdd_verify_full is that mode).
+ * Caching the committed prefix leaves the call's result unchanged: attention
+ * of a position depends only on the positions before it (the causal decoder
+ * the target is).  Errors: SDD_EINVAL (NULL pointer, seq outside
+ * [0, max_batch), n < 1), SDD_ECAPACITY (n - 1 > max_len, workspace too
+ * small for a 16-row chunk); a token outside [0, vocab) is replaced by 0 on
+ * the device and sets sticky error bit1. */
 int sdd_kv_prefill(sdd_model* m, sdd_kv* kv, int seq, const int32_t* tokens, int n,
                    void* ws, size_t ws_bytes, sdd_stream_t stream);
 
@@ -175,8 +184,16 @@ int sdd_verify_block(sdd_model* m, sdd_kv* kv, const int32_t* seq_ids, int n_seq
 int sdd_verify_full(sdd_model* m, sdd_kv* scratch, const int32_t* tokens, int n, int gamma, float* logits,
                     int32_t* argmax, void* ws, size_t ws_bytes, sdd_stream_t stream);
 
-/* Commit after acceptance (device int32 arrays): len += accepted_len + 1,
- * pending = next_token (the target's correction or bonus token). */
+/* Commit after acceptance (Sec. 3.1: the target accepts the prefix
+ * x^_1..x^_L and supplies one more token, its correction at L or the bonus
+ * token after a fully accepted block; Sec. 4.1 commit rule, a strict round
+ * advances by the verified prefix plus that token).  Device int32 arrays
+ * [n_seq]: for sequence seq_ids[i], len += accepted_len[i] + 1 and pending =
+ * next_token[i]; the cache rows len..len+L written by the verify call become
+ * committed, later rows are overwritten by the next call.  Errors: SDD_EINVAL
+ * (NULL pointer, n_seq outside [1, max_batch]); on the device a sequence id
+ * out of range (sticky bit2), a negative length, an overflow of max_len or a
+ * token outside [0, vocab) (sticky bit0) leave that sequence unchanged. */
 int sdd_kv_commit(sdd_kv* kv, const int32_t* seq_ids, int n_seq, const int32_t* accepted_len,
                   const int32_t* next_token, sdd_stream_t stream);
 /* ---- acceptance and confidence ---------------------------------------- */

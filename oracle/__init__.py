@@ -45,8 +45,13 @@ def lib():
         L.orc_model_create.restype = P
         L.orc_model_create.argtypes = [C.POINTER(_Cfg), C.c_uint64, C.c_double]
         L.orc_model_free.argtypes = [P]
+        L.orc_model_create_streamed.restype = P
+        L.orc_model_create_streamed.argtypes = [C.POINTER(_Cfg), C.c_uint64, C.c_double]
         L.orc_model_set_tensor.argtypes = [P, C.c_int, C.c_int, P]
         L.orc_forward_full.argtypes = [P, P, C.c_int, C.c_int, P]
+        L.orc_embed.argtypes = [P, P, C.c_int, P]
+        L.orc_layer_full.argtypes = [P, C.c_int, C.c_int, P]
+        L.orc_final_logits.argtypes = [P, P, C.c_int, P]
         L.orc_forward_full_hidden.argtypes = [P, P, C.c_int, C.c_int, P]
         L.orc_kv_create.restype = P
         L.orc_kv_create.argtypes = [P, C.c_int]
@@ -101,14 +106,19 @@ def tensor_shape(shape, kind: int):
 
 
 class Model:
-    """The target decoder with synthetic weights (seed, sigma) held in host memory."""
+    """The target decoder with synthetic weights (seed, sigma) held in host memory.
 
-    def __init__(self, shape, seed: int = 0, sigma: float = 0.02):
+    streamed=True holds only the embedding, LM head and final norm and generates each layer's
+    weights when a forward reaches it (same values; for shapes whose fp32 copy exceeds host memory)."""
+
+    def __init__(self, shape, seed: int = 0, sigma: float = 0.02, streamed: bool = False):
         self.shape = shape
+        self.streamed = streamed
         c = _Cfg(shape.n_layers, shape.d_model, shape.n_q_heads, shape.n_kv_heads,
                  shape.head_dim, shape.d_ff, shape.vocab, shape.rms_eps, shape.rope_theta,
                  int(shape.qk_norm), int(shape.dtype == "bf16"))
-        self._h = lib().orc_model_create(C.byref(c), seed, sigma)
+        create = lib().orc_model_create_streamed if streamed else lib().orc_model_create
+        self._h = create(C.byref(c), seed, sigma)
         if not self._h:
             raise MemoryError("oracle model creation failed")
 
@@ -123,11 +133,26 @@ class Model:
         if lib().orc_model_set_tensor(self._h, kind, layer, _p(v)) != 0:
             raise ValueError("bad tensor")
 
-    def forward_full(self, tokens, row0: int = 0) -> np.ndarray:
-        """Logits of rows [row0, n) from full recomputation (no cache)."""
+    def forward_full(self, tokens, row0: int = 0, progress=None) -> np.ndarray:
+        """Logits of rows [row0, n) from full recomputation (no cache).
+
+        progress: optional callable(layer) called after each layer (the forward then runs layer by layer
+        through orc_embed / orc_layer_full / orc_final_logits: the same computation)."""
         t = np.ascontiguousarray(tokens, np.int32)
         out = np.empty((len(t) - row0, self.shape.vocab), np.float64)
-        if lib().orc_forward_full(self._h, _p(t), len(t), row0, _p(out)) != 0:
+        if progress is None:
+            if lib().orc_forward_full(self._h, _p(t), len(t), row0, _p(out)) != 0:
+                raise ValueError("forward_full failed")
+            return out
+        x = np.empty((len(t), self.shape.d_model), np.float64)
+        if lib().orc_embed(self._h, _p(t), len(t), _p(x)) != 0:
+            raise ValueError("forward_full failed")
+        for layer in range(self.shape.n_layers):
+            if lib().orc_layer_full(self._h, layer, len(t), _p(x)) != 0:
+                raise ValueError(f"layer {layer} failed")
+            progress(layer)
+        xr = np.ascontiguousarray(x[row0:])
+        if lib().orc_final_logits(self._h, _p(xr), len(t) - row0, _p(out)) != 0:
             raise ValueError("forward_full failed")
         return out
 

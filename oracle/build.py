@@ -9,7 +9,7 @@ LIB = os.path.join(HERE, "libsdd_oracle.so")
 def build(verbose: bool = False) -> str:
     """Compiles oracle/sdd_oracle.c with gcc (IEEE semantics: no fast-math, no FMA contraction)."""
     src = os.path.join(HERE, "sdd_oracle.c")
-    cmd = ["gcc", "-O2", "-fopenmp", "-fPIC", "-shared", "-std=c11", "-ffp-contract=off",
+    cmd = ["gcc", "-O2", "-fopenmp", "-fPIC", "-shared", "-std=c11", "-ffp-contract=off", "-fno-semantic-interposition",
            "-fno-fast-math", "-Wall", "-Wno-unknown-pragmas", "-o", LIB + ".tmp", src, "-lm"]
     if verbose:
         print(" ".join(cmd))

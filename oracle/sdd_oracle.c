@@ -117,6 +117,15 @@ struct orc_model {
     float *wq, *wk, *wv, *wo, *wg, *wu, *wd;
     float *attn_norm, *ffn_norm, *q_norm, *k_norm;
   } * L;
+  /* Layer streaming (orc_model_create_streamed): the layers' tensors are not
+   * held; a forward generates a layer's tensors when it reaches the layer and
+   * frees them after it, so a model whose fp32 copy exceeds host memory (the
+   * 64-layer Qwen3-32B shape: 131 GB) can still be run.  The values are the
+   * ones a materialized model holds (same generator, same indices). */
+  int streamed;
+  uint64_t seed;
+  double sigma;
+  float* stream_buf[ORC_K_NORM + 1]; /* one layer's tensors, reused by every layer (indexed by kind) */
 };
 
 int orc_tensor_shape(const orc_config* c, int kind, int64_t* rows, int64_t* cols) {
@@ -160,16 +169,14 @@ static int orc_is_norm(int kind) {
          kind == ORC_Q_NORM || kind == ORC_K_NORM;
 }
 
-static float* orc_make_tensor(const orc_config* c, int kind, int layer, uint64_t seed,
-                              double sigma) {
+/* Writes tensor (kind, layer)'s synthetic values into t. */
+static void orc_fill_tensor(const orc_config* c, int kind, int layer, uint64_t seed, double sigma, float* t) {
   int64_t rows, cols;
   orc_tensor_shape(c, kind, &rows, &cols);
   int64_t n = rows * cols;
-  float* t = (float*)malloc((size_t)n * sizeof(float));
-  if (!t) return NULL;
   if (orc_is_norm(kind)) { /* RMSNorm gains start at one */
     for (int64_t i = 0; i < n; ++i) t[i] = 1.0f;
-    return t;
+    return;
   }
   int id = orc_tensor_id(kind, layer);
   const int64_t chunk = 1 << 16;
@@ -178,15 +185,24 @@ static float* orc_make_tensor(const orc_config* c, int kind, int layer, uint64_t
     int64_t cnt = (n - s < chunk) ? n - s : chunk;
     orc_weight_values(seed, id, (uint64_t)s, (uint64_t)cnt, sigma, c->bf16_weights, t + s);
   }
+}
+
+static float* orc_make_tensor(const orc_config* c, int kind, int layer, uint64_t seed,
+                              double sigma) {
+  int64_t rows, cols;
+  orc_tensor_shape(c, kind, &rows, &cols);
+  float* t = (float*)malloc((size_t)(rows * cols) * sizeof(float));
+  if (t) orc_fill_tensor(c, kind, layer, seed, sigma, t);
   return t;
 }
 
 void orc_model_free(orc_model* m) {
   if (!m) return;
+  for (int kind = 0; kind <= ORC_K_NORM; ++kind) free(m->stream_buf[kind]);
   free(m->embed);
   free(m->lm_head);
   free(m->final_norm);
-  if (m->L) {
+  if (m->L && !m->streamed) {
     for (int l = 0; l < m->c.n_layers; ++l) {
       free(m->L[l].wq); free(m->L[l].wk); free(m->L[l].wv); free(m->L[l].wo);
       free(m->L[l].wg); free(m->L[l].wu); free(m->L[l].wd);
@@ -226,9 +242,59 @@ orc_model* orc_model_create(const orc_config* cfg, uint64_t seed, double sigma) 
   return m;
 }
 
+orc_model* orc_model_create_streamed(const orc_config* cfg, uint64_t seed, double sigma) {
+  if (!cfg || cfg->n_layers < 0 || cfg->d_model <= 0 || cfg->n_q_heads <= 0 ||
+      cfg->n_kv_heads <= 0 || cfg->n_q_heads % cfg->n_kv_heads || cfg->head_dim <= 0 ||
+      cfg->head_dim % 2 || cfg->d_ff <= 0 || cfg->vocab <= 0)
+    return NULL;
+  orc_model* m = (orc_model*)calloc(1, sizeof(orc_model));
+  if (!m) return NULL;
+  m->c = *cfg;
+  m->streamed = 1;
+  m->seed = seed;
+  m->sigma = sigma;
+  m->L = calloc((size_t)(cfg->n_layers > 0 ? cfg->n_layers : 1), sizeof(*m->L));
+  int ok = m->L != NULL;
+  for (int kind = ORC_EMBED; ok && kind <= ORC_FINAL_NORM; ++kind) {
+    float** s = orc_slot(m, kind, 0);
+    *s = orc_make_tensor(cfg, kind, 0, seed, sigma);
+    ok = *s != NULL;
+  }
+  if (!ok) {
+    orc_model_free(m);
+    return NULL;
+  }
+  return m;
+}
+
+/* Layer l's tensors for a forward: present in a materialized model, generated
+ * now in a streamed one (0 on success). */
+static int layer_acquire(const orc_model* cm, int l) {
+  if (!cm->streamed) return 0;
+  orc_model* m = (orc_model*)cm; /* a streamed model's layer slots are a per-forward cache */
+  for (int kind = ORC_WQ; kind <= ORC_K_NORM; ++kind) {
+    if (!m->stream_buf[kind]) { /* every layer has the same shapes: one buffer per kind */
+      int64_t rows, cols;
+      orc_tensor_shape(&m->c, kind, &rows, &cols);
+      m->stream_buf[kind] = (float*)malloc((size_t)(rows * cols) * sizeof(float));
+      if (!m->stream_buf[kind]) return -1;
+    }
+    orc_fill_tensor(&m->c, kind, l, m->seed, m->sigma, m->stream_buf[kind]);
+    *orc_slot(m, kind, l) = m->stream_buf[kind];
+  }
+  return 0;
+}
+
+static void layer_release(const orc_model* cm, int l) {
+  if (!cm->streamed) return;
+  orc_model* m = (orc_model*)cm;
+  for (int kind = ORC_WQ; kind <= ORC_K_NORM; ++kind) *orc_slot(m, kind, l) = NULL;
+}
+
 int orc_model_set_tensor(orc_model* m, int kind, int layer, const float* src) {
   if (!m || !src || kind < ORC_EMBED || kind > ORC_K_NORM) return -1;
   if (kind >= ORC_WQ && (layer < 0 || layer >= m->c.n_layers)) return -1;
+  if (kind >= ORC_WQ && m->streamed) return -1; /* a streamed model regenerates its layers */
   int64_t rows, cols;
   orc_tensor_shape(&m->c, kind, &rows, &cols);
   memcpy(*orc_slot(m, kind, layer), src, (size_t)(rows * cols) * sizeof(float));
@@ -239,11 +305,31 @@ int orc_model_set_tensor(orc_model* m, int kind, int layer, const float* src) {
 /* Decoder building blocks, fp64 */
 
 /* Y[r][n] = sum_k X[r][k] * W[n][k]  (PyTorch Linear convention W[out][in]) */
+/* Every Y[r][n] is one running sum over k = 0..K-1 in increasing order.  Four
+ * rows walk W's row n together (four independent running sums: the same
+ * additions, in the same order, as one row at a time; it only keeps the
+ * processor's adders busy). */
 static void linear(const float* W, int N, int K, const double* X, int R, double* Y) {
 #pragma omp parallel for schedule(static)
   for (int n = 0; n < N; ++n) {
     const float* w = W + (size_t)n * K;
-    for (int r = 0; r < R; ++r) {
+    int r = 0;
+    for (; r + 4 <= R; r += 4) {
+      const double *x0 = X + (size_t)r * K, *x1 = x0 + K, *x2 = x1 + K, *x3 = x2 + K;
+      double a0 = 0.0, a1 = 0.0, a2 = 0.0, a3 = 0.0;
+      for (int k = 0; k < K; ++k) {
+        const double wk = (double)w[k];
+        a0 += x0[k] * wk;
+        a1 += x1[k] * wk;
+        a2 += x2[k] * wk;
+        a3 += x3[k] * wk;
+      }
+      Y[(size_t)r * N + n] = a0;
+      Y[(size_t)(r + 1) * N + n] = a1;
+      Y[(size_t)(r + 2) * N + n] = a2;
+      Y[(size_t)(r + 3) * N + n] = a3;
+    }
+    for (; r < R; ++r) {
       const double* x = X + (size_t)r * K;
       double acc = 0.0;
       for (int k = 0; k < K; ++k) acc += x[k] * (double)w[k];
@@ -345,55 +431,87 @@ static int tokens_ok(const orc_model* m, const int32_t* tok, int n) {
 /* Route 1: full recomputation, no cache.  Every row attends to rows 0..i of
  * the same pass (causal mask). */
 
-static int forward_full_x(const orc_model* m, const int32_t* tokens, int n, double* x) {
+/* Layer l of the full recomputation applied to the n rows x in place. */
+static int layer_full(const orc_model* m, int l, int n, double* x) {
   const orc_config* c = &m->c;
   int d = c->d_model, hd = c->head_dim, hq = c->n_q_heads, hk = c->n_kv_heads;
   int grp = hq / hk;
   size_t nq = (size_t)hq * hd, nk = (size_t)hk * hd;
+  int rc = layer_acquire(m, l);
+  if (rc) return rc;
   double* h = (double*)malloc(sizeof(double) * (size_t)n * d);
   double* q = (double*)malloc(sizeof(double) * (size_t)n * nq);
   double* k = (double*)malloc(sizeof(double) * (size_t)n * nk);
   double* v = (double*)malloc(sizeof(double) * (size_t)n * nk);
   double* o = (double*)malloc(sizeof(double) * (size_t)n * nq);
   double* y = (double*)malloc(sizeof(double) * (size_t)n * d);
-  embed_rows(m, tokens, n, x);
   double scale = 1.0 / sqrt((double)hd);
-  for (int l = 0; l < c->n_layers; ++l) {
-    for (int r = 0; r < n; ++r) rmsnorm(x + (size_t)r * d, d, m->L[l].attn_norm, c->rms_eps, h + (size_t)r * d);
-    linear(m->L[l].wq, (int)nq, d, h, n, q);
-    linear(m->L[l].wk, (int)nk, d, h, n, k);
-    linear(m->L[l].wv, (int)nk, d, h, n, v);
-    qk_post(m, l, q, k, n, 0);
+  for (int r = 0; r < n; ++r) rmsnorm(x + (size_t)r * d, d, m->L[l].attn_norm, c->rms_eps, h + (size_t)r * d);
+  linear(m->L[l].wq, (int)nq, d, h, n, q);
+  linear(m->L[l].wk, (int)nk, d, h, n, k);
+  linear(m->L[l].wv, (int)nk, d, h, n, v);
+  qk_post(m, l, q, k, n, 0);
 #pragma omp parallel for schedule(dynamic)
-    for (int i = 0; i < n; ++i) {
-      double* s = (double*)malloc(sizeof(double) * (size_t)(i + 1));
-      for (int hh = 0; hh < hq; ++hh) {
-        int kh = hh / grp;
-        const double* qi = q + ((size_t)i * hq + hh) * hd;
-        double mx = -INFINITY;
-        for (int j = 0; j <= i; ++j) {
-          const double* kj = k + ((size_t)j * hk + kh) * hd;
-          double dot = 0.0;
-          for (int t = 0; t < hd; ++t) dot += qi[t] * kj[t];
-          s[j] = dot * scale;
-          if (s[j] > mx) mx = s[j];
-        }
-        double den = 0.0;
-        for (int j = 0; j <= i; ++j) { s[j] = exp(s[j] - mx); den += s[j]; }
-        double* oi = o + ((size_t)i * hq + hh) * hd;
-        for (int t = 0; t < hd; ++t) {
-          double acc = 0.0;
-          for (int j = 0; j <= i; ++j) acc += s[j] * v[((size_t)j * hk + kh) * hd + t];
-          oi[t] = acc / den;
-        }
+  for (int i = 0; i < n; ++i) {
+    double* s = (double*)malloc(sizeof(double) * (size_t)(i + 1));
+    for (int hh = 0; hh < hq; ++hh) {
+      int kh = hh / grp;
+      const double* qi = q + ((size_t)i * hq + hh) * hd;
+      double mx = -INFINITY;
+      for (int j = 0; j <= i; ++j) {
+        const double* kj = k + ((size_t)j * hk + kh) * hd;
+        double dot = 0.0;
+        for (int t = 0; t < hd; ++t) dot += qi[t] * kj[t];
+        s[j] = dot * scale;
+        if (s[j] > mx) mx = s[j];
       }
-      free(s);
+      double den = 0.0;
+      for (int j = 0; j <= i; ++j) { s[j] = exp(s[j] - mx); den += s[j]; }
+      /* o_t = sum_j s_j v_j,t / den: every o_t sums over j = 0..i in order (the
+       * loops are interchanged only so that V is read row by row) */
+      double* oi = o + ((size_t)i * hq + hh) * hd;
+      for (int t = 0; t < hd; ++t) oi[t] = 0.0;
+      for (int j = 0; j <= i; ++j) {
+        const double* vj = v + ((size_t)j * hk + kh) * hd;
+        for (int t = 0; t < hd; ++t) oi[t] += s[j] * vj[t];
+      }
+      for (int t = 0; t < hd; ++t) oi[t] /= den;
     }
-    linear(m->L[l].wo, d, (int)nq, o, n, y);
-    for (size_t i = 0; i < (size_t)n * d; ++i) x[i] += y[i];
-    ffn_block(m, l, x, n);
+    free(s);
   }
+  linear(m->L[l].wo, d, (int)nq, o, n, y);
+  for (size_t i = 0; i < (size_t)n * d; ++i) x[i] += y[i];
+  ffn_block(m, l, x, n);
+  layer_release(m, l);
   free(h); free(q); free(k); free(v); free(o); free(y);
+  return 0;
+}
+
+static int forward_full_x(const orc_model* m, const int32_t* tokens, int n, double* x) {
+  embed_rows(m, tokens, n, x);
+  for (int l = 0; l < m->c.n_layers; ++l) {
+    int rc = layer_full(m, l, n, x);
+    if (rc) return rc;
+  }
+  return 0;
+}
+
+/* The full recomputation in steps (the same functions orc_forward_full runs),
+ * so that a caller can follow a long forward layer by layer. */
+int orc_embed(const orc_model* m, const int32_t* tokens, int n, double* x) {
+  if (!m || !tokens || !x || n <= 0 || !tokens_ok(m, tokens, n)) return -1;
+  embed_rows(m, tokens, n, x);
+  return 0;
+}
+
+int orc_layer_full(const orc_model* m, int layer, int n, double* x) {
+  if (!m || !x || n <= 0 || layer < 0 || layer >= m->c.n_layers) return -1;
+  return layer_full(m, layer, n, x);
+}
+
+int orc_final_logits(const orc_model* m, const double* x, int R, double* logits) {
+  if (!m || !x || !logits || R <= 0) return -1;
+  lm_head(m, x, R, logits);
   return 0;
 }
 
@@ -401,20 +519,20 @@ int orc_forward_full(const orc_model* m, const int32_t* tokens, int n, int row0,
   if (!m || !tokens || !logits || n <= 0 || row0 < 0 || row0 >= n || !tokens_ok(m, tokens, n)) return -1;
   int d = m->c.d_model;
   double* x = (double*)malloc(sizeof(double) * (size_t)n * d);
-  forward_full_x(m, tokens, n, x);
-  lm_head(m, x + (size_t)row0 * d, n - row0, logits);
+  int rc = forward_full_x(m, tokens, n, x);
+  if (rc == 0) lm_head(m, x + (size_t)row0 * d, n - row0, logits);
   free(x);
-  return 0;
+  return rc;
 }
 
 int orc_forward_full_hidden(const orc_model* m, const int32_t* tokens, int n, int row0, double* hidden) {
   if (!m || !tokens || !hidden || n <= 0 || row0 < 0 || row0 >= n || !tokens_ok(m, tokens, n)) return -1;
   int d = m->c.d_model;
   double* x = (double*)malloc(sizeof(double) * (size_t)n * d);
-  forward_full_x(m, tokens, n, x);
-  memcpy(hidden, x + (size_t)row0 * d, sizeof(double) * (size_t)(n - row0) * d);
+  int rc = forward_full_x(m, tokens, n, x);
+  if (rc == 0) memcpy(hidden, x + (size_t)row0 * d, sizeof(double) * (size_t)(n - row0) * d);
   free(x);
-  return 0;
+  return rc;
 }
 
 /* ------------------------------------------------------------------------ */
@@ -465,7 +583,7 @@ int orc_kv_read(const orc_kv* kv, int layer, int pos, double* k, double* v) {
 }
 
 /* Runs R rows at positions pos0.. through all layers, appending K/V. */
-static void block_forward(orc_kv* kv, const int32_t* tok, int R, int pos0, double* x) {
+static int block_forward(orc_kv* kv, const int32_t* tok, int R, int pos0, double* x) {
   const orc_model* m = kv->m;
   const orc_config* c = &m->c;
   int d = c->d_model, hd = c->head_dim, hq = c->n_q_heads, hk = c->n_kv_heads;
@@ -479,7 +597,9 @@ static void block_forward(orc_kv* kv, const int32_t* tok, int R, int pos0, doubl
   double* y = (double*)malloc(sizeof(double) * (size_t)R * d);
   embed_rows(m, tok, R, x);
   double scale = 1.0 / sqrt((double)hd);
+  int rc = 0;
   for (int l = 0; l < c->n_layers; ++l) {
+    if ((rc = layer_acquire(m, l))) break;
     double* K = kv->k + (size_t)l * kv->max_len * nk;
     double* V = kv->v + (size_t)l * kv->max_len * nk;
     for (int r = 0; r < R; ++r) rmsnorm(x + (size_t)r * d, d, m->L[l].attn_norm, c->rms_eps, h + (size_t)r * d);
@@ -506,20 +626,24 @@ static void block_forward(orc_kv* kv, const int32_t* tok, int R, int pos0, doubl
         }
         double den = 0.0;
         for (int j = 0; j <= last; ++j) { s[j] = exp(s[j] - mx); den += s[j]; }
+        /* every o_t sums over j = 0..last in order (loops interchanged to read V row by row) */
         double* oi = o + ((size_t)r * hq + hh) * hd;
-        for (int t = 0; t < hd; ++t) {
-          double acc = 0.0;
-          for (int j = 0; j <= last; ++j) acc += s[j] * V[(size_t)j * nk + (size_t)kh * hd + t];
-          oi[t] = acc / den;
+        for (int t = 0; t < hd; ++t) oi[t] = 0.0;
+        for (int j = 0; j <= last; ++j) {
+          const double* vj = V + (size_t)j * nk + (size_t)kh * hd;
+          for (int t = 0; t < hd; ++t) oi[t] += s[j] * vj[t];
         }
+        for (int t = 0; t < hd; ++t) oi[t] /= den;
       }
       free(s);
     }
     linear(m->L[l].wo, d, (int)nq, o, R, y);
     for (size_t i = 0; i < (size_t)R * d; ++i) x[i] += y[i];
     ffn_block(m, l, x, R);
+    layer_release(m, l);
   }
   free(h); free(q); free(k); free(v); free(o); free(y);
+  return rc;
 }
 
 int orc_kv_prefill(orc_kv* kv, const int32_t* tokens, int n) {
@@ -527,8 +651,9 @@ int orc_kv_prefill(orc_kv* kv, const int32_t* tokens, int n) {
   int d = kv->m->c.d_model;
   if (n > 1) {
     double* x = (double*)malloc(sizeof(double) * (size_t)(n - 1) * d);
-    block_forward(kv, tokens, n - 1, 0, x);
+    int rc = block_forward(kv, tokens, n - 1, 0, x);
     free(x);
+    if (rc) return rc;
   }
   kv->len = n - 1;
   kv->pending = tokens[n - 1];
@@ -544,11 +669,11 @@ int orc_verify(orc_kv* kv, const int32_t* drafts, int gamma, double* logits) {
   tok[0] = kv->pending;
   for (int j = 0; j < gamma; ++j) tok[j + 1] = drafts[j];
   double* x = (double*)malloc(sizeof(double) * (size_t)R * d);
-  block_forward(kv, tok, R, kv->len, x);
-  lm_head(kv->m, x, R, logits);
+  int rc = block_forward(kv, tok, R, kv->len, x);
+  if (rc == 0) lm_head(kv->m, x, R, logits);
   free(x);
   free(tok);
-  return 0;
+  return rc;
 }
 
 int orc_commit(orc_kv* kv, int accepted_len, int next_token) {

@@ -57,6 +57,12 @@ void orc_weight_values(uint64_t seed, int tensor_id, uint64_t start, uint64_t co
 typedef struct orc_model orc_model;
 orc_model* orc_model_create(const orc_config* cfg, uint64_t seed, double sigma);
 void orc_model_free(orc_model* m);
+/* The same model with layer streaming: only the embedding, LM head and final
+ * norm are held; every forward (full or cached route) generates a layer's
+ * tensors when it reaches the layer and frees them after it.  Same values as
+ * orc_model_create; norm gains are 1 and cannot be replaced
+ * (orc_model_set_tensor refuses layer tensors). */
+orc_model* orc_model_create_streamed(const orc_config* cfg, uint64_t seed, double sigma);
 /* shape of a tensor kind: rows x cols (row-major, PyTorch Linear [out][in]) */
 int orc_tensor_shape(const orc_config* cfg, int kind, int64_t* rows, int64_t* cols);
 int orc_model_set_tensor(orc_model* m, int kind, int layer, const float* src);
@@ -67,6 +73,15 @@ int orc_forward_full(const orc_model* m, const int32_t* tokens, int n, int row0,
 /* Same, but returns the final hidden rows (after the last layer, before the
  * final norm) for rows [row0, n): hidden[(n-row0) * d]. */
 int orc_forward_full_hidden(const orc_model* m, const int32_t* tokens, int n, int row0, double* hidden);
+
+/* orc_forward_full in steps: x[n][d] (fp64) = embedding rows of tokens;
+ * orc_layer_full applies layer `layer` to all n rows in place (causal
+ * attention among them); orc_final_logits applies the final norm and the LM
+ * head to R rows.  Embedding, layers 0..n_layers-1 in order, then the rows
+ * from row0 give exactly orc_forward_full's logits. */
+int orc_embed(const orc_model* m, const int32_t* tokens, int n, double* x);
+int orc_layer_full(const orc_model* m, int layer, int n, double* x);
+int orc_final_logits(const orc_model* m, const double* x, int R, double* logits);
 
 /* Cached mode: one sequence, K/V of every layer kept in fp64. */
 typedef struct orc_kv orc_kv;

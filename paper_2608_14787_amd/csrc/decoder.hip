@@ -1122,18 +1122,21 @@ __global__ void __launch_bounds__(kAttnWaves * 64) attention_mfma_kernel(AttnMfm
   // are only consumed by an empty asm statement; they are issued before the
   // stream's own loads and land while its first steps wait.
   constexpr int kPre = 4;  // blocks per wave
-  constexpr int kBlk = 2 * KK + DB;  // 1 KB blocks per step and cache: K then V
+  // 1 KB blocks of one step: 2 KK of K (the step's 32 x HD elements), then DB of V (the same amount)
+  constexpr int kBlk = 2 * KK + DB;
   uint4 pre[kPre];
   {
     const int n_steps_all = (kv_end + 31) / 32;
 #pragma unroll
     for (int i = 0; i < kPre; ++i) {
       const int j = wave + kAttnWaves * i;         // this workgroup's j-th block
-      const int st = qb + a.qblocks * (j / (2 * kBlk));
-      const int bi = j % (2 * kBlk);
-      const int stc = st < n_steps_all ? st : 0;   // past the end: step 0 again (in range, already wanted)
-      const uint16_t* src = bi < kBlk ? K : Vt;
-      pre[i] = load16(src + (int64_t)stc * 32 * HD + (bi % kBlk) * 512 + lane * 8);  // unconditional (one load order)
+      const int st = qb + a.qblocks * (j / kBlk);  // the step it belongs to
+      const int bi = j % kBlk;                     // its block inside the step
+      // past the last step: step 0 again (in range, already wanted).  Step stc lies inside the head's
+      // cache: (stc + 1) * 32 <= 32 * ceil(kv_end / 32) <= ld, ld being a multiple of 64 >= kv_end.
+      const int stc = st < n_steps_all ? st : 0;
+      const uint16_t* src = bi < 2 * KK ? K + bi * 512 : Vt + (bi - 2 * KK) * 512;
+      pre[i] = load16(src + (int64_t)stc * 32 * HD + lane * 8);  // unconditional (one load order)
     }
   }
   // The loads sit only inside the loop (a first pass issues them and skips

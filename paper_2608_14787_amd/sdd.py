@@ -113,6 +113,26 @@ def _stream(stream=None):
     return C.c_void_p(s.cuda_stream)
 
 
+def _need(cond: bool, msg: str):
+    if not cond:
+        raise ValueError(msg)
+
+
+def _i32(t, name: str, allow_none: bool = False):
+    """An int32 contiguous device tensor (the C ABI reads int32 arrays with no strides)."""
+    if t is None:
+        _need(allow_none, f"{name} is required")
+        return
+    _need(t.dtype == torch.int32, f"{name} must be int32, got {t.dtype}")
+    _need(t.is_contiguous(), f"{name} must be contiguous")
+
+
+def _rows(t, name: str):
+    """Logit rows the C ABI addresses as base + b * stride(0) + j * V: unit element stride, rows V apart."""
+    _need(t.dim() == 3, f"{name} must be [B, rows, V]")
+    _need(t.stride(2) == 1 and t.stride(1) == t.shape[2], f"{name}: rows must be contiguous and V elements apart")
+
+
 def _dtype_code(t: torch.Tensor) -> int:
     if t.dtype == torch.float32:
         return F32
@@ -153,8 +173,15 @@ def accept(draft: torch.Tensor, p: torch.Tensor, mode: int, *, q: torch.Tensor |
     if out is None:
         out = tuple(torch.empty(B, dtype=torch.int32, device=p.device) for _ in range(3))
     L, nxt, fl = out
+    _need(p.is_contiguous(), "p must be contiguous [B, gamma+1, V]")
+    _i32(draft, "draft", allow_none=gamma == 0)
+    for t, nm in ((L, "accepted_len"), (nxt, "next_token"), (fl, "flags")):
+        _i32(t, nm, allow_none=nm == "flags")
+    if uniforms is not None:
+        _need(uniforms.dtype == torch.float32 and uniforms.is_contiguous(), "uniforms must be contiguous fp32")
     qd, qs = F32, 0
     if q is not None:
+        _rows(q, "q")
         qd, qs = _dtype_code(q), q.stride(0)
     _check(lib().sdd_accept(_ptr(draft), _ptr(p), _dtype_code(p), _ptr(q), qd, qs, _ptr(uniforms),
                             B, gamma, V, mode, k, lenience, _ptr(L), _ptr(nxt), _ptr(fl), _ptr(ws),
@@ -169,6 +196,8 @@ def confidence_prefix(logits: torch.Tensor, gamma: int, tau: float, *, draft=Non
     log_conf: False, True (allocate) or a contiguous fp32 [B, gamma] tensor to write into.
     Returns skip_len int32 [B] (and log_conf, log_p_draft fp32 [B, gamma] when requested)."""
     B, R, V = logits.shape
+    _rows(logits, "logits")
+    _i32(draft, "draft", allow_none=True)
     if ws is None:
         ws = rowstats_workspace(B, gamma, V, logits.device)
     sk = out if out is not None else torch.empty(B, dtype=torch.int32, device=logits.device)
@@ -329,12 +358,18 @@ class KVCache:
         return p.value
 
     def prefill(self, seq: int, tokens: torch.Tensor, ws: torch.Tensor, stream=None):
+        _i32(tokens, "tokens")
         _check(lib().sdd_kv_prefill(self.model.handle, self.handle, seq, _ptr(tokens), tokens.numel(),
                                     _ptr(ws), ws.numel(), _stream(stream)))
 
     def verify(self, seq_ids: torch.Tensor, drafts: torch.Tensor, logits: torch.Tensor,
                argmax: torch.Tensor | None, ws: torch.Tensor, stream=None):
         n_seq, gamma = drafts.shape
+        _i32(seq_ids, "seq_ids")
+        _i32(drafts, "drafts")
+        _i32(argmax, "argmax", allow_none=True)
+        _need(logits.dtype == torch.float32 and logits.is_contiguous(), "logits must be contiguous fp32")
+        _need(logits.numel() >= n_seq * (gamma + 1) * self.model.shape.vocab, "logits too small")
         _check(lib().sdd_verify_block(self.model.handle, self.handle, _ptr(seq_ids), n_seq,
                                       _ptr(drafts) if gamma else None, gamma, _ptr(logits), _ptr(argmax),
                                       _ptr(ws), ws.numel(), _stream(stream)))
@@ -342,9 +377,14 @@ class KVCache:
     def verify_full(self, tokens: torch.Tensor, gamma: int, logits: torch.Tensor, argmax: torch.Tensor | None,
                     ws: torch.Tensor, stream=None):
         """sdd_verify_full: this cache is the scratch (slot 0 overwritten); tokens int32 [n] = context + drafts."""
+        _i32(tokens, "tokens")
+        _i32(argmax, "argmax", allow_none=True)
+        _need(logits.dtype == torch.float32 and logits.is_contiguous(), "logits must be contiguous fp32")
         _check(lib().sdd_verify_full(self.model.handle, self.handle, _ptr(tokens), tokens.numel(), gamma, _ptr(logits),
                                      _ptr(argmax), _ptr(ws), ws.numel(), _stream(stream)))
 
     def commit(self, seq_ids: torch.Tensor, accepted_len: torch.Tensor, next_token: torch.Tensor, stream=None):
+        for t, nm in ((seq_ids, "seq_ids"), (accepted_len, "accepted_len"), (next_token, "next_token")):
+            _i32(t, nm)
         _check(lib().sdd_kv_commit(self.handle, _ptr(seq_ids), seq_ids.numel(), _ptr(accepted_len),
                                    _ptr(next_token), _stream(stream)))

@@ -38,3 +38,19 @@ def argmax_near_tie(z: np.ndarray, tol: np.ndarray) -> np.ndarray:
     """True where the top-2 gap of a row is below tol (an argmax that rounding may flip)."""
     s = np.sort(z, axis=-1)
     return (s[..., -1] - s[..., -2]) < tol
+
+
+# tensor kinds of include/sdd.h for the norm gains (the oracle numbers them alike)
+_GAIN_KIND = {"final": 2, "attn": 10, "ffn": 11, "q": 12, "k": 13}
+
+
+def load_gains(model, gains: dict):
+    """Loads workloads.norm_gains into a GPU model (sdd_model_load_tensor)."""
+    for (name, layer), v in gains.items():
+        model.load_tensor(_GAIN_KIND[name], layer, torch.from_numpy(np.ascontiguousarray(v, np.float32)).cuda())
+
+
+def oracle_gains(om, gains: dict):
+    """The same gains into an oracle model (orc_model_set_tensor)."""
+    for (name, layer), v in gains.items():
+        om.set_tensor(_GAIN_KIND[name], layer, v)

@@ -44,31 +44,53 @@ def _rope_torch(x, pos, theta):
     return x * cos + torch.cat([-x2, x1], -1) * sin
 
 
-def _torch_reference(shape, w, tokens):
-    """Decoder as a composition of torch.nn.functional ops, float64 on the CPU."""
+def _torch_reference(shape, w, tokens, gains=None):
+    """Decoder as a composition of torch.nn.functional ops, float64 on the CPU.
+
+    gains: optional dict of RMSNorm gains keyed like w ((kind, layer) or FINAL_NORM); missing ones are 1."""
     t = lambda a: torch.from_numpy(np.asarray(a, np.float64))
     d, hd, hq, hk = shape.d_model, shape.head_dim, shape.n_q_heads, shape.n_kv_heads
     n = len(tokens)
+    gains = gains or {}
+    g = lambda key, size: t(gains[key]) if key in gains else torch.ones(size, dtype=torch.float64)
     x = F.embedding(torch.from_numpy(np.asarray(tokens, np.int64)), t(w[oracle.EMBED]))
     pos = torch.arange(n)
-    one = torch.ones(d, dtype=torch.float64)
     for l in range(shape.n_layers):
-        h = F.rms_norm(x, (d,), one, eps=shape.rms_eps)
+        h = F.rms_norm(x, (d,), g((oracle.ATTN_NORM, l), d), eps=shape.rms_eps)
         q = F.linear(h, t(w[(oracle.WQ, l)])).view(n, hq, hd)
         k = F.linear(h, t(w[(oracle.WK, l)])).view(n, hk, hd)
         v = F.linear(h, t(w[(oracle.WV, l)])).view(n, hk, hd)
         if shape.qk_norm:
-            q = F.rms_norm(q, (hd,), torch.ones(hd, dtype=torch.float64), eps=shape.rms_eps)
-            k = F.rms_norm(k, (hd,), torch.ones(hd, dtype=torch.float64), eps=shape.rms_eps)
+            q = F.rms_norm(q, (hd,), g((oracle.Q_NORM, l), hd), eps=shape.rms_eps)
+            k = F.rms_norm(k, (hd,), g((oracle.K_NORM, l), hd), eps=shape.rms_eps)
         q, k = _rope_torch(q, pos, shape.rope_theta), _rope_torch(k, pos, shape.rope_theta)
         o = F.scaled_dot_product_attention(q.transpose(0, 1), k.transpose(0, 1), v.transpose(0, 1),
                                            is_causal=True, enable_gqa=True)
         x = x + F.linear(o.transpose(0, 1).reshape(n, hq * hd), t(w[(oracle.WO, l)]))
-        h = F.rms_norm(x, (d,), one, eps=shape.rms_eps)
+        h = F.rms_norm(x, (d,), g((oracle.FFN_NORM, l), d), eps=shape.rms_eps)
         a = F.silu(F.linear(h, t(w[(oracle.WGATE, l)]))) * F.linear(h, t(w[(oracle.WUP, l)]))
         x = x + F.linear(a, t(w[(oracle.WDOWN, l)]))
-    h = F.rms_norm(x, (d,), one, eps=shape.rms_eps)
+    h = F.rms_norm(x, (d,), g(oracle.FINAL_NORM, d), eps=shape.rms_eps)
     return F.linear(h, t(w[oracle.LM_HEAD])).numpy()
+
+
+_GAIN_KIND = {"final": oracle.FINAL_NORM, "attn": oracle.ATTN_NORM, "ffn": oracle.FFN_NORM,
+              "q": oracle.Q_NORM, "k": oracle.K_NORM}
+
+
+def random_gains(shape, seed):
+    """workloads.norm_gains keyed like _weights: (kind, layer), or FINAL_NORM."""
+    out = {}
+    for (name, layer), v in W.norm_gains(seed, shape).items():
+        kind = _GAIN_KIND[name]
+        out[kind if kind == oracle.FINAL_NORM else (kind, layer)] = v
+    return out
+
+
+def _set_gains(m, gains):
+    for key, v in gains.items():
+        kind, layer = key if isinstance(key, tuple) else (key, 0)
+        m.set_tensor(kind, layer, v)
 
 
 @pytest.mark.parametrize("shape", [SMALL, SMALL_BF16], ids=["qknorm-f32", "gqa4-bf16"])
@@ -172,3 +194,59 @@ def test_capacity_and_bad_tokens():
         kv.verify([1, 2, 3, 4, 5, 6])  # 2 + 7 rows > 8
     with pytest.raises(ValueError):
         kv.verify([SMALL.vocab])
+
+
+@pytest.mark.parametrize("shape", [SMALL, SMALL_BF16], ids=["qknorm-f32", "gqa4-bf16"])
+def test_nonunit_norm_gains_match_torch(shape):
+    """Every RMSNorm gain (attention, FFN, final, and q/k with QK-norm) applied where the decoder applies it:
+    random gains per tensor and layer, against torch's rms_norm with the same weights."""
+    gains = random_gains(shape, 17)
+    m = oracle.Model(shape)
+    _set_gains(m, gains)
+    toks = W.prompt(18, 15, shape.vocab)
+    want = _torch_reference(shape, _weights(shape), toks, gains)
+    np.testing.assert_allclose(m.forward_full(toks), want, rtol=0, atol=1e-10 * np.abs(want).max())
+    # a gain moved to another layer or norm changes the logits (the check above sees misplaced gains)
+    swapped = dict(gains)
+    swapped[(oracle.ATTN_NORM, 0)], swapped[(oracle.FFN_NORM, 0)] = gains[(oracle.FFN_NORM, 0)], gains[(oracle.ATTN_NORM, 0)]
+    other = _torch_reference(shape, _weights(shape), toks, swapped)
+    assert np.abs(other - want).max() > 1e-6 * np.abs(want).max()
+    # the cached route agrees
+    kv = oracle.KV(m, 32)
+    kv.prefill(toks[:9])
+    np.testing.assert_allclose(kv.verify(toks[9:15]), want[8:15], rtol=0, atol=1e-10 * np.abs(want).max())
+
+
+def test_long_sequence_matches_torch_functional():
+    """Attention over a few hundred positions (the loops whose order was interchanged to read V by rows)."""
+    shape = SMALL.with_layers(1)
+    toks = W.prompt(19, 300, shape.vocab)
+    m = oracle.Model(shape)
+    want = _torch_reference(shape, _weights(shape), toks)
+    np.testing.assert_allclose(m.forward_full(toks, 250), want[250:], rtol=0, atol=1e-10 * np.abs(want).max())
+    kv = oracle.KV(m, 320)
+    kv.prefill(toks[:280])
+    np.testing.assert_allclose(kv.verify(toks[280:300]), want[279:300], rtol=0, atol=1e-10 * np.abs(want).max())
+
+
+@pytest.mark.parametrize("shape", [SMALL, SMALL_BF16, W.TINY], ids=["small", "small-bf16", "tiny"])
+def test_streamed_model_equals_materialized(shape):
+    """Layer streaming generates each layer's weights when the forward reaches it: the same values, so both
+    routes give bit-identical logits to the materialized model."""
+    m = oracle.Model(shape)
+    ms = oracle.Model(shape, streamed=True)
+    toks = W.prompt(20, 24, shape.vocab)
+    a = m.forward_full(toks, 10)
+    b = ms.forward_full(toks, 10)
+    assert np.array_equal(a, b)
+    kv, kvs = oracle.KV(m, 32), oracle.KV(ms, 32)
+    kv.prefill(toks[:12])
+    kvs.prefill(toks[:12])
+    assert np.array_equal(kv.verify(toks[12:20]), kvs.verify(toks[12:20]))
+    # a second forward regenerates the layers (nothing was kept from the first); the layer-by-layer steps
+    # compute the same
+    seen = []
+    assert np.array_equal(ms.forward_full(toks, 10, progress=seen.append), a)
+    assert seen == list(range(shape.n_layers))
+    with pytest.raises(ValueError):
+        ms.set_tensor(oracle.WO, 0, np.zeros(oracle.tensor_shape(shape, oracle.WO), np.float32))

@@ -150,6 +150,21 @@ def accept_inputs(seed: int, B: int = 16, gamma: int = 32, vocab: int = 151936,
     return AcceptInputs(draft, to_bf16_bits(t), to_bf16_bits(d), u)
 
 
+def norm_gains(seed: int, shape: ModelShape, spread: float = 0.25) -> dict:
+    """Non-unit RMSNorm gains 1 + spread * N(0,1) (fp32) for every norm of the shape, keyed
+    ("final", 0), ("attn", layer), ("ffn", layer) and, with QK-norm, ("q", layer), ("k", layer)."""
+    g = rng(seed)
+    gn = lambda n: (1.0 + spread * g.standard_normal(n)).astype(np.float32)
+    out = {("final", 0): gn(shape.d_model)}
+    for l in range(shape.n_layers):
+        out[("attn", l)] = gn(shape.d_model)
+        out[("ffn", l)] = gn(shape.d_model)
+        if shape.qk_norm:
+            out[("q", l)] = gn(shape.head_dim)
+            out[("k", l)] = gn(shape.head_dim)
+    return out
+
+
 def batch8_lengths(seed: int, n: int = 8, lo: int = 256, hi: int = 4096) -> np.ndarray:
     """Ragged prompt lengths U[lo, hi]."""
     return rng(seed).integers(lo, hi + 1, size=n, dtype=np.int64).astype(np.int32)
