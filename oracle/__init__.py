@@ -27,7 +27,7 @@ class _Cfg(C.Structure):
     _fields_ = [("n_layers", C.c_int), ("d_model", C.c_int), ("n_q_heads", C.c_int),
                 ("n_kv_heads", C.c_int), ("head_dim", C.c_int), ("d_ff", C.c_int),
                 ("vocab", C.c_int), ("rms_eps", C.c_double), ("rope_theta", C.c_double),
-                ("qk_norm", C.c_int), ("bf16_weights", C.c_int)]
+                ("qk_norm", C.c_int), ("bf16_weights", C.c_int), ("bf16_operands", C.c_int)]
 
 
 def lib():
@@ -109,14 +109,17 @@ class Model:
     """The target decoder with synthetic weights (seed, sigma) held in host memory.
 
     streamed=True holds only the embedding, LM head and final norm and generates each layer's
-    weights when a forward reaches it (same values; for shapes whose fp32 copy exceeds host memory)."""
+    weights when a forward reaches it (same values; for shapes whose fp32 copy exceeds host memory).
+    bf16_operands=True: every activation entering a matrix product is rounded to BF16 (the verifier
+    as a BF16 model); otherwise everything is exact fp64."""
 
-    def __init__(self, shape, seed: int = 0, sigma: float = 0.02, streamed: bool = False):
+    def __init__(self, shape, seed: int = 0, sigma: float = 0.02, streamed: bool = False,
+                 bf16_operands: bool = False):
         self.shape = shape
         self.streamed = streamed
         c = _Cfg(shape.n_layers, shape.d_model, shape.n_q_heads, shape.n_kv_heads,
                  shape.head_dim, shape.d_ff, shape.vocab, shape.rms_eps, shape.rope_theta,
-                 int(shape.qk_norm), int(shape.dtype == "bf16"))
+                 int(shape.qk_norm), int(shape.dtype == "bf16"), int(bf16_operands))
         create = lib().orc_model_create_streamed if streamed else lib().orc_model_create
         self._h = create(C.byref(c), seed, sigma)
         if not self._h:

@@ -346,6 +346,59 @@ static void rmsnorm(const double* x, int d, const float* g, double eps, double* 
   for (int i = 0; i < d; ++i) y[i] = x[i] * inv * (double)g[i];
 }
 
+/* BF16-operand mode (orc_config.bf16_operands).  The paper runs its verifier
+ * as a BF16 model (Appendix "Evaluation and Throughput": BF16 weights, logits
+ * converted to FP32).  Taken literally for the matrix products: every operand
+ * of a product is a BF16 value (the weights already are; the activations are
+ * rounded to BF16 where they enter a product: the gained input x * g of every
+ * projection, q, k and v, the attention output, the FFN hidden state), every
+ * sum is exact (fp64 here), and RMSNorm's row scale r = 1/sqrt(mean x^2 + eps)
+ * multiplies the product, (r x * g) W = r ((x * g) W).  Softmax, norms, RoPE
+ * and the residual stream stay exact.  Off (0), the oracle is exact fp64. */
+
+/* Nearest BF16 value (8 significant bits, ties to even) of a finite double. */
+static double round_bf16(double x) {
+  if (!isfinite(x) || x == 0.0) return x;
+  int e;
+  frexp(x, &e); /* |x| = f 2^e, f in [0.5, 1) */
+  if (e < -125) e = -125; /* BF16 subnormals: spacing 2^-133 */
+  const double s = ldexp(1.0, 8 - e);
+  return nearbyint(x * s) / s; /* default rounding mode: ties to even */
+}
+
+/* Rounds the n values of an operand to BF16 in BF16-operand mode. */
+static void bf16_operand(const orc_model* m, double* a, size_t n) {
+  if (!m->c.bf16_operands) return;
+  for (size_t i = 0; i < n; ++i) a[i] = round_bf16(a[i]);
+}
+
+/* Operand of the projections that follow an RMSNorm with gain g, for R rows of
+ * x: exact mode h = RMSNorm(x) * g and rs = 1; BF16-operand mode h = BF16(x * g)
+ * and rs = the row scales, applied to the products by scale_rows. */
+static void norm_operand(const orc_model* m, const double* x, int R, const float* g, double* h, double* rs) {
+  const orc_config* c = &m->c;
+  int d = c->d_model;
+  for (int r = 0; r < R; ++r) {
+    const double* xr = x + (size_t)r * d;
+    double* hr = h + (size_t)r * d;
+    if (!c->bf16_operands) {
+      rmsnorm(xr, d, g, c->rms_eps, hr);
+      rs[r] = 1.0;
+    } else {
+      double ss = 0.0;
+      for (int i = 0; i < d; ++i) ss += xr[i] * xr[i];
+      rs[r] = 1.0 / sqrt(ss / d + c->rms_eps);
+      for (int i = 0; i < d; ++i) hr[i] = round_bf16(xr[i] * (double)g[i]);
+    }
+  }
+}
+
+/* Y[r][n] *= rs[r] */
+static void scale_rows(double* Y, int R, int N, const double* rs) {
+  for (int r = 0; r < R; ++r)
+    for (int n = 0; n < N; ++n) Y[(size_t)r * N + n] *= rs[r];
+}
+
 /* Rotate-half RoPE at absolute position pos: pairs (i, i + hd/2) rotate by
  * pos * theta^(-2i/hd). */
 static void rope(double* v, int hd, int pos, double theta) {
@@ -396,13 +449,17 @@ static void ffn_block(const orc_model* m, int l, double* x, int R) {
   double* g = (double*)malloc(sizeof(double) * (size_t)R * f);
   double* u = (double*)malloc(sizeof(double) * (size_t)R * f);
   double* y = (double*)malloc(sizeof(double) * (size_t)R * d);
-  for (int r = 0; r < R; ++r) rmsnorm(x + (size_t)r * d, d, m->L[l].ffn_norm, c->rms_eps, h + (size_t)r * d);
+  double* rs = (double*)malloc(sizeof(double) * (size_t)R);
+  norm_operand(m, x, R, m->L[l].ffn_norm, h, rs);
   linear(m->L[l].wg, f, d, h, R, g);
   linear(m->L[l].wu, f, d, h, R, u);
+  scale_rows(g, R, f, rs);
+  scale_rows(u, R, f, rs);
   for (size_t i = 0; i < (size_t)R * f; ++i) g[i] = silu(g[i]) * u[i];
+  bf16_operand(m, g, (size_t)R * f);
   linear(m->L[l].wd, d, f, g, R, y);
   for (size_t i = 0; i < (size_t)R * d; ++i) x[i] += y[i];
-  free(h); free(g); free(u); free(y);
+  free(h); free(g); free(u); free(y); free(rs);
 }
 
 /* final RMSNorm + LM head on R rows */
@@ -410,9 +467,12 @@ static void lm_head(const orc_model* m, const double* x, int R, double* logits) 
   const orc_config* c = &m->c;
   int d = c->d_model;
   double* h = (double*)malloc(sizeof(double) * (size_t)R * d);
-  for (int r = 0; r < R; ++r) rmsnorm(x + (size_t)r * d, d, m->final_norm, c->rms_eps, h + (size_t)r * d);
+  double* rs = (double*)malloc(sizeof(double) * (size_t)R);
+  norm_operand(m, x, R, m->final_norm, h, rs);
   linear(m->lm_head, c->vocab, d, h, R, logits);
+  scale_rows(logits, R, c->vocab, rs);
   free(h);
+  free(rs);
 }
 
 static void embed_rows(const orc_model* m, const int32_t* tok, int R, double* x) {
@@ -445,12 +505,19 @@ static int layer_full(const orc_model* m, int l, int n, double* x) {
   double* v = (double*)malloc(sizeof(double) * (size_t)n * nk);
   double* o = (double*)malloc(sizeof(double) * (size_t)n * nq);
   double* y = (double*)malloc(sizeof(double) * (size_t)n * d);
+  double* rs = (double*)malloc(sizeof(double) * (size_t)n);
   double scale = 1.0 / sqrt((double)hd);
-  for (int r = 0; r < n; ++r) rmsnorm(x + (size_t)r * d, d, m->L[l].attn_norm, c->rms_eps, h + (size_t)r * d);
+  norm_operand(m, x, n, m->L[l].attn_norm, h, rs);
   linear(m->L[l].wq, (int)nq, d, h, n, q);
   linear(m->L[l].wk, (int)nk, d, h, n, k);
   linear(m->L[l].wv, (int)nk, d, h, n, v);
+  scale_rows(q, n, (int)nq, rs);
+  scale_rows(k, n, (int)nk, rs);
+  scale_rows(v, n, (int)nk, rs);
   qk_post(m, l, q, k, n, 0);
+  bf16_operand(m, q, (size_t)n * nq);
+  bf16_operand(m, k, (size_t)n * nk);
+  bf16_operand(m, v, (size_t)n * nk);
 #pragma omp parallel for schedule(dynamic)
   for (int i = 0; i < n; ++i) {
     double* s = (double*)malloc(sizeof(double) * (size_t)(i + 1));
@@ -479,11 +546,12 @@ static int layer_full(const orc_model* m, int l, int n, double* x) {
     }
     free(s);
   }
+  bf16_operand(m, o, (size_t)n * nq);
   linear(m->L[l].wo, d, (int)nq, o, n, y);
   for (size_t i = 0; i < (size_t)n * d; ++i) x[i] += y[i];
   ffn_block(m, l, x, n);
   layer_release(m, l);
-  free(h); free(q); free(k); free(v); free(o); free(y);
+  free(h); free(q); free(k); free(v); free(o); free(y); free(rs);
   return 0;
 }
 
@@ -595,6 +663,7 @@ static int block_forward(orc_kv* kv, const int32_t* tok, int R, int pos0, double
   double* v = (double*)malloc(sizeof(double) * (size_t)R * nk);
   double* o = (double*)malloc(sizeof(double) * (size_t)R * nq);
   double* y = (double*)malloc(sizeof(double) * (size_t)R * d);
+  double* rs = (double*)malloc(sizeof(double) * (size_t)R);
   embed_rows(m, tok, R, x);
   double scale = 1.0 / sqrt((double)hd);
   int rc = 0;
@@ -602,11 +671,17 @@ static int block_forward(orc_kv* kv, const int32_t* tok, int R, int pos0, double
     if ((rc = layer_acquire(m, l))) break;
     double* K = kv->k + (size_t)l * kv->max_len * nk;
     double* V = kv->v + (size_t)l * kv->max_len * nk;
-    for (int r = 0; r < R; ++r) rmsnorm(x + (size_t)r * d, d, m->L[l].attn_norm, c->rms_eps, h + (size_t)r * d);
+    norm_operand(m, x, R, m->L[l].attn_norm, h, rs);
     linear(m->L[l].wq, (int)nq, d, h, R, q);
     linear(m->L[l].wk, (int)nk, d, h, R, k);
     linear(m->L[l].wv, (int)nk, d, h, R, v);
+    scale_rows(q, R, (int)nq, rs);
+    scale_rows(k, R, (int)nk, rs);
+    scale_rows(v, R, (int)nk, rs);
     qk_post(m, l, q, k, R, pos0);
+    bf16_operand(m, q, (size_t)R * nq);
+    bf16_operand(m, k, (size_t)R * nk);
+    bf16_operand(m, v, (size_t)R * nk);
     memcpy(K + (size_t)pos0 * nk, k, sizeof(double) * (size_t)R * nk);
     memcpy(V + (size_t)pos0 * nk, v, sizeof(double) * (size_t)R * nk);
 #pragma omp parallel for schedule(dynamic)
@@ -637,12 +712,13 @@ static int block_forward(orc_kv* kv, const int32_t* tok, int R, int pos0, double
       }
       free(s);
     }
+    bf16_operand(m, o, (size_t)R * nq);
     linear(m->L[l].wo, d, (int)nq, o, R, y);
     for (size_t i = 0; i < (size_t)R * d; ++i) x[i] += y[i];
     ffn_block(m, l, x, R);
     layer_release(m, l);
   }
-  free(h); free(q); free(k); free(v); free(o); free(y);
+  free(h); free(q); free(k); free(v); free(o); free(y); free(rs);
   return rc;
 }
 

@@ -32,6 +32,13 @@ typedef struct {
   double rms_eps, rope_theta;
   int qk_norm;      /* 1: per-head RMSNorm of q and k before RoPE */
   int bf16_weights; /* 1: weights are bf16 values; 0: fp32 values */
+  /* 1: BF16-operand mode (the verifier as a BF16 model, Appendix "Evaluation
+   * and Throughput"): every activation that enters a matrix product (x * g of
+   * each projection with the RMSNorm row scale applied to the product, q, k,
+   * v, the attention output, the FFN hidden state) is rounded to BF16 (ties to
+   * even); sums, softmax, norms, RoPE and the residual stream stay exact.
+   * 0: exact fp64 throughout. */
+  int bf16_operands;
 } orc_config;
 
 /* Tensor kinds for orc_model_set_tensor / orc_weight_values. */

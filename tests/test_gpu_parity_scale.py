@@ -1,10 +1,11 @@
 """GPU parity against the oracle at the workloads' real depths, cache lengths and batch sizes.
 
-* Full depth: the 64-layer Qwen3-32B shape and the 28-layer 7B shape (random N(0, 0.02)-like weights,
-  unit gains) verify a gamma = 32 block after a 16-token prompt; the oracle runs the same model with
-  layer streaming (its fp32 copy of the 32B weights would need 131 GB), so the accumulated bf16 error of
-  every layer is measured against the 2e-2 logit-scale tolerance.  A narrow 64-layer model does the
-  same at a fraction of the cost.
+* Full depth: the 64-layer Qwen3-32B shape, the 28-layer 7B shape and the first 16 layers of the 32B
+  shape (random N(0, 0.02)-like weights, unit gains) verify a gamma = 32 block after a 16-token prompt;
+  the oracle runs the same model with layer streaming (its fp32 copy of the 32B weights would need
+  131 GB), exactly and as a BF16 forward, and the GPU's deviation from the exact logits is bounded by
+  the 2e-2 logit-scale tolerance or, where BF16 rounding itself exceeds it, by 1.5 times the BF16
+  forward's own deviation (the bar at depth, below).  A narrow 64-layer model does the same cheaply.
 * Long caches: verify blocks whose attention spans ~600 to 4129 positions (the Qwen3-32B workloads'
   1024-1552-position caches and the batched workload's U[256, 4096] prompts plus a 33-row block), on a
   2-layer GQA model and on a model with the Qwen3-32B attention configuration (64 query / 8 KV heads of
@@ -71,8 +72,19 @@ def _gpu_model(S, shape, gains=None):
 # full depth
 
 
-@pytest.mark.parametrize("shape", [W.QWEN32B, W.QWEN7B, MID_BF16.with_layers(64)],
-                         ids=["qwen32b-64layers", "qwen7b-28layers", "narrow-64layers"])
+# The bar at depth.  The 2e-2 bound is a BF16-agreement bar, and BF16 rounding of the activations is
+# what limits agreement: a BF16 forward of these random-weight models (the oracle in its BF16-operand
+# mode: every activation entering a matrix product rounded to BF16, every sum exact) deviates from the
+# exact forward by about 2e-2 of the logit scale at 16 layers of the Qwen3-32B shape and 3.4e-2 at 64,
+# growing as sqrt(depth) (5.8e-3 at one layer).  Two BF16 forwards that round differently anywhere
+# (fp32 against fp64 sums, the online softmax's probabilities) stop rounding alike and drift apart by
+# the same amount, so at depth the GPU is bounded by the BF16 forward's own deviation: per row,
+# max |z_gpu - z_exact| <= max(2e-2, 1.5 * max |z_bf16 - z_exact| / max |z_exact|) * max |z_exact|.
+DEPTH_FACTOR = 1.5
+
+
+@pytest.mark.parametrize("shape", [W.QWEN32B, W.QWEN7B, W.QWEN32B.with_layers(16), MID_BF16.with_layers(64)],
+                         ids=["qwen32b-64layers", "qwen7b-28layers", "qwen32b-16layers", "narrow-64layers"])
 def test_full_depth_verify_vs_streamed_oracle(S, shape):
     P, gamma = 16, 32
     print(f"full depth {shape}", flush=True)
@@ -89,18 +101,33 @@ def test_full_depth_verify_vs_streamed_oracle(S, shape):
     amg = am[0].cpu().numpy()
     del kv, ws, m, logits
     torch.cuda.empty_cache()
-    # the oracle: full recomputation over prompt + drafts (the paper's cache-free verifier), layer streamed
-    t0 = time.time()
-    om = oracle.Model(shape, W.WEIGHT_SEED, W.WEIGHT_SIGMA, streamed=True)
+    # the oracle: full recomputation over prompt + drafts (the paper's cache-free verifier), layer streamed,
+    # exact and as a BF16 forward
+    wants = {}
+    for bf16 in (False, True):
+        t0 = time.time()
+        om = oracle.Model(shape, W.WEIGHT_SEED, W.WEIGHT_SIGMA, streamed=True, bf16_operands=bf16)
 
-    def progress(layer):
-        if layer % 8 == 7 or layer == shape.n_layers - 1:
-            print(f"  oracle layer {layer + 1}/{shape.n_layers} ({time.time() - t0:.0f} s)", flush=True)
+        def progress(layer):
+            if layer % 16 == 15 or layer == shape.n_layers - 1:
+                print(f"  oracle ({'bf16 operands' if bf16 else 'exact'}) layer {layer + 1}/{shape.n_layers} "
+                      f"({time.time() - t0:.0f} s)", flush=True)
 
-    want = om.forward_full(np.concatenate([toks, drafts]), P - 1, progress=progress)
-    rel, _ = _check_rows(got, want, f"{shape.n_layers} layers")
-    near = argmax_near_tie(want, TOL * np.abs(want).max(-1))
+        wants[bf16] = om.forward_full(np.concatenate([toks, drafts]), P - 1, progress=progress)
+        del om
+    want = wants[False]
+    scale = np.abs(want).max(-1)
+    err_gpu = np.abs(got - want).max(-1) / scale
+    err_bf16 = np.abs(wants[True] - want).max(-1) / scale
+    bound = np.maximum(TOL, DEPTH_FACTOR * err_bf16)
+    print(f"  {shape.n_layers} layers: GPU vs exact max rel {err_gpu.max():.3e} median {np.median(err_gpu):.3e}; "
+          f"BF16 forward vs exact max {err_bf16.max():.3e} median {np.median(err_bf16):.3e}; "
+          f"worst ratio {(err_gpu / err_bf16).max():.2f}", flush=True)
+    assert (err_gpu <= bound).all(), (err_gpu / bound).max()
+    near = argmax_near_tie(want, bound * scale)
+    print(f"  argmax near-ties excluded {int(near.sum())} of {gamma + 1}", flush=True)
     assert (amg[~near] == want.argmax(-1)[~near]).all()
+    assert (got.argmax(-1)[~near] == want.argmax(-1)[~near]).all()
     # greedy acceptance on both sides agrees outside near-ties
     L, _, _ = S.accept(to_dev_i32(drafts.reshape(1, gamma)), torch.from_numpy(got[None]).cuda(), S.GREEDY)
     ref = oracle.accept(oracle.GREEDY, drafts.reshape(1, gamma), want[None].astype(np.float32), margins=False)

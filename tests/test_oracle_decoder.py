@@ -44,34 +44,55 @@ def _rope_torch(x, pos, theta):
     return x * cos + torch.cat([-x2, x1], -1) * sin
 
 
-def _torch_reference(shape, w, tokens, gains=None):
+def _bf16_f64(a: torch.Tensor) -> torch.Tensor:
+    """Nearest BF16 value of each float64 (ties to even), by bit arithmetic on the binary64 encoding:
+    keep 7 of the 52 fraction bits, round the dropped 45 half to even."""
+    u = a.contiguous().numpy().view(np.uint64)
+    drop = np.uint64(45)
+    lsb = (u >> drop) & np.uint64(1)
+    r = (u + np.uint64((1 << 44) - 1) + lsb) & ~np.uint64((1 << 45) - 1)
+    return torch.from_numpy(r.view(np.float64).copy())
+
+
+def _torch_reference(shape, w, tokens, gains=None, bf16_operands=False):
     """Decoder as a composition of torch.nn.functional ops, float64 on the CPU.
 
-    gains: optional dict of RMSNorm gains keyed like w ((kind, layer) or FINAL_NORM); missing ones are 1."""
+    gains: optional dict of RMSNorm gains keyed like w ((kind, layer) or FINAL_NORM); missing ones are 1.
+    bf16_operands: the activations entering each matrix product are rounded to BF16 (x * g of each
+    projection, whose row scale 1/rms(x) then multiplies the product; q, k, v; attention output; FFN
+    hidden state)."""
     t = lambda a: torch.from_numpy(np.asarray(a, np.float64))
     d, hd, hq, hk = shape.d_model, shape.head_dim, shape.n_q_heads, shape.n_kv_heads
     n = len(tokens)
     gains = gains or {}
     g = lambda key, size: t(gains[key]) if key in gains else torch.ones(size, dtype=torch.float64)
+    b = _bf16_f64 if bf16_operands else (lambda a: a)
+
+    def norm_linear(x, gain, *mats):
+        if not bf16_operands:
+            h = F.rms_norm(x, (x.shape[-1],), gain, eps=shape.rms_eps)
+            return [F.linear(h, W) for W in mats]
+        r = torch.rsqrt((x * x).mean(-1, keepdim=True) + shape.rms_eps)
+        h = _bf16_f64(x * gain)
+        return [F.linear(h, W) * r for W in mats]
+
     x = F.embedding(torch.from_numpy(np.asarray(tokens, np.int64)), t(w[oracle.EMBED]))
     pos = torch.arange(n)
     for l in range(shape.n_layers):
-        h = F.rms_norm(x, (d,), g((oracle.ATTN_NORM, l), d), eps=shape.rms_eps)
-        q = F.linear(h, t(w[(oracle.WQ, l)])).view(n, hq, hd)
-        k = F.linear(h, t(w[(oracle.WK, l)])).view(n, hk, hd)
-        v = F.linear(h, t(w[(oracle.WV, l)])).view(n, hk, hd)
+        q, k, v = norm_linear(x, g((oracle.ATTN_NORM, l), d), t(w[(oracle.WQ, l)]), t(w[(oracle.WK, l)]),
+                              t(w[(oracle.WV, l)]))
+        q, k, v = q.view(n, hq, hd), k.view(n, hk, hd), v.view(n, hk, hd)
         if shape.qk_norm:
             q = F.rms_norm(q, (hd,), g((oracle.Q_NORM, l), hd), eps=shape.rms_eps)
             k = F.rms_norm(k, (hd,), g((oracle.K_NORM, l), hd), eps=shape.rms_eps)
         q, k = _rope_torch(q, pos, shape.rope_theta), _rope_torch(k, pos, shape.rope_theta)
+        q, k, v = b(q), b(k), b(v)
         o = F.scaled_dot_product_attention(q.transpose(0, 1), k.transpose(0, 1), v.transpose(0, 1),
                                            is_causal=True, enable_gqa=True)
-        x = x + F.linear(o.transpose(0, 1).reshape(n, hq * hd), t(w[(oracle.WO, l)]))
-        h = F.rms_norm(x, (d,), g((oracle.FFN_NORM, l), d), eps=shape.rms_eps)
-        a = F.silu(F.linear(h, t(w[(oracle.WGATE, l)]))) * F.linear(h, t(w[(oracle.WUP, l)]))
-        x = x + F.linear(a, t(w[(oracle.WDOWN, l)]))
-    h = F.rms_norm(x, (d,), g(oracle.FINAL_NORM, d), eps=shape.rms_eps)
-    return F.linear(h, t(w[oracle.LM_HEAD])).numpy()
+        x = x + F.linear(b(o.transpose(0, 1).reshape(n, hq * hd)), t(w[(oracle.WO, l)]))
+        gt, up = norm_linear(x, g((oracle.FFN_NORM, l), d), t(w[(oracle.WGATE, l)]), t(w[(oracle.WUP, l)]))
+        x = x + F.linear(b(F.silu(gt) * up), t(w[(oracle.WDOWN, l)]))
+    return norm_linear(x, g(oracle.FINAL_NORM, d), t(w[oracle.LM_HEAD]))[0].numpy()
 
 
 _GAIN_KIND = {"final": oracle.FINAL_NORM, "attn": oracle.ATTN_NORM, "ffn": oracle.FFN_NORM,
@@ -250,3 +271,38 @@ def test_streamed_model_equals_materialized(shape):
     assert seen == list(range(shape.n_layers))
     with pytest.raises(ValueError):
         ms.set_tensor(oracle.WO, 0, np.zeros(oracle.tensor_shape(shape, oracle.WO), np.float32))
+
+
+@pytest.mark.parametrize("shape", [SMALL, SMALL_BF16], ids=["qknorm-f32", "gqa4-bf16"])
+def test_bf16_operand_mode_matches_torch(shape):
+    """BF16-operand mode (the verifier as a BF16 model): against torch.nn.functional with the same
+    activations rounded by bit arithmetic on float64 (an implementation independent of the oracle's
+    frexp / nearbyint rounding), with non-unit gains; the cached route agrees with full recompute."""
+    gains = random_gains(shape, 21)
+    m = oracle.Model(shape, bf16_operands=True)
+    _set_gains(m, gains)
+    toks = W.prompt(22, 15, shape.vocab)
+    want = _torch_reference(shape, _weights(shape), toks, gains, bf16_operands=True)
+    np.testing.assert_allclose(m.forward_full(toks), want, rtol=0, atol=1e-10 * np.abs(want).max())
+    kv = oracle.KV(m, 32)
+    kv.prefill(toks[:9])
+    np.testing.assert_allclose(kv.verify(toks[9:15]), want[8:15], rtol=0, atol=1e-10 * np.abs(want).max())
+    # the mode changes the logits by about the BF16 rounding scale, and turning it off restores exactness
+    exact = _torch_reference(shape, _weights(shape), toks, gains)
+    rel = np.abs(want - exact).max() / np.abs(exact).max()
+    assert 1e-5 < rel < 5e-2, rel
+    m0 = oracle.Model(shape)
+    _set_gains(m0, gains)
+    np.testing.assert_allclose(m0.forward_full(toks), exact, rtol=0, atol=1e-10 * np.abs(exact).max())
+
+
+def test_bf16_rounding_of_the_bit_method_matches_fp32_rounding():
+    """The test's float64 -> BF16 rounding agrees with workloads' fp32 -> BF16 bit rounding on values that
+    are exactly representable in fp32 (so no double rounding is involved), ties included."""
+    rg = W.rng(23)
+    a = (rg.standard_normal(100000) * 10.0 ** rg.integers(-6, 6, 100000)).astype(np.float32)
+    ties = ((W.bf16_bits_to_f32(W.to_bf16_bits(a)).view(np.uint32) | np.uint32(0x8000)).view(np.float32))
+    a = np.concatenate([a, ties])
+    want = W.bf16_bits_to_f32(W.to_bf16_bits(a)).astype(np.float64)
+    got = _bf16_f64(torch.from_numpy(a.astype(np.float64))).numpy()
+    assert np.array_equal(got, want)
