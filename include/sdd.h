@@ -231,6 +231,22 @@ int sdd_accept(const int32_t* draft, const void* p_logits, int p_dtype, const vo
                int mode, int k, float lenience, int32_t* accepted_len, int32_t* next_token,
                int32_t* flags, void* ws, size_t ws_bytes, sdd_stream_t stream);
 
+/* sdd_accept for callers that cannot allocate device memory (code under HIP
+ * graph capture, tight serving loops, harnesses that forbid hipMalloc): the
+ * same arguments and results as sdd_accept without the workspace.  Its
+ * workspace is a 256 KiB array inside the library, one per GPU, held until the
+ * process ends; the call allocates nothing.  Calls on one GPU share that
+ * array: calls that overlap in time on one GPU (other streams, other host
+ * threads) race and must be serialized by the caller.  The first call on a
+ * device looks up the array's address and enqueues a kernel that clears it
+ * on the stream.  Errors: those of sdd_accept, and SDD_ECAPACITY when the
+ * shape needs more than 256 KiB of workspace (sdd_rowstats_workspace_bytes;
+ * e.g. B = 64 with gamma = 64 fits, about B * (gamma + 1) <= 7000 rows). */
+int sdd_accept_noalloc(const int32_t* draft, const void* p_logits, int p_dtype, const void* q_logits,
+                       int q_dtype, size_t q_seq_stride, const float* uniforms, int B, int gamma, int V,
+                       int mode, int k, float lenience, int32_t* accepted_len, int32_t* next_token,
+                       int32_t* flags, sdd_stream_t stream);
+
 /* Raw-confidence prefix (Sec. 4.1 local gate B_k = min_{j<=k} q_j; Sec. 4.2
  * raw confidence = max softmax of the drafter row).  Row j < gamma of
  * sequence b at logits + b*seq_stride + j*V elements.  skip_len[b] =

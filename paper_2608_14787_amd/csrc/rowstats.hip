@@ -19,6 +19,8 @@
 // sequence to finish (arrival counter) combines that sequence's records in a
 // fixed order, so results are bit-reproducible, and takes the decisions; it
 // resets the counter so the workspace can be reused.
+#include <mutex>
+
 #include "sdd_internal.h"
 
 namespace sdd {
@@ -961,6 +963,63 @@ extern "C" int sdd_accept(const int32_t* draft, const void* p_logits, int p_dtyp
       return bf ? launch_t<kAccept, true, false, true, uint16_t, uint16_t>(job, vec, st)
                 : launch_t<kAccept, true, false, true, float, float>(job, vec, st);
   }
+}
+
+// ---------------------------------------------------------------------------
+// sdd_accept_noalloc: the acceptance test for callers that cannot allocate device memory.  Its workspace
+// is this file-scope array (one copy per GPU, held until the process ends).  In host code `scratch` names a
+// host-side stand-in, never the device memory: every host use goes through the per-device address that
+// hipGetSymbolAddress returns.
+constexpr size_t kNoallocScratchBytes = 256 * 1024;
+static __device__ __align__(256) char scratch[kNoallocScratchBytes];
+
+namespace {
+__global__ void zero_scratch_kernel(uint32_t* p, int n) {
+  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) p[i] = 0u;
+}
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices];  // device address of `scratch` on each device (nullptr: not set up)
+
+// The current device's scratch address; set up once per device (address lookup, and a kernel that zeroes the
+// arrival counters on `st`; every call leaves them zero again).
+int scratch_for_current_device(hipStream_t st, void** out) {
+  int dev = 0;
+  SDD_HIP(hipGetDevice(&dev));
+  if (dev < 0 || dev >= kMaxDevices) return fail(SDD_EUNSUPPORTED, "device %d beyond the %d supported", dev, kMaxDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    SDD_HIP(hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)));
+    if (!ptr) return fail(SDD_EHIP, "hipGetSymbolAddress returned no address for the scratch array");
+    // a kernel, not hipMemsetAsync: the first call may sit inside a captured graph
+    const int n = (int)(kNoallocScratchBytes / 4);
+    hipLaunchKernelGGL(zero_scratch_kernel, dim3(64), dim3(256), 0, st, reinterpret_cast<uint32_t*>(ptr), n);
+    int rc = check_launch("zero_scratch_kernel");
+    if (rc) return rc;
+    g_scratch_ptr[dev] = ptr;
+  }
+  *out = g_scratch_ptr[dev];
+  return SDD_OK;
+}
+}  // namespace
+
+extern "C" int sdd_accept_noalloc(const int32_t* draft, const void* p_logits, int p_dtype, const void* q_logits,
+                                  int q_dtype, size_t q_seq_stride, const float* uniforms, int B, int gamma, int V,
+                                  int mode, int k, float lenience, int32_t* accepted_len, int32_t* next_token,
+                                  int32_t* flags, sdd_stream_t stream) {
+  SDD_REQUIRE(B > 0 && gamma >= 0 && gamma <= 64 && V > 0, "bad shape B=%d gamma=%d V=%d", B, gamma, V);
+  const size_t need = rowstats_ws(B, gamma + 1, V);
+  if (need > kNoallocScratchBytes)
+    return fail(SDD_ECAPACITY, "B=%d, gamma=%d needs %zu bytes of scratch; sdd_accept_noalloc holds %zu (use sdd_accept)",
+                B, gamma, need, kNoallocScratchBytes);
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  void* ws = nullptr;
+  int rc = scratch_for_current_device(st, &ws);
+  if (rc) return rc;
+  return sdd_accept(draft, p_logits, p_dtype, q_logits, q_dtype, q_seq_stride, uniforms, B, gamma, V, mode, k, lenience,
+                    accepted_len, next_token, flags, ws, kNoallocScratchBytes, stream);
 }
 
 extern "C" int sdd_confidence_prefix(const void* logits, int dtype, size_t seq_stride, int B, int gamma,

@@ -63,6 +63,7 @@ _SIGS = {
     "sdd_kv_commit": (I, [P, P, I, P, P, P]),
     "sdd_rowstats_workspace_bytes": (I, [I, I, I, P]),
     "sdd_accept": (I, [P, P, I, P, I, SZ, P, I, I, I, I, I, F, P, P, P, P, SZ, P]),
+    "sdd_accept_noalloc": (I, [P, P, I, P, I, SZ, P, I, I, I, I, I, F, P, P, P, P]),
     "sdd_confidence_prefix": (I, [P, I, SZ, I, I, I, F, P, P, P, P, P, SZ, P]),
     "sdd_schedule": (I, [P, P, P, I, I, I, C.c_double, C.c_double, I, I, P, I, I, P, P, P, P, P]),
     "sdd_verify_full": (I, [P, P, P, I, I, P, P, P, SZ, P]),
