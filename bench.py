@@ -220,6 +220,92 @@ def full_recompute(sdd, torch, model, shape: W.ModelShape, P: int, gamma: int, w
             "frac_mfma_bf16": flops / (ms * 1e-3) / 2.5e15}
 
 
+def batch8(sdd, torch, model, shape: W.ModelShape, gamma: int, reps: int = 6) -> dict:
+    """Batched verification: 8 sequences of the verify workload's model with prompts of U[256, 4096] tokens
+    (seeded), a skip mask from the confidence prefix of each sequence's drafter logits at tau = 0.7 with
+    K_min = 6, then one verify call over the sequences that are not skipped (B_eff of them, M = 33 B_eff rows),
+    greedy acceptance and the commit.  Drafter logits 3 N(0, 1) as stated (no sequence skips: B_eff = 8), and a
+    variant boosting the draft token to the row maximum + U[3, 12] so that some sequences skip."""
+    dev = "cuda"
+    V, d, L = shape.vocab, shape.d_model, shape.n_layers
+    lens = W.batch8_lengths(5)
+    n = len(lens)
+    max_len = int(lens.max()) + (reps + 2) * (gamma + 1) + 8
+    kv = sdd.KVCache(model, n, max_len)
+    ws = model.workspace(n * (gamma + 1))
+    t0 = time.perf_counter()
+    for s, ln in enumerate(lens):
+        kv.prefill(s, torch.from_numpy(W.prompt(200 + s, int(ln), V)).to(dev), ws)
+    torch.cuda.synchronize()
+    prefill_s = time.perf_counter() - t0
+    log(f"batch8: prefill of {int(lens.sum())} tokens in {prefill_s:.2f} s")
+    drafts_np = W.prompt(300, n * gamma, V).reshape(n, gamma)
+    drafts = torch.from_numpy(drafts_np).to(dev)
+    conf_ws = sdd.rowstats_workspace(n, gamma, V)
+    skbuf = torch.empty(n, dtype=torch.int32, device=dev)
+    out = {"workload": f"8 sequences, prompts {lens.tolist()} (U[256, 4096]), gamma {gamma}, tau {TAU}, K_min {K_MIN}",
+           "prefill_s": prefill_s, "prefill_tokens_per_s": float(lens.sum()) / prefill_s}
+    hd, hq, hkv = shape.head_dim, shape.n_q_heads, shape.n_kv_heads
+    for variant, boost in (("literal", None), ("boosted", (3.0, 12.0))):
+        if boost is None:
+            dl = W.drafter_logits(301, drafts_np, gamma + 1, V, scale=3.0, boost=0.0)
+        else:
+            dl = W.drafter_logits(301, drafts_np, gamma + 1, V, scale=3.0, boost=boost[0], boost_hi=boost[1])
+        dlt = torch.from_numpy(W.to_bf16_bits(dl).view(np.int16)).to(dev).view(torch.bfloat16)
+        del dl
+        sk = sdd.confidence_prefix(dlt, gamma, TAU, ws=conf_ws, out=skbuf)
+        active = (sk < K_MIN).nonzero().flatten().to(torch.int32).contiguous()
+        B = int(active.numel())
+        d_act = drafts[active.long()].contiguous()
+        logits = torch.empty((B, gamma + 1, V), dtype=torch.float32, device=dev)
+        am = torch.empty((B, gamma + 1), dtype=torch.int32, device=dev)
+        acc_ws = sdd.rowstats_workspace(B, gamma, V)
+        outs = tuple(torch.empty(B, dtype=torch.int32, device=dev) for _ in range(3))
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+
+        def step(i=None):
+            sdd.confidence_prefix(dlt, gamma, TAU, ws=conf_ws, out=skbuf)
+            if i is not None:
+                ev[i][0].record()
+            kv.verify(active, d_act, logits, am, ws)
+            if i is not None:
+                ev[i][1].record()
+            Lacc, nxt, _ = sdd.accept(d_act, logits, sdd.GREEDY, ws=acc_ws, out=outs)
+            kv.commit(active, Lacc, nxt)
+
+        step()
+        torch.cuda.synchronize()
+        lens_before = kv.state()[0]
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for i in range(reps):
+            step(i)
+        e1.record()
+        torch.cuda.synchronize()
+        round_ms = e0.elapsed_time(e1) / reps
+        verify_ms = float(np.median([a.elapsed_time(b) for a, b in ev]))
+        M = B * (gamma + 1)
+        act = active.cpu().numpy()
+        ctx = float(np.mean(lens_before[act])) + reps / 2.0  # mean cache length over the timed rounds
+        weight_bytes = (L * layer_params(shape) + V * d) * 2
+        kv_bytes = B * ctx * L * 2 * hkv * hd * 2
+        nbytes = weight_bytes + kv_bytes + M * V * 4
+        flops = 2.0 * M * (L * layer_params(shape) + V * d) + L * hq * hd * 4.0 * M * ctx
+        out[variant] = {"B_eff": B, "rows": M, "skip_len": sk.cpu().numpy().tolist(), "ms_per_round": round_ms,
+                        "verify_ms": verify_ms, "verify_calls_per_s": 1e3 / verify_ms,
+                        "sequence_blocks_verified_per_s": B * 1e3 / verify_ms,
+                        "drafted_tokens_verified_per_s": B * gamma * 1e3 / verify_ms,
+                        "bytes": nbytes, "flops": flops,
+                        "frac_hbm": nbytes / (verify_ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
+                        "frac_mfma_bf16": flops / (verify_ms * 1e-3) / 2.5e15,
+                        "floor_ms_hbm": nbytes / (HBM_PEAK_GBS * 1e9) * 1e3, "floor_ms_mfma": flops / 2.5e15 * 1e3}
+        log(f"batch8 {variant}: B_eff {B}, verify {verify_ms:.2f} ms, round {round_ms:.2f} ms")
+        del dlt, logits
+    del kv, ws
+    torch.cuda.empty_cache()
+    return out
+
+
 def main():
     a = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -391,6 +477,7 @@ def main():
         result["next_rows"] = next_rows(sdd, torch)
         if a.workload != "tiny":
             result["next_rows"]["full_recompute_verify"] = full_recompute(sdd, torch, model, shape, P, gamma, ws)
+            result["next_rows"]["batch8"] = batch8(sdd, torch, model, shape, gamma)
     if not a.no_cpu_baseline:
         del model, kv, ws
         torch.cuda.empty_cache()

@@ -1,0 +1,484 @@
+// GEMM building blocks shared by the 33-row stream-K kernel (decoder.hip) and
+// the many-row kernel (rows.hip): launch arguments, the fragment-major K/V
+// cache indexing, and the fused epilogues that run on a [rows][C] output tile.
+#pragma once
+
+#include <algorithm>
+#include <type_traits>
+#include <cmath>
+
+#include "model.h"
+
+namespace sdd {
+
+enum Epi { EPI_QKV = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_LOGITS = 3 };
+
+constexpr int kGemmThreads = 256;
+constexpr int kXcds = 8;  // XCDs of the MI355X (32 CUs each); workgroups go to them round-robin by linear id
+constexpr int kMaxPassRows = 64;  // rows per GEMM pass (TB <= 4 row tiles of 16)
+
+struct GemmArgs {
+  const char* W;  // tiled weights
+  int KT;         // k-tiles per row strip
+  int G;          // column groups
+  int N;          // valid output columns
+  const char* X;  // activations, row-major [rows][ldx], element type T
+  int ldx;
+  int m0, M;      // rows of this pass
+  int mp;         // padded row stride of per-row scratch
+  int n_wg;
+  float* part;    // partial tiles [n_wg][2][M][NG*16]
+  int* cnt;       // arrival counter per column group
+  const RowInfo* rows;
+  // RMSNorm of the input rows: r_m = 1/sqrt(sum_g ss_in[g][m] / d_in + eps),
+  // from per-column-group sums of squares written by the producer (NULL: none)
+  const float* ss_in;
+  int ss_groups, d_in;
+  float eps;
+  // EPI_QKV
+  char* q_out;
+  int hq, hkv, hd, qk_norm;
+  const float* qn;
+  const float* kn;
+  const float* rope;
+  int kv_ld;  // position stride of the K / V^T caches
+  char* kc;
+  char* vc;
+  // EPI_RESID
+  float* x;
+  char* xa;
+  int d;
+  const float* g_next;
+  float* ss_part;  // sums of squares of this GEMM's output rows per column group
+  // EPI_SWIGLU
+  char* ffh;
+  int dff;
+  // EPI_LOGITS
+  float* logits;
+  int V;
+  float* amax_v;
+  int* amax_i;
+  // the forward's next GEMM (NULL: none), whose first k-steps a workgroup that
+  // only contributed a partial loads into L2 before it ends
+  const char* Wn;
+  int KTn, Gn, ngn, nwg_n;
+};
+
+template <typename T>
+__device__ inline void mma_tile(const uint4& a, const uint4& b, f32x4& acc) {
+  if constexpr (sizeof(T) == 2) {
+    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), acc, 0,
+                                                  0, 0);
+  } else {
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__builtin_bit_cast(float, a.x), __builtin_bit_cast(float, b.x), acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__builtin_bit_cast(float, a.y), __builtin_bit_cast(float, b.y), acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__builtin_bit_cast(float, a.z), __builtin_bit_cast(float, b.z), acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__builtin_bit_cast(float, a.w), __builtin_bit_cast(float, b.w), acc, 0, 0, 0);
+  }
+}
+
+// bf16 K / V caches, fragment-major.  Per (sequence, KV head) a cache holds ld positions (a multiple of
+// 64) as 32-position steps of 32 x HD elements.  A step is the list of 1 KB blocks that one attention step
+// loads, one block per 16-byte-per-lane load, lane-major (lane l holds elements 8 l .. 8 l + 7), so every
+// load reads whole cache lines:
+//   K block b * HD/32 + kk, lane 16 g + rho: K[32 s + kv_row(rho, b)][32 kk + 8 g + e],  e = 0..7
+//   V block db,             lane 16 g + rho: V[32 s + 8 g + e][16 db + rho],             e = 0..7
+// kv_row(rho, b) is the position that K sub-tile b feeds to MFMA row rho; it leaves the scores of lane
+// group g on positions 8 g .. 8 g + 7 of the step, the positions of that lane's V block entries.
+__device__ inline int kv_row(int rho, int b) { return 8 * (rho / 4) + 4 * b + rho % 4; }
+__device__ inline int64_t kfrag_index(int p, int d, int HD) {
+  const int i = p % 32, rho = 4 * (i / 8) + i % 4, b = (i / 4) % 2;
+  return (int64_t)(p / 32) * 32 * HD + (b * (HD / 32) + d / 32) * 512 + (16 * ((d % 32) / 8) + rho) * 8 + d % 8;
+}
+__device__ inline int64_t vfrag_index(int p, int d, int HD) {
+  const int i = p % 32;
+  return (int64_t)(p / 32) * 32 * HD + (d / 16) * 512 + (16 * (i / 8) + d % 16) * 8 + i % 8;
+}
+
+template <typename T>
+__device__ inline void store_t(char* base, int64_t idx, float v) {
+  reinterpret_cast<T*>(base)[idx] = Elem<T>::from_f32(v);
+}
+
+// Stream-K bookkeeping in 32-bit unsigned arithmetic (64-bit division is a
+// long software sequence on this GPU); the host guarantees units x workgroups
+// < 2^31.  Workgroup w owns units [w*U/n, (w+1)*U/n); unit_owner(x) is the
+// workgroup whose share contains unit x.
+__device__ inline int unit_owner(uint32_t x, uint32_t U, uint32_t n) { return (int)(((x + 1) * n + U - 1) / U) - 1; }
+__device__ inline uint32_t unit_start(uint32_t w, uint32_t U, uint32_t n) { return w * U / n; }
+
+// Loads into L2 the first three k-steps of the segment that workgroup w of a
+// GEMM launch (tiled weights Wn, KTn k-steps, Gn column groups of ngn tiles,
+// nwg workgroups) streams first, wave `wave` (0..3) the k-steps that wave
+// streams there (every fourth from the segment's start + wave).  Called from
+// a workgroup on XCD w mod 8: workgroups are dispatched to the XCDs
+// round-robin, so the lines land in the L2 that serves them.  Plain (cached) loads whose values are consumed by an empty asm
+// statement.
+__device__ inline void prefetch_gemm_start(const char* Wn, int KTn_, int Gn, int ngn, int nwg, int w_, int wave,
+                                           int lane) {
+  const uint32_t KTn = (uint32_t)KTn_, Un = (uint32_t)Gn * KTn, n = (uint32_t)nwg, w = (uint32_t)w_;
+  const uint32_t v0 = unit_start(w, Un, n), v1 = unit_start(w + 1, Un, n);
+  const uint32_t g = v0 / KTn;
+  const int kb = (int)(v0 - g * KTn);
+  const int ke = (int)std::min<uint32_t>(KTn, kb + (v1 - v0));
+  const int nk = ke - kb > wave ? (ke - kb - wave + 3) / 4 : 0;  // this wave's k-steps
+  if (nk == 0) return;
+  const int64_t ntn = (int64_t)Gn * ngn;  // tiles per k-step
+  const uint4* base = reinterpret_cast<const uint4*>(Wn) + (int64_t)g * ngn * kWave + lane;
+  uint4 v[3][8];  // unconditional loads (k-step clamped to the wave's last, tile to the group's last)
+#pragma unroll
+  for (int st = 0; st < 3; ++st) {
+    const int kt = kb + wave + 4 * min(st, nk - 1);
+#pragma unroll
+    for (int nt = 0; nt < 8; ++nt) v[st][nt] = base[((int64_t)kt * ntn + min(nt, ngn - 1)) * kWave];
+  }
+  uint32_t x = 0;
+#pragma unroll
+  for (int st = 0; st < 3; ++st)
+#pragma unroll
+    for (int nt = 0; nt < 8; ++nt) x ^= v[st][nt].x ^ v[st][nt].w;
+  asm volatile("" ::"v"(x));
+}
+
+// the same for the workgroup of the same index of the forward's next GEMM
+__device__ inline void prefetch_next(const GemmArgs& a, int wave, int lane) {
+  prefetch_gemm_start(a.Wn, a.KTn, a.Gn, a.ngn, a.nwg_n, blockIdx.x, wave, lane);
+}
+
+// Epilogues run on the final [rows][C] tile of one column group (LDS, row
+// stride C + 4).  Each wave owns rows wave, wave + 4, ... (R / 4 of them, the
+// padded ones included: their results are computed and not stored), so the
+// rows' work is straight-line code that the compiler interleaves.  A row's
+// reductions run over its columns lane, lane + 64 and then across the wave,
+// in an order that does not depend on the number of rows, so a row's result
+// is the same whatever block it is verified in (floating-point contraction is
+// off here, so that the compiler cannot fuse a row's operations differently in
+// instantiations for different row counts).  Every global load a wave needs is
+// issued before any of them is used.
+template <typename T, int NG, int R>
+__device__ void epilogue_qkv(const GemmArgs& a, const float* tile, int g, const float* rsl, const RowInfo* ri_s) {
+  // no contraction: every instantiation (row count) must round each row alike
+#pragma clang fp contract(off)
+  constexpr int C = NG * 16;  // == head_dim
+  constexpr int CP = C + 4, RPW = R / 4;
+  if constexpr (C == 64 || C == 128) {
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave), lane = threadIdx.x % kWave;
+    const int h = g;
+    const bool is_q = h < a.hq, is_k = !is_q && h < a.hq + a.hkv;
+    if (!is_q && !is_k) {
+      // V head: lane = row, so that consecutive positions of a cached
+      // dimension are written together (adjacent in both cache layouts)
+      const int mm = lane;
+      const bool ok = mm < a.M && ri_s[mm < a.M ? mm : 0].valid;
+      const RowInfo ri = ri_s[mm < a.M ? mm : 0];
+      const float r = rsl[mm < a.M ? mm : 0];
+      const int64_t head = (int64_t)ri.seq * a.hkv + (h - a.hq - a.hkv);
+      constexpr int DPW = C / 4;  // dimensions per wave
+#pragma unroll 8
+      for (int dd = 0; dd < DPW; ++dd) {
+        const int dim = wave * DPW + dd;
+        const float y = tile[(mm < R ? mm : 0) * CP + dim] * r;
+        if (ok) {
+          if constexpr (sizeof(T) == 2)
+            store_t<T>(a.vc, head * a.kv_ld * C + vfrag_index(ri.pos, dim, C), y);
+          else
+            store_t<T>(a.vc, (head * C + dim) * a.kv_ld + ri.pos, y);  // fp32: V^T rows
+        }
+      }
+      return;
+    }
+    float gn0 = 1.f, gn1 = 1.f;
+    if (a.qk_norm) {
+      const float* gp = is_q ? a.qn : a.kn;
+      gn0 = gp[lane];
+      if constexpr (C == 128) gn1 = gp[lane + 64];
+    }
+    // (cos, sin) of each row's position: table [pos][C/2] of float2
+    float2 cs[RPW];
+    float y0[RPW], y1[RPW];
+#pragma unroll
+    for (int j = 0; j < RPW; ++j) {
+      const int mm = wave + 4 * j;
+      const int mc = mm < a.M ? mm : 0;
+      const RowInfo ri = ri_s[mc];
+      cs[j] = reinterpret_cast<const float2*>(a.rope)[(size_t)(ri.valid ? ri.pos : 0) * (C / 2) + (C == 128 ? lane : lane % 32)];
+      const float r = rsl[mc];
+      y0[j] = tile[mm * CP + lane] * r;
+      y1[j] = C == 128 ? tile[mm * CP + (lane + 64) % C] * r : 0.f;
+    }
+    if (a.qk_norm) {
+      float ss[RPW];
+#pragma unroll
+      for (int j = 0; j < RPW; ++j) ss[j] = (C == 128) ? y0[j] * y0[j] + y1[j] * y1[j] : y0[j] * y0[j];
+      wave_sum_fast_n(ss);
+#pragma unroll
+      for (int j = 0; j < RPW; ++j) {
+        const float inv = 1.f / sqrtf(ss[j] / (float)C + a.eps);
+        y0[j] *= inv * gn0;
+        if constexpr (C == 128) y1[j] *= inv * gn1;
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < RPW; ++j) {
+      const float c = cs[j].x, sn = cs[j].y;
+      if constexpr (C == 128) {
+        const float t0 = y0[j], t1 = y1[j];
+        y0[j] = t0 * c - t1 * sn;
+        y1[j] = t1 * c + t0 * sn;
+      } else {
+        const float other = __shfl_xor(y0[j], 32);
+        y0[j] = lane < 32 ? y0[j] * c - other * sn : y0[j] * c + other * sn;
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < RPW; ++j) {
+      const int mm = wave + 4 * j;
+      if (mm < a.M && ri_s[mm].valid) {
+        const RowInfo ri = ri_s[mm];
+        if (is_q) {
+          const int64_t base = ((int64_t)(a.m0 + mm) * a.hq + h) * C;
+          store_t<T>(a.q_out, base + lane, y0[j]);
+          if constexpr (C == 128) store_t<T>(a.q_out, base + lane + 64, y1[j]);
+        } else if constexpr (sizeof(T) == 2) {
+          const int64_t base = ((int64_t)ri.seq * a.hkv + (h - a.hq)) * a.kv_ld * C;
+          store_t<T>(a.kc, base + kfrag_index(ri.pos, lane, C), y0[j]);
+          if constexpr (C == 128) store_t<T>(a.kc, base + kfrag_index(ri.pos, lane + 64, C), y1[j]);
+        } else {
+          const int64_t base = (((int64_t)ri.seq * a.hkv + (h - a.hq)) * a.kv_ld + ri.pos) * C;  // fp32: [pos][hd]
+          store_t<T>(a.kc, base + lane, y0[j]);
+          if constexpr (C == 128) store_t<T>(a.kc, base + lane + 64, y1[j]);
+        }
+      }
+    }
+  }
+}
+
+template <typename T, int NG, int R>
+__device__ void epilogue_resid(const GemmArgs& a, const float* tile, int g) {
+  // no contraction: every instantiation (row count) must round each row alike
+#pragma clang fp contract(off)
+  constexpr int C = NG * 16, CP = C + 4, RPW = R / 4, NCL = (C + kWave - 1) / kWave;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave), lane = threadIdx.x % kWave;
+  float gv[NCL], xv[RPW][NCL], ss[RPW];
+#pragma unroll
+  for (int k = 0; k < NCL; ++k) {
+    const int c = lane + k * kWave;
+    gv[k] = c < C ? a.g_next[(int64_t)g * C + c] : 0.f;
+  }
+  // unconditional loads (padded rows read row 0, columns past C the group's last), all in flight together
+#pragma unroll
+  for (int j = 0; j < RPW; ++j) {
+    const int mm = wave + 4 * j;
+#pragma unroll
+    for (int k = 0; k < NCL; ++k) {
+      const int c = min(lane + k * kWave, C - 1);
+      xv[j][k] = a.x[(int64_t)(a.m0 + (mm < a.M ? mm : 0)) * a.d + (int64_t)g * C + c];
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < RPW; ++j) {
+    const int mm = wave + 4 * j;
+    ss[j] = 0.f;
+#pragma unroll
+    for (int k = 0; k < NCL; ++k) {
+      const int c = lane + k * kWave;
+      if (c < C) {
+        xv[j][k] += tile[mm * CP + c];
+        ss[j] += xv[j][k] * xv[j][k];
+      }
+    }
+  }
+  wave_sum_fast_n(ss);
+#pragma unroll
+  for (int j = 0; j < RPW; ++j) {
+    const int mm = wave + 4 * j;
+    if (mm < a.M) {
+      const int m = a.m0 + mm;
+#pragma unroll
+      for (int k = 0; k < NCL; ++k) {
+        const int c = lane + k * kWave;
+        if (c < C) {
+          const int64_t n = (int64_t)g * C + c;
+          a.x[(int64_t)m * a.d + n] = xv[j][k];
+          store_t<T>(a.xa, (int64_t)m * a.d + n, xv[j][k] * gv[k]);
+        }
+      }
+      if (lane == 0) a.ss_part[(int64_t)g * a.mp + m] = ss[j];
+    }
+  }
+}
+
+template <typename T, int NG, int R>
+__device__ void epilogue_swiglu(const GemmArgs& a, const float* tile, int g, const float* rsl) {
+  // no contraction: every instantiation (row count) must round each row alike
+#pragma clang fp contract(off)
+  constexpr int C = NG * 16, CP = C + 4, P = NG / 2, RPW = R / 4;
+  constexpr int NI = (P * 16 + kWave - 1) / kWave;  // gate/up pairs per lane and row
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave), lane = threadIdx.x % kWave;
+  // every row of the padded tile is computed (straight-line code, LDS reads batched); only real rows are stored
+  float hv[RPW][NI];
+#pragma unroll
+  for (int j = 0; j < RPW; ++j) {
+    const int mm = wave + 4 * j;
+    const float r = rsl[mm];
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+      const int idx = min(lane + i * kWave, P * 16 - 1);
+      const int t = idx / 16, jj = idx % 16;
+      const float gt = tile[mm * CP + (2 * t) * 16 + jj] * r;
+      const float up = tile[mm * CP + (2 * t + 1) * 16 + jj] * r;
+      hv[j][i] = gt / (1.f + expf(-gt)) * up;
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < RPW; ++j) {
+    const int mm = wave + 4 * j;
+    if (mm < a.M) {
+      const int64_t row = (int64_t)(a.m0 + mm) * a.dff + (int64_t)g * P * 16;
+#pragma unroll
+      for (int i = 0; i < NI; ++i) {
+        const int idx = lane + i * kWave;
+        if (idx < P * 16) store_t<T>(a.ffh, row + idx, hv[j][i]);
+      }
+    }
+  }
+}
+
+__device__ inline bool arg_better(float v2, int i2, float v1, int i1) {
+  if (i2 < 0 || v2 != v2) return false;
+  if (i1 < 0) return true;
+  return v2 > v1 || (v2 == v1 && i2 < i1);
+}
+
+// Best (value, lowest index) over a fully active wave.  The combine is
+// associative and commutative, so the order of the steps does not matter.
+__device__ inline void wave_argmax(float& bv, int& bi) {
+  auto step = [&](float v2, int i2) {
+    if (arg_better(v2, i2, bv, bi)) {
+      bv = v2;
+      bi = i2;
+    }
+  };
+  step(dpp_f<kDppXor1>(bv), dpp_i<kDppXor1>(bi));
+  step(dpp_f<kDppXor2>(bv), dpp_i<kDppXor2>(bi));
+  step(dpp_f<kDppHalfMirror>(bv), dpp_i<kDppHalfMirror>(bi));
+  step(dpp_f<kDppMirror>(bv), dpp_i<kDppMirror>(bi));
+  float rv = lane_f(bv, 0);
+  int ri = __builtin_amdgcn_readlane(bi, 0);
+#pragma unroll
+  for (int r = 16; r < 64; r += 16) {
+    const float v2 = lane_f(bv, r);
+    const int i2 = __builtin_amdgcn_readlane(bi, r);
+    if (arg_better(v2, i2, rv, ri)) {
+      rv = v2;
+      ri = i2;
+    }
+  }
+  bv = rv;
+  bi = ri;
+}
+
+// wave_argmax of N independent (value, index) pairs at once
+template <int N>
+__device__ inline void wave_argmax_n(float (&bv)[N], int (&bi)[N]) {
+  auto step = [&](auto ctrl) {
+    constexpr int CTRL = decltype(ctrl)::value;
+#pragma unroll
+    for (int j = 0; j < N; ++j) {
+      const float v2 = dpp_f<CTRL>(bv[j]);
+      const int i2 = dpp_i<CTRL>(bi[j]);
+      if (arg_better(v2, i2, bv[j], bi[j])) {
+        bv[j] = v2;
+        bi[j] = i2;
+      }
+    }
+  };
+  step(std::integral_constant<int, kDppXor1>{});
+  step(std::integral_constant<int, kDppXor2>{});
+  step(std::integral_constant<int, kDppHalfMirror>{});
+  step(std::integral_constant<int, kDppMirror>{});
+#pragma unroll
+  for (int j = 0; j < N; ++j) {
+    float rv = lane_f(bv[j], 0);
+    int ri = __builtin_amdgcn_readlane(bi[j], 0);
+#pragma unroll
+    for (int r = 16; r < 64; r += 16) {
+      const float v2 = lane_f(bv[j], r);
+      const int i2 = __builtin_amdgcn_readlane(bi[j], r);
+      if (arg_better(v2, i2, rv, ri)) {
+        rv = v2;
+        ri = i2;
+      }
+    }
+    bv[j] = rv;
+    bi[j] = ri;
+  }
+}
+
+template <int NG, int R>
+__device__ void epilogue_logits(const GemmArgs& a, const float* tile, int g, const float* rsl, const RowInfo* ri_s) {
+  // no contraction: every instantiation (row count) must round each row alike
+#pragma clang fp contract(off)
+  constexpr int C = NG * 16, CP = C + 4, RPW = R / 4, NCL = (C + kWave - 1) / kWave;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave), lane = threadIdx.x % kWave;
+  float v[RPW][NCL], bv[RPW];
+  int bi[RPW];
+#pragma unroll
+  for (int j = 0; j < RPW; ++j) {
+    const int mm = wave + 4 * j;
+    const float r = rsl[mm < a.M ? mm : 0];
+    bv[j] = -INFINITY;
+    bi[j] = -1;
+#pragma unroll
+    for (int k = 0; k < NCL; ++k) {
+      const int c = lane + k * kWave, n = g * C + c;
+      v[j][k] = c < C ? tile[mm * CP + c] * r : 0.f;
+      if (c < C && n < a.V && arg_better(v[j][k], n, bv[j], bi[j])) {
+        bv[j] = v[j][k];
+        bi[j] = n;
+      }
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < RPW; ++j) {
+    const int mm = wave + 4 * j;
+    if (mm < a.M && ri_s[mm].valid) {
+      const int64_t row = (int64_t)(a.m0 + mm) * a.V;
+#pragma unroll
+      for (int k = 0; k < NCL; ++k) {
+        const int c = lane + k * kWave, n = g * C + c;
+        if (c < C && n < a.V) a.logits[row + n] = v[j][k];
+      }
+    }
+  }
+  wave_argmax_n(bv, bi);
+  // one lane per row, so the rows' candidates take two store instructions, not
+  // two per row: with the next segment's loads in flight, a wave's outstanding
+  // memory operations would otherwise exceed the 63 the counter holds, and
+  // issue would stall until those loads land
+  float av = bv[0];
+  int ai = bi[0];
+#pragma unroll
+  for (int j = 1; j < RPW; ++j)
+    if (lane == j) {
+      av = bv[j];
+      ai = bi[j];
+    }
+  const int mm = wave + 4 * lane;
+  if (lane < RPW && mm < a.M) {
+    a.amax_v[(int64_t)g * a.mp + a.m0 + mm] = av;
+    a.amax_i[(int64_t)g * a.mp + a.m0 + mm] = ai;
+  }
+}
+
+// Many-row GEMM (rows.hip): bf16 weights, column groups of 8 or 4 tiles, up to
+// kRowsMaxRows rows [a.m0, a.m0 + a.M) per launch of nblocks workgroups (the
+// stream-K partition of a.G x a.KT units); fused epilogue `epi`.  Partial
+// tiles need kRowsPartBytes per workgroup in a.part.  Returns SDD_OK or
+// SDD_EUNSUPPORTED (other group widths, too many rows).
+constexpr int kRowsMaxTBW = 5;     // row tiles per computing wave
+constexpr int kRowsMaxRows = 288;  // rows per launch: the final tile of 288 x 132 fp32 fits the 160 KB of LDS
+constexpr size_t kRowsPartBytes = (size_t)2 * kRowsMaxTBW * 8 * 4 * 64 * 16;
+int launch_gemm_rows(int ng, int epi, const GemmArgs& a, int nblocks, hipStream_t st);
+
+}  // namespace sdd
