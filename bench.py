@@ -96,17 +96,20 @@ def layer_params(s: W.ModelShape) -> int:
     return d * (s.n_q_heads + 2 * s.n_kv_heads) * hd + s.n_q_heads * hd * d + 3 * d * s.d_ff
 
 
-def cpu_baseline(shape: W.ModelShape, gamma: int) -> dict:
-    """The oracle on this host: gamma-row verify calls through 1 layer + LM head, scaled to all layers."""
+def cpu_baseline(shape: W.ModelShape, gamma: int, P: int) -> dict:
+    """The oracle on this host: gamma-row verify calls through 1 layer + LM head against a cache of the bench's
+    prompt length (attention over the cache included), scaled to all layers."""
     import oracle
 
     s1 = shape.with_layers(1)
     log("cpu baseline: building 1-layer oracle model")
     m = oracle.Model(s1, W.WEIGHT_SEED, W.WEIGHT_SIGMA)
-    kv = oracle.KV(m, 64)
-    kv.prefill(W.prompt(101, 16, shape.vocab))
+    kv = oracle.KV(m, P + gamma + 8)
+    t0 = time.perf_counter()
+    kv.prefill(W.prompt(1, P, shape.vocab))
+    log(f"cpu baseline: oracle prefill of {P} tokens through 1 layer in {time.perf_counter() - t0:.1f} s (untimed)")
     drafts = W.prompt(102, gamma, shape.vocab)
-    n_calls = 8  # about 10 s of CPU work on the 16-thread host share
+    n_calls = 6  # about 10 s of CPU work on the 16-thread host share
     t0 = time.perf_counter()
     for _ in range(n_calls):
         kv.verify(drafts)
@@ -117,7 +120,7 @@ def cpu_baseline(shape: W.ModelShape, gamma: int) -> dict:
     return {"value": gamma / call_s, "unit": "drafted tokens verified/s", "cores": oracle.num_threads(),
             "kind": "oracle",
             "sample": (f"{n_calls} gamma={gamma} verify calls ({gamma + 1} rows) through 1 of {shape.n_layers} layers "
-                       f"plus the LM head, 16-token cache, fp64 oracle: {t:.2f} s per call, scaled by the MAC ratio "
+                       f"plus the LM head, {P - 1}-token cache, fp64 oracle: {t:.2f} s per call, scaled by the MAC ratio "
                        f"{scale:.1f} to {call_s:.1f} s per full call")}
 
 
@@ -160,16 +163,26 @@ def next_rows(sdd, torch, reps: int = 20) -> dict:
     ws = sdd.rowstats_workspace(B, gamma, V)
     outs = tuple(torch.empty(B, dtype=torch.int32, device=dev) for _ in range(3))
     row_bytes = V * 2
-    for name, mode in (("greedy", sdd.GREEDY), ("ratio", sdd.RATIO), ("ratio_sample", sdd.RATIO_SAMPLE)):
-        us = timed(lambda i: sdd.accept(draft, sets[i % 4][0], mode, q=sets[i % 4][1], uniforms=u, ws=ws, out=outs))
+    modes = (("greedy", sdd.GREEDY, 1, 1.0), ("topk4", sdd.TOPK, 4, 1.0), ("topk16", sdd.TOPK, 16, 1.0),
+             ("lenience0.3", sdd.LENIENT, 1, 0.3), ("ratio", sdd.RATIO, 1, 1.0),
+             ("ratio_sample", sdd.RATIO_SAMPLE, 1, 1.0))
+    for name, mode, k, lam in modes:
+        us = timed(lambda i: sdd.accept(draft, sets[i % 4][0], mode, q=sets[i % 4][1], uniforms=u, k=k,
+                                        lenience=lam, ws=ws, out=outs))
         L = outs[0].cpu().numpy()
         # bytes: target rows up to the first rejection and the drafter rows they compare (the kernel reads every
         # row: one pass over [B][33][V] target + [B][32][V] drafter), plus the draw's row L of p and q
-        nbytes = B * (gamma + 1) * row_bytes + (B * gamma * row_bytes if mode != sdd.GREEDY else 0)
+        nbytes = B * (gamma + 1) * row_bytes + (B * gamma * row_bytes if mode in (sdd.RATIO, sdd.RATIO_SAMPLE) else 0)
         if mode == sdd.RATIO_SAMPLE:
             nbytes += int(sum(2 * row_bytes if l < gamma else row_bytes for l in L))
         out[f"accept_{name}"] = {"workload": f"accept-{B}x{gamma + 1}x{V}-bf16", "us": us, "bytes": nbytes,
                                  "GB/s": nbytes / (us * 1e-6) / 1e9, "frac_hbm": nbytes / (us * 1e-6) / 1e9 / HBM_PEAK_GBS}
+    # confidence prefix over the drafter rows (the same [16, 33, V] bf16 sets: gamma rows per sequence read)
+    sk = torch.empty(B, dtype=torch.int32, device=dev)
+    us = timed(lambda i: sdd.confidence_prefix(sets[i % 4][0], gamma, TAU, ws=ws, out=sk))
+    nbytes = B * gamma * row_bytes
+    out["confidence"] = {"workload": f"confidence-{B}x{gamma}x{V}-bf16-tau{TAU}", "us": us, "bytes": nbytes,
+                         "GB/s": nbytes / (us * 1e-6) / 1e9, "frac_hbm": nbytes / (us * 1e-6) / 1e9 / HBM_PEAK_GBS}
     del sets
     # survival predictor, 32 positions of the paper's shape
     x = W.survival_inputs(seed=1, n=32)
@@ -304,6 +317,63 @@ def batch8(sdd, torch, model, shape: W.ModelShape, gamma: int, reps: int = 6) ->
     del kv, ws
     torch.cuda.empty_cache()
     return out
+
+
+def qwen7b_leg(sdd, torch, rounds: int = 8, warmup: int = 2) -> dict:
+    """The Qwen2.5-7B-shaped verifier (28 layers, d 3584, 28/4 heads x 128, FFN 18944, V 152064, bf16, random
+    weights) with a 512-token prompt at gamma = 32: per round the confidence prefix on the drafter's logits, the
+    verify call, greedy acceptance and the commit (random drafts: about one token committed per round)."""
+    dev = "cuda"
+    shape, P, gamma = W.QWEN7B, W.QWEN7B_PROMPT, W.GAMMA
+    V, d, L = shape.vocab, shape.d_model, shape.n_layers
+    model = sdd.Model(shape)
+    model.init_random(W.WEIGHT_SEED, W.WEIGHT_SIGMA)
+    kv = sdd.KVCache(model, 1, P + (rounds + warmup) * (gamma + 1) + 8)
+    ws = model.workspace(256)
+    kv.prefill(0, torch.from_numpy(W.prompt(1, P, V)).to(dev), ws)
+    seq0 = torch.zeros(1, dtype=torch.int32, device=dev)
+    drafts = torch.from_numpy(W.prompt(41, (rounds + warmup) * gamma, V).reshape(rounds + warmup, gamma)).to(dev)
+    dl = torch.from_numpy(W.to_bf16_bits(W.rng(8).standard_normal((1, gamma + 1, V), dtype=np.float32) *
+                                         np.float32(3.0)).view(np.int16)).to(dev).view(torch.bfloat16)
+    logits = torch.empty((1, gamma + 1, V), dtype=torch.float32, device=dev)
+    am = torch.empty((1, gamma + 1), dtype=torch.int32, device=dev)
+    acc_ws = sdd.rowstats_workspace(1, gamma, V)
+    conf_ws = sdd.rowstats_workspace(1, gamma, V)
+    outs = tuple(torch.empty(1, dtype=torch.int32, device=dev) for _ in range(3))
+    sk = torch.empty(1, dtype=torch.int32, device=dev)
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(rounds)]
+
+    def step(r, i=None):
+        sdd.confidence_prefix(dl, gamma, TAU, ws=conf_ws, out=sk)
+        if i is not None:
+            ev[i][0].record()
+        kv.verify(seq0, drafts[r:r + 1], logits, am, ws)
+        if i is not None:
+            ev[i][1].record()
+        Lacc, nxt, _ = sdd.accept(drafts[r:r + 1], logits, sdd.GREEDY, ws=acc_ws, out=outs)
+        kv.commit(seq0, Lacc, nxt)
+
+    for r in range(warmup):
+        step(r)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for i in range(rounds):
+        step(warmup + i, i)
+    e1.record()
+    torch.cuda.synchronize()
+    round_ms = e0.elapsed_time(e1) / rounds
+    verify_ms = float(np.median([a.elapsed_time(b) for a, b in ev]))
+    ctx = float(kv.state()[0][0]) - rounds / 2.0
+    nbytes = (L * layer_params(shape) + V * d) * 2 + ctx * L * 2 * shape.n_kv_heads * shape.head_dim * 2 + \
+        (gamma + 1) * V * 4
+    del kv, ws, model
+    torch.cuda.empty_cache()
+    return {"workload": f"qwen7b-verify-gamma{gamma}, prompt {P}, batch 1", "ms_per_round": round_ms,
+            "verify_ms": verify_ms, "verify_calls_per_s": 1e3 / verify_ms,
+            "drafted_tokens_verified_per_s": gamma * 1e3 / verify_ms, "bytes": nbytes,
+            "frac_hbm": nbytes / (verify_ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
+            "floor_ms_hbm": nbytes / (HBM_PEAK_GBS * 1e9) * 1e3}
 
 
 def main():
@@ -478,10 +548,12 @@ def main():
         if a.workload != "tiny":
             result["next_rows"]["full_recompute_verify"] = full_recompute(sdd, torch, model, shape, P, gamma, ws)
             result["next_rows"]["batch8"] = batch8(sdd, torch, model, shape, gamma)
+        if a.workload == "qwen32b":
+            result["next_rows"]["qwen7b_verify"] = qwen7b_leg(sdd, torch)
     if not a.no_cpu_baseline:
         del model, kv, ws
         torch.cuda.empty_cache()
-        result["cpu_baseline"] = cpu_baseline(shape, gamma)
+        result["cpu_baseline"] = cpu_baseline(shape, gamma, P)
     print(json.dumps(result), flush=True)
 
 

@@ -89,8 +89,9 @@ int sdd_device_ok(void);
 
 /* ---- model ------------------------------------------------------------ */
 
-/* Bytes of the device weight buffer for cfg.  Weights are stored in the
- * library's MFMA-tiled layout, not row-major. */
+/* Bytes of the device weight buffer for cfg on the current device.  Weights
+ * are stored in the library's MFMA-tiled layout, not row-major, in an order
+ * that depends on the device's compute-unit count (sdd_model_matrix_layout). */
 int sdd_weights_bytes(const sdd_model_config* cfg, size_t* bytes);
 
 /* Wraps a caller-owned device buffer of at least sdd_weights_bytes() bytes.
@@ -109,6 +110,21 @@ int sdd_model_init_random(sdd_model* m, uint64_t seed, float sigma, sdd_stream_t
 /* Copies one row-major tensor (device pointer; model dtype for matrices and
  * embeddings, fp32 for norm gains) into the tiled layout. */
 int sdd_model_load_tensor(sdd_model* m, int kind, int layer, const void* src, sdd_stream_t stream);
+
+/* Layout of one tiled weight matrix (kind SDD_T_LM_HEAD, or SDD_T_WQ..SDD_T_WDOWN
+ * of `layer`; q/k/v share one fused matrix [Wq; Wk; Wv], gate/up one matrix whose
+ * 16-row tiles alternate gate, up).  A tile is 1 KiB: 16 rows x kt columns
+ * (kt 32 for bf16, 16 for fp32), lane l's 16 bytes holding row l % 16 and the
+ * 16 / elem columns from (l / 16) * 16 / elem.  Row tiles form column groups
+ * of *ng; unit (g, k) is the ng tiles of group g at k-step k, and the plan
+ * splits the U = G * KT units over *n_wg workgroups, workgroup w owning units
+ * [w U / n_wg, (w + 1) U / n_wg) (integer division).  The i-th unit of
+ * workgroup w is stored at slot i * n_wg + w, its tile j (row tile g * ng + j)
+ * at byte *offset + (slot * ng + j) * 1024 of the weight buffer; slots past a
+ * shorter share are zero.  *bytes is the matrix's extent.  Host-only (no
+ * device access).  Errors: SDD_EINVAL for a NULL pointer, a bad kind or layer. */
+int sdd_model_matrix_layout(const sdd_model* m, int kind, int layer, size_t* offset, size_t* bytes, int* KT,
+                            int* G, int* ng, int* n_wg);
 
 /* ---- KV cache ---------------------------------------------------------- */
 

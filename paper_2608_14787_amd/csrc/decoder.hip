@@ -62,7 +62,7 @@ __global__ void __launch_bounds__(256) row_argmax_kernel(const float* amax_v, co
   if (t == 0 && rows[m].valid) out[m] = si[0] < 0 ? 0 : si[0];
 }
 
-template <typename T, int TB, int NG, int EPI, bool MR = false>
+template <typename T, int TB, int NG, int EPI>
 __global__ void __launch_bounds__(kGemmThreads, 1) gemm_kernel(GemmArgs a) {
   constexpr int C = NG * 16;       // output columns of a column group
   constexpr int CP = C + 4;        // LDS row stride of the output tile (16-byte row writes hit distinct banks)
@@ -82,22 +82,7 @@ __global__ void __launch_bounds__(kGemmThreads, 1) gemm_kernel(GemmArgs a) {
   static_assert(4 * NACC * kWave * 4 >= R * CP, "tile must fit the reduction buffer");
   touch_kernargs<GemmArgs>();
 
-  // Many-row launch (prefill chunks, MR): a.M rows from a.m0 in 64-row tiles;
-  // each workgroup takes one column group whole (n_wg = G: one segment, no
-  // partials) for one row tile.  The row tiles of a group are consecutive
-  // workgroups of one XCD, so they stream the group's weights together through
-  // that XCD's L2 and HBM delivers them about once per chunk.
-  int w = blockIdx.x;
-  if constexpr (MR) {
-    const int nrt = (a.M + kMaxPassRows - 1) / kMaxPassRows;
-    const int j = blockIdx.x / kXcds;
-    const int g = (j / nrt) * kXcds + blockIdx.x % kXcds, rt = j % nrt;
-    if (g >= a.G) return;
-    a.m0 += rt * kMaxPassRows;
-    a.M = min(kMaxPassRows, a.M - rt * kMaxPassRows);
-    w = g;
-  }
-  constexpr int kWCpol = MR ? 0 : kNtCpol;  // row tiles re-read the weights from L2
+  const int w = blockIdx.x;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave), lane = threadIdx.x % kWave;
   const uint32_t KT = (uint32_t)a.KT, U = (uint32_t)a.G * KT;
   const uint32_t u0 = unit_start(w, U, a.n_wg), u1 = unit_start(w + 1, U, a.n_wg);
@@ -114,10 +99,12 @@ __global__ void __launch_bounds__(kGemmThreads, 1) gemm_kernel(GemmArgs a) {
       const_cast<char*>(a.X), 0, (a.m0 + a.M) * a.ldx * (int)sizeof(T), kBufferRsrcWord3);
   const int xlane = ((a.m0 + lane % 16) * a.ldx + (lane / 16) * EPL) * (int)sizeof(T);  // < 2^31: checked on the host
   const int xrow16 = 16 * a.ldx * (int)sizeof(T);
-  // the whole matrix: k-step kt of every column group is one contiguous run of G x NG tiles
-  const __amdgpu_buffer_rsrc_t wrs =
-      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint4*>(W), 0, (int)(KT * a.G * NG * kWave * 16), kBufferRsrcWord3);
-  const uint32_t kstep4w = 4u * a.G * NG * kWave * 16;    // bytes between a wave's consecutive k-steps
+  // the whole matrix, stored in the order of this launch's plan: the i-th unit (NG tiles) of workgroup w at
+  // slot i * n_wg + w, so a workgroup's consecutive units are n_wg slots apart
+  const uint32_t slot_bytes = (uint32_t)NG * kWave * 16, wstride = (uint32_t)a.n_wg * slot_bytes;
+  const __amdgpu_buffer_rsrc_t wrs = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint4*>(W), 0, (int)(((U + a.n_wg - 1) / a.n_wg) * wstride), kBufferRsrcWord3);
+  const uint32_t kstep4w = 4u * wstride;    // bytes between a wave's consecutive k-steps
   const uint32_t kstep4x = 4u * KTILE * (uint32_t)sizeof(T);
   const int wlane = lane * 16;
 
@@ -139,7 +126,7 @@ __global__ void __launch_bounds__(kGemmThreads, 1) gemm_kernel(GemmArgs a) {
 #pragma unroll
     for (int nt = 0; nt < NG; ++nt)
       wa[nt] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(
-                                             wd, wlane, (int)(wo + (uint32_t)kt * kstep4w + (uint32_t)nt * kWave * 16), kWCpol));
+                                             wd, wlane, (int)(wo + (uint32_t)kt * kstep4w + (uint32_t)nt * kWave * 16), kNtCpol));
 #pragma unroll
     for (int tb = 0; tb < TB; ++tb)
       xb[tb] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(xd, xlane + tb * xrow16,
@@ -166,7 +153,7 @@ __global__ void __launch_bounds__(kGemmThreads, 1) gemm_kernel(GemmArgs a) {
     s.ka = 0;
     s.kz = __builtin_amdgcn_readfirstlane(S > wave ? (S - wave + 3) / 4 : 0);
     const uint32_t k0 = (uint32_t)(s.kb + wave);
-    s.wo = __builtin_amdgcn_readfirstlane(k0 * (kstep4w / 4) + (uint32_t)s.g * NG * kWave * 16);
+    s.wo = __builtin_amdgcn_readfirstlane((u - u0 + (uint32_t)wave) * wstride + (uint32_t)w * slot_bytes);
     s.xo = __builtin_amdgcn_readfirstlane(k0 * KTILE * (uint32_t)sizeof(T));
     return s;
   };
@@ -947,7 +934,6 @@ struct CallCtx {
   char* ws;
   WsLayout L;
   hipStream_t st;
-  bool many_rows = false;  // prefill chunk: GEMMs over more than 64 rows run all row tiles in one launch
 };
 
 template <typename T, int NG, int EPI>
@@ -961,15 +947,6 @@ static void launch_gemm_tb(int tb, const GemmArgs& a, int nblocks, hipStream_t s
 }
 
 template <typename T, int EPI>
-static void launch_rows_ng(int ng, const GemmArgs& a, int nblocks, hipStream_t st) {
-  switch (ng) {
-    case 8: hipLaunchKernelGGL((gemm_kernel<T, 4, 8, EPI, true>), dim3(nblocks), dim3(kGemmThreads), 0, st, a); break;
-    case 4: hipLaunchKernelGGL((gemm_kernel<T, 4, 4, EPI, true>), dim3(nblocks), dim3(kGemmThreads), 0, st, a); break;
-    default: hipLaunchKernelGGL((gemm_kernel<T, 4, 2, EPI, true>), dim3(nblocks), dim3(kGemmThreads), 0, st, a); break;
-  }
-}
-
-template <typename T, int EPI>
 static void launch_gemm_ng(int ng, int tb, const GemmArgs& a, int nblocks, hipStream_t st) {
   switch (ng) {
     case 8: launch_gemm_tb<T, 8, EPI>(tb, a, nblocks, st); break;
@@ -977,11 +954,6 @@ static void launch_gemm_ng(int ng, int tb, const GemmArgs& a, int nblocks, hipSt
     default: launch_gemm_tb<T, 2, EPI>(tb, a, nblocks, st); break;
   }
 }
-
-// Runs one GEMM over rows [0, M) in passes of at most 64 rows.
-// Weight bytes one workgroup streams in the time a segment's tail takes
-// (about 9 us at the ~25 GB/s per CU of a full-chip stream).
-constexpr double kTailStreamBytes = 224.0 * 1024;
 
 // A GEMM of the forward: tiled weights at w_off, N output columns, K inputs,
 // column groups of ng tiles.
@@ -991,29 +963,9 @@ struct GemmRef {
   int K, ng;
 };
 
-// Column groups, k-steps and workgroups of a GEMM launch.
-struct GemmPlan {
-  int G, KT, n_wg;
-};
-
-static GemmPlan plan_gemm(const CallCtx& cx, const GemmRef& r) {
-  GemmPlan p;
-  p.KT = (int)ceil_div(r.K, cx.m->ktile);
-  p.G = (int)(ceil_div(r.N, 16) / r.ng);
-  const int64_t U = (int64_t)p.G * p.KT;
-  p.n_wg = (int)std::min<int64_t>(U, cx.L.n_wg);
-  // With at most one column group per workgroup, equal shares of the whole
-  // unit range leave about a third of the workgroups straddling two groups,
-  // and such a workgroup pays a second tail (reduction, partial publish,
-  // fix-up, epilogue).  Splitting every group into s equal k-ranges over
-  // G x s workgroups gives each workgroup exactly one segment; it is taken
-  // when the longer share costs less stream time than one tail.
-  if (p.G <= cx.L.n_wg) {
-    const int s = std::min(cx.L.n_wg / p.G, p.KT);
-    const double extra_units = (double)p.KT / s - (double)U / p.n_wg;
-    if (extra_units * r.ng * 1024 < kTailStreamBytes) p.n_wg = p.G * s;
-  }
-  return p;
+// The streaming plan of a GEMM of the forward (the order its matrix is stored in).
+static MatPlan plan_gemm(const CallCtx& cx, const GemmRef& r) {
+  return plan_matrix(r.N, r.K, cx.m->ktile, r.ng, cx.L.n_wg);
 }
 
 // Runs one GEMM over rows [0, M) in passes of at most 64 rows; `next` is the
@@ -1021,7 +973,7 @@ static GemmPlan plan_gemm(const CallCtx& cx, const GemmRef& r) {
 static int run_gemm(CallCtx& cx, int epi, unsigned prof, size_t w_off, int64_t N, int K, const char* X, GemmArgs a,
                     int M, int ng, const GemmRef* next = nullptr) {
   const sdd_model* m = cx.m;
-  const GemmPlan plan = plan_gemm(cx, GemmRef{w_off, N, K, ng});
+  const MatPlan plan = plan_gemm(cx, GemmRef{w_off, N, K, ng});
   a.W = m->base + w_off;
   a.KT = plan.KT;
   a.G = plan.G;
@@ -1036,12 +988,12 @@ static int run_gemm(CallCtx& cx, int epi, unsigned prof, size_t w_off, int64_t N
   const int64_t U = (int64_t)a.G * a.KT;
   const int nblocks = plan.n_wg;
   a.n_wg = nblocks;
-  GemmPlan np{};
+  MatPlan np{};
   if (next) np = plan_gemm(cx, *next);
   if ((U + 1) * nblocks >= (int64_t(1) << 31))
     return fail(SDD_EUNSUPPORTED, "matrix of %lld weight tiles exceeds the 32-bit stream-K bookkeeping", (long long)U);
   // weight buffer offsets, k-steps up to 4 past a wave's range included
-  if ((int64_t)a.G * ng * (a.KT + 4) * 1024 >= (int64_t(1) << 31))
+  if ((plan_slots(plan) + 4 * (int64_t)plan.n_wg) * ng * 1024 >= (int64_t(1) << 31))
     return fail(SDD_EUNSUPPORTED, "matrix of %lld x %d exceeds the 32-bit buffer offsets", (long long)N, K);
   if ((int64_t)(M + 64) * K * m->es >= (int64_t(1) << 31))
     return fail(SDD_EUNSUPPORTED, "activations of %d rows x %d exceed the 32-bit buffer offsets", M, K);
@@ -1060,30 +1012,6 @@ static int run_gemm(CallCtx& cx, int epi, unsigned prof, size_t w_off, int64_t N
       if (rc) return rc;
     }
     return SDD_OK;
-  }
-  if (cx.many_rows && M > kMaxPassRows && epi != EPI_LOGITS) {
-    // prefill chunk: every (column group, 64-row tile) in one launch, one group per workgroup
-    a.m0 = 0;
-    a.M = M;
-    a.n_wg = a.G;
-    a.Wn = nullptr;
-    const int nb = (int)(ceil_div(a.G, kXcds) * kXcds * ceil_div(M, kMaxPassRows));
-    prof_begin(prof, cx.st);
-    if (m->es == 2) {
-      switch (epi) {
-        case EPI_QKV: launch_rows_ng<uint16_t, EPI_QKV>(ng, a, nb, cx.st); break;
-        case EPI_RESID: launch_rows_ng<uint16_t, EPI_RESID>(ng, a, nb, cx.st); break;
-        default: launch_rows_ng<uint16_t, EPI_SWIGLU>(ng, a, nb, cx.st); break;
-      }
-    } else {
-      switch (epi) {
-        case EPI_QKV: launch_rows_ng<float, EPI_QKV>(ng, a, nb, cx.st); break;
-        case EPI_RESID: launch_rows_ng<float, EPI_RESID>(ng, a, nb, cx.st); break;
-        default: launch_rows_ng<float, EPI_SWIGLU>(ng, a, nb, cx.st); break;
-      }
-    }
-    prof_end(prof, cx.st);
-    return check_launch("gemm_kernel (row tiles)");
   }
   for (int m0 = 0; m0 < M; m0 += kMaxPassRows) {
     a.m0 = m0;
@@ -1173,7 +1101,7 @@ static int forward_rows(CallCtx& cx, int nb, int R, float* logits, int32_t* argm
       a.scale = 1.f / sqrtf((float)c.head_dim);
       a.n_attn = kXcds * a.qblocks * (int)ceil_div((int64_t)nb * a.hkv, kXcds);
       // the CUs the attention leaves idle load the o_proj's first k-steps into L2
-      const GemmPlan op = plan_gemm(cx, GemmRef{Ly.o, d, (int)hq, m->ng_o});
+      const MatPlan op = plan_gemm(cx, GemmRef{Ly.o, d, (int)hq, m->ng_o});
       a.n_pref = std::max(0, std::min((m->n_cu - a.n_attn) / kXcds * kXcds, (op.n_wg + 1) / 2 + kXcds));
       a.n_pref = a.n_pref / kXcds * kXcds;
       a.Wn = a.n_pref > 0 ? m->base + Ly.o : nullptr;
@@ -1411,7 +1339,6 @@ extern "C" int sdd_kv_prefill(sdd_model* m, sdd_kv* kv, int seq, const int32_t* 
     CallCtx cx;
     int rc = make_ctx(cx, m, kv, ws, ws_bytes, chunk, st);
     if (rc) return rc;
-    cx.many_rows = true;
     EmbedArgs e{};
     e.prefill = 1;
     e.seq = seq;

@@ -100,37 +100,29 @@ __device__ inline void store_t(char* base, int64_t idx, float v) {
   reinterpret_cast<T*>(base)[idx] = Elem<T>::from_f32(v);
 }
 
-// Stream-K bookkeeping in 32-bit unsigned arithmetic (64-bit division is a
-// long software sequence on this GPU); the host guarantees units x workgroups
-// < 2^31.  Workgroup w owns units [w*U/n, (w+1)*U/n); unit_owner(x) is the
-// workgroup whose share contains unit x.
-__device__ inline int unit_owner(uint32_t x, uint32_t U, uint32_t n) { return (int)(((x + 1) * n + U - 1) / U) - 1; }
-__device__ inline uint32_t unit_start(uint32_t w, uint32_t U, uint32_t n) { return w * U / n; }
+// Stream-K bookkeeping (unit_start, unit_owner: model.h) is 32-bit unsigned
+// arithmetic: 64-bit division is a long software sequence on this GPU.
 
-// Loads into L2 the first three k-steps of the segment that workgroup w of a
-// GEMM launch (tiled weights Wn, KTn k-steps, Gn column groups of ngn tiles,
-// nwg workgroups) streams first, wave `wave` (0..3) the k-steps that wave
-// streams there (every fourth from the segment's start + wave).  Called from
-// a workgroup on XCD w mod 8: workgroups are dispatched to the XCDs
-// round-robin, so the lines land in the L2 that serves them.  Plain (cached) loads whose values are consumed by an empty asm
-// statement.
-__device__ inline void prefetch_gemm_start(const char* Wn, int KTn_, int Gn, int ngn, int nwg, int w_, int wave,
+// Loads into L2 the first three k-steps that workgroup w of a GEMM launch
+// (weights Wn stored in the order of their plan: workgroup w's i-th unit of
+// ngn tiles at slot i * nwg + w) streams, wave `wave` (0..3) the k-steps that
+// wave streams (local units wave, wave + 4, wave + 8).  Called from a
+// workgroup on XCD w mod 8: workgroups are dispatched to the XCDs round-robin,
+// so the lines land in the L2 that serves them.  Plain (cached) loads whose
+// values are consumed by an empty asm statement.
+__device__ inline void prefetch_gemm_start(const char* Wn, int KTn, int Gn, int ngn, int nwg, int w_, int wave,
                                            int lane) {
-  const uint32_t KTn = (uint32_t)KTn_, Un = (uint32_t)Gn * KTn, n = (uint32_t)nwg, w = (uint32_t)w_;
-  const uint32_t v0 = unit_start(w, Un, n), v1 = unit_start(w + 1, Un, n);
-  const uint32_t g = v0 / KTn;
-  const int kb = (int)(v0 - g * KTn);
-  const int ke = (int)std::min<uint32_t>(KTn, kb + (v1 - v0));
-  const int nk = ke - kb > wave ? (ke - kb - wave + 3) / 4 : 0;  // this wave's k-steps
+  const uint32_t Un = (uint32_t)Gn * (uint32_t)KTn, n = (uint32_t)nwg, w = (uint32_t)w_;
+  const int nloc = (int)(unit_start(w + 1, Un, n) - unit_start(w, Un, n));
+  const int nk = nloc > wave ? (nloc - wave + 3) / 4 : 0;  // this wave's units
   if (nk == 0) return;
-  const int64_t ntn = (int64_t)Gn * ngn;  // tiles per k-step
-  const uint4* base = reinterpret_cast<const uint4*>(Wn) + (int64_t)g * ngn * kWave + lane;
-  uint4 v[3][8];  // unconditional loads (k-step clamped to the wave's last, tile to the group's last)
+  const uint4* base = reinterpret_cast<const uint4*>(Wn) + (int64_t)w * ngn * kWave + lane;
+  uint4 v[3][8];  // unconditional loads (unit clamped to the wave's last, tile to the group's last)
 #pragma unroll
   for (int st = 0; st < 3; ++st) {
-    const int kt = kb + wave + 4 * min(st, nk - 1);
+    const int64_t i = wave + 4 * min(st, nk - 1);
 #pragma unroll
-    for (int nt = 0; nt < 8; ++nt) v[st][nt] = base[((int64_t)kt * ntn + min(nt, ngn - 1)) * kWave];
+    for (int nt = 0; nt < 8; ++nt) v[st][nt] = base[(i * nwg * ngn + min(nt, ngn - 1)) * kWave];
   }
   uint32_t x = 0;
 #pragma unroll

@@ -93,10 +93,11 @@ __global__ void __launch_bounds__(kRowsThreads, 1) gemm_rows_kernel(GemmArgs a) 
   const uint32_t u0 = unit_start(w, U, a.n_wg), u1 = unit_start(w + 1, U, a.n_wg);
   const int g_first = (int)(u0 / KT);
   const int ntiles = (a.M + 15) / 16;
-  const uint32_t kstep_w = (uint32_t)a.G * NG * 1024;  // bytes of one k-step of the whole matrix
-  // weights: tile (nt, kt) of the matrix at byte kt * kstep_w + nt * 1 KiB, lane l's fragment at 16 l
-  const __amdgpu_buffer_rsrc_t wrs =
-      __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(a.W), 0, (int)(KT * kstep_w), kBufferRsrcWord3);
+  // weights, stored in the order of the launch's plan: the i-th unit (NG tiles of 1 KiB, lane l's fragment at
+  // 16 l) of workgroup w at slot i * n_wg + w, so this workgroup's consecutive units are kstep_w bytes apart
+  const uint32_t kstep_w = (uint32_t)a.n_wg * NG * 1024;
+  const __amdgpu_buffer_rsrc_t wrs = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<char*>(a.W), 0, (int)(((U + a.n_wg - 1) / a.n_wg) * kstep_w), kBufferRsrcWord3);
   // a descriptor with no range: loads through it return zero without a memory access
   const __amdgpu_buffer_rsrc_t nrs = __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(a.W), 0, 0, kBufferRsrcWord3);
   // activations: row r of the launch at X + (m0 + r) * ldx elements.  Row tile tb's fragment of k-step kt: lane l
@@ -118,7 +119,7 @@ __global__ void __launch_bounds__(kRowsThreads, 1) gemm_rows_kernel(GemmArgs a) 
     s.kb = (int)(u - (uint32_t)s.g * KT);
     s.ke = (int)std::min<uint32_t>(KT, s.kb + (u1 - u));
     s.nk = s.ke - s.kb;
-    s.wo = (uint32_t)s.kb * kstep_w + (uint32_t)s.g * NG * 1024;
+    s.wo = (u - u0) * kstep_w + (uint32_t)w * NG * 1024;
     s.xo = (uint32_t)s.kb * 64;
     return s;
   };

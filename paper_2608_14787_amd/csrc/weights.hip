@@ -39,7 +39,8 @@ __device__ inline float synth_value(uint64_t key, uint64_t idx, float scale) {
 // Source of a tiled matrix: rows of a fused matrix map to (part, logical row).
 struct TiledSrc {
   int kind;  // 0 plain, 1 fused q/k/v, 2 gate/up interleaved per 16-row tile
-  int K, ktile, KT, ng;
+  int K, ktile;
+  MatPlan plan;   // storage order of the tiles
   int64_t N;      // physical rows
   int n0, n1;     // fused q/k/v row boundaries
   uint64_t key[3];
@@ -67,14 +68,25 @@ __device__ inline void map_row(const TiledSrc& s, int64_t row, int& part, int64_
 template <typename T>
 __global__ void fill_tiled_kernel(char* dst, TiledSrc s, int only_part) {
   constexpr int EPL = 16 / sizeof(T);
-  const int64_t slices = ceil_div(s.N, 16) * (int64_t)s.KT * 64;
+  const MatPlan& p = s.plan;
+  const uint32_t U = (uint32_t)p.G * p.KT;
+  const int64_t slices = plan_slots(p) * p.ng * 64;
   for (int64_t id = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; id < slices;
        id += (int64_t)gridDim.x * blockDim.x) {
-    const int64_t tile = id / 64;  // physical: kt * NT + nt (k-step major, NT = ceil(N / 16) row tiles)
+    // physical tile (slot, j): the j-th row tile of the unit stored at slot = i * n_wg + w, that is the i-th
+    // unit of workgroup w; slots past a shorter share are padding (zero)
+    const int64_t tile = id / 64;
     const int lane = (int)(id % 64);
-    const int64_t NT = ceil_div(s.N, 16);
-    const int kt = (int)(tile / NT);
-    const int64_t nt = tile % NT;
+    const int64_t slot = tile / p.ng;
+    const int j = (int)(tile % p.ng);
+    const uint32_t w = (uint32_t)(slot % p.n_wg), i = (uint32_t)(slot / p.n_wg);
+    const uint32_t u = unit_start(w, U, p.n_wg) + i;
+    if (u >= unit_start(w + 1, U, p.n_wg)) {
+      *reinterpret_cast<uint4*>(dst + id * 16) = uint4{0, 0, 0, 0};
+      continue;
+    }
+    const int g = (int)(u / p.KT), kt = (int)(u % p.KT);
+    const int64_t nt = (int64_t)g * p.ng + j;
     const int64_t row = nt * 16 + lane % 16;
     const int k0 = kt * s.ktile + (lane / 16) * EPL;
     int part = 0;
@@ -130,10 +142,36 @@ static int validate_cfg(const sdd_model_config* c) {
 }
 
 // Computes offsets; returns total bytes.
-static size_t plan_weights(const sdd_model_config* c, sdd_model* m) {
+// CUs of the current device (256 when it cannot be queried): the workgroup count of the streaming plans,
+// which fix the order the matrices are stored in
+static int device_cus() {
+  int dev = 0, ncu = 0;
+  if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+      ncu <= 0) {
+    (void)hipGetLastError();
+    ncu = 256;
+  }
+  return ncu;
+}
+
+static size_t plan_weights(const sdd_model_config* c, sdd_model* m, int n_cu) {
   const int es = c->dtype == SDD_BF16 ? 2 : 4;
   const int kt = 64 / es;  // 4 lane groups x (16 / es) elements
   const int64_t d = c->d_model, hd = c->head_dim, hq = c->n_q_heads * hd, hk = c->n_kv_heads * hd;
+  // row tiles per column group
+  const int ng_qkv = (int)(hd / 16);
+  // o_proj has few output columns and a long K, so 128-column groups would
+  // each be split over ~6 workgroups' equal shares; 64-column groups halve
+  // the contributors a split group's last workgroup reduces.  (down_proj
+  // streams 3x the bytes and keeps 128-column groups: their 8 KiB k-steps
+  // keep more bytes in flight per wave.)
+  const int ng_o = pick_ng(d / 16, false, 4);
+  const int ng_gu = pick_ng(2 * (int64_t)c->d_ff / 16, true);
+  const int ng_down = pick_ng(d / 16, false);
+  const int ng_lm = pick_ng(c->vocab / 16, false);
+  const MatPlan p_qkv = plan_matrix(hq + 2 * hk, d, kt, ng_qkv, n_cu), p_o = plan_matrix(d, hq, kt, ng_o, n_cu),
+                p_gu = plan_matrix(2 * (int64_t)c->d_ff, d, kt, ng_gu, n_cu),
+                p_down = plan_matrix(d, c->d_ff, kt, ng_down, n_cu), p_lm = plan_matrix(c->vocab, d, kt, ng_lm, n_cu);
   size_t off = 0;
   auto take = [&](size_t bytes) {
     size_t o = off;
@@ -141,7 +179,7 @@ static size_t plan_weights(const sdd_model_config* c, sdd_model* m) {
     return o;
   };
   size_t e = take((size_t)c->vocab * d * es);
-  size_t lm = take(tiled_bytes(c->vocab, d, kt));
+  size_t lm = take(plan_bytes(p_lm));
   size_t fn = take((size_t)d * 4);
   if (m) {
     m->es = es;
@@ -149,23 +187,23 @@ static size_t plan_weights(const sdd_model_config* c, sdd_model* m) {
     m->off_embed = e;
     m->off_lm = lm;
     m->off_final_norm = fn;
-    m->ng_qkv = (int)(hd / 16);
-    // o_proj has few output columns and a long K, so 128-column groups would
-    // each be split over ~6 workgroups' equal shares; 64-column groups halve
-    // the contributors a split group's last workgroup reduces.  (down_proj
-    // streams 3x the bytes and keeps 128-column groups: their 8 KiB k-steps
-    // keep more bytes in flight per wave.)
-    m->ng_o = pick_ng(d / 16, false, 4);
-    m->ng_gu = pick_ng(2 * (int64_t)c->d_ff / 16, true);
-    m->ng_down = pick_ng(d / 16, false);
-    m->ng_lm = pick_ng(c->vocab / 16, false);
+    m->ng_qkv = ng_qkv;
+    m->ng_o = ng_o;
+    m->ng_gu = ng_gu;
+    m->ng_down = ng_down;
+    m->ng_lm = ng_lm;
+    m->plan_qkv = p_qkv;
+    m->plan_o = p_o;
+    m->plan_gu = p_gu;
+    m->plan_down = p_down;
+    m->plan_lm = p_lm;
   }
   for (int l = 0; l < c->n_layers; ++l) {
     sdd_model::Layer L;
-    L.qkv = take(tiled_bytes(hq + 2 * hk, d, kt));
-    L.o = take(tiled_bytes(d, hq, kt));
-    L.gu = take(tiled_bytes(2 * (int64_t)c->d_ff, d, kt));
-    L.down = take(tiled_bytes(d, c->d_ff, kt));
+    L.qkv = take(plan_bytes(p_qkv));
+    L.o = take(plan_bytes(p_o));
+    L.gu = take(plan_bytes(p_gu));
+    L.down = take(plan_bytes(p_down));
     L.attn_norm = take((size_t)d * 4);
     L.ffn_norm = take((size_t)d * 4);
     L.q_norm = take((size_t)hd * 4);
@@ -177,12 +215,11 @@ static size_t plan_weights(const sdd_model_config* c, sdd_model* m) {
 
 static int launch_blocks(int64_t work) { return (int)std::max<int64_t>(1, std::min<int64_t>(ceil_div(work, 256), 8192)); }
 
-static int fill_tiled(sdd_model* m, char* dst, TiledSrc s, int ng, int only_part, hipStream_t st) {
-  s.ng = ng;
+static int fill_tiled(sdd_model* m, char* dst, TiledSrc s, const MatPlan& plan, int only_part, hipStream_t st) {
+  s.plan = plan;
   s.ktile = m->ktile;
-  s.KT = (int)ceil_div(s.K, s.ktile);
   s.bf16 = m->cfg.dtype == SDD_BF16;
-  const int64_t slices = ceil_div(s.N, 16) * (int64_t)s.KT * 64;
+  const int64_t slices = plan_slots(plan) * plan.ng * 64;
   if (m->es == 2)
     hipLaunchKernelGGL(fill_tiled_kernel<uint16_t>, dim3(launch_blocks(slices)), dim3(256), 0, st, dst, s, only_part);
   else
@@ -198,7 +235,7 @@ extern "C" int sdd_weights_bytes(const sdd_model_config* cfg, size_t* bytes) {
   int rc = validate_cfg(cfg);
   if (rc) return rc;
   SDD_REQUIRE(bytes != nullptr, "bytes is NULL");
-  *bytes = plan_weights(cfg, nullptr);
+  *bytes = plan_weights(cfg, nullptr, device_cus());
   return SDD_OK;
 }
 
@@ -207,7 +244,8 @@ extern "C" int sdd_model_create(const sdd_model_config* cfg, void* weights, size
   if (rc) return rc;
   SDD_REQUIRE(weights != nullptr && out != nullptr, "NULL pointer");
   SDD_REQUIRE((uintptr_t)weights % 256 == 0, "weight buffer must be 256-byte aligned");
-  size_t need = plan_weights(cfg, nullptr);
+  const int ncu = device_cus();
+  size_t need = plan_weights(cfg, nullptr, ncu);
   if (bytes < need) return fail(SDD_ENOMEM, "weight buffer needs %zu bytes, got %zu", need, bytes);
   sdd_model* m = new (std::nothrow) sdd_model();
   if (!m) return fail(SDD_ENOMEM, "host allocation failed");
@@ -219,11 +257,7 @@ extern "C" int sdd_model_create(const sdd_model_config* cfg, void* weights, size
   m->cfg = *cfg;
   m->base = reinterpret_cast<char*>(weights);
   m->bytes = bytes;
-  plan_weights(cfg, m);
-  int dev = 0, ncu = 0;
-  if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
-      ncu <= 0)
-    ncu = 256;
+  plan_weights(cfg, m, ncu);
   m->n_cu = ncu;
   *out = m;
   return SDD_OK;
@@ -257,7 +291,7 @@ extern "C" int sdd_model_init_random(sdd_model* m, uint64_t seed, float sigma, s
                          reinterpret_cast<float*>(m->base + m->off_embed), ne, key, scale, (const float*)nullptr);
     if ((rc = check_launch("fill_rowmajor_kernel"))) return rc;
   }
-  auto gen = [&](char* dst, int ng, int kind, int64_t N, int K, uint64_t k0, uint64_t k1, uint64_t k2, int n0,
+  auto gen = [&](char* dst, const MatPlan& plan, int kind, int64_t N, int K, uint64_t k0, uint64_t k1, uint64_t k2, int n0,
                  int n1) {
     TiledSrc s{};
     s.kind = kind;
@@ -270,9 +304,9 @@ extern "C" int sdd_model_init_random(sdd_model* m, uint64_t seed, float sigma, s
     s.key[2] = k2;
     s.scale = scale;
     s.gen = 1;
-    return fill_tiled(m, dst, s, ng, -1, st);
+    return fill_tiled(m, dst, s, plan, -1, st);
   };
-  if ((rc = gen(m->base + m->off_lm, m->ng_lm, 0, c.vocab, (int)d, tensor_key(seed, tensor_id(SDD_T_LM_HEAD, 0)), 0, 0, 0, 0)))
+  if ((rc = gen(m->base + m->off_lm, m->plan_lm, 0, c.vocab, (int)d, tensor_key(seed, tensor_id(SDD_T_LM_HEAD, 0)), 0, 0, 0, 0)))
     return rc;
   auto ones = [&](size_t off, int64_t n) {
     hipLaunchKernelGGL(fill_f32_kernel, dim3(launch_blocks(n)), dim3(256), 0, st,
@@ -283,14 +317,42 @@ extern "C" int sdd_model_init_random(sdd_model* m, uint64_t seed, float sigma, s
   for (int l = 0; l < c.n_layers; ++l) {
     const sdd_model::Layer& L = m->layers[l];
     auto key = [&](int kind) { return tensor_key(seed, tensor_id(kind, l)); };
-    if ((rc = gen(m->base + L.qkv, m->ng_qkv, 1, hq + 2 * hk, (int)d, key(SDD_T_WQ), key(SDD_T_WK), key(SDD_T_WV), (int)hq, (int)hk)))
+    if ((rc = gen(m->base + L.qkv, m->plan_qkv, 1, hq + 2 * hk, (int)d, key(SDD_T_WQ), key(SDD_T_WK), key(SDD_T_WV), (int)hq, (int)hk)))
       return rc;
-    if ((rc = gen(m->base + L.o, m->ng_o, 0, d, (int)hq, key(SDD_T_WO), 0, 0, 0, 0))) return rc;
-    if ((rc = gen(m->base + L.gu, m->ng_gu, 2, 2 * (int64_t)c.d_ff, (int)d, key(SDD_T_WGATE), key(SDD_T_WUP), 0, 0, 0))) return rc;
-    if ((rc = gen(m->base + L.down, m->ng_down, 0, d, c.d_ff, key(SDD_T_WDOWN), 0, 0, 0, 0))) return rc;
+    if ((rc = gen(m->base + L.o, m->plan_o, 0, d, (int)hq, key(SDD_T_WO), 0, 0, 0, 0))) return rc;
+    if ((rc = gen(m->base + L.gu, m->plan_gu, 2, 2 * (int64_t)c.d_ff, (int)d, key(SDD_T_WGATE), key(SDD_T_WUP), 0, 0, 0))) return rc;
+    if ((rc = gen(m->base + L.down, m->plan_down, 0, d, c.d_ff, key(SDD_T_WDOWN), 0, 0, 0, 0))) return rc;
     if ((rc = ones(L.attn_norm, d)) || (rc = ones(L.ffn_norm, d)) || (rc = ones(L.q_norm, hd)) || (rc = ones(L.k_norm, hd)))
       return rc;
   }
+  return SDD_OK;
+}
+
+extern "C" int sdd_model_matrix_layout(const sdd_model* m, int kind, int layer, size_t* offset, size_t* bytes,
+                                       int* KT, int* G, int* ng, int* n_wg) {
+  SDD_REQUIRE(m && offset && bytes && KT && G && ng && n_wg, "NULL pointer");
+  SDD_REQUIRE(kind == SDD_T_LM_HEAD || (kind >= SDD_T_WQ && kind <= SDD_T_WDOWN), "bad matrix kind %d", kind);
+  if (kind != SDD_T_LM_HEAD) SDD_REQUIRE(layer >= 0 && layer < m->cfg.n_layers, "bad layer %d", layer);
+  const MatPlan* p = nullptr;
+  size_t off = 0;
+  if (kind == SDD_T_LM_HEAD) {
+    p = &m->plan_lm;
+    off = m->off_lm;
+  } else {
+    const sdd_model::Layer& L = m->layers[layer];
+    switch (kind) {
+      case SDD_T_WQ: case SDD_T_WK: case SDD_T_WV: p = &m->plan_qkv; off = L.qkv; break;
+      case SDD_T_WO: p = &m->plan_o; off = L.o; break;
+      case SDD_T_WGATE: case SDD_T_WUP: p = &m->plan_gu; off = L.gu; break;
+      default: p = &m->plan_down; off = L.down; break;
+    }
+  }
+  *offset = off;
+  *bytes = plan_bytes(*p);
+  *KT = p->KT;
+  *G = p->G;
+  *ng = p->ng;
+  *n_wg = p->n_wg;
   return SDD_OK;
 }
 
@@ -306,7 +368,7 @@ extern "C" int sdd_model_load_tensor(sdd_model* m, int kind, int layer, const vo
                        reinterpret_cast<float*>(m->base + off), n, 0.f, reinterpret_cast<const float*>(src));
     return check_launch("fill_f32_kernel");
   };
-  auto tiled = [&](size_t off, int ng, int skind, int64_t N, int K, int part, int n0, int n1) {
+  auto tiled = [&](size_t off, const MatPlan& plan, int skind, int64_t N, int K, int part, int n0, int n1) {
     TiledSrc s{};
     s.kind = skind;
     s.K = K;
@@ -315,7 +377,7 @@ extern "C" int sdd_model_load_tensor(sdd_model* m, int kind, int layer, const vo
     s.n1 = n1;
     s.src[part] = src;
     s.gen = 0;
-    return fill_tiled(m, m->base + off, s, ng, part, st);
+    return fill_tiled(m, m->base + off, s, plan, part, st);
   };
   if (kind == SDD_T_EMBED) {
     const int64_t ne = (int64_t)c.vocab * d;
@@ -329,17 +391,17 @@ extern "C" int sdd_model_load_tensor(sdd_model* m, int kind, int layer, const vo
                          reinterpret_cast<const float*>(src));
     return check_launch("fill_rowmajor_kernel");
   }
-  if (kind == SDD_T_LM_HEAD) return tiled(m->off_lm, m->ng_lm, 0, c.vocab, (int)d, 0, 0, 0);
+  if (kind == SDD_T_LM_HEAD) return tiled(m->off_lm, m->plan_lm, 0, c.vocab, (int)d, 0, 0, 0);
   if (kind == SDD_T_FINAL_NORM) return copy_f32(m->off_final_norm, d);
   const sdd_model::Layer& L = m->layers[layer];
   switch (kind) {
-    case SDD_T_WQ: return tiled(L.qkv, m->ng_qkv, 1, hq + 2 * hk, (int)d, 0, (int)hq, (int)hk);
-    case SDD_T_WK: return tiled(L.qkv, m->ng_qkv, 1, hq + 2 * hk, (int)d, 1, (int)hq, (int)hk);
-    case SDD_T_WV: return tiled(L.qkv, m->ng_qkv, 1, hq + 2 * hk, (int)d, 2, (int)hq, (int)hk);
-    case SDD_T_WO: return tiled(L.o, m->ng_o, 0, d, (int)hq, 0, 0, 0);
-    case SDD_T_WGATE: return tiled(L.gu, m->ng_gu, 2, 2 * (int64_t)c.d_ff, (int)d, 0, 0, 0);
-    case SDD_T_WUP: return tiled(L.gu, m->ng_gu, 2, 2 * (int64_t)c.d_ff, (int)d, 1, 0, 0);
-    case SDD_T_WDOWN: return tiled(L.down, m->ng_down, 0, d, c.d_ff, 0, 0, 0);
+    case SDD_T_WQ: return tiled(L.qkv, m->plan_qkv, 1, hq + 2 * hk, (int)d, 0, (int)hq, (int)hk);
+    case SDD_T_WK: return tiled(L.qkv, m->plan_qkv, 1, hq + 2 * hk, (int)d, 1, (int)hq, (int)hk);
+    case SDD_T_WV: return tiled(L.qkv, m->plan_qkv, 1, hq + 2 * hk, (int)d, 2, (int)hq, (int)hk);
+    case SDD_T_WO: return tiled(L.o, m->plan_o, 0, d, (int)hq, 0, 0, 0);
+    case SDD_T_WGATE: return tiled(L.gu, m->plan_gu, 2, 2 * (int64_t)c.d_ff, (int)d, 0, 0, 0);
+    case SDD_T_WUP: return tiled(L.gu, m->plan_gu, 2, 2 * (int64_t)c.d_ff, (int)d, 1, 0, 0);
+    case SDD_T_WDOWN: return tiled(L.down, m->plan_down, 0, d, c.d_ff, 0, 0, 0);
     case SDD_T_ATTN_NORM: return copy_f32(L.attn_norm, d);
     case SDD_T_FFN_NORM: return copy_f32(L.ffn_norm, d);
     case SDD_T_Q_NORM: return copy_f32(L.q_norm, hd);

@@ -5,21 +5,29 @@ import torch
 import workloads as W
 
 
-def untile(buf: np.ndarray, rows: int, cols: int, dtype: str) -> np.ndarray:
-    """Decodes libsdd's documented tiled weight layout back to a row-major [rows][cols] matrix.
+def untile(buf: np.ndarray, layout: dict, rows: int, cols: int, dtype: str) -> np.ndarray:
+    """Decodes libsdd's documented tiled weight layout (sdd_model_matrix_layout) back to a row-major
+    [rows][cols] matrix.
 
-    Tiles of 16 rows x ktile columns (ktile 32 for bf16, 16 for fp32), 1 KiB each; tile (nt, kt) at
-    index kt * NT + nt (k-step major, NT = ceil(rows / 16)); lane l of a tile holds row l%16 and
-    EPL = 16/sizeof(elem) columns from (l//16)*EPL."""
+    Tiles of 16 rows x kt columns (kt 32 for bf16, 16 for fp32), 1 KiB each; lane l of a tile holds row l%16
+    and 16/elem columns from (l//16)*16/elem.  Unit (g, k) = the ng row tiles of column group g at k-step k;
+    workgroup w of n_wg owns units [w*U//n_wg, (w+1)*U//n_wg) of U = G*KT (u = g*KT + k), and its i-th unit
+    sits at slot i*n_wg + w; tile j of a unit at byte offset + (slot*ng + j)*1024."""
     es = 2 if dtype == "bf16" else 4
     epl = 16 // es
     kt = 4 * epl
-    NT, KT = -(-rows // 16), -(-cols // kt)
+    KT, G, ng, nwg = layout["KT"], layout["G"], layout["ng"], layout["n_wg"]
+    U = G * KT
+    u = np.arange(U, dtype=np.int64)
+    w = np.searchsorted(np.arange(1, nwg + 1, dtype=np.int64) * U // nwg, u, side="right")  # owner of unit u
+    slot = (u - w * U // nwg) * nwg + w
+    raw = buf[layout["offset"]: layout["offset"] + layout["bytes"]]
     if dtype == "bf16":
-        vals = W.bf16_bits_to_f32(buf[: NT * KT * 1024].view(np.uint16))
+        vals = W.bf16_bits_to_f32(raw.view(np.uint16))
     else:
-        vals = buf[: NT * KT * 1024].view(np.float32)
-    a = vals.reshape(KT, NT, 4, 16, epl).transpose(1, 3, 0, 2, 4).reshape(NT * 16, KT * kt)
+        vals = raw.view(np.float32)
+    tiles = vals.reshape(-1, ng, 4, 16, epl)[slot]            # [U = (g, k)][ng][lane group][row][epl]
+    a = tiles.reshape(G, KT, ng, 4, 16, epl).transpose(0, 2, 4, 1, 3, 5).reshape(G * ng * 16, KT * kt)
     return a[:rows, :cols]
 
 

@@ -41,8 +41,33 @@ def test_host_side_argument_errors(S):
     assert L.sdd_rowstats_workspace_bytes(2, 4, 10, C.byref(out)) == S.OK and out.value > 0
     cfg = S.ModelConfig(2, 256, 4, 2, 64, 688, 4096, 1e-6, 1e4, 0, S.F32)
     assert L.sdd_weights_bytes(C.byref(cfg), C.byref(out)) == S.OK
-    # 14.2 MB of fp32 weights for the tiny decoder (plus alignment)
-    assert 14.0e6 < out.value < 14.6e6
+    # 14.2 MB of fp32 weights for the tiny decoder, plus alignment and at most n_wg padding slots (of <= 8 KiB)
+    # per tiled matrix (9 of them)
+    total = out.value
+    assert 14.0e6 < total < 14.6e6 + 9 * 256 * 8192
+    # the tiled matrices' documented layouts (host-only queries on a model over an unused, aligned address)
+    h = C.c_void_p()
+    assert L.sdd_model_create(C.byref(cfg), C.c_void_p(1 << 20), total, C.byref(h)) == S.OK
+    off, nb = C.c_size_t(), C.c_size_t()
+    kt, g, ng, nwg = C.c_int(), C.c_int(), C.c_int(), C.c_int()
+    d, hd, V, dff = 256, 64, 4096, 688
+    spans = []
+    for kind, layer, rows, cols in [(1, 0, V, d)] + [(k, l, r, c) for l in range(2) for k, r, c in
+                                                      ((3, 4 * hd + 2 * 2 * hd, d), (6, d, 4 * hd),
+                                                       (7, 2 * dff, d), (9, d, dff))]:
+        assert L.sdd_model_matrix_layout(h, kind, layer, C.byref(off), C.byref(nb), C.byref(kt), C.byref(g),
+                                         C.byref(ng), C.byref(nwg)) == S.OK
+        U = g.value * kt.value
+        assert g.value * ng.value * 16 >= rows and kt.value * 16 >= cols
+        assert 1 <= nwg.value <= U and nb.value == -(-U // nwg.value) * nwg.value * ng.value * 1024
+        spans.append((off.value, off.value + nb.value))
+    spans.sort()
+    assert all(a1 <= b0 for (_, a1), (b0, _) in zip(spans, spans[1:])) and spans[-1][1] <= total
+    assert L.sdd_model_matrix_layout(h, 2, 0, C.byref(off), C.byref(nb), C.byref(kt), C.byref(g), C.byref(ng),
+                                     C.byref(nwg)) == S.EINVAL
+    assert L.sdd_model_matrix_layout(h, 3, 2, C.byref(off), C.byref(nb), C.byref(kt), C.byref(g), C.byref(ng),
+                                     C.byref(nwg)) == S.EINVAL
+    assert L.sdd_model_destroy(h) == S.OK
     bad = S.ModelConfig(2, 256, 4, 2, 96, 688, 4096, 1e-6, 1e4, 0, S.F32)
     assert L.sdd_weights_bytes(C.byref(bad), C.byref(out)) == S.EUNSUPPORTED
     bad = S.ModelConfig(2, 256, 5, 2, 64, 688, 4096, 1e-6, 1e4, 0, S.F32)
