@@ -39,12 +39,11 @@ int check_launch(const char* what);
 __host__ __device__ inline float bf16_to_f32(uint16_t b) {
   return __builtin_bit_cast(float, (uint32_t)b << 16);
 }
-__host__ __device__ inline uint16_t f32_to_bf16(float f) {
-  uint32_t u = __builtin_bit_cast(uint32_t, f);
-  if ((u & 0x7f800000u) == 0x7f800000u) return (uint16_t)((u >> 16) | ((u & 0xffffu) ? 0x40u : 0u));
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return (uint16_t)(u >> 16);
-}
+// Round to nearest even by the gfx950 conversion instruction (v_cvt_pk_bf16_f32): one branch-free
+// instruction, where a bit-level version needs a divergent branch for NaN and infinity.  Finite values and
+// infinities round exactly as the bit-level definition (add 0x7fff plus the kept lsb, truncate); a NaN
+// stays a quiet NaN.
+__device__ inline uint16_t f32_to_bf16(float f) { return __builtin_bit_cast(uint16_t, (__bf16)f); }
 
 template <typename T> struct Elem;
 template <> struct Elem<float> {
