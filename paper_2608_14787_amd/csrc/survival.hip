@@ -3,16 +3,21 @@
 // the scalar features), normalized as (x - mu) / sigma, then d_in -> H -> H -> H -> 1 with GELU (erf form)
 // after each hidden layer; the output is log sigmoid(z), the log position score the skip scheduler reads.
 //
-// Three launches, every contraction on fp32 MFMA (v_mfma_f32_16x16x4_f32, weights as the A operand so a
-// wave's accumulators hold 16 output columns x 16 positions):
-//   layer1_kernel: (16-column tile, k-split, 64-row tile) per workgroup; the input slice is normalized while
-//                  it is staged into LDS; partial tiles are published with device-coherent 16-byte stores
-//                  and the last arriving split of a tile adds them in split order, adds the bias, applies
-//                  GELU and writes h1.
-//   dense_kernel:  (16-column tile, 64-row tile) per workgroup over K = H, bias + GELU (layers 2 and 3);
-//                  the layer-3 launch also forms each tile's share of w4 . h3, and the last tile of a row
-//                  tile adds the shares in tile order, adds b4 and writes log sigmoid(z).
-// The k-order of every sum is fixed, so results are bit-reproducible.
+// One launch; every contraction on fp32 MFMA (v_mfma_f32_16x16x4_f32, weights as the A operand so a wave's
+// accumulators hold 16 output columns x 16 positions).  The grid holds three sets of workgroups, in id order:
+//   layer 1:    (16-column tile, k-split, 64-row tile) per workgroup; the input slice is normalized while it is
+//               staged into LDS; partial tiles are published with device-coherent 16-byte stores and the last
+//               arriving split of a tile adds them in split order, adds the bias, applies GELU, writes its h1
+//               tile and counts it done for its row tile;
+//   layer 2:    (16-column tile, 64-row tile) per workgroup over K = H, bias + GELU, once every h1 tile of its
+//               row tile is done; counts its h2 tile done;
+//   layer 3(+4): the same from h2, then each tile's share of w4 . h3; the last tile of a row tile adds the
+//               shares in tile order, adds b4 and writes log sigmoid(z).
+// A workgroup of layers 2 and 3 waits for its inputs by polling a counter (bounded; past the bound the scores
+// come out NaN, and stay so).  Workgroups are dispatched in id order, so every workgroup it waits for was
+// dispatched before it: the wait never holds a compute unit that those need.  Hidden activations move
+// through device-coherent stores and loads.  The k-order of every sum is fixed, so results are
+// bit-reproducible.
 #include "sdd_internal.h"
 
 namespace sdd {
@@ -36,6 +41,9 @@ struct MlpArgs {
   float* zpart;     // [rt][ct][64]
   int* cnt1;        // [rt][ct]
   int* cnt3;        // [rt]
+  int* done1;       // [rt]: h1 tiles written
+  int* done2;       // [rt]: h2 tiles written
+  int* err;         // sticky: a wait ran past its bound
   float* log_score;
   float* logit;
 };
@@ -49,12 +57,38 @@ __device__ inline float dot4(const float* h, const float* w) { return ((h[0] * w
 
 __device__ inline f32x4 mfma4(float a, float b, f32x4 c) { return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0); }
 
-__global__ void __launch_bounds__(kMlpThreads) layer1_kernel(MlpArgs a) {
-  __shared__ float sW[16][kKc + 1];
-  __shared__ float sX[kRowTile][kKc + 1];
-  __shared__ int s_last;
+constexpr int kSpinMax = 1 << 17;  // polls of a wait (each after a short sleep): tens of milliseconds
+
+// Thread 0 polls *cnt until it reaches `target` (device-coherent loads), within a bound; true (in every
+// thread) when it did.
+__device__ bool wait_count(const int* cnt, int target, int* s_flag) {
+  if (threadIdx.x == 0) {
+    int ok = 0;
+    for (int it = 0; it < kSpinMax; ++it) {
+      if (__hip_atomic_load(cnt, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >= target) {
+        ok = 1;
+        break;
+      }
+      __builtin_amdgcn_s_sleep(4);
+    }
+    *s_flag = ok;
+  }
+  __syncthreads();
+  return *s_flag != 0;
+}
+
+// Counts one tile done (after this workgroup's coherent stores have completed).
+__device__ void count_done(int* cnt) {
+  wait_stores();
+  __syncthreads();
+  if (threadIdx.x == 0) __hip_atomic_fetch_add(cnt, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__device__ void layer1_body(const MlpArgs& a, int bid, float* smem, int* s_flag) {
+  float (*sW)[kKc + 1] = reinterpret_cast<float (*)[kKc + 1]>(smem);
+  float (*sX)[kKc + 1] = reinterpret_cast<float (*)[kKc + 1]>(smem + 16 * (kKc + 1));
   const int CT = a.H / 16;
-  const int ct = blockIdx.x % CT, s = (blockIdx.x / CT) % a.S, rt = blockIdx.x / (CT * a.S);
+  const int ct = bid % CT, s = (bid / CT) % a.S, rt = bid / (CT * a.S);
   const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
   const int c0 = ct * 16, r0 = rt * kRowTile;
   const int kb = s * a.kc_split, ke = min(a.d_in, kb + a.kc_split);
@@ -97,31 +131,40 @@ __global__ void __launch_bounds__(kMlpThreads) layer1_kernel(MlpArgs a) {
   const int row_l = wave * 16 + lane % 16, col4 = 4 * (lane / 16);
   const int off = (((tile * a.S + s) * kRowTile + row_l) * 16 + col4) * 4;  // bytes (< 2^31: checked on the host)
   __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, acc), prs, off, 0, kCoherentCpol);
-  if (!arrive_last(&a.cnt1[tile], a.S, &s_last)) return;
+  if (!arrive_last(&a.cnt1[tile], a.S, s_flag)) return;
   // last split of this tile: sum the splits in order, bias, GELU
+  // (eight splits' loads in flight at a time, added in split order)
   f32x4 sum = f32x4{0.f, 0.f, 0.f, 0.f};
-  for (int ss = 0; ss < a.S; ++ss) {
-    const int o = (((tile * a.S + ss) * kRowTile + row_l) * 16 + col4) * 4;
-    sum += __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(prs, o, 0, kCoherentCpol));
+  for (int s0 = 0; s0 < a.S; s0 += 8) {
+    f32x4 pv[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      const int ss = min(s0 + q, a.S - 1);
+      pv[q] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                                            prs, (((tile * a.S + ss) * kRowTile + row_l) * 16 + col4) * 4, 0, kCoherentCpol));
+    }
+#pragma unroll
+    for (int q = 0; q < 8; ++q)
+      if (s0 + q < a.S) sum += pv[q];
   }
   const int row = r0 + row_l;
-  if (row < a.n) {
+  f32x4 hv;
 #pragma unroll
-    for (int t = 0; t < 4; ++t) {
-      const int c = c0 + col4 + t;
-      a.h1[(int64_t)row * a.H + c] = gelu_erf(sum[t] + a.b1[c]);
-    }
-  }
+  for (int t = 0; t < 4; ++t) hv[t] = gelu_erf(sum[t] + a.b1[c0 + col4 + t]);
+  const __amdgpu_buffer_rsrc_t hrs = __builtin_amdgcn_make_buffer_rsrc(a.h1, 0, 0x7fffffff, kBufferRsrcWord3);
+  if (row < a.n)
+    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, hv), hrs, (row * a.H + c0 + col4) * 4, 0,
+                                           kCoherentCpol);
+  count_done(&a.done1[rt]);
 }
 
 template <bool LAST>
-__global__ void __launch_bounds__(kMlpThreads) dense_kernel(MlpArgs a, const float* hin, const float* W, const float* b,
-                                                            float* hout) {
-  __shared__ float sW[16][kMaxH + 1];
-  __shared__ float sX[kRowTile][kMaxH + 1];
-  __shared__ int s_last;
+__device__ void dense_body(const MlpArgs& a, int bid, const float* hin, const float* W, const float* b, float* hout,
+                           float* smem, int* s_flag) {
+  float (*sW)[kMaxH + 1] = reinterpret_cast<float (*)[kMaxH + 1]>(smem);
+  float (*sX)[kMaxH + 1] = reinterpret_cast<float (*)[kMaxH + 1]>(smem + 16 * (kMaxH + 1));
   const int CT = a.H / 16;
-  const int ct = blockIdx.x % CT, rt = blockIdx.x / CT;
+  const int ct = bid % CT, rt = bid / CT;
   const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
   const int c0 = ct * 16, r0 = rt * kRowTile, H = a.H;
   // stage the weight slice [16][H] and the input rows [64][H] with 16-byte loads, all issued before use
@@ -133,11 +176,16 @@ __global__ void __launch_bounds__(kMlpThreads) dense_kernel(MlpArgs a, const flo
     const int i = tid + kMlpThreads * u;
     wv[u] = i < 16 * H4 ? *reinterpret_cast<const f32x4*>(W + (int64_t)(c0 + i / H4) * H + 4 * (i % H4)) : f32x4{0.f, 0.f, 0.f, 0.f};
   }
+  // the input rows were written by other workgroups of this launch: device-coherent loads
+  const __amdgpu_buffer_rsrc_t irs = __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(hin), 0, 0x7fffffff,
+                                                                       kBufferRsrcWord3);
 #pragma unroll
   for (int u = 0; u < kMaxH / 4; ++u) {
     const int i = tid + kMlpThreads * u, r = i / H4;
-    xv[u] = (i < kRowTile * H4 && r0 + r < a.n) ? *reinterpret_cast<const f32x4*>(hin + (int64_t)(r0 + r) * H + 4 * (i % H4))
-                                                 : f32x4{0.f, 0.f, 0.f, 0.f};
+    xv[u] = (i < kRowTile * H4 && r0 + r < a.n)
+                ? __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                                                irs, ((r0 + r) * H + 4 * (i % H4)) * 4, 0, kCoherentCpol))
+                : f32x4{0.f, 0.f, 0.f, 0.f};
   }
 #pragma unroll
   for (int u = 0; u < kMaxH / 64; ++u) {
@@ -161,9 +209,11 @@ __global__ void __launch_bounds__(kMlpThreads) dense_kernel(MlpArgs a, const flo
 #pragma unroll
   for (int t = 0; t < 4; ++t) hv[t] = gelu_erf(acc[t] + b[c0 + col4 + t]);
   if constexpr (!LAST) {
+    const __amdgpu_buffer_rsrc_t ors = __builtin_amdgcn_make_buffer_rsrc(hout, 0, 0x7fffffff, kBufferRsrcWord3);
     if (row < a.n)
-#pragma unroll
-      for (int t = 0; t < 4; ++t) hout[(int64_t)row * H + c0 + col4 + t] = hv[t];
+      __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, (f32x4){hv[0], hv[1], hv[2], hv[3]}), ors,
+                                             (row * H + c0 + col4) * 4, 0, kCoherentCpol);
+    count_done(&a.done2[rt]);
   } else {
     // this tile's share of w4 . h3 for the row: the lane's 4 columns in order, then the 4 lane groups in order
     const float zs = dot4(hv, a.w4 + c0 + col4);
@@ -173,21 +223,53 @@ __global__ void __launch_bounds__(kMlpThreads) dense_kernel(MlpArgs a, const flo
     if (lane < 16)
       __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, tz), zrs, ((rt * CT + ct) * kRowTile + row_l) * 4,
                                             0, kCoherentCpol);
-    if (!arrive_last(&a.cnt3[rt], CT, &s_last)) return;
+    if (!arrive_last(&a.cnt3[rt], CT, s_flag)) return;
+    // every wait of this row tile has ended: its counters go back to zero for the next call
+    if (tid == 0) {
+      __hip_atomic_store(&a.done1[rt], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(&a.done2[rt], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    const bool bad = __hip_atomic_load(a.err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0;
     if (tid < kRowTile && r0 + tid < a.n) {
+      // every tile's share loaded at once (CT <= 16), added in tile order
+      float zt[kMaxH / 16];
+#pragma unroll
+      for (int t = 0; t < kMaxH / 16; ++t)
+        zt[t] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
+                                              zrs, ((rt * CT + min(t, CT - 1)) * kRowTile + tid) * 4, 0, kCoherentCpol));
       float z = 0.f;
-      for (int t = 0; t < CT; ++t)
-        z += __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(zrs, ((rt * CT + t) * kRowTile + tid) * 4, 0,
-                                                                            kCoherentCpol));
+#pragma unroll
+      for (int t = 0; t < kMaxH / 16; ++t)
+        if (t < CT) z += zt[t];
       z += a.b4;
+      if (bad) z = __builtin_nanf("");
       a.log_score[r0 + tid] = log_sigmoid(z);
       if (a.logit) a.logit[r0 + tid] = z;
     }
   }
 }
 
+__global__ void __launch_bounds__(kMlpThreads) survival_kernel(MlpArgs a) {
+  __shared__ __attribute__((aligned(16))) float smem[(16 + kRowTile) * (kMaxH + 1)];
+  __shared__ int s_flag;
+  const int CT = a.H / 16, RT = (a.n + kRowTile - 1) / kRowTile;
+  const int n1 = RT * CT * a.S, n2 = RT * CT;
+  const int bid = blockIdx.x;
+  if (bid < n1) {
+    layer1_body(a, bid, smem, &s_flag);
+  } else if (bid < n1 + n2) {
+    const int b2 = bid - n1;
+    if (!wait_count(&a.done1[b2 / CT], CT, &s_flag) && threadIdx.x == 0) atomicOr(a.err, 1);
+    dense_body<false>(a, b2, a.h1, a.W2, a.b2, a.h2, smem, &s_flag);
+  } else {
+    const int b3 = bid - n1 - n2;
+    if (!wait_count(&a.done2[b3 / CT], CT, &s_flag) && threadIdx.x == 0) atomicOr(a.err, 1);
+    dense_body<true>(a, b3, a.h2, a.W3, a.b3, nullptr, smem, &s_flag);
+  }
+}
+
 struct MlpWs {
-  size_t part, h1, h2, zpart, cnt1, cnt3, total;
+  size_t part, h1, h2, zpart, cnt1, cnt3, done, total;
 };
 
 MlpWs mlp_ws(int n, int H, int S) {
@@ -201,6 +283,7 @@ MlpWs mlp_ws(int n, int H, int S) {
   };
   w.cnt1 = take((size_t)RT * CT * sizeof(int));
   w.cnt3 = take((size_t)RT * sizeof(int));
+  w.done = take((size_t)(2 * RT + 1) * sizeof(int));  // done1 [RT], done2 [RT], the sticky error word
   w.part = take((size_t)RT * CT * S * kRowTile * 16 * sizeof(float));
   w.h1 = take((size_t)RT * kRowTile * H * sizeof(float));
   w.h2 = take((size_t)RT * kRowTile * H * sizeof(float));
@@ -279,19 +362,16 @@ extern "C" int sdd_survival_mlp(const sdd_mlp* m, const uint16_t* hidden, const 
   a.zpart = reinterpret_cast<float*>(w + L.zpart);
   a.cnt1 = reinterpret_cast<int*>(w + L.cnt1);
   a.cnt3 = reinterpret_cast<int*>(w + L.cnt3);
+  a.done1 = reinterpret_cast<int*>(w + L.done);
+  a.done2 = a.done1 + RT;
+  a.err = a.done2 + RT;
   a.log_score = log_score;
   a.logit = logit;
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  if ((int64_t)RT * kRowTile * a.H * 4 >= (int64_t(1) << 31))
+    return fail(SDD_EUNSUPPORTED, "%d positions exceed the 32-bit activation offsets", n);
   prof_begin(PROF_MLP, st);
-  hipLaunchKernelGGL(layer1_kernel, dim3(RT * CT * a.S), dim3(kMlpThreads), 0, st, a);
+  hipLaunchKernelGGL(survival_kernel, dim3(RT * CT * (a.S + 2)), dim3(kMlpThreads), 0, st, a);
   prof_end(PROF_MLP, st);
-  if ((rc = check_launch("layer1_kernel"))) return rc;
-  prof_begin(PROF_MLP, st);
-  hipLaunchKernelGGL(dense_kernel<false>, dim3(RT * CT), dim3(kMlpThreads), 0, st, a, a.h1, a.W2, a.b2, a.h2);
-  prof_end(PROF_MLP, st);
-  if ((rc = check_launch("dense_kernel"))) return rc;
-  prof_begin(PROF_MLP, st);
-  hipLaunchKernelGGL(dense_kernel<true>, dim3(RT * CT), dim3(kMlpThreads), 0, st, a, a.h2, a.W3, a.b3, nullptr);
-  prof_end(PROF_MLP, st);
-  return check_launch("dense_kernel");
+  return check_launch("survival_kernel");
 }
