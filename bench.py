@@ -76,6 +76,8 @@ def parse():
                                                                "survival predictor workloads")
     p.add_argument("--drafts", default="greedy", choices=["greedy", "random"])
     p.add_argument("--all-kernels", action="store_true", help="report every kernel class (extra pass)")
+    p.add_argument("--leg", default=None, choices=["batch8", "qwen7b"],
+                   help="only run one next_rows leg on the Qwen3-32B-shaped model (profiling) and print its JSON")
     p.add_argument("--copy-calibration", action="store_true",
                    help="only run a plain 1 GiB device copy: the reference kernel whose rocprofv3 FETCH_SIZE / "
                         "WRITE_SIZE readings scale the verify kernels' counters to bytes")
@@ -400,6 +402,9 @@ def main():
         print(json.dumps({"copy_bytes_read": n, "copy_bytes_written": n, "launches": 3}))
         return
 
+    if a.leg == "qwen7b":
+        print(json.dumps({"qwen7b_verify": qwen7b_leg(sdd, torch)}), flush=True)
+        return
     shape, P, gamma = SHAPES[a.workload]
     V = shape.vocab
     rounds = a.warmup + a.steps
@@ -409,6 +414,9 @@ def main():
     model.init_random(W.WEIGHT_SEED, W.WEIGHT_SIGMA)
     torch.cuda.synchronize()
     log(f"weights {model.weight_bytes / 1e9:.2f} GB generated in {time.perf_counter() - t0:.2f} s")
+    if a.leg == "batch8":
+        print(json.dumps({"batch8": batch8(sdd, torch, model, shape, gamma)}), flush=True)
+        return
 
     # committed tokens per round average about 5 at a 20% replacement rate; past the end of the
     # continuation, drafts repeat its last token and are rejected
