@@ -245,57 +245,76 @@ __device__ void epilogue_qkv(const GemmArgs& a, const float* tile, int g, const 
   }
 }
 
+// Sum over the n lanes of each aligned group of n (n in 1, 2, 4, 8, 16) by DPP row permutations, the same
+// butterfly in every lane (the wave must be fully active).
+template <int N>
+__device__ inline float group_sum(float v) {
+  if constexpr (N >= 2) v += dpp_f<kDppXor1>(v);
+  if constexpr (N >= 4) v += dpp_f<kDppXor2>(v);
+  if constexpr (N >= 8) v += dpp_f<kDppHalfMirror>(v);
+  if constexpr (N >= 16) v += dpp_f<kDppMirror>(v);
+  return v;
+}
+
+// Residual epilogue, 8 consecutive columns per lane: LPR = C / 8 lanes hold a row (16-byte loads and
+// stores), RPI = 64 / LPR rows per pass; a row's sum of squares adds the lane's 8 squares in column order,
+// then the LPR lanes by a fixed butterfly.
 template <typename T, int NG, int R>
 __device__ void epilogue_resid(const GemmArgs& a, const float* tile, int g) {
   // no contraction: every instantiation (row count) must round each row alike
 #pragma clang fp contract(off)
-  constexpr int C = NG * 16, CP = C + 4, RPW = R / 4, NCL = (C + kWave - 1) / kWave;
+  constexpr int C = NG * 16, CP = C + 4, RPW = R / 4;
+  constexpr int LPR = C / 8, RPI = kWave / LPR, NIT = (RPW + RPI - 1) / RPI;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave), lane = threadIdx.x % kWave;
-  float gv[NCL], xv[RPW][NCL], ss[RPW];
+  const int rsub = lane / LPR, c0 = 8 * (lane % LPR);
+  const int64_t n0 = (int64_t)g * C + c0;
+  const f32x4 gv0 = *reinterpret_cast<const f32x4*>(a.g_next + n0), gv1 = *reinterpret_cast<const f32x4*>(a.g_next + n0 + 4);
+  // every pass's residual loads first (padded rows read row 0)
+  f32x4 xa0[NIT], xa1[NIT];
 #pragma unroll
-  for (int k = 0; k < NCL; ++k) {
-    const int c = lane + k * kWave;
-    gv[k] = c < C ? a.g_next[(int64_t)g * C + c] : 0.f;
+  for (int it = 0; it < NIT; ++it) {
+    const int j = it * RPI + rsub, mm = wave + 4 * j;
+    const int mc = (j < RPW && mm < a.M) ? mm : 0;
+    const float* xr = a.x + (int64_t)(a.m0 + mc) * a.d + n0;
+    xa0[it] = *reinterpret_cast<const f32x4*>(xr);
+    xa1[it] = *reinterpret_cast<const f32x4*>(xr + 4);
   }
-  // unconditional loads (padded rows read row 0, columns past C the group's last), all in flight together
 #pragma unroll
-  for (int j = 0; j < RPW; ++j) {
-    const int mm = wave + 4 * j;
+  for (int it = 0; it < NIT; ++it) {
+    const int j = it * RPI + rsub, mm = wave + 4 * j;
+    const int mt = wave + 4 * min(j, RPW - 1);  // tile row (a valid one for the last pass's spare lanes)
+    const f32x4 t0 = *reinterpret_cast<const f32x4*>(&tile[mt * CP + c0]);
+    const f32x4 t1 = *reinterpret_cast<const f32x4*>(&tile[mt * CP + c0 + 4]);
+    float xv[8];
 #pragma unroll
-    for (int k = 0; k < NCL; ++k) {
-      const int c = min(lane + k * kWave, C - 1);
-      xv[j][k] = a.x[(int64_t)(a.m0 + (mm < a.M ? mm : 0)) * a.d + (int64_t)g * C + c];
+    for (int e = 0; e < 4; ++e) {
+      xv[e] = xa0[it][e] + t0[e];
+      xv[4 + e] = xa1[it][e] + t1[e];
     }
-  }
+    float ss = 0.f;
 #pragma unroll
-  for (int j = 0; j < RPW; ++j) {
-    const int mm = wave + 4 * j;
-    ss[j] = 0.f;
-#pragma unroll
-    for (int k = 0; k < NCL; ++k) {
-      const int c = lane + k * kWave;
-      if (c < C) {
-        xv[j][k] += tile[mm * CP + c];
-        ss[j] += xv[j][k] * xv[j][k];
-      }
-    }
-  }
-  wave_sum_fast_n(ss);
-#pragma unroll
-  for (int j = 0; j < RPW; ++j) {
-    const int mm = wave + 4 * j;
-    if (mm < a.M) {
+    for (int e = 0; e < 8; ++e) ss += xv[e] * xv[e];
+    ss = group_sum<LPR>(ss);
+    if (j < RPW && mm < a.M) {
       const int m = a.m0 + mm;
+      float* xr = a.x + (int64_t)m * a.d + n0;
+      *reinterpret_cast<f32x4*>(xr) = f32x4{xv[0], xv[1], xv[2], xv[3]};
+      *reinterpret_cast<f32x4*>(xr + 4) = f32x4{xv[4], xv[5], xv[6], xv[7]};
+      float y[8];
 #pragma unroll
-      for (int k = 0; k < NCL; ++k) {
-        const int c = lane + k * kWave;
-        if (c < C) {
-          const int64_t n = (int64_t)g * C + c;
-          a.x[(int64_t)m * a.d + n] = xv[j][k];
-          store_t<T>(a.xa, (int64_t)m * a.d + n, xv[j][k] * gv[k]);
-        }
+      for (int e = 0; e < 4; ++e) {
+        y[e] = xv[e] * gv0[e];
+        y[4 + e] = xv[4 + e] * gv1[e];
       }
-      if (lane == 0) a.ss_part[(int64_t)g * a.mp + m] = ss[j];
+      if constexpr (sizeof(T) == 2) {
+        *reinterpret_cast<uint4*>(reinterpret_cast<uint16_t*>(a.xa) + (int64_t)m * a.d + n0) =
+            make_uint4(pack_bf16x2(y[0], y[1]), pack_bf16x2(y[2], y[3]), pack_bf16x2(y[4], y[5]), pack_bf16x2(y[6], y[7]));
+      } else {
+        float* ar = reinterpret_cast<float*>(a.xa) + (int64_t)m * a.d + n0;
+        *reinterpret_cast<f32x4*>(ar) = f32x4{y[0], y[1], y[2], y[3]};
+        *reinterpret_cast<f32x4*>(ar + 4) = f32x4{y[4], y[5], y[6], y[7]};
+      }
+      if (lane % LPR == 0) a.ss_part[(int64_t)g * a.mp + m] = ss;
     }
   }
 }

@@ -15,6 +15,8 @@ namespace sdd {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef float float2v __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
 constexpr int kWave = 64;
 
@@ -44,6 +46,10 @@ __host__ __device__ inline float bf16_to_f32(uint16_t b) {
 // infinities round exactly as the bit-level definition (add 0x7fff plus the kept lsb, truncate); a NaN
 // stays a quiet NaN.
 __device__ inline uint16_t f32_to_bf16(float f) { return __builtin_bit_cast(uint16_t, (__bf16)f); }
+// two values in one instruction: a in the low half, b in the high half
+__device__ inline uint32_t pack_bf16x2(float a, float b) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((float2v){a, b}, bf16x2));
+}
 
 template <typename T> struct Elem;
 template <> struct Elem<float> {
