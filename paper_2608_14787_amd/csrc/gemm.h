@@ -319,37 +319,45 @@ __device__ void epilogue_resid(const GemmArgs& a, const float* tile, int g) {
   }
 }
 
+// SwiGLU epilogue: the group's C columns are P = NG / 2 pairs of 16 gate and 16 up columns, i.e. P * 16
+// hidden outputs per row; a lane computes 8 consecutive ones (LPR = NG lanes per row, RPI = 64 / LPR rows
+// per pass) and stores them with one 16-byte store.
 template <typename T, int NG, int R>
 __device__ void epilogue_swiglu(const GemmArgs& a, const float* tile, int g, const float* rsl) {
   // no contraction: every instantiation (row count) must round each row alike
 #pragma clang fp contract(off)
   constexpr int C = NG * 16, CP = C + 4, P = NG / 2, RPW = R / 4;
-  constexpr int NI = (P * 16 + kWave - 1) / kWave;  // gate/up pairs per lane and row
+  constexpr int LPR = P * 2, RPI = kWave / LPR, NIT = (RPW + RPI - 1) / RPI;
+  static_assert(NG % 2 == 0, "gate/up groups hold whole pairs");
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave), lane = threadIdx.x % kWave;
-  // every row of the padded tile is computed (straight-line code, LDS reads batched); only real rows are stored
-  float hv[RPW][NI];
+  const int rsub = lane / LPR, h0 = 8 * (lane % LPR);      // first hidden column of the lane
+  const int cg = (h0 / 16) * 32 + h0 % 16, cu = cg + 16;  // its gate and up tile columns
 #pragma unroll
-  for (int j = 0; j < RPW; ++j) {
-    const int mm = wave + 4 * j;
-    const float r = rsl[mm];
+  for (int it = 0; it < NIT; ++it) {
+    const int j = it * RPI + rsub, mm = wave + 4 * j;
+    const int mt = wave + 4 * min(j, RPW - 1);
+    const float r = rsl[mt];
+    const f32x4 g0 = *reinterpret_cast<const f32x4*>(&tile[mt * CP + cg]);
+    const f32x4 g1 = *reinterpret_cast<const f32x4*>(&tile[mt * CP + cg + 4]);
+    const f32x4 u0 = *reinterpret_cast<const f32x4*>(&tile[mt * CP + cu]);
+    const f32x4 u1 = *reinterpret_cast<const f32x4*>(&tile[mt * CP + cu + 4]);
+    float hv[8];
 #pragma unroll
-    for (int i = 0; i < NI; ++i) {
-      const int idx = min(lane + i * kWave, P * 16 - 1);
-      const int t = idx / 16, jj = idx % 16;
-      const float gt = tile[mm * CP + (2 * t) * 16 + jj] * r;
-      const float up = tile[mm * CP + (2 * t + 1) * 16 + jj] * r;
-      hv[j][i] = gt / (1.f + expf(-gt)) * up;
+    for (int e = 0; e < 8; ++e) {
+      const float gt = (e < 4 ? g0[e] : g1[e - 4]) * r;
+      const float up = (e < 4 ? u0[e] : u1[e - 4]) * r;
+      hv[e] = gt / (1.f + expf(-gt)) * up;
     }
-  }
-#pragma unroll
-  for (int j = 0; j < RPW; ++j) {
-    const int mm = wave + 4 * j;
-    if (mm < a.M) {
-      const int64_t row = (int64_t)(a.m0 + mm) * a.dff + (int64_t)g * P * 16;
-#pragma unroll
-      for (int i = 0; i < NI; ++i) {
-        const int idx = lane + i * kWave;
-        if (idx < P * 16) store_t<T>(a.ffh, row + idx, hv[j][i]);
+    if (j < RPW && mm < a.M) {
+      const int64_t off = (int64_t)(a.m0 + mm) * a.dff + (int64_t)g * P * 16 + h0;
+      if constexpr (sizeof(T) == 2) {
+        *reinterpret_cast<uint4*>(reinterpret_cast<uint16_t*>(a.ffh) + off) =
+            make_uint4(pack_bf16x2(hv[0], hv[1]), pack_bf16x2(hv[2], hv[3]), pack_bf16x2(hv[4], hv[5]),
+                       pack_bf16x2(hv[6], hv[7]));
+      } else {
+        float* hr = reinterpret_cast<float*>(a.ffh) + off;
+        *reinterpret_cast<f32x4*>(hr) = f32x4{hv[0], hv[1], hv[2], hv[3]};
+        *reinterpret_cast<f32x4*>(hr + 4) = f32x4{hv[4], hv[5], hv[6], hv[7]};
       }
     }
   }
@@ -361,119 +369,93 @@ __device__ inline bool arg_better(float v2, int i2, float v1, int i1) {
   return v2 > v1 || (v2 == v1 && i2 < i1);
 }
 
-// Best (value, lowest index) over a fully active wave.  The combine is
-// associative and commutative, so the order of the steps does not matter.
-__device__ inline void wave_argmax(float& bv, int& bi) {
-  auto step = [&](float v2, int i2) {
+// Best (value, lowest index) over the n lanes of each aligned group of n (n in 1, 2, 4, 8, 16), left in
+// every lane of the group; the combine is associative and commutative, so the butterfly's order is free.
+template <int N>
+__device__ inline void group_argmax(float& bv, int& bi) {
+  auto step = [&](auto ctrl) {
+    constexpr int CTRL = decltype(ctrl)::value;
+    const float v2 = dpp_f<CTRL>(bv);
+    const int i2 = dpp_i<CTRL>(bi);
     if (arg_better(v2, i2, bv, bi)) {
       bv = v2;
       bi = i2;
     }
   };
-  step(dpp_f<kDppXor1>(bv), dpp_i<kDppXor1>(bi));
-  step(dpp_f<kDppXor2>(bv), dpp_i<kDppXor2>(bi));
-  step(dpp_f<kDppHalfMirror>(bv), dpp_i<kDppHalfMirror>(bi));
-  step(dpp_f<kDppMirror>(bv), dpp_i<kDppMirror>(bi));
-  float rv = lane_f(bv, 0);
-  int ri = __builtin_amdgcn_readlane(bi, 0);
-#pragma unroll
-  for (int r = 16; r < 64; r += 16) {
-    const float v2 = lane_f(bv, r);
-    const int i2 = __builtin_amdgcn_readlane(bi, r);
-    if (arg_better(v2, i2, rv, ri)) {
-      rv = v2;
-      ri = i2;
-    }
-  }
-  bv = rv;
-  bi = ri;
+  if constexpr (N >= 2) step(std::integral_constant<int, kDppXor1>{});
+  if constexpr (N >= 4) step(std::integral_constant<int, kDppXor2>{});
+  if constexpr (N >= 8) step(std::integral_constant<int, kDppHalfMirror>{});
+  if constexpr (N >= 16) step(std::integral_constant<int, kDppMirror>{});
 }
 
-// wave_argmax of N independent (value, index) pairs at once
-template <int N>
-__device__ inline void wave_argmax_n(float (&bv)[N], int (&bi)[N]) {
-  auto step = [&](auto ctrl) {
-    constexpr int CTRL = decltype(ctrl)::value;
-#pragma unroll
-    for (int j = 0; j < N; ++j) {
-      const float v2 = dpp_f<CTRL>(bv[j]);
-      const int i2 = dpp_i<CTRL>(bi[j]);
-      if (arg_better(v2, i2, bv[j], bi[j])) {
-        bv[j] = v2;
-        bi[j] = i2;
-      }
-    }
-  };
-  step(std::integral_constant<int, kDppXor1>{});
-  step(std::integral_constant<int, kDppXor2>{});
-  step(std::integral_constant<int, kDppHalfMirror>{});
-  step(std::integral_constant<int, kDppMirror>{});
-#pragma unroll
-  for (int j = 0; j < N; ++j) {
-    float rv = lane_f(bv[j], 0);
-    int ri = __builtin_amdgcn_readlane(bi[j], 0);
-#pragma unroll
-    for (int r = 16; r < 64; r += 16) {
-      const float v2 = lane_f(bv[j], r);
-      const int i2 = __builtin_amdgcn_readlane(bi[j], r);
-      if (arg_better(v2, i2, rv, ri)) {
-        rv = v2;
-        ri = i2;
-      }
-    }
-    bv[j] = rv;
-    bi[j] = ri;
-  }
-}
-
+// LM-head epilogue: fp32 logits of the valid rows and each row's best (value, index) over the group's
+// columns below V.  A lane takes 8 consecutive columns (LPR = C / 8 lanes per row, RPI = 64 / LPR rows per
+// pass): 16-byte stores where V keeps rows 16-byte aligned and the 8 columns are all below V.
 template <int NG, int R>
 __device__ void epilogue_logits(const GemmArgs& a, const float* tile, int g, const float* rsl, const RowInfo* ri_s) {
   // no contraction: every instantiation (row count) must round each row alike
 #pragma clang fp contract(off)
-  constexpr int C = NG * 16, CP = C + 4, RPW = R / 4, NCL = (C + kWave - 1) / kWave;
+  constexpr int C = NG * 16, CP = C + 4, RPW = R / 4;
+  constexpr int LPR = C / 8, RPI = kWave / LPR, NIT = (RPW + RPI - 1) / RPI;
+  static_assert(LPR <= 16, "a row's lanes must lie in one DPP row");
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave), lane = threadIdx.x % kWave;
-  float v[RPW][NCL], bv[RPW];
-  int bi[RPW];
+  const int rsub = lane / LPR, c0 = 8 * (lane % LPR), n0 = g * C + c0;
+  const bool vec = (a.V & 3) == 0 && n0 + 8 <= a.V;
+  float bv[NIT];
+  int bi[NIT];
 #pragma unroll
-  for (int j = 0; j < RPW; ++j) {
-    const int mm = wave + 4 * j;
-    const float r = rsl[mm < a.M ? mm : 0];
-    bv[j] = -INFINITY;
-    bi[j] = -1;
+  for (int it = 0; it < NIT; ++it) {
+    const int j = it * RPI + rsub, mm = wave + 4 * j;
+    const int mt = wave + 4 * min(j, RPW - 1);
+    const float r = rsl[mt < a.M ? mt : 0];
+    const f32x4 t0 = *reinterpret_cast<const f32x4*>(&tile[mt * CP + c0]);
+    const f32x4 t1 = *reinterpret_cast<const f32x4*>(&tile[mt * CP + c0 + 4]);
+    float v[8];
 #pragma unroll
-    for (int k = 0; k < NCL; ++k) {
-      const int c = lane + k * kWave, n = g * C + c;
-      v[j][k] = c < C ? tile[mm * CP + c] * r : 0.f;
-      if (c < C && n < a.V && arg_better(v[j][k], n, bv[j], bi[j])) {
-        bv[j] = v[j][k];
-        bi[j] = n;
+    for (int e = 0; e < 4; ++e) {
+      v[e] = t0[e] * r;
+      v[4 + e] = t1[e] * r;
+    }
+    bv[it] = -INFINITY;
+    bi[it] = -1;
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+      if (n0 + e < a.V && arg_better(v[e], n0 + e, bv[it], bi[it])) {
+        bv[it] = v[e];
+        bi[it] = n0 + e;
+      }
+    if (j < RPW && mm < a.M && ri_s[mm].valid) {
+      float* lr = a.logits + (int64_t)(a.m0 + mm) * a.V + n0;
+      if (vec) {
+        *reinterpret_cast<f32x4*>(lr) = f32x4{v[0], v[1], v[2], v[3]};
+        *reinterpret_cast<f32x4*>(lr + 4) = f32x4{v[4], v[5], v[6], v[7]};
+      } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          if (n0 + e < a.V) lr[e] = v[e];
       }
     }
+    group_argmax<LPR>(bv[it], bi[it]);
   }
-#pragma unroll
-  for (int j = 0; j < RPW; ++j) {
-    const int mm = wave + 4 * j;
-    if (mm < a.M && ri_s[mm].valid) {
-      const int64_t row = (int64_t)(a.m0 + mm) * a.V;
-#pragma unroll
-      for (int k = 0; k < NCL; ++k) {
-        const int c = lane + k * kWave, n = g * C + c;
-        if (c < C && n < a.V) a.logits[row + n] = v[j][k];
-      }
-    }
-  }
-  wave_argmax_n(bv, bi);
   // one lane per row, so the rows' candidates take two store instructions, not
   // two per row: with the next segment's loads in flight, a wave's outstanding
   // memory operations would otherwise exceed the 63 the counter holds, and
   // issue would stall until those loads land
-  float av = bv[0];
-  int ai = bi[0];
+  float av = 0.f;
+  int ai = -1;
 #pragma unroll
-  for (int j = 1; j < RPW; ++j)
-    if (lane == j) {
-      av = bv[j];
-      ai = bi[j];
+  for (int it = 0; it < NIT; ++it)
+#pragma unroll
+    for (int q = 0; q < RPI; ++q) {
+      const int j = it * RPI + q;
+      if (j < RPW) {
+        const float v2 = lane_f(bv[it], q * LPR);
+        const int i2 = __builtin_amdgcn_readlane(bi[it], q * LPR);
+        if (lane == j) {
+          av = v2;
+          ai = i2;
+        }
+      }
     }
   const int mm = wave + 4 * lane;
   if (lane < RPW && mm < a.M) {
