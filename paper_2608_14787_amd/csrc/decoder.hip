@@ -278,6 +278,19 @@ __global__ void __launch_bounds__(kGemmThreads, 1) gemm_kernel(GemmArgs a) {
     const int which = g == g_first ? 0 : 1;
     u += s.ke - s.kb;
     const bool more = u < u1;
+    // Epilogues that read nothing from global memory: the next segment's first
+    // three stages go out now, so that they stream while this segment is
+    // reduced, published and (by its last arriver) finished.  Every older load
+    // has landed (the segment's stages were consumed; the clamped reloads past
+    // its end touch no memory): waiting for them first, on every path, tells
+    // the compiler so.  Otherwise a register that one of them last wrote makes
+    // it wait for every load, the next segment's too, before it is reused.
+    Seg sn = s;
+    if constexpr (kEarly) __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+    if (more) {
+      sn = make_seg(u);
+      if constexpr (kEarly) issue(sn);
+    }
 
     // ---- sum the four waves, (w0 + w2) + (w1 + w3) per element ----
     __syncthreads();  // the previous tile's readers are done
@@ -358,17 +371,6 @@ __global__ void __launch_bounds__(kGemmThreads, 1) gemm_kernel(GemmArgs a) {
       }
     }
 
-    // Every older load has landed by now (the stream's clamped reloads, the
-    // fix-up's partials); waiting for them here, on every path and before the
-    // next segment's loads, tells the compiler so.  Otherwise an epilogue
-    // register that one of them last wrote makes it wait for every load, the
-    // next segment's too.
-    if constexpr (kEarly) __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
-    Seg sn = s;
-    if (more) {
-      sn = make_seg(u);
-      if constexpr (kEarly) issue(sn);
-    }
     // A workgroup whose last segment only contributed a partial is done; it
     // loads the next GEMM's first k-steps into L2 while the group's last
     // arriver reduces and runs the epilogue.
