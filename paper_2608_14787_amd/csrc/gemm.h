@@ -147,8 +147,41 @@ __device__ inline void prefetch_next(const GemmArgs& a, int wave, int lane) {
 // off here, so that the compiler cannot fuse a row's operations differently in
 // instantiations for different row counts).  Every global load a wave needs is
 // issued before any of them is used.
+// Global inputs of the Q / K epilogue of column group g (head g): the QK-norm
+// gains of the lane's dimensions and each of the wave's rows' RoPE (cos, sin)
+// (table [pos][C/2] of float2).  Loaded ahead of the epilogue, so that their
+// latency hides behind the group's cross-workgroup reduction.
+template <int NG, int R>
+struct QkvPre {
+  float2 cs[R / 4];
+  float gn0, gn1;
+};
+template <int NG, int R>
+__device__ inline void qkv_pre_load(const GemmArgs& a, int g, const RowInfo* ri_s, QkvPre<NG, R>& p) {
+  constexpr int C = NG * 16, RPW = R / 4;
+  if constexpr (C == 64 || C == 128) {
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave), lane = threadIdx.x % kWave;
+    const bool is_q = g < a.hq;
+    p.gn0 = 1.f;
+    p.gn1 = 1.f;
+    if (g >= a.hq + a.hkv) return;  // V head: no inputs
+    if (a.qk_norm) {
+      const float* gp = is_q ? a.qn : a.kn;
+      p.gn0 = gp[lane];
+      if constexpr (C == 128) p.gn1 = gp[lane + 64];
+    }
+#pragma unroll
+    for (int j = 0; j < RPW; ++j) {
+      const int mm = wave + 4 * j;
+      const RowInfo ri = ri_s[mm < a.M ? mm : 0];
+      p.cs[j] = reinterpret_cast<const float2*>(a.rope)[(size_t)(ri.valid ? ri.pos : 0) * (C / 2) + (C == 128 ? lane : lane % 32)];
+    }
+  }
+}
+
 template <typename T, int NG, int R>
-__device__ void epilogue_qkv(const GemmArgs& a, const float* tile, int g, const float* rsl, const RowInfo* ri_s) {
+__device__ void epilogue_qkv(const GemmArgs& a, const float* tile, int g, const float* rsl, const RowInfo* ri_s,
+                             const QkvPre<NG, R>* pre = nullptr) {
   // no contraction: every instantiation (row count) must round each row alike
 #pragma clang fp contract(off)
   constexpr int C = NG * 16;  // == head_dim
@@ -179,21 +212,16 @@ __device__ void epilogue_qkv(const GemmArgs& a, const float* tile, int g, const 
       }
       return;
     }
-    float gn0 = 1.f, gn1 = 1.f;
-    if (a.qk_norm) {
-      const float* gp = is_q ? a.qn : a.kn;
-      gn0 = gp[lane];
-      if constexpr (C == 128) gn1 = gp[lane + 64];
-    }
-    // (cos, sin) of each row's position: table [pos][C/2] of float2
-    float2 cs[RPW];
+    QkvPre<NG, R> pl;
+    if (!pre) qkv_pre_load<NG, R>(a, g, ri_s, pl);
+    const QkvPre<NG, R>& pp = pre ? *pre : pl;
+    const float gn0 = pp.gn0, gn1 = pp.gn1;
+    const float2* cs = pp.cs;  // (cos, sin) of each row's position
     float y0[RPW], y1[RPW];
 #pragma unroll
     for (int j = 0; j < RPW; ++j) {
       const int mm = wave + 4 * j;
       const int mc = mm < a.M ? mm : 0;
-      const RowInfo ri = ri_s[mc];
-      cs[j] = reinterpret_cast<const float2*>(a.rope)[(size_t)(ri.valid ? ri.pos : 0) * (C / 2) + (C == 128 ? lane : lane % 32)];
       const float r = rsl[mc];
       y0[j] = tile[mm * CP + lane] * r;
       y1[j] = C == 128 ? tile[mm * CP + (lane + 64) % C] * r : 0.f;
