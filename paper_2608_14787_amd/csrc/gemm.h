@@ -147,34 +147,56 @@ __device__ inline void prefetch_next(const GemmArgs& a, int wave, int lane) {
 // off here, so that the compiler cannot fuse a row's operations differently in
 // instantiations for different row counts).  Every global load a wave needs is
 // issued before any of them is used.
+// Sum over the n lanes of each aligned group of n (n in 1, 2, 4, 8, 16) by DPP row permutations, the same
+// butterfly in every lane (the wave must be fully active).
+template <int N>
+__device__ inline float group_sum(float v) {
+  if constexpr (N >= 2) v += dpp_f<kDppXor1>(v);
+  if constexpr (N >= 4) v += dpp_f<kDppXor2>(v);
+  if constexpr (N >= 8) v += dpp_f<kDppHalfMirror>(v);
+  if constexpr (N >= 16) v += dpp_f<kDppMirror>(v);
+  return v;
+}
+
+// The Q / K epilogue works on 8 consecutive dimensions per lane: LPR = C / 8
+// lanes hold a row, RPI = 64 / LPR rows per pass, NIT passes over the wave's
+// R / 4 rows (row wave + 4 j, j = it * RPI + lane / LPR).
+template <int NG, int R>
+struct QkvShape {
+  static constexpr int C = NG * 16, RPW = R / 4, LPR = C / 8, RPI = kWave / LPR, NIT = (RPW + RPI - 1) / RPI;
+};
 // Global inputs of the Q / K epilogue of column group g (head g): the QK-norm
-// gains of the lane's dimensions and each of the wave's rows' RoPE (cos, sin)
-// (table [pos][C/2] of float2).  Loaded ahead of the epilogue, so that their
-// latency hides behind the group's cross-workgroup reduction.
+// gains of the lane's 8 dimensions and, for each pass, the RoPE (cos, sin) of
+// those dimensions at its row's position (table [pos][C/2] of float2; dimension
+// d uses entry d mod C/2).  Loaded ahead of the epilogue, so that their latency
+// hides behind the group's cross-workgroup reduction.
 template <int NG, int R>
 struct QkvPre {
-  float2 cs[R / 4];
-  float gn0, gn1;
+  f32x4 gn[2];
+  f32x4 cs[QkvShape<NG, R>::NIT][4];  // (cos, sin) pairs of dimensions d0 .. d0 + 7
 };
 template <int NG, int R>
 __device__ inline void qkv_pre_load(const GemmArgs& a, int g, const RowInfo* ri_s, QkvPre<NG, R>& p) {
-  constexpr int C = NG * 16, RPW = R / 4;
+  using S = QkvShape<NG, R>;
+  constexpr int C = S::C;
   if constexpr (C == 64 || C == 128) {
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave), lane = threadIdx.x % kWave;
+    const int rsub = lane / S::LPR, d0 = 8 * (lane % S::LPR);
     const bool is_q = g < a.hq;
-    p.gn0 = 1.f;
-    p.gn1 = 1.f;
+    p.gn[0] = p.gn[1] = f32x4{1.f, 1.f, 1.f, 1.f};
     if (g >= a.hq + a.hkv) return;  // V head: no inputs
     if (a.qk_norm) {
-      const float* gp = is_q ? a.qn : a.kn;
-      p.gn0 = gp[lane];
-      if constexpr (C == 128) p.gn1 = gp[lane + 64];
+      const float* gp = (is_q ? a.qn : a.kn) + d0;
+      p.gn[0] = *reinterpret_cast<const f32x4*>(gp);
+      p.gn[1] = *reinterpret_cast<const f32x4*>(gp + 4);
     }
 #pragma unroll
-    for (int j = 0; j < RPW; ++j) {
-      const int mm = wave + 4 * j;
+    for (int it = 0; it < S::NIT; ++it) {
+      const int mm = wave + 4 * min(it * S::RPI + rsub, S::RPW - 1);
       const RowInfo ri = ri_s[mm < a.M ? mm : 0];
-      p.cs[j] = reinterpret_cast<const float2*>(a.rope)[(size_t)(ri.valid ? ri.pos : 0) * (C / 2) + (C == 128 ? lane : lane % 32)];
+      const f32x4* t = reinterpret_cast<const f32x4*>(a.rope + ((size_t)(ri.valid ? ri.pos : 0) * (C / 2) + d0 % (C / 2)) * 2);
+#pragma unroll
+      for (int k = 0; k < 4; ++k) p.cs[it][k] = t[k];
     }
   }
 }
@@ -212,77 +234,76 @@ __device__ void epilogue_qkv(const GemmArgs& a, const float* tile, int g, const 
       }
       return;
     }
+    using S = QkvShape<NG, R>;
     QkvPre<NG, R> pl;
     if (!pre) qkv_pre_load<NG, R>(a, g, ri_s, pl);
     const QkvPre<NG, R>& pp = pre ? *pre : pl;
-    const float gn0 = pp.gn0, gn1 = pp.gn1;
-    const float2* cs = pp.cs;  // (cos, sin) of each row's position
-    float y0[RPW], y1[RPW];
+    const int rsub = lane / S::LPR, d0 = 8 * (lane % S::LPR);
+    const bool lo = d0 < C / 2;  // the rotation pairs dimension d with d + C/2
 #pragma unroll
-    for (int j = 0; j < RPW; ++j) {
-      const int mm = wave + 4 * j;
-      const int mc = mm < a.M ? mm : 0;
-      const float r = rsl[mc];
-      y0[j] = tile[mm * CP + lane] * r;
-      y1[j] = C == 128 ? tile[mm * CP + (lane + 64) % C] * r : 0.f;
-    }
-    if (a.qk_norm) {
-      float ss[RPW];
+    for (int it = 0; it < S::NIT; ++it) {
+      const int j = it * S::RPI + rsub, mm = wave + 4 * j;
+      const int mt = wave + 4 * min(j, RPW - 1);  // tile row (a valid one for the last pass's spare lanes)
+      const float r = rsl[mt < a.M ? mt : 0];
+      const f32x4 t0 = *reinterpret_cast<const f32x4*>(&tile[mt * CP + d0]);
+      const f32x4 t1 = *reinterpret_cast<const f32x4*>(&tile[mt * CP + d0 + 4]);
+      float y[8];
 #pragma unroll
-      for (int j = 0; j < RPW; ++j) ss[j] = (C == 128) ? y0[j] * y0[j] + y1[j] * y1[j] : y0[j] * y0[j];
-      wave_sum_fast_n(ss);
-#pragma unroll
-      for (int j = 0; j < RPW; ++j) {
-        const float inv = 1.f / sqrtf(ss[j] / (float)C + a.eps);
-        y0[j] *= inv * gn0;
-        if constexpr (C == 128) y1[j] *= inv * gn1;
+      for (int e = 0; e < 4; ++e) {
+        y[e] = t0[e] * r;
+        y[4 + e] = t1[e] * r;
       }
-    }
+      if (a.qk_norm) {
+        float ss = 0.f;
 #pragma unroll
-    for (int j = 0; j < RPW; ++j) {
-      const float c = cs[j].x, sn = cs[j].y;
-      if constexpr (C == 128) {
-        const float t0 = y0[j], t1 = y1[j];
-        y0[j] = t0 * c - t1 * sn;
-        y1[j] = t1 * c + t0 * sn;
-      } else {
-        const float other = __shfl_xor(y0[j], 32);
-        y0[j] = lane < 32 ? y0[j] * c - other * sn : y0[j] * c + other * sn;
+        for (int e = 0; e < 8; ++e) ss += y[e] * y[e];
+        ss = group_sum<S::LPR>(ss);
+        const float inv = 1.f / sqrtf(ss / (float)C + a.eps);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) y[e] *= inv * (e < 4 ? pp.gn[0][e] : pp.gn[1][e - 4]);
       }
-    }
+      // the partner dimensions (d +- C/2) sit LPR / 2 lanes away in the row's lane group
+      float o[8];
 #pragma unroll
-    for (int j = 0; j < RPW; ++j) {
-      const int mm = wave + 4 * j;
-      if (mm < a.M && ri_s[mm].valid) {
+      for (int e = 0; e < 8; ++e) {
+        if constexpr (C == 128)
+          o[e] = dpp_f<kDppRor8>(y[e]);
+        else
+          o[e] = __shfl_xor(y[e], S::LPR / 2);
+      }
+      float z[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float c = pp.cs[it][e / 2][2 * (e % 2)], sn = pp.cs[it][e / 2][2 * (e % 2) + 1];
+        z[e] = lo ? y[e] * c - o[e] * sn : y[e] * c + o[e] * sn;
+      }
+      if (j < RPW && mm < a.M && ri_s[mm].valid) {
         const RowInfo ri = ri_s[mm];
+        int64_t off;  // element offset of the lane's 8 dimensions (16-byte aligned, contiguous)
+        char* base;
         if (is_q) {
-          const int64_t base = ((int64_t)(a.m0 + mm) * a.hq + h) * C;
-          store_t<T>(a.q_out, base + lane, y0[j]);
-          if constexpr (C == 128) store_t<T>(a.q_out, base + lane + 64, y1[j]);
+          base = a.q_out;
+          off = ((int64_t)(a.m0 + mm) * a.hq + h) * C + d0;
         } else if constexpr (sizeof(T) == 2) {
-          const int64_t base = ((int64_t)ri.seq * a.hkv + (h - a.hq)) * a.kv_ld * C;
-          store_t<T>(a.kc, base + kfrag_index(ri.pos, lane, C), y0[j]);
-          if constexpr (C == 128) store_t<T>(a.kc, base + kfrag_index(ri.pos, lane + 64, C), y1[j]);
+          base = a.kc;
+          off = ((int64_t)ri.seq * a.hkv + (h - a.hq)) * a.kv_ld * C + kfrag_index(ri.pos, d0, C);
         } else {
-          const int64_t base = (((int64_t)ri.seq * a.hkv + (h - a.hq)) * a.kv_ld + ri.pos) * C;  // fp32: [pos][hd]
-          store_t<T>(a.kc, base + lane, y0[j]);
-          if constexpr (C == 128) store_t<T>(a.kc, base + lane + 64, y1[j]);
+          base = a.kc;
+          off = (((int64_t)ri.seq * a.hkv + (h - a.hq)) * a.kv_ld + ri.pos) * C + d0;  // fp32: [pos][hd]
+        }
+        if constexpr (sizeof(T) == 2) {
+          *reinterpret_cast<uint4*>(reinterpret_cast<uint16_t*>(base) + off) =
+              make_uint4(pack_bf16x2(z[0], z[1]), pack_bf16x2(z[2], z[3]), pack_bf16x2(z[4], z[5]), pack_bf16x2(z[6], z[7]));
+        } else {
+          float* dst = reinterpret_cast<float*>(base) + off;
+          *reinterpret_cast<f32x4*>(dst) = f32x4{z[0], z[1], z[2], z[3]};
+          *reinterpret_cast<f32x4*>(dst + 4) = f32x4{z[4], z[5], z[6], z[7]};
         }
       }
     }
   }
 }
 
-// Sum over the n lanes of each aligned group of n (n in 1, 2, 4, 8, 16) by DPP row permutations, the same
-// butterfly in every lane (the wave must be fully active).
-template <int N>
-__device__ inline float group_sum(float v) {
-  if constexpr (N >= 2) v += dpp_f<kDppXor1>(v);
-  if constexpr (N >= 4) v += dpp_f<kDppXor2>(v);
-  if constexpr (N >= 8) v += dpp_f<kDppHalfMirror>(v);
-  if constexpr (N >= 16) v += dpp_f<kDppMirror>(v);
-  return v;
-}
 
 // Residual epilogue, 8 consecutive columns per lane: LPR = C / 8 lanes hold a row (16-byte loads and
 // stores), RPI = 64 / LPR rows per pass; a row's sum of squares adds the lane's 8 squares in column order,

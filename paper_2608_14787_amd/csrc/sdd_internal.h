@@ -158,6 +158,7 @@ constexpr int kDppXor1 = 0xB1;        // quad_perm [1,0,3,2]
 constexpr int kDppXor2 = 0x4E;        // quad_perm [2,3,0,1]
 constexpr int kDppHalfMirror = 0x141; // lane i <- lane 7-i within each 8
 constexpr int kDppMirror = 0x140;     // lane i <- lane 15-i within each 16
+constexpr int kDppRor8 = 0x128;       // row rotate by 8: lane i <- lane i ^ 8 within each 16
 template <int CTRL>
 __device__ inline int dpp_i(int v) {
   return __builtin_amdgcn_update_dpp(0, v, CTRL, 0xF, 0xF, false);
@@ -194,34 +195,6 @@ __device__ inline float xor32_op(float v, Op op) {
   unsigned a = __builtin_bit_cast(unsigned, v), b = a;
   permlane32_swap(a, b);
   return op(__builtin_bit_cast(float, a), __builtin_bit_cast(float, b));
-}
-
-// Sum over a fully active wave, the same value in every lane.  Fixed order:
-// pairs, quads, eights and sixteens inside each row (each step adds two equal
-// partial sums in either operand order, which IEEE addition treats alike),
-// then the four row sums as (r0 + r1) + (r2 + r3).
-__device__ inline float wave_sum_fast(float v) {
-  v += dpp_f<kDppXor1>(v);
-  v += dpp_f<kDppXor2>(v);
-  v += dpp_f<kDppHalfMirror>(v);
-  v += dpp_f<kDppMirror>(v);
-  return (lane_f(v, 0) + lane_f(v, 16)) + (lane_f(v, 32) + lane_f(v, 48));
-}
-
-// wave_sum_fast of N independent values at once (the DPP steps of the N sums
-// interleave); each result is bit-identical to wave_sum_fast of that value.
-template <int N>
-__device__ inline void wave_sum_fast_n(float (&v)[N]) {
-#pragma unroll
-  for (int j = 0; j < N; ++j) v[j] += dpp_f<kDppXor1>(v[j]);
-#pragma unroll
-  for (int j = 0; j < N; ++j) v[j] += dpp_f<kDppXor2>(v[j]);
-#pragma unroll
-  for (int j = 0; j < N; ++j) v[j] += dpp_f<kDppHalfMirror>(v[j]);
-#pragma unroll
-  for (int j = 0; j < N; ++j) v[j] += dpp_f<kDppMirror>(v[j]);
-#pragma unroll
-  for (int j = 0; j < N; ++j) v[j] = (lane_f(v[j], 0) + lane_f(v[j], 16)) + (lane_f(v[j], 32) + lane_f(v[j], 48));
 }
 
 // wave-level reductions (64 lanes)
