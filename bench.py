@@ -39,7 +39,8 @@ ETA_B, ETA_C, K_MIN, S_MAX = 0.90, 0.93, 6, 64
 
 
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gateup_gemm_qwen32b_hbm_traffic.txt")
-KERNEL_SOURCES = [os.path.join(ROOT, "paper_2608_14787_amd", "csrc", f) for f in ("decoder.hip", "sdd_internal.h", "model.h")]
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2608_14787_amd", "csrc", f)
+                  for f in ("decoder.hip", "gemm.h", "sdd_internal.h", "model.h")]
 
 
 def measured_traffic():
