@@ -273,9 +273,6 @@ __global__ void __launch_bounds__(kGemmThreads, 1) gemm_kernel(GemmArgs a) {
     }
     if constexpr (kPreSS > 0)
       if (first) prologue_finish();
-    // the Q / K epilogue's global inputs, in flight while the group is reduced
-    QkvPre<NG, R> qpre;
-    if constexpr (EPI == EPI_QKV) qkv_pre_load<NG, R>(a, s.g, s_ri, qpre);
     const int g = s.g;
     const bool full = s.kb == 0 && s.ke == a.KT;
     const int which = g == g_first ? 0 : 1;
@@ -380,7 +377,7 @@ __global__ void __launch_bounds__(kGemmThreads, 1) gemm_kernel(GemmArgs a) {
     if (!fin && !more && a.Wn && (int)blockIdx.x < a.nwg_n) prefetch_next(a, wave, lane);
     // ---- epilogue on the final tile of column group g ----
     if (fin) {
-      if constexpr (EPI == EPI_QKV) epilogue_qkv<T, NG, R>(a, tile, g, s_rs, s_ri, &qpre);
+      if constexpr (EPI == EPI_QKV) epilogue_qkv<T, NG, R>(a, tile, g, s_rs, s_ri);
       if constexpr (EPI == EPI_RESID) epilogue_resid<T, NG, R>(a, tile, g);
       if constexpr (EPI == EPI_SWIGLU) epilogue_swiglu<T, NG, R>(a, tile, g, s_rs);
       if constexpr (EPI == EPI_LOGITS) epilogue_logits<NG, R>(a, tile, g, s_rs, s_ri);

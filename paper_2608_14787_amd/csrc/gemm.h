@@ -168,8 +168,7 @@ struct QkvShape {
 // Global inputs of the Q / K epilogue of column group g (head g): the QK-norm
 // gains of the lane's 8 dimensions and, for each pass, the RoPE (cos, sin) of
 // those dimensions at its row's position (table [pos][C/2] of float2; dimension
-// d uses entry d mod C/2).  Loaded ahead of the epilogue, so that their latency
-// hides behind the group's cross-workgroup reduction.
+// d uses entry d mod C/2), all loaded before any is used.
 template <int NG, int R>
 struct QkvPre {
   f32x4 gn[2];
@@ -202,8 +201,7 @@ __device__ inline void qkv_pre_load(const GemmArgs& a, int g, const RowInfo* ri_
 }
 
 template <typename T, int NG, int R>
-__device__ void epilogue_qkv(const GemmArgs& a, const float* tile, int g, const float* rsl, const RowInfo* ri_s,
-                             const QkvPre<NG, R>* pre = nullptr) {
+__device__ void epilogue_qkv(const GemmArgs& a, const float* tile, int g, const float* rsl, const RowInfo* ri_s) {
   // no contraction: every instantiation (row count) must round each row alike
 #pragma clang fp contract(off)
   constexpr int C = NG * 16;  // == head_dim
@@ -235,9 +233,8 @@ __device__ void epilogue_qkv(const GemmArgs& a, const float* tile, int g, const 
       return;
     }
     using S = QkvShape<NG, R>;
-    QkvPre<NG, R> pl;
-    if (!pre) qkv_pre_load<NG, R>(a, g, ri_s, pl);
-    const QkvPre<NG, R>& pp = pre ? *pre : pl;
+    QkvPre<NG, R> pp;
+    qkv_pre_load<NG, R>(a, g, ri_s, pp);
     const int rsub = lane / S::LPR, d0 = 8 * (lane % S::LPR);
     const bool lo = d0 < C / 2;  // the rotation pairs dimension d with d + C/2
 #pragma unroll
