@@ -334,7 +334,7 @@ __global__ void __launch_bounds__(kGemmThreads, 1) gemm_kernel(GemmArgs a) {
       }
       const int wf = unit_owner((uint32_t)g * KT, U, a.n_wg);
       const int wl = unit_owner((uint32_t)(g + 1) * KT - 1, U, a.n_wg);
-      fin = arrive_last(&a.cnt[g], wl - wf + 1, &s_flag);
+      fin = arrive_last(&a.cnt[g * kCntStride], wl - wf + 1, &s_flag);
       if (fin) {
         // contributors added in workgroup order; FB contributors' loads in flight at once
         constexpr int FB = EPT4 >= 8 ? 2 : EPT4 >= 4 ? 4 : 8;
@@ -894,7 +894,7 @@ static int64_t gemm_counter_count(const sdd_model* m) {
 }
 
 static size_t counters_bytes(const sdd_model* m) {
-  return align_up((size_t)gemm_counter_count(m) * 4, 256);
+  return align_up((size_t)gemm_counter_count(m) * 4 * kCntStride, 256);
 }
 
 WsLayout ws_layout(const sdd_model* m, int max_rows) {

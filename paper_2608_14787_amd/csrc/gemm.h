@@ -16,6 +16,9 @@ enum Epi { EPI_QKV = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_LOGITS = 3 };
 constexpr int kGemmThreads = 256;
 constexpr int kXcds = 8;  // XCDs of the MI355X (32 CUs each); workgroups go to them round-robin by linear id
 constexpr int kMaxPassRows = 64;  // rows per GEMM pass (TB <= 4 row tiles of 16)
+// Arrival counters of split column groups sit one 128-byte line apart: the groups of a launch finish
+// together, and device-scope atomics on one line serialize.
+constexpr int kCntStride = 32;
 
 struct GemmArgs {
   const char* W;  // tiled weights
@@ -28,7 +31,7 @@ struct GemmArgs {
   int mp;         // padded row stride of per-row scratch
   int n_wg;
   float* part;    // partial tiles [n_wg][2][M][NG*16]
-  int* cnt;       // arrival counter per column group
+  int* cnt;       // arrival counter per column group (group g at cnt[g * kCntStride])
   const RowInfo* rows;
   // RMSNorm of the input rows: r_m = 1/sqrt(sum_g ss_in[g][m] / d_in + eps),
   // from per-column-group sums of squares written by the producer (NULL: none)

@@ -198,7 +198,7 @@ __global__ void __launch_bounds__(kRowsThreads, 1) gemm_rows_kernel(GemmArgs a) 
       if (!(s.kb == 0 && s.ke == a.KT)) {
         int wf, wl;
         contributors(s.g, wf, wl);
-        fin = arrive_last(&a.cnt[s.g], wl - wf + 1, &s_flag);
+        fin = arrive_last(&a.cnt[s.g * kCntStride], wl - wf + 1, &s_flag);
       }
       if (fin) {
         __syncthreads();
@@ -254,7 +254,7 @@ __global__ void __launch_bounds__(kRowsThreads, 1) gemm_rows_kernel(GemmArgs a) 
                                                    kCoherentCpol);
       int wf, wl;
       contributors(g, wf, wl);
-      fin = arrive_last(&a.cnt[g], wl - wf + 1, &s_flag);
+      fin = arrive_last(&a.cnt[g * kCntStride], wl - wf + 1, &s_flag);
       if (fin) {
 #pragma unroll
         for (int nt = 0; nt < NG; ++nt)

@@ -28,6 +28,9 @@ namespace sdd {
 namespace {
 
 constexpr int kThreads = 256;
+// per-sequence arrival counters one 128-byte line apart: a sequence's workgroups all arrive within a few
+// microseconds, and device-scope atomics on one line serialize
+constexpr int kSeqCntStride = 32;
 constexpr int kRecBatch = 512;  // chunk records staged in LDS at a time by the finishing workgroup (16 KB)
 
 struct RowRec {
@@ -419,7 +422,7 @@ __global__ void __launch_bounds__(kThreads) rowstats_kernel(Job job) {
     st_coherent(&dst->qs, rec.qs);
     st_coherent(&dst->flags, rec.flags);
   }
-  if (!arrive_last(&job.counters[b], job.rows * job.C, &s_last)) return;
+  if (!arrive_last(&job.counters[b * kSeqCntStride], job.rows * job.C, &s_last)) return;
 
   // ---- last workgroup of sequence b: combine and decide ----
   // (1) every row's decision inputs at once (thread t: row t): draft token, uniform, and the target and
@@ -704,7 +707,7 @@ __global__ void __launch_bounds__(kThreads) resample_kernel(Job job) {
       }
     }
   }
-  if (!arrive_last(&job.counters2[b], job.C2, &s_last)) return;
+  if (!arrive_last(&job.counters2[b * kSeqCntStride], job.C2, &s_last)) return;
 
   // ---- last workgroup of sequence b: select the chunk, then the lane, thread and element ----
   if (tid < kWave) {
@@ -788,7 +791,7 @@ int chunks_for(int nrows, int V, int resident = 2048) {
   return max(1, c);
 }
 
-size_t counters_region(int B) { return ((size_t)B * sizeof(int) + 255) / 256 * 256; }
+size_t counters_region(int B) { return ((size_t)B * kSeqCntStride * sizeof(int) + 255) / 256 * 256; }
 // Residual draw records: per sequence the row-L statistics and up to 64 chunk totals.
 size_t draw_region(int B) { return (size_t)B * (sizeof(SeqRec) + 64 * sizeof(ResRec)); }
 
