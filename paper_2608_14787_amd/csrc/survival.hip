@@ -27,6 +27,7 @@ constexpr int kMlpThreads = 256;
 constexpr int kRowTile = 64;   // positions per workgroup (4 waves x 16)
 constexpr int kKc = 128;       // k-chunk staged in LDS by layer 1
 constexpr int kMaxH = 256;
+constexpr int kCntLine = 32;  // ints per 128-byte line
 
 struct MlpArgs {
   const uint16_t* hidden;  // [n][d_hid] bf16
@@ -39,6 +40,8 @@ struct MlpArgs {
   float* h1;        // [rt*64][H]
   float* h2;
   float* zpart;     // [rt][ct][64]
+  // counters one 128-byte line apart (index x at [x * kCntLine]): the workgroups that count on them, and
+  // those polling them, do so at about the same time, and device-scope atomics on one line serialize
   int* cnt1;        // [rt][ct]
   int* cnt3;        // [rt]
   int* done1;       // [rt]: h1 tiles written
@@ -131,7 +134,7 @@ __device__ void layer1_body(const MlpArgs& a, int bid, float* smem, int* s_flag)
   const int row_l = wave * 16 + lane % 16, col4 = 4 * (lane / 16);
   const int off = (((tile * a.S + s) * kRowTile + row_l) * 16 + col4) * 4;  // bytes (< 2^31: checked on the host)
   __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, acc), prs, off, 0, kCoherentCpol);
-  if (!arrive_last(&a.cnt1[tile], a.S, s_flag)) return;
+  if (!arrive_last(&a.cnt1[tile * kCntLine], a.S, s_flag)) return;
   // last split of this tile: sum the splits in order, bias, GELU
   // (eight splits' loads in flight at a time, added in split order)
   f32x4 sum = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -155,7 +158,7 @@ __device__ void layer1_body(const MlpArgs& a, int bid, float* smem, int* s_flag)
   if (row < a.n)
     __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, hv), hrs, (row * a.H + c0 + col4) * 4, 0,
                                            kCoherentCpol);
-  count_done(&a.done1[rt]);
+  count_done(&a.done1[rt * kCntLine]);
 }
 
 template <bool LAST>
@@ -213,7 +216,7 @@ __device__ void dense_body(const MlpArgs& a, int bid, const float* hin, const fl
     if (row < a.n)
       __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, (f32x4){hv[0], hv[1], hv[2], hv[3]}), ors,
                                              (row * H + c0 + col4) * 4, 0, kCoherentCpol);
-    count_done(&a.done2[rt]);
+    count_done(&a.done2[rt * kCntLine]);
   } else {
     // this tile's share of w4 . h3 for the row: the lane's 4 columns in order, then the 4 lane groups in order
     const float zs = dot4(hv, a.w4 + c0 + col4);
@@ -223,11 +226,11 @@ __device__ void dense_body(const MlpArgs& a, int bid, const float* hin, const fl
     if (lane < 16)
       __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, tz), zrs, ((rt * CT + ct) * kRowTile + row_l) * 4,
                                             0, kCoherentCpol);
-    if (!arrive_last(&a.cnt3[rt], CT, s_flag)) return;
+    if (!arrive_last(&a.cnt3[rt * kCntLine], CT, s_flag)) return;
     // every wait of this row tile has ended: its counters go back to zero for the next call
     if (tid == 0) {
-      __hip_atomic_store(&a.done1[rt], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      __hip_atomic_store(&a.done2[rt], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(&a.done1[rt * kCntLine], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(&a.done2[rt * kCntLine], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
     const bool bad = __hip_atomic_load(a.err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0;
     if (tid < kRowTile && r0 + tid < a.n) {
@@ -259,11 +262,11 @@ __global__ void __launch_bounds__(kMlpThreads) survival_kernel(MlpArgs a) {
     layer1_body(a, bid, smem, &s_flag);
   } else if (bid < n1 + n2) {
     const int b2 = bid - n1;
-    if (!wait_count(&a.done1[b2 / CT], CT, &s_flag) && threadIdx.x == 0) atomicOr(a.err, 1);
+    if (!wait_count(&a.done1[(b2 / CT) * kCntLine], CT, &s_flag) && threadIdx.x == 0) atomicOr(a.err, 1);
     dense_body<false>(a, b2, a.h1, a.W2, a.b2, a.h2, smem, &s_flag);
   } else {
     const int b3 = bid - n1 - n2;
-    if (!wait_count(&a.done2[b3 / CT], CT, &s_flag) && threadIdx.x == 0) atomicOr(a.err, 1);
+    if (!wait_count(&a.done2[(b3 / CT) * kCntLine], CT, &s_flag) && threadIdx.x == 0) atomicOr(a.err, 1);
     dense_body<true>(a, b3, a.h2, a.W3, a.b3, nullptr, smem, &s_flag);
   }
 }
@@ -281,9 +284,9 @@ MlpWs mlp_ws(int n, int H, int S) {
     o += (bytes + 255) / 256 * 256;
     return at;
   };
-  w.cnt1 = take((size_t)RT * CT * sizeof(int));
-  w.cnt3 = take((size_t)RT * sizeof(int));
-  w.done = take((size_t)(2 * RT + 1) * sizeof(int));  // done1 [RT], done2 [RT], the sticky error word
+  w.cnt1 = take((size_t)RT * CT * kCntLine * sizeof(int));
+  w.cnt3 = take((size_t)RT * kCntLine * sizeof(int));
+  w.done = take((size_t)(2 * RT + 1) * kCntLine * sizeof(int));  // done1 [RT], done2 [RT], the sticky error word
   w.part = take((size_t)RT * CT * S * kRowTile * 16 * sizeof(float));
   w.h1 = take((size_t)RT * kRowTile * H * sizeof(float));
   w.h2 = take((size_t)RT * kRowTile * H * sizeof(float));
@@ -363,8 +366,8 @@ extern "C" int sdd_survival_mlp(const sdd_mlp* m, const uint16_t* hidden, const 
   a.cnt1 = reinterpret_cast<int*>(w + L.cnt1);
   a.cnt3 = reinterpret_cast<int*>(w + L.cnt3);
   a.done1 = reinterpret_cast<int*>(w + L.done);
-  a.done2 = a.done1 + RT;
-  a.err = a.done2 + RT;
+  a.done2 = a.done1 + (size_t)RT * kCntLine;
+  a.err = a.done2 + (size_t)RT * kCntLine;
   a.log_score = log_score;
   a.logit = logit;
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
