@@ -517,7 +517,8 @@ __global__ void __launch_bounds__(kAttnWaves * 64) attention_mfma_kernel(AttnMfm
     // multiples of 8), one per four waves
     const int p = blockIdx.x - a.n_attn, wave4 = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
     const int w = p + (wave4 / 4) * a.n_pref;
-    if (a.Wn && w < a.nwg_n) prefetch_gemm_start(a.Wn, a.KTn, a.Gn, a.ngn, a.nwg_n, w, wave4 % 4, threadIdx.x % kWave);
+    // (six k-steps per wave: about what lands while the attention runs; deeper ones hold it open)
+    if (a.Wn && w < a.nwg_n) prefetch_gemm_start<6>(a.Wn, a.KTn, a.Gn, a.ngn, a.nwg_n, w, wave4 % 4, threadIdx.x % kWave);
     return;
   }
   // Workgroups are dispatched to the XCDs round-robin by linear id; all query

@@ -106,30 +106,31 @@ __device__ inline void store_t(char* base, int64_t idx, float v) {
 // Stream-K bookkeeping (unit_start, unit_owner: model.h) is 32-bit unsigned
 // arithmetic: 64-bit division is a long software sequence on this GPU.
 
-// Loads into L2 the first three k-steps that workgroup w of a GEMM launch
+// Loads into L2 the k-steps st0 .. st0 + NS - 1 that workgroup w of a GEMM launch
 // (weights Wn stored in the order of their plan: workgroup w's i-th unit of
 // ngn tiles at slot i * nwg + w) streams, wave `wave` (0..3) the k-steps that
-// wave streams (local units wave, wave + 4, wave + 8).  Called from a
+// wave streams (local units wave + 4 st, st0 <= st < st0 + NS).  Called from a
 // workgroup on XCD w mod 8: workgroups are dispatched to the XCDs round-robin,
 // so the lines land in the L2 that serves them.  Plain (cached) loads whose
 // values are consumed by an empty asm statement.
+template <int NS = 3>
 __device__ inline void prefetch_gemm_start(const char* Wn, int KTn, int Gn, int ngn, int nwg, int w_, int wave,
-                                           int lane) {
+                                           int lane, int st0 = 0) {
   const uint32_t Un = (uint32_t)Gn * (uint32_t)KTn, n = (uint32_t)nwg, w = (uint32_t)w_;
   const int nloc = (int)(unit_start(w + 1, Un, n) - unit_start(w, Un, n));
   const int nk = nloc > wave ? (nloc - wave + 3) / 4 : 0;  // this wave's units
-  if (nk == 0) return;
+  if (nk <= st0) return;
   const uint4* base = reinterpret_cast<const uint4*>(Wn) + (int64_t)w * ngn * kWave + lane;
-  uint4 v[3][8];  // unconditional loads (unit clamped to the wave's last, tile to the group's last)
+  uint4 v[NS][8];  // unconditional loads (unit clamped to the wave's last, tile to the group's last)
 #pragma unroll
-  for (int st = 0; st < 3; ++st) {
-    const int64_t i = wave + 4 * min(st, nk - 1);
+  for (int st = 0; st < NS; ++st) {
+    const int64_t i = wave + 4 * min(st0 + st, nk - 1);
 #pragma unroll
     for (int nt = 0; nt < 8; ++nt) v[st][nt] = base[(i * nwg * ngn + min(nt, ngn - 1)) * kWave];
   }
   uint32_t x = 0;
 #pragma unroll
-  for (int st = 0; st < 3; ++st)
+  for (int st = 0; st < NS; ++st)
 #pragma unroll
     for (int nt = 0; nt < 8; ++nt) x ^= v[st][nt].x ^ v[st][nt].w;
   asm volatile("" ::"v"(x));
