@@ -266,9 +266,10 @@ __device__ __attribute__((always_inline)) inline void stats_update(ThreadStats& 
 
 // Streams this thread's vectors of [base, base + n) of a row (and of the drafter row) with kDepth to
 // 2 kDepth 16-byte loads of each in flight, updating the running statistics.  Vector i of the thread starts
-// at element base + (i * kThreads + threadIdx.x) * VEC.  The loads are unconditional (an index past the
-// thread's last vector re-reads that vector, an L2 hit, and its values are not used) and the trip count is
-// uniform over the workgroup, so the compiler can wait for exactly the older group.
+// at element base + (i * kThreads + threadIdx.x) * VEC.  The loads are unconditional (a vector past the
+// thread's last one reads zero without a memory access, or, for rows that are not 16-byte aligned, re-reads
+// the last one, and its values are not used) and the trip count is uniform over the workgroup, so the
+// compiler can wait for exactly the older group.
 template <typename T, typename TQ, int VEC, bool kSum, bool kCount, bool kQ>
 __device__ __attribute__((always_inline)) inline void stream_stats(const T* row, const TQ* qrow, int base, int n, float zx,
                                                                    int x, ThreadStats& st, ThreadStats& qst) {
@@ -281,14 +282,26 @@ __device__ __attribute__((always_inline)) inline void stream_stats(const T* row,
   const int tofs = nvt > 0 ? (int)threadIdx.x : 0;  // a thread with no vector reads the chunk's first one
   auto elem = [&](int i) { return base + (min(i, last) * kThreads + tofs) * VEC; };
   const bool hq = kQ && qrow != nullptr;
+  // 16-byte vectors through buffer descriptors over the chunk: a vector past the thread's last one lies past
+  // the descriptor's range, so its load returns zero without a memory access (no clamped re-reads)
+  const __amdgpu_buffer_rsrc_t prs = __builtin_amdgcn_make_buffer_rsrc(const_cast<T*>(row + base), 0, n * (int)sizeof(T),
+                                                                       kBufferRsrcWord3);
+  const __amdgpu_buffer_rsrc_t qrs = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<TQ*>(hq ? qrow + base : reinterpret_cast<const TQ*>(row)), 0, hq ? n * (int)sizeof(TQ) : 0, kBufferRsrcWord3);
   // two register buffers of kDepth vectors: the next group's loads are issued (and kept ahead of the
   // arithmetic by a scheduling barrier) before the current group is consumed
   uint4 pa[kDepth], pb[kDepth], qa[kQ ? kDepth : 1], qb[kQ ? kDepth : 1];
   auto load_group = [&](int i, uint4* pv, uint4* qv) {
 #pragma unroll
     for (int d = 0; d < kDepth; ++d) {
-      pv[d] = load_vec<T, VEC>(row, elem(i + d));
-      if (kQ) qv[d] = hq ? load_vec<TQ, VEC>(qrow, elem(i + d)) : uint4{0, 0, 0, 0};
+      if constexpr (VEC > 1) {
+        const int off = ((i + d) * kThreads + (int)threadIdx.x) * 16;
+        pv[d] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(prs, off, 0, kNtCpol));
+        if (kQ) qv[d] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(qrs, off, 0, kNtCpol));
+      } else {
+        pv[d] = load_vec<T, VEC>(row, elem(i + d));
+        if (kQ) qv[d] = hq ? load_vec<TQ, VEC>(qrow, elem(i + d)) : uint4{0, 0, 0, 0};
+      }
     }
     __builtin_amdgcn_sched_barrier(0);
   };
