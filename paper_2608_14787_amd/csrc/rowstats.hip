@@ -856,10 +856,16 @@ int resident_wgs() {
   return cached;
 }
 
+// Arrivals on one sequence's counter (rows x chunks) at most: they serialize on its line, and past a few
+// hundred they cost more than the extra chunks gain (one sequence of 33 rows: 18 chunks per row 21 us, 8
+// chunks 13 us)
+constexpr int kMaxSeqArrivals = 256;
+
 // Chunks per row for this kernel's occupancy; never more than the workspace was sized for.
 inline void fit_chunks(Job& job, int vec, int resident) {
   const int nrows = job.B * job.rows;
-  const int c = std::min(job.C, chunks_for(nrows, job.V, std::min(resident, 2048)));
+  const int c = std::min({job.C, chunks_for(nrows, job.V, std::min(resident, 2048)),
+                          std::max(1, kMaxSeqArrivals / std::max(1, job.rows))});
   job.chunk = (int)ceil_div(ceil_div(job.V, c), vec) * vec;
   job.C = (int)ceil_div(job.V, job.chunk);
 }
