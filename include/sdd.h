@@ -116,15 +116,20 @@ int sdd_model_load_tensor(sdd_model* m, int kind, int layer, const void* src, sd
  * 16-row tiles alternate gate, up).  A tile is 1 KiB: 16 rows x kt columns
  * (kt 32 for bf16, 16 for fp32), lane l's 16 bytes holding row l % 16 and the
  * 16 / elem columns from (l / 16) * 16 / elem.  Row tiles form column groups
- * of *ng; unit (g, k) is the ng tiles of group g at k-step k, and the plan
- * splits the U = G * KT units over *n_wg workgroups, workgroup w owning units
- * [w U / n_wg, (w + 1) U / n_wg) (integer division).  The i-th unit of
- * workgroup w is stored at slot i * n_wg + w, its tile j (row tile g * ng + j)
- * at byte *offset + (slot * ng + j) * 1024 of the weight buffer; slots past a
- * shorter share are zero.  *bytes is the matrix's extent.  Host-only (no
- * device access).  Errors: SDD_EINVAL for a NULL pointer, a bad kind or layer. */
+ * of *ng; unit (g, k) is the ng tiles of group g at k-step k (u = g KT + k),
+ * and the plan splits the G * KT units over *n_wg workgroups by cost: each
+ * group counts as KT + c units (c = *seg_units, the cost of a workgroup's
+ * entering one more group; 0 gives equal shares), and workgroup w owns units
+ * [start(w), start(w + 1)) with start(w) = g KT + max(0, o - c) for
+ * x = w G (KT + c) / n_wg, g = x / (KT + c), o = x mod (KT + c) (integer
+ * division).  The i-th unit of workgroup w is stored at slot i * n_wg + w, its
+ * tile j (row tile g * ng + j) at byte *offset + (slot * ng + j) * 1024 of the
+ * weight buffer; the matrix holds n_wg times the longest share of slots, and
+ * slots past a shorter share are zero.  *bytes is the matrix's extent.
+ * Host-only (no device access).  Errors: SDD_EINVAL for a NULL pointer, a bad
+ * kind or layer. */
 int sdd_model_matrix_layout(const sdd_model* m, int kind, int layer, size_t* offset, size_t* bytes, int* KT,
-                            int* G, int* ng, int* n_wg);
+                            int* G, int* ng, int* n_wg, int* seg_units);
 
 /* ---- KV cache ---------------------------------------------------------- */
 

@@ -84,8 +84,8 @@ __global__ void __launch_bounds__(kGemmThreads, 1) gemm_kernel(GemmArgs a) {
 
   const int w = blockIdx.x;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave), lane = threadIdx.x % kWave;
-  const uint32_t KT = (uint32_t)a.KT, U = (uint32_t)a.G * KT;
-  const uint32_t u0 = unit_start(w, U, a.n_wg), u1 = unit_start(w + 1, U, a.n_wg);
+  const uint32_t KT = (uint32_t)a.KT, G = (uint32_t)a.G, SC = (uint32_t)a.segc;
+  const uint32_t u0 = unit_start(w, KT, G, SC, a.n_wg), u1 = unit_start(w + 1, KT, G, SC, a.n_wg);
   const int g_first = (int)(u0 / KT);
   const uint4* W = reinterpret_cast<const uint4*>(a.W);
   const int MC = a.M * C;
@@ -103,7 +103,7 @@ __global__ void __launch_bounds__(kGemmThreads, 1) gemm_kernel(GemmArgs a) {
   // slot i * n_wg + w, so a workgroup's consecutive units are n_wg slots apart
   const uint32_t slot_bytes = (uint32_t)NG * kWave * 16, wstride = (uint32_t)a.n_wg * slot_bytes;
   const __amdgpu_buffer_rsrc_t wrs = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<uint4*>(W), 0, (int)(((U + a.n_wg - 1) / a.n_wg) * wstride), kBufferRsrcWord3);
+      const_cast<uint4*>(W), 0, (int)(a.share * wstride), kBufferRsrcWord3);
   const uint32_t kstep4w = 4u * wstride;    // bytes between a wave's consecutive k-steps
   const uint32_t kstep4x = 4u * KTILE * (uint32_t)sizeof(T);
   const int wlane = lane * 16;
@@ -332,8 +332,8 @@ __global__ void __launch_bounds__(kGemmThreads, 1) gemm_kernel(GemmArgs a) {
         const int i = 4 * (threadIdx.x + e * kGemmThreads);
         if (i < MC) __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, pv[e]), prs, my_off + 4 * i, 0, kCoherentCpol);
       }
-      const int wf = unit_owner((uint32_t)g * KT, U, a.n_wg);
-      const int wl = unit_owner((uint32_t)(g + 1) * KT - 1, U, a.n_wg);
+      const int wf = unit_owner((uint32_t)g * KT, KT, G, SC, a.n_wg);
+      const int wl = unit_owner((uint32_t)(g + 1) * KT - 1, KT, G, SC, a.n_wg);
       fin = arrive_last(&a.cnt[g * kCntStride], wl - wf + 1, &s_flag);
       if (fin) {
         // contributors added in workgroup order; FB contributors' loads in flight at once
@@ -341,12 +341,15 @@ __global__ void __launch_bounds__(kGemmThreads, 1) gemm_kernel(GemmArgs a) {
         f32x4 sum[EPT4];
 #pragma unroll
         for (int e = 0; e < EPT4; ++e) sum[e] = f32x4{0.f, 0.f, 0.f, 0.f};
+        // a contributor published into its slot 0 when g is its share's first group: every contributor but
+        // the first, whose share starts inside group g or before it
+        const bool wf_first = unit_start(wf, KT, G, SC, a.n_wg) == (uint32_t)g * KT;
         for (int ww = wf; ww <= wl; ww += FB) {
           f32x4 v[FB][EPT4];
 #pragma unroll
           for (int q = 0; q < FB; ++q) {
             const int wq = std::min(ww + q, wl);
-            const int slot = (g == (int)(unit_start(wq, U, a.n_wg) / KT)) ? 0 : 1;
+            const int slot = (wq > wf || wf_first) ? 0 : 1;
             const int src_off = ((wq * 2 + slot) * MC) * 4;
 #pragma unroll
             for (int e = 0; e < EPT4; ++e) {
@@ -502,7 +505,7 @@ struct AttnMfmaArgs {
   // p + n_pref (NULL Wn: none)
   int n_attn, n_pref;
   const char* Wn;
-  int KTn, Gn, ngn, nwg_n;
+  int KTn, Gn, ngn, nwg_n, cn;
 };
 
 template <int HD>
@@ -518,7 +521,7 @@ __global__ void __launch_bounds__(kAttnWaves * 64) attention_mfma_kernel(AttnMfm
     const int p = blockIdx.x - a.n_attn, wave4 = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
     const int w = p + (wave4 / 4) * a.n_pref;
     // (six k-steps per wave: about what lands while the attention runs; deeper ones hold it open)
-    if (a.Wn && w < a.nwg_n) prefetch_gemm_start<6>(a.Wn, a.KTn, a.Gn, a.ngn, a.nwg_n, w, wave4 % 4, threadIdx.x % kWave);
+    if (a.Wn && w < a.nwg_n) prefetch_gemm_start<6>(a.Wn, a.KTn, a.Gn, a.cn, a.ngn, a.nwg_n, w, wave4 % 4, threadIdx.x % kWave);
     return;
   }
   // Workgroups are dispatched to the XCDs round-robin by linear id; all query
@@ -988,13 +991,16 @@ static int run_gemm(CallCtx& cx, int epi, unsigned prof, size_t w_off, int64_t N
   a.cnt = reinterpret_cast<int*>(cx.ws + cx.L.cnt);
   a.rows = reinterpret_cast<const RowInfo*>(cx.ws + cx.L.rowinfo);
   a.eps = m->cfg.rms_eps;
-  const int64_t U = (int64_t)a.G * a.KT;
+  const int64_t V = (int64_t)a.G * (a.KT + plan.c);
   const int nblocks = plan.n_wg;
   a.n_wg = nblocks;
+  a.segc = plan.c;
+  a.share = plan.S;
   MatPlan np{};
   if (next) np = plan_gemm(cx, *next);
-  if ((U + 1) * nblocks >= (int64_t(1) << 31))
-    return fail(SDD_EUNSUPPORTED, "matrix of %lld weight tiles exceeds the 32-bit stream-K bookkeeping", (long long)U);
+  if ((V + 1) * nblocks >= (int64_t(1) << 31))
+    return fail(SDD_EUNSUPPORTED, "matrix of %lld weight tiles exceeds the 32-bit stream-K bookkeeping",
+                (long long)a.G * a.KT);
   // weight buffer offsets, k-steps up to 4 past a wave's range included
   if ((plan_slots(plan) + 4 * (int64_t)plan.n_wg) * ng * 1024 >= (int64_t(1) << 31))
     return fail(SDD_EUNSUPPORTED, "matrix of %lld x %d exceeds the 32-bit buffer offsets", (long long)N, K);
@@ -1024,6 +1030,7 @@ static int run_gemm(CallCtx& cx, int epi, unsigned prof, size_t w_off, int64_t N
     a.Gn = np.G;
     a.ngn = next ? next->ng : 1;
     a.nwg_n = np.n_wg;
+    a.cn = np.c;
     const int tb = (int)ceil_div(a.M, 16);
     prof_begin(prof, cx.st);
     if (m->es == 2) {
@@ -1112,6 +1119,7 @@ static int forward_rows(CallCtx& cx, int nb, int R, float* logits, int32_t* argm
       a.Gn = op.G;
       a.ngn = m->ng_o;
       a.nwg_n = op.n_wg;
+      a.cn = op.c;
       const dim3 grid(a.n_attn + a.n_pref);
       prof_begin(PROF_ATTN, cx.st);
       if (c.head_dim == 128)

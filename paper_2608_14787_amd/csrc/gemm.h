@@ -30,6 +30,8 @@ struct GemmArgs {
   int m0, M;      // rows of this pass
   int mp;         // padded row stride of per-row scratch
   int n_wg;
+  int segc;       // virtual units per column group of the plan (cost-balanced shares; 0: equal)
+  int share;      // longest share (units): the stored matrix holds share x n_wg slots
   float* part;    // partial tiles [n_wg][2][M][NG*16]
   int* cnt;       // arrival counter per column group (group g at cnt[g * kCntStride])
   const RowInfo* rows;
@@ -64,7 +66,7 @@ struct GemmArgs {
   // the forward's next GEMM (NULL: none), whose first k-steps a workgroup that
   // only contributed a partial loads into L2 before it ends
   const char* Wn;
-  int KTn, Gn, ngn, nwg_n;
+  int KTn, Gn, ngn, nwg_n, cn;
 };
 
 template <typename T>
@@ -114,10 +116,10 @@ __device__ inline void store_t(char* base, int64_t idx, float v) {
 // so the lines land in the L2 that serves them.  Plain (cached) loads whose
 // values are consumed by an empty asm statement.
 template <int NS = 3>
-__device__ inline void prefetch_gemm_start(const char* Wn, int KTn, int Gn, int ngn, int nwg, int w_, int wave,
-                                           int lane, int st0 = 0) {
-  const uint32_t Un = (uint32_t)Gn * (uint32_t)KTn, n = (uint32_t)nwg, w = (uint32_t)w_;
-  const int nloc = (int)(unit_start(w + 1, Un, n) - unit_start(w, Un, n));
+__device__ inline void prefetch_gemm_start(const char* Wn, int KTn, int Gn, int cn, int ngn, int nwg, int w_,
+                                           int wave, int lane, int st0 = 0) {
+  const uint32_t n = (uint32_t)nwg, w = (uint32_t)w_;
+  const int nloc = (int)(unit_start(w + 1, KTn, Gn, cn, n) - unit_start(w, KTn, Gn, cn, n));
   const int nk = nloc > wave ? (nloc - wave + 3) / 4 : 0;  // this wave's units
   if (nk <= st0) return;
   const uint4* base = reinterpret_cast<const uint4*>(Wn) + (int64_t)w * ngn * kWave + lane;
@@ -138,7 +140,7 @@ __device__ inline void prefetch_gemm_start(const char* Wn, int KTn, int Gn, int 
 
 // the same for the workgroup of the same index of the forward's next GEMM
 __device__ inline void prefetch_next(const GemmArgs& a, int wave, int lane) {
-  prefetch_gemm_start(a.Wn, a.KTn, a.Gn, a.ngn, a.nwg_n, blockIdx.x, wave, lane);
+  prefetch_gemm_start(a.Wn, a.KTn, a.Gn, a.cn, a.ngn, a.nwg_n, blockIdx.x, wave, lane);
 }
 
 // Epilogues run on the final [rows][C] tile of one column group (LDS, row

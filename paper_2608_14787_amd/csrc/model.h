@@ -31,30 +31,49 @@ namespace sdd {
 // epilogue); splitting every group into equal k-ranges pays when the longer
 // share streams for less than this.
 constexpr double kTailStreamBytes = 224.0 * 1024;
-
-// Workgroup w owns the units [w U / n, (w + 1) U / n) (32-bit: U * n < 2^31 is
-// checked on the host); unit_owner(x) is the workgroup whose share holds unit x.
-__host__ __device__ inline uint32_t unit_start(uint32_t w, uint32_t U, uint32_t n) { return w * U / n; }
-__host__ __device__ inline int unit_owner(uint32_t x, uint32_t U, uint32_t n) {
-  return (int)(((x + 1) * n + U - 1) / U) - 1;
-}
+// Stream-K shares are balanced by cost rather than by units: every segment
+// (one column group's part of a share) beyond the first costs a workgroup a
+// cross-wave reduction and a partial publish or an epilogue, about as long as
+// streaming this many bytes (measured: gate/up workgroups whose share touches
+// three groups ended their stream ~4 us after those touching two).
+constexpr int kSegmentCostBytes = 96 * 1024;
 
 // Streaming plan of one weight matrix: KT k-steps of G column groups of ng row
-// tiles over n_wg workgroups.  With more groups than CUs, stream-K: the unit
-// range is split into n_cu equal shares.  With at most one group per CU, equal
-// shares would leave about a third of the workgroups straddling two groups,
-// each paying a second tail; then every group is split into s = n_cu / G equal
-// k-ranges over G x s workgroups (one segment each) when the longer share
-// costs less stream time than one tail.
+// tiles over n_wg workgroups.  With more groups than CUs, stream-K: each group
+// counts as KT + c units, the c leading ones virtual (the cost of entering one
+// more group), the virtual range V = G (KT + c) is split into n_wg equal shares
+// and mapped back onto the real units, so that a share touching one more group
+// holds c fewer real units.  With at most one group per CU, equal shares would
+// leave about a third of the workgroups straddling two groups, each paying a
+// second tail; then every group is split into s = n_cu / G equal k-ranges over
+// G x s workgroups (one segment each, c = 0) when the longer share costs less
+// stream time than one tail.  S is the longest share (units).
 struct MatPlan {
-  int KT, G, ng, n_wg;
+  int KT, G, ng, n_wg, c, S;
 };
+
+// First unit of workgroup w's share (unit u = g * KT + kt), from the virtual
+// position x = w V / n_wg: its group x / (KT + c), its offset past the group's
+// c virtual units.  32-bit: V * n_wg < 2^31 is checked on the host.  c = 0:
+// the equal shares [w U / n_wg, (w + 1) U / n_wg) of U = G * KT units.
+__host__ __device__ inline uint32_t unit_start(uint32_t w, uint32_t KT, uint32_t G, uint32_t c, uint32_t n) {
+  if (c == 0) return w * (G * KT) / n;  // (one division: this runs before a launch's first loads)
+  const uint32_t L = KT + c, x = w * (G * L) / n, g = x / L, o = x - g * L;
+  return g * KT + (o > c ? o - c : 0);
+}
+// The workgroup whose share holds unit u: the one whose virtual range holds u's
+// virtual position g (KT + c) + c + kt.
+__host__ __device__ inline int unit_owner(uint32_t u, uint32_t KT, uint32_t G, uint32_t c, uint32_t n) {
+  const uint32_t V = G * (KT + c), x = c ? u + (u / KT + 1) * c : u;
+  return (int)(((x + 1) * n + V - 1) / V) - 1;
+}
 
 inline MatPlan plan_matrix(int64_t N, int64_t K, int ktile, int ng, int n_cu) {
   MatPlan p;
   p.KT = (int)ceil_div(K, ktile);
   p.ng = ng;
   p.G = (int)(ceil_div(N, 16) / ng);
+  p.c = 0;
   const int64_t U = (int64_t)p.G * p.KT;
   p.n_wg = (int)std::min<int64_t>(U, n_cu);
   if (p.G <= n_cu) {
@@ -62,20 +81,34 @@ inline MatPlan plan_matrix(int64_t N, int64_t K, int ktile, int ng, int n_cu) {
     const double extra_units = (double)p.KT / s - (double)U / p.n_wg;
     if (extra_units * ng * 1024 < kTailStreamBytes) p.n_wg = p.G * s;
   }
+  auto shares = [&](int c, int& lo, int& hi) {
+    lo = p.KT, hi = 0;
+    for (int w = 0; w < p.n_wg; ++w) {
+      const int n = (int)(unit_start(w + 1, p.KT, p.G, c, p.n_wg) - unit_start(w, p.KT, p.G, c, p.n_wg));
+      lo = std::min(lo, n), hi = std::max(hi, n);
+    }
+  };
+  int lo, hi;
+  if (p.n_wg < p.G && (int64_t)p.G * (p.KT + kSegmentCostBytes / (ng * 1024)) * p.n_wg < (int64_t(1) << 31)) {
+    // cost-balanced shares where no share is left without a real unit
+    p.c = kSegmentCostBytes / (ng * 1024);
+    shares(p.c, lo, hi);
+    if (lo < 1) p.c = 0;
+  }
+  shares(p.c, lo, hi);
+  p.S = hi;
   return p;
 }
 
-// slots of the stored matrix: the longest share times n_wg (shorter shares leave one empty slot at the end)
-__host__ __device__ inline int64_t plan_slots(const MatPlan& p) {
-  return ceil_div((int64_t)p.G * p.KT, p.n_wg) * p.n_wg;
-}
+// slots of the stored matrix: the longest share times n_wg (shorter shares leave empty slots at the end)
+__host__ __device__ inline int64_t plan_slots(const MatPlan& p) { return (int64_t)p.S * p.n_wg; }
 inline size_t plan_bytes(const MatPlan& p) { return (size_t)plan_slots(p) * p.ng * 1024; }
 
 // slot of unit (g, kt)
 __host__ __device__ inline int64_t plan_slot(const MatPlan& p, int g, int kt) {
-  const uint32_t U = (uint32_t)p.G * p.KT, u = (uint32_t)g * p.KT + kt;
-  const int w = unit_owner(u, U, p.n_wg);
-  return (int64_t)(u - unit_start(w, U, p.n_wg)) * p.n_wg + w;
+  const uint32_t u = (uint32_t)g * p.KT + kt;
+  const int w = unit_owner(u, p.KT, p.G, p.c, p.n_wg);
+  return (int64_t)(u - unit_start(w, p.KT, p.G, p.c, p.n_wg)) * p.n_wg + w;
 }
 
 }  // namespace sdd

@@ -89,15 +89,15 @@ __global__ void __launch_bounds__(kRowsThreads, 1) gemm_rows_kernel(GemmArgs a) 
   const bool loader = wv >= 4;
   const int wave = wv & 3;
   const int w = blockIdx.x;
-  const uint32_t KT = (uint32_t)a.KT, U = (uint32_t)a.G * KT;
-  const uint32_t u0 = unit_start(w, U, a.n_wg), u1 = unit_start(w + 1, U, a.n_wg);
+  const uint32_t KT = (uint32_t)a.KT, G = (uint32_t)a.G, SC = (uint32_t)a.segc;
+  const uint32_t u0 = unit_start(w, KT, G, SC, a.n_wg), u1 = unit_start(w + 1, KT, G, SC, a.n_wg);
   const int g_first = (int)(u0 / KT);
   const int ntiles = (a.M + 15) / 16;
   // weights, stored in the order of the launch's plan: the i-th unit (NG tiles of 1 KiB, lane l's fragment at
   // 16 l) of workgroup w at slot i * n_wg + w, so this workgroup's consecutive units are kstep_w bytes apart
   const uint32_t kstep_w = (uint32_t)a.n_wg * NG * 1024;
   const __amdgpu_buffer_rsrc_t wrs = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<char*>(a.W), 0, (int)(((U + a.n_wg - 1) / a.n_wg) * kstep_w), kBufferRsrcWord3);
+      const_cast<char*>(a.W), 0, (int)(a.share * kstep_w), kBufferRsrcWord3);
   // a descriptor with no range: loads through it return zero without a memory access
   const __amdgpu_buffer_rsrc_t nrs = __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(a.W), 0, 0, kBufferRsrcWord3);
   // activations: row r of the launch at X + (m0 + r) * ldx elements.  Row tile tb's fragment of k-step kt: lane l
@@ -178,8 +178,8 @@ __global__ void __launch_bounds__(kRowsThreads, 1) gemm_rows_kernel(GemmArgs a) 
   // registers) with the same sequence of barriers: the prologue's on the first segment, one per k-step, two
   // in arrive_last for a split group, two around the final tile's staging, one between segments.
   auto contributors = [&](int g, int& wf, int& wl) {
-    wf = unit_owner((uint32_t)g * KT, U, a.n_wg);
-    wl = unit_owner((uint32_t)(g + 1) * KT - 1, U, a.n_wg);
+    wf = unit_owner((uint32_t)g * KT, KT, G, SC, a.n_wg);
+    wl = unit_owner((uint32_t)(g + 1) * KT - 1, KT, G, SC, a.n_wg);
   };
   uint32_t u = u0;
   if (loader) {
@@ -260,8 +260,11 @@ __global__ void __launch_bounds__(kRowsThreads, 1) gemm_rows_kernel(GemmArgs a) 
         for (int nt = 0; nt < NG; ++nt)
 #pragma unroll
           for (int j = 0; j < TBW; ++j) acc[nt][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+        // a contributor published into its slot 0 when g is its share's first group: every contributor but
+        // the first, whose share starts inside group g or before it
+        const bool wf_first = unit_start(wf, KT, G, SC, a.n_wg) == (uint32_t)g * KT;
         for (int ww = wf; ww <= wl; ++ww) {
-          const int slot = (g == (int)(unit_start(ww, U, a.n_wg) / KT)) ? 0 : 1;
+          const int slot = (ww > wf || wf_first) ? 0 : 1;
           // one row tile at a time (NG loads in flight), so that the loaded partials fit beside the sums
 #pragma unroll
           for (int j = 0; j < TBW; ++j) {

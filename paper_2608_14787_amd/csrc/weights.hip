@@ -69,7 +69,6 @@ template <typename T>
 __global__ void fill_tiled_kernel(char* dst, TiledSrc s, int only_part) {
   constexpr int EPL = 16 / sizeof(T);
   const MatPlan& p = s.plan;
-  const uint32_t U = (uint32_t)p.G * p.KT;
   const int64_t slices = plan_slots(p) * p.ng * 64;
   for (int64_t id = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; id < slices;
        id += (int64_t)gridDim.x * blockDim.x) {
@@ -80,8 +79,8 @@ __global__ void fill_tiled_kernel(char* dst, TiledSrc s, int only_part) {
     const int64_t slot = tile / p.ng;
     const int j = (int)(tile % p.ng);
     const uint32_t w = (uint32_t)(slot % p.n_wg), i = (uint32_t)(slot / p.n_wg);
-    const uint32_t u = unit_start(w, U, p.n_wg) + i;
-    if (u >= unit_start(w + 1, U, p.n_wg)) {
+    const uint32_t u = unit_start(w, p.KT, p.G, p.c, p.n_wg) + i;
+    if (u >= unit_start(w + 1, p.KT, p.G, p.c, p.n_wg)) {
       *reinterpret_cast<uint4*>(dst + id * 16) = uint4{0, 0, 0, 0};
       continue;
     }
@@ -329,8 +328,8 @@ extern "C" int sdd_model_init_random(sdd_model* m, uint64_t seed, float sigma, s
 }
 
 extern "C" int sdd_model_matrix_layout(const sdd_model* m, int kind, int layer, size_t* offset, size_t* bytes,
-                                       int* KT, int* G, int* ng, int* n_wg) {
-  SDD_REQUIRE(m && offset && bytes && KT && G && ng && n_wg, "NULL pointer");
+                                       int* KT, int* G, int* ng, int* n_wg, int* seg_units) {
+  SDD_REQUIRE(m && offset && bytes && KT && G && ng && n_wg && seg_units, "NULL pointer");
   SDD_REQUIRE(kind == SDD_T_LM_HEAD || (kind >= SDD_T_WQ && kind <= SDD_T_WDOWN), "bad matrix kind %d", kind);
   if (kind != SDD_T_LM_HEAD) SDD_REQUIRE(layer >= 0 && layer < m->cfg.n_layers, "bad layer %d", layer);
   const MatPlan* p = nullptr;
@@ -353,6 +352,7 @@ extern "C" int sdd_model_matrix_layout(const sdd_model* m, int kind, int layer, 
   *G = p->G;
   *ng = p->ng;
   *n_wg = p->n_wg;
+  *seg_units = p->c;
   return SDD_OK;
 }
 

@@ -51,7 +51,7 @@ _SIGS = {
     "sdd_model_destroy": (I, [P]),
     "sdd_model_init_random": (I, [P, C.c_uint64, F, P]),
     "sdd_model_load_tensor": (I, [P, I, I, P, P]),
-    "sdd_model_matrix_layout": (I, [P, I, I, P, P, P, P, P, P]),
+    "sdd_model_matrix_layout": (I, [P, I, I, P, P, P, P, P, P, P]),
     "sdd_kv_bytes": (I, [P, I, I, P]),
     "sdd_kv_create": (I, [P, I, I, P, SZ, P, P]),
     "sdd_kv_destroy": (I, [P]),
@@ -324,11 +324,11 @@ class Model:
     def matrix_layout(self, kind: int, layer: int = 0) -> dict:
         """sdd_model_matrix_layout: where and in which order a tiled matrix is stored."""
         off, nb = C.c_size_t(), C.c_size_t()
-        kt, g, ng, nwg = C.c_int(), C.c_int(), C.c_int(), C.c_int()
+        kt, g, ng, nwg, c = C.c_int(), C.c_int(), C.c_int(), C.c_int(), C.c_int()
         _check(lib().sdd_model_matrix_layout(self.handle, kind, layer, C.byref(off), C.byref(nb), C.byref(kt),
-                                             C.byref(g), C.byref(ng), C.byref(nwg)))
+                                             C.byref(g), C.byref(ng), C.byref(nwg), C.byref(c)))
         return {"offset": off.value, "bytes": nb.value, "KT": kt.value, "G": g.value, "ng": ng.value,
-                "n_wg": nwg.value}
+                "n_wg": nwg.value, "c": c.value}
 
     def workspace(self, max_rows: int) -> torch.Tensor:
         n = _size_out(lib().sdd_workspace_bytes, self.handle, max_rows)

@@ -5,22 +5,32 @@ import torch
 import workloads as W
 
 
+def share_starts(KT: int, G: int, c: int, nwg: int) -> np.ndarray:
+    """start(w) for w = 0..n_wg of the documented stream-K plan (sdd_model_matrix_layout): each column group
+    counts as KT + c units, the virtual range is split into n_wg equal parts, and a virtual position x maps to
+    unit g*KT + max(0, o - c) with g = x // (KT + c), o = x % (KT + c)."""
+    L = KT + c
+    x = np.arange(nwg + 1, dtype=np.int64) * (G * L) // nwg
+    return x // L * KT + np.maximum(0, x % L - c)
+
+
 def untile(buf: np.ndarray, layout: dict, rows: int, cols: int, dtype: str) -> np.ndarray:
     """Decodes libsdd's documented tiled weight layout (sdd_model_matrix_layout) back to a row-major
     [rows][cols] matrix.
 
     Tiles of 16 rows x kt columns (kt 32 for bf16, 16 for fp32), 1 KiB each; lane l of a tile holds row l%16
     and 16/elem columns from (l//16)*16/elem.  Unit (g, k) = the ng row tiles of column group g at k-step k;
-    workgroup w of n_wg owns units [w*U//n_wg, (w+1)*U//n_wg) of U = G*KT (u = g*KT + k), and its i-th unit
-    sits at slot i*n_wg + w; tile j of a unit at byte offset + (slot*ng + j)*1024."""
+    workgroup w of n_wg owns units [start(w), start(w+1)) of U = G*KT (u = g*KT + k; share_starts), and its
+    i-th unit sits at slot i*n_wg + w; tile j of a unit at byte offset + (slot*ng + j)*1024."""
     es = 2 if dtype == "bf16" else 4
     epl = 16 // es
     kt = 4 * epl
     KT, G, ng, nwg = layout["KT"], layout["G"], layout["ng"], layout["n_wg"]
     U = G * KT
+    st = share_starts(KT, G, layout["c"], nwg)
     u = np.arange(U, dtype=np.int64)
-    w = np.searchsorted(np.arange(1, nwg + 1, dtype=np.int64) * U // nwg, u, side="right")  # owner of unit u
-    slot = (u - w * U // nwg) * nwg + w
+    w = np.searchsorted(st[1:], u, side="right")  # owner of unit u
+    slot = (u - st[w]) * nwg + w
     raw = buf[layout["offset"]: layout["offset"] + layout["bytes"]]
     if dtype == "bf16":
         vals = W.bf16_bits_to_f32(raw.view(np.uint16))

@@ -4,7 +4,10 @@ import ctypes as C
 import os
 import re
 
+import numpy as np
 import pytest
+
+from gpu_helpers import share_starts
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
@@ -49,24 +52,46 @@ def test_host_side_argument_errors(S):
     h = C.c_void_p()
     assert L.sdd_model_create(C.byref(cfg), C.c_void_p(1 << 20), total, C.byref(h)) == S.OK
     off, nb = C.c_size_t(), C.c_size_t()
-    kt, g, ng, nwg = C.c_int(), C.c_int(), C.c_int(), C.c_int()
+    kt, g, ng, nwg, sc = C.c_int(), C.c_int(), C.c_int(), C.c_int(), C.c_int()
     d, hd, V, dff = 256, 64, 4096, 688
     spans = []
     for kind, layer, rows, cols in [(1, 0, V, d)] + [(k, l, r, c) for l in range(2) for k, r, c in
                                                       ((3, 4 * hd + 2 * 2 * hd, d), (6, d, 4 * hd),
                                                        (7, 2 * dff, d), (9, d, dff))]:
         assert L.sdd_model_matrix_layout(h, kind, layer, C.byref(off), C.byref(nb), C.byref(kt), C.byref(g),
-                                         C.byref(ng), C.byref(nwg)) == S.OK
+                                         C.byref(ng), C.byref(nwg), C.byref(sc)) == S.OK
         U = g.value * kt.value
         assert g.value * ng.value * 16 >= rows and kt.value * 16 >= cols
-        assert 1 <= nwg.value <= U and nb.value == -(-U // nwg.value) * nwg.value * ng.value * 1024
+        # at most 256 groups: equal shares (or equal k-ranges of every group)
+        assert sc.value == 0 and 1 <= nwg.value <= U and nb.value == -(-U // nwg.value) * nwg.value * ng.value * 1024
         spans.append((off.value, off.value + nb.value))
     spans.sort()
     assert all(a1 <= b0 for (_, a1), (b0, _) in zip(spans, spans[1:])) and spans[-1][1] <= total
     assert L.sdd_model_matrix_layout(h, 2, 0, C.byref(off), C.byref(nb), C.byref(kt), C.byref(g), C.byref(ng),
-                                     C.byref(nwg)) == S.EINVAL
+                                     C.byref(nwg), C.byref(sc)) == S.EINVAL
     assert L.sdd_model_matrix_layout(h, 3, 2, C.byref(off), C.byref(nb), C.byref(kt), C.byref(g), C.byref(ng),
-                                     C.byref(nwg)) == S.EINVAL
+                                     C.byref(nwg), C.byref(sc)) == S.EINVAL
+    assert L.sdd_model_matrix_layout(h, 3, 0, C.byref(off), C.byref(nb), C.byref(kt), C.byref(g), C.byref(ng),
+                                     C.byref(nwg), None) == S.EINVAL
+    assert L.sdd_model_destroy(h) == S.OK
+    # a 51200-token vocabulary gives the LM head 400 column groups of 8 tiles: stream-K over the 256-CU count
+    # the library plans for, with cost-balanced shares (every share non-empty and contiguous; the matrix holds
+    # n_wg times the longest share; a share entering one more group holds fewer units)
+    wide = S.ModelConfig(2, 256, 4, 2, 64, 688, 51200, 1e-6, 1e4, 0, S.F32)
+    assert L.sdd_weights_bytes(C.byref(wide), C.byref(out)) == S.OK
+    h = C.c_void_p()
+    assert L.sdd_model_create(C.byref(wide), C.c_void_p(1 << 20), out.value, C.byref(h)) == S.OK
+    assert L.sdd_model_matrix_layout(h, 1, 0, C.byref(off), C.byref(nb), C.byref(kt), C.byref(g), C.byref(ng),
+                                     C.byref(nwg), C.byref(sc)) == S.OK
+    KT, G, n, c = kt.value, g.value, nwg.value, sc.value
+    assert G * ng.value * 16 == 51200 and G > n and c > 0
+    st = share_starts(KT, G, c, n)
+    shares = np.diff(st)
+    assert st[0] == 0 and st[-1] == G * KT and shares.min() >= 1
+    assert nb.value == shares.max() * n * ng.value * 1024
+    segs = (st[1:] - 1) // KT - st[:-1] // KT + 1
+    cost = shares + c * (segs - 1)
+    assert cost.max() - cost.min() <= c + 1 and shares.max() > shares.min()
     assert L.sdd_model_destroy(h) == S.OK
     bad = S.ModelConfig(2, 256, 4, 2, 96, 688, 4096, 1e-6, 1e4, 0, S.F32)
     assert L.sdd_weights_bytes(C.byref(bad), C.byref(out)) == S.EUNSUPPORTED

@@ -16,6 +16,8 @@ pytestmark = pytest.mark.gpu
 
 MID_BF16 = W.ModelShape(2, 512, 8, 2, 64, 1024, 2048, 1e-6, 1e6, True, "bf16")
 MID_GQA128 = W.ModelShape(2, 256, 8, 2, 128, 512, 1024, 1e-6, 1e6, False, "bf16")
+# 400 column groups of LM head over 256 workgroups: stream-K with unequal (cost-balanced) shares
+WIDE_VOCAB = W.ModelShape(2, 256, 8, 2, 128, 512, 51200, 1e-6, 1e6, False, "bf16")
 
 
 @pytest.fixture(scope="module")
@@ -56,6 +58,16 @@ def test_weight_generator_bit_identical(S):
     want = oracle.weight_values(0, oracle.tensor_id(oracle.EMBED), 0, V * d, 0.02, True).reshape(V, d)
     assert np.array_equal(emb, want)
     lm = untile(b2, m2.matrix_layout(1), V, d, "bf16")
+    want = oracle.weight_values(0, oracle.tensor_id(oracle.LM_HEAD), 0, V * d, 0.02, True).reshape(V, d)
+    assert np.array_equal(lm, want)
+    # an LM head stored in cost-balanced stream-K order (unequal shares)
+    m3 = _gpu_model(S, WIDE_VOCAB)
+    torch.cuda.synchronize()
+    lay = m3.matrix_layout(1)
+    assert lay["c"] > 0 and lay["G"] > lay["n_wg"]
+    b3 = m3.buf.cpu().numpy()
+    V, d = WIDE_VOCAB.vocab, WIDE_VOCAB.d_model
+    lm = untile(b3, lay, V, d, "bf16")
     want = oracle.weight_values(0, oracle.tensor_id(oracle.LM_HEAD), 0, V * d, 0.02, True).reshape(V, d)
     assert np.array_equal(lm, want)
 
@@ -109,7 +121,7 @@ def test_tiny_fp32_prefill_verify_commit(S):
     _run_case(S, W.TINY, W.TINY_PROMPT, W.GAMMA_TINY, seed=1, n_rounds=3)
 
 
-@pytest.mark.parametrize("shape", [MID_BF16, MID_GQA128], ids=["hd64-qknorm", "hd128-gqa4"])
+@pytest.mark.parametrize("shape", [MID_BF16, MID_GQA128, WIDE_VOCAB], ids=["hd64-qknorm", "hd128-gqa4", "wide-vocab"])
 def test_small_bf16(S, shape):
     _run_case(S, shape, 40, 32, seed=2, n_rounds=2)
 
