@@ -391,6 +391,314 @@ __global__ void __launch_bounds__(kGemmThreads, 1) gemm_kernel(GemmArgs a) {
 }
 
 // ---------------------------------------------------------------------------
+// Stream-K GEMM with the segment boundaries taken off the stream (bf16, column
+// groups of 8 tiles, the register-only epilogues: SwiGLU and the LM head; at
+// most 48 rows).  At a segment boundary the 4-wave kernel above issues no new
+// loads until the four waves have summed their accumulators, published or
+// finished the group: every boundary delays the workgroup's stream by its
+// length.  Here a workgroup is 8 waves.  Waves 0-3 stream exactly as the four
+// waves above (same k-steps, same accumulation) and at the end of a segment
+// only drop their accumulators into LDS and go on streaming the next one.
+// Wave 4 + f (f < TB) owns rows 16 f .. 16 f + 15: per segment it sums the
+// four streaming waves' accumulators of that row tile, publishes them or
+// finishes the group (its arrival counter is per (group, row tile), so these
+// waves never wait for each other) and runs the epilogue in the accumulators'
+// register layout.  Every sum is taken in the order of the kernel above, so
+// both give the same bits.  The two roles hand over through two LDS counters
+// (accumulators filled, released): one segment's accumulators at a time.
+// Two waves share a SIMD, so a streaming wave keeps 3 register stages (2 in
+// flight) where the 4-wave kernel keeps 4.
+constexpr int kWsThreads = 512;
+// LDS waits give up after this many polls (about 0.2 s): a broken hand-off
+// ends the kernel with wrong results instead of hanging it
+constexpr int kWsSpinMax = 1 << 22;
+
+__device__ inline bool ws_wait_geq(int* p, int target) {
+  for (int it = 0; it < kWsSpinMax; ++it) {
+    if (__hip_atomic_load(p, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP) >= target) return true;
+    __builtin_amdgcn_s_sleep(1);
+  }
+  return false;
+}
+// one arrival per wave (lane 0), after the wave's earlier LDS accesses
+__device__ inline void ws_signal(int* p, int lane) {
+  if (lane == 0) __hip_atomic_fetch_add(p, 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
+}
+
+// SwiGLU of one row tile in the accumulator layout: lane l holds row 16 f + l % 16 and, of tile nt,
+// columns nt * 16 + 4 (l / 16) + e; gate tile 2 t and up tile 2 t + 1 hold the same hidden units, so a
+// lane computes 4 consecutive hidden outputs per pair on its own.
+__device__ inline void ws_epilogue_swiglu(const GemmArgs& a, const f32x4* v, int g, int f, float r, int lane) {
+#pragma clang fp contract(off)
+  const int mm = 16 * f + lane % 16;
+  if (mm >= a.M) return;
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    float hv[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float gt = v[2 * t][e] * r;
+      const float up = v[2 * t + 1][e] * r;
+      hv[e] = gt / (1.f + expf(-gt)) * up;
+    }
+    const int64_t off = (int64_t)(a.m0 + mm) * a.dff + (int64_t)g * 64 + t * 16 + 4 * (lane / 16);
+    *reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(a.ffh) + off) =
+        make_uint2(pack_bf16x2(hv[0], hv[1]), pack_bf16x2(hv[2], hv[3]));
+  }
+}
+
+// LM head of one row tile in the accumulator layout: fp32 logits of the valid rows and each row's best
+// (value, lowest index) over the group's columns below V (a row's 4 lanes combined by exchanges).
+__device__ inline void ws_epilogue_logits(const GemmArgs& a, const f32x4* v, int g, int f, float r, bool valid,
+                                          int lane) {
+#pragma clang fp contract(off)
+  const int mm = 16 * f + lane % 16;
+  float bv = -INFINITY;
+  int bi = -1;
+#pragma unroll
+  for (int nt = 0; nt < 8; ++nt) {
+    const int n0 = g * 128 + nt * 16 + 4 * (lane / 16);
+    float x[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) x[e] = v[nt][e] * r;
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      if (n0 + e < a.V && arg_better(x[e], n0 + e, bv, bi)) {
+        bv = x[e];
+        bi = n0 + e;
+      }
+    if (mm < a.M && valid) {
+      float* lr = a.logits + (int64_t)(a.m0 + mm) * a.V + n0;
+      if ((a.V & 3) == 0 && n0 + 4 <= a.V) {
+        *reinterpret_cast<f32x4*>(lr) = f32x4{x[0], x[1], x[2], x[3]};
+      } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          if (n0 + e < a.V) lr[e] = x[e];
+      }
+    }
+  }
+#pragma unroll
+  for (int o = 16; o <= 32; o *= 2) {
+    const float v2 = __shfl_xor(bv, o);
+    const int i2 = __shfl_xor(bi, o);
+    if (arg_better(v2, i2, bv, bi)) {
+      bv = v2;
+      bi = i2;
+    }
+  }
+  if (lane < 16 && mm < a.M) {
+    a.amax_v[(int64_t)g * a.mp + a.m0 + mm] = bv;
+    a.amax_i[(int64_t)g * a.mp + a.m0 + mm] = bi;
+  }
+}
+
+template <int TB, int EPI>
+__global__ void __launch_bounds__(kWsThreads, 1) gemm_ws_kernel(GemmArgs a) {
+  static_assert(EPI == EPI_SWIGLU || EPI == EPI_LOGITS, "register-only epilogues");
+  static_assert(TB >= 1 && TB <= 3, "at most 48 rows");
+  constexpr int NG = 8, C = NG * 16, NACC = NG * TB, EPL = 8, KTILE = 32;
+  __shared__ f32x4 red[4][NACC][kWave];
+  __shared__ int s_fill, s_free;
+  touch_kernargs<GemmArgs>();
+  const int w = blockIdx.x;
+  const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave), lane = threadIdx.x % kWave;
+  const uint32_t KT = (uint32_t)a.KT, G = (uint32_t)a.G, SC = (uint32_t)a.segc;
+  const uint32_t u0 = unit_start(w, KT, G, SC, a.n_wg), u1 = unit_start(w + 1, KT, G, SC, a.n_wg);
+  if (threadIdx.x == 0) {
+    s_fill = 0;
+    s_free = 0;
+  }
+  __syncthreads();  // the only workgroup barrier: the roles part here
+
+  if (wv < 4) {
+    // ---- streaming waves ----
+    const int wave = wv;
+    const __amdgpu_buffer_rsrc_t xrs = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<char*>(a.X), 0, (a.m0 + a.M) * a.ldx * 2, kBufferRsrcWord3);
+    const int xlane = ((a.m0 + lane % 16) * a.ldx + (lane / 16) * EPL) * 2;  // < 2^31: checked on the host
+    const int xrow16 = 16 * a.ldx * 2;
+    const uint32_t slot_bytes = (uint32_t)NG * kWave * 16, wstride = (uint32_t)a.n_wg * slot_bytes;
+    const __amdgpu_buffer_rsrc_t wrs =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(a.W), 0, (int)(a.share * wstride), kBufferRsrcWord3);
+    const __amdgpu_buffer_rsrc_t nrs = __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(a.W), 0, 0, kBufferRsrcWord3);
+    const uint32_t kstep4w = 4u * wstride, kstep4x = 4u * KTILE * 2;
+    const int wlane = lane * 16;
+    // local k-step kt of this wave in its segment (as in the 4-wave kernel)
+    auto load = [&](uint32_t wo, uint32_t xo, int kt, int kz, uint4* wa, uint4* xb) {
+      const bool in = kt < kz;
+      const __amdgpu_buffer_rsrc_t wd = in ? wrs : nrs, xd = in ? xrs : nrs;
+#pragma unroll
+      for (int nt = 0; nt < NG; ++nt)
+        wa[nt] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(
+                                               wd, wlane, (int)(wo + (uint32_t)kt * kstep4w + (uint32_t)nt * kWave * 16), kNtCpol));
+#pragma unroll
+      for (int tb = 0; tb < TB; ++tb)
+        xb[tb] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(xd, xlane + tb * xrow16,
+                                                                                   (int)(xo + (uint32_t)kt * kstep4x), 0));
+      __builtin_amdgcn_sched_barrier(0);
+    };
+    struct Seg {
+      int kz;
+      uint32_t wo, xo, len;
+    };
+    auto make_seg = [&](uint32_t u) {
+      Seg s;
+      const int g = (int)(u / KT), kb = (int)(u - (uint32_t)g * KT);
+      const int ke = (int)std::min<uint32_t>(KT, kb + (u1 - u));
+      const int S = ke - kb;
+      s.len = (uint32_t)S;
+      s.kz = __builtin_amdgcn_readfirstlane(S > wave ? (S - wave + 3) / 4 : 0);
+      s.wo = __builtin_amdgcn_readfirstlane((u - u0 + (uint32_t)wave) * wstride + (uint32_t)w * slot_bytes);
+      s.xo = __builtin_amdgcn_readfirstlane((uint32_t)(kb + wave) * KTILE * 2);
+      return s;
+    };
+    uint4 wa0[NG], wa1[NG], wa2[NG], xb0[TB], xb1[TB], xb2[TB];
+    auto issue = [&](const Seg& sg) {
+      load(sg.wo, sg.xo, 0, sg.kz, wa0, xb0);
+      load(sg.wo, sg.xo, 1, sg.kz, wa1, xb1);
+    };
+    uint32_t u = u0;
+    Seg s = make_seg(u);
+    issue(s);
+    for (int j = 0;; ++j) {
+      f32x4 acc[NACC];
+#pragma unroll
+      for (int i = 0; i < NACC; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+      auto mma = [&](const uint4* wa, const uint4* xb) {
+#pragma unroll
+        for (int nt = 0; nt < NG; ++nt)
+#pragma unroll
+          for (int tb = 0; tb < TB; ++tb) mma_tile<uint16_t>(wa[nt], xb[tb], acc[nt * TB + tb]);
+      };
+      const uint32_t wo = s.wo, xo = s.xo;
+      int kt = 0;
+      for (; kt + 3 <= s.kz; kt += 3) {
+        load(wo, xo, kt + 2, s.kz, wa2, xb2);
+        mma(wa0, xb0);
+        load(wo, xo, kt + 3, s.kz, wa0, xb0);
+        mma(wa1, xb1);
+        load(wo, xo, kt + 4, s.kz, wa1, xb1);
+        mma(wa2, xb2);
+      }
+      // 0..2 k-steps left, already loaded in stages 0 and 1
+      const int left = s.kz - kt;
+      if (left > 0) mma(wa0, xb0);
+      if (left > 1) mma(wa1, xb1);
+      u += s.len;
+      const bool more = u < u1;
+      // the next segment's first stages go out before the hand-off (every
+      // older load has landed: waiting for them first tells the compiler so)
+      __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+      if (more) {
+        s = make_seg(u);
+        issue(s);
+      }
+      // hand the accumulators over once the finishing waves have released the previous segment's
+      if (!ws_wait_geq(&s_free, TB * j)) return;
+#pragma unroll
+      for (int i = 0; i < NACC; ++i) red[wave][i][lane] = acc[i];
+      ws_signal(&s_fill, lane);
+      if (!more) break;
+    }
+    // this workgroup's stream is done: the next GEMM's first k-steps into L2
+    if (a.Wn && (int)blockIdx.x < a.nwg_n) prefetch_next(a, wave, lane);
+    return;
+  }
+
+  // ---- finishing waves: wave 4 + f owns row tile f ----
+  const int f = wv - 4;
+  if (f >= TB) return;
+  const int row = 16 * f + lane % 16;  // this lane's row (of the padded rows)
+  // RMSNorm row scale from the producer's per-group sums of squares, summed as
+  // in the 4-wave kernel: four partial sums over every fourth group (lane / 16
+  // selects which), then (s0 + s1) + (s2 + s3)
+  float r = 1.f;
+  bool valid = false;
+  {
+    const int ng_in = a.ss_in ? a.ss_groups : 0;
+    const int q4 = lane / 16;
+    float ssum = 0.f;
+    if (row < a.M)
+      for (int gg = q4; gg < ng_in; gg += 4) ssum += a.ss_in[(int64_t)gg * a.mp + a.m0 + row];
+    float t = xor16_op(ssum, [](float x, float y) { return x + y; });
+    t = xor32_op(t, [](float x, float y) { return x + y; });
+    if (ng_in) r = 1.f / sqrtf(t / (float)a.d_in + a.eps);
+    if constexpr (EPI == EPI_LOGITS) valid = row < a.M && a.rows[a.m0 + row].valid;
+  }
+  const int g_first = (int)(u0 / KT);
+  const int MC = a.M * C;
+  const __amdgpu_buffer_rsrc_t prs = __builtin_amdgcn_make_buffer_rsrc(a.part, 0, 0x7fffffff, kBufferRsrcWord3);
+  const bool rin = row < a.M;
+  const int elt = row * C + 4 * (lane / 16);  // float offset of the lane's first element (tile 0) in a partial
+  uint32_t u = u0;
+  for (int j = 0; u < u1; ++j) {
+    const int g = (int)(u / KT), kb = (int)(u - (uint32_t)g * KT);
+    const int ke = (int)std::min<uint32_t>(KT, kb + (u1 - u));
+    u += (uint32_t)(ke - kb);
+    if (!ws_wait_geq(&s_fill, 4 * (j + 1))) return;
+    f32x4 v[NG];
+#pragma unroll
+    for (int nt = 0; nt < NG; ++nt) {
+      const int i = nt * TB + f;
+      v[nt] = (red[0][i][lane] + red[2][i][lane]) + (red[1][i][lane] + red[3][i][lane]);
+    }
+    ws_signal(&s_free, lane);
+    bool fin = true;
+    if (!(kb == 0 && ke == (int)KT)) {
+      // split group: publish this row tile's partial; the last contributor's wave f finishes it
+      const int which = g == g_first ? 0 : 1;
+      const int my_off = ((w * 2 + which) * MC) * 4;
+#pragma unroll
+      for (int nt = 0; nt < NG; ++nt)
+        if (rin)
+          __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v[nt]), prs, my_off + 4 * (elt + nt * 16), 0,
+                                                 kCoherentCpol);
+      const int wf = unit_owner((uint32_t)g * KT, KT, G, SC, a.n_wg);
+      const int wl = unit_owner((uint32_t)(g + 1) * KT - 1, KT, G, SC, a.n_wg);
+      wait_stores();
+      int last = 0;
+      if (lane == 0) {
+        int* cnt = &a.cnt[(g * 4 + f) * kCntStride];
+        const int old = __hip_atomic_fetch_add(cnt, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        last = old == wl - wf;
+        if (last) __hip_atomic_store(cnt, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      }
+      fin = __builtin_amdgcn_readfirstlane(last) != 0;
+      if (fin) {
+        // contributors added in workgroup order (as the 4-wave kernel), two in flight at once
+        const bool wf_first = unit_start(wf, KT, G, SC, a.n_wg) == (uint32_t)g * KT;
+#pragma unroll
+        for (int nt = 0; nt < NG; ++nt) v[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int ww = wf; ww <= wl; ww += 2) {
+          f32x4 p[2][NG];
+#pragma unroll
+          for (int q = 0; q < 2; ++q) {
+            const int wq = std::min(ww + q, wl);
+            const int slot = (wq > wf || wf_first) ? 0 : 1;
+            const int src = ((wq * 2 + slot) * MC) * 4;
+#pragma unroll
+            for (int nt = 0; nt < NG; ++nt)
+              p[q][nt] = (rin && ww + q <= wl) ? __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                                                                                prs, src + 4 * (elt + nt * 16), 0, kCoherentCpol))
+                                               : f32x4{0.f, 0.f, 0.f, 0.f};
+          }
+#pragma unroll
+          for (int q = 0; q < 2; ++q)
+            if (ww + q <= wl)
+#pragma unroll
+              for (int nt = 0; nt < NG; ++nt) v[nt] += p[q][nt];
+        }
+      }
+    }
+    if (fin) {
+      if constexpr (EPI == EPI_SWIGLU) ws_epilogue_swiglu(a, v, g, f, r, lane);
+      if constexpr (EPI == EPI_LOGITS) ws_epilogue_logits(a, v, g, f, r, valid, lane);
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Attention, plain VALU version (fp32 models): one workgroup per (row, query
 // head).  Scores of a chunk of positions go to LDS; the softmax is carried
 // online across chunks.
@@ -952,6 +1260,16 @@ static void launch_gemm_tb(int tb, const GemmArgs& a, int nblocks, hipStream_t s
   }
 }
 
+// the 8-wave stream-K kernel (bf16, 8-tile groups, SwiGLU or LM head, at most 3 row tiles)
+template <int EPI>
+static void launch_gemm_ws(int tb, const GemmArgs& a, int nblocks, hipStream_t st) {
+  switch (tb) {
+    case 1: hipLaunchKernelGGL((gemm_ws_kernel<1, EPI>), dim3(nblocks), dim3(kWsThreads), 0, st, a); break;
+    case 2: hipLaunchKernelGGL((gemm_ws_kernel<2, EPI>), dim3(nblocks), dim3(kWsThreads), 0, st, a); break;
+    default: hipLaunchKernelGGL((gemm_ws_kernel<3, EPI>), dim3(nblocks), dim3(kWsThreads), 0, st, a); break;
+  }
+}
+
 template <typename T, int EPI>
 static void launch_gemm_ng(int ng, int tb, const GemmArgs& a, int nblocks, hipStream_t st) {
   switch (ng) {
@@ -1037,8 +1355,18 @@ static int run_gemm(CallCtx& cx, int epi, unsigned prof, size_t w_off, int64_t N
       switch (epi) {
         case EPI_QKV: launch_gemm_ng<uint16_t, EPI_QKV>(ng, tb, a, nblocks, cx.st); break;
         case EPI_RESID: launch_gemm_ng<uint16_t, EPI_RESID>(ng, tb, a, nblocks, cx.st); break;
-        case EPI_SWIGLU: launch_gemm_ng<uint16_t, EPI_SWIGLU>(ng, tb, a, nblocks, cx.st); break;
-        default: launch_gemm_ng<uint16_t, EPI_LOGITS>(ng, tb, a, nblocks, cx.st); break;
+        case EPI_SWIGLU:
+          if (ng == 8 && tb <= 3)
+            launch_gemm_ws<EPI_SWIGLU>(tb, a, nblocks, cx.st);
+          else
+            launch_gemm_ng<uint16_t, EPI_SWIGLU>(ng, tb, a, nblocks, cx.st);
+          break;
+        default:
+          if (ng == 8 && tb <= 3)
+            launch_gemm_ws<EPI_LOGITS>(tb, a, nblocks, cx.st);
+          else
+            launch_gemm_ng<uint16_t, EPI_LOGITS>(ng, tb, a, nblocks, cx.st);
+          break;
       }
     } else {
       switch (epi) {
