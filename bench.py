@@ -536,7 +536,7 @@ def main():
         "accepted_tokens_per_s": float((acc_l + 1).sum()) * 1e3 / (ms * a.steps),
         "call_hbm_frac": call_bytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
         "call_bytes": call_bytes,
-        "roofline": {"bound": "hbm", "kernel": "gemm_kernel gate/up (SwiGLU epilogue)",
+        "roofline": {"bound": "hbm", "kernel": "gemm_ws_kernel gate/up (SwiGLU epilogue)",
                      "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
                      "traffic": measured_traffic() if a.workload == "qwen32b" else None,
                      "traffic_source": os.path.relpath(TRAFFIC_FILE, ROOT), "bytes_per_launch": gu_bytes, "launches": n_dom,
