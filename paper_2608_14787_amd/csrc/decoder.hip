@@ -612,19 +612,35 @@ __global__ void __launch_bounds__(kWsThreads, 1) gemm_ws_kernel(GemmArgs a) {
   const int row = 16 * f + lane % 16;  // this lane's row (of the padded rows)
   // RMSNorm row scale from the producer's per-group sums of squares, summed as
   // in the 4-wave kernel: four partial sums over every fourth group (lane / 16
-  // selects which), then (s0 + s1) + (s2 + s3)
+  // selects which), then (s0 + s1) + (s2 + s3).  The loads go out in one batch
+  // (kPre per lane, groups past 4 kPre in a plain loop): one at a time, at the
+  // latency of a memory system the streaming waves keep full, they held the
+  // first segment's finishing back by ~45 us.
   float r = 1.f;
   bool valid = false;
   {
+    constexpr int kPre = 24;
     const int ng_in = a.ss_in ? a.ss_groups : 0;
     const int q4 = lane / 16;
+    const int64_t rr = a.m0 + (row < a.M ? row : 0);
+    float pre[kPre];
+    if (ng_in > 0) {
+#pragma unroll
+      for (int j = 0; j < kPre; ++j) pre[j] = a.ss_in[(int64_t)min(q4 + 4 * j, ng_in - 1) * a.mp + rr];
+    }
+    int vld = 0;
+    if constexpr (EPI == EPI_LOGITS) vld = a.rows[rr].valid;
     float ssum = 0.f;
-    if (row < a.M)
-      for (int gg = q4; gg < ng_in; gg += 4) ssum += a.ss_in[(int64_t)gg * a.mp + a.m0 + row];
+    if (ng_in > 0 && row < a.M) {
+#pragma unroll
+      for (int j = 0; j < kPre; ++j)
+        if (q4 + 4 * j < ng_in) ssum += pre[j];
+      for (int gg = q4 + 4 * kPre; gg < ng_in; gg += 4) ssum += a.ss_in[(int64_t)gg * a.mp + rr];
+    }
     float t = xor16_op(ssum, [](float x, float y) { return x + y; });
     t = xor32_op(t, [](float x, float y) { return x + y; });
     if (ng_in) r = 1.f / sqrtf(t / (float)a.d_in + a.eps);
-    if constexpr (EPI == EPI_LOGITS) valid = row < a.M && a.rows[a.m0 + row].valid;
+    if constexpr (EPI == EPI_LOGITS) valid = row < a.M && vld != 0;
   }
   const int g_first = (int)(u0 / KT);
   const int MC = a.M * C;
