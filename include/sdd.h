@@ -144,7 +144,8 @@ int sdd_kv_destroy(sdd_kv* kv);
  * (host pointers, either may be NULL) and the sticky error word (bit0: a
  * capacity overflow was refused on the device, bit1: a token outside
  * [0, vocab) was replaced by 0, bit2: a sequence id outside [0, max_batch)
- * was refused). */
+ * was refused, bit3: a GEMM workgroup's internal hand-off between its waves
+ * gave up after its bounded wait, so that call's outputs are invalid). */
 int sdd_kv_state(sdd_kv* kv, int32_t* len, int32_t* pending, int32_t* error_bits,
                  sdd_stream_t stream);
 

@@ -420,6 +420,10 @@ __device__ inline bool ws_wait_geq(int* p, int target) {
   }
   return false;
 }
+// a hand-off that gave up: the call's results are invalid, reported in the sticky error word
+__device__ inline void ws_fail(int32_t* err, int lane) {
+  if (err && lane == 0) atomicOr(err, 8);
+}
 // one arrival per wave (lane 0), after the wave's earlier LDS accesses
 __device__ inline void ws_signal(int* p, int lane) {
   if (lane == 0) __hip_atomic_fetch_add(p, 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
@@ -595,7 +599,7 @@ __global__ void __launch_bounds__(kWsThreads, 1) gemm_ws_kernel(GemmArgs a) {
         issue(s);
       }
       // hand the accumulators over once the finishing waves have released the previous segment's
-      if (!ws_wait_geq(&s_free, TB * j)) return;
+      if (!ws_wait_geq(&s_free, TB * j)) return ws_fail(a.err, lane);
 #pragma unroll
       for (int i = 0; i < NACC; ++i) red[wave][i][lane] = acc[i];
       ws_signal(&s_fill, lane);
@@ -652,7 +656,7 @@ __global__ void __launch_bounds__(kWsThreads, 1) gemm_ws_kernel(GemmArgs a) {
     const int g = (int)(u / KT), kb = (int)(u - (uint32_t)g * KT);
     const int ke = (int)std::min<uint32_t>(KT, kb + (u1 - u));
     u += (uint32_t)(ke - kb);
-    if (!ws_wait_geq(&s_fill, 4 * (j + 1))) return;
+    if (!ws_wait_geq(&s_fill, 4 * (j + 1))) return ws_fail(a.err, lane);
     f32x4 v[NG];
 #pragma unroll
     for (int nt = 0; nt < NG; ++nt) {
@@ -1322,6 +1326,7 @@ static int run_gemm(CallCtx& cx, int epi, unsigned prof, size_t w_off, int64_t N
   a.ldx = K;
   a.mp = cx.L.mp;
   a.part = reinterpret_cast<float*>(cx.ws + cx.L.part);
+  a.err = cx.kv ? cx.kv->err : nullptr;
   a.cnt = reinterpret_cast<int*>(cx.ws + cx.L.cnt);
   a.rows = reinterpret_cast<const RowInfo*>(cx.ws + cx.L.rowinfo);
   a.eps = m->cfg.rms_eps;

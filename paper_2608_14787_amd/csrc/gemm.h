@@ -33,6 +33,7 @@ struct GemmArgs {
   int segc;       // virtual units per column group of the plan (cost-balanced shares; 0: equal)
   int share;      // longest share (units): the stored matrix holds share x n_wg slots
   float* part;    // partial tiles [n_wg][2][M][NG*16]
+  int32_t* err;   // the KV cache's sticky error word (bit3: a workgroup's internal hand-off gave up)
   int* cnt;       // arrival counter per column group (group g at cnt[g * kCntStride])
   const RowInfo* rows;
   // RMSNorm of the input rows: r_m = 1/sqrt(sum_g ss_in[g][m] / d_in + eps),
