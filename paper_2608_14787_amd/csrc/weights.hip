@@ -159,12 +159,12 @@ static size_t plan_weights(const sdd_model_config* c, sdd_model* m, int n_cu) {
   const int64_t d = c->d_model, hd = c->head_dim, hq = c->n_q_heads * hd, hk = c->n_kv_heads * hd;
   // row tiles per column group
   const int ng_qkv = (int)(hd / 16);
-  // 128-column groups everywhere: o_proj's (few output columns, long K) are
-  // split over ~6 workgroups each, whose last one sums more partials than with
-  // 64-column groups, but each 8 KiB k-step carries twice the weight bytes per
-  // activation fragment loaded (measured on the Qwen3-32B step: o_proj 23.4 ->
-  // 22.2 us per layer)
-  const int ng_o = pick_ng(d / 16, false);
+  // o_proj has few output columns and a long K, so 128-column groups would
+  // each be split over ~6 workgroups' equal shares; 64-column groups halve
+  // the contributors a split group's last workgroup reduces.  (down_proj
+  // streams 3x the bytes and keeps 128-column groups: their 8 KiB k-steps
+  // keep more bytes in flight per wave.)
+  const int ng_o = pick_ng(d / 16, false, 4);
   const int ng_gu = pick_ng(2 * (int64_t)c->d_ff / 16, true);
   const int ng_down = pick_ng(d / 16, false);
   const int ng_lm = pick_ng(c->vocab / 16, false);
