@@ -135,3 +135,43 @@ def test_host_side_argument_errors(S):
     assert sched(special=None, n_special=1, draft=P) == S.EINVAL
     assert sched(special=P, n_special=1, draft=None) == S.EINVAL  # the special-token guard reads drafts
     assert sched(rep_max=2, draft=None) == S.EINVAL
+
+
+@pytest.mark.parametrize("which", ["QWEN32B", "QWEN7B"])
+def test_streaming_plans_of_the_real_shapes(S, which):
+    """Host-only layout queries of the Qwen-shaped models (weights over an unused address): every
+    stream-K plan (more column groups than workgroups) balances its shares by cost (c > 0, every share
+    non-empty, costs within c + 1 of each other); every plan with fewer groups than workgroups splits
+    each group into equal k-ranges (c = 0); each matrix's extent is n_wg times its longest share."""
+    import workloads as W
+    shape = getattr(W, which)
+    L = S.lib()
+    cfg = S.ModelConfig.from_shape(shape)
+    out = C.c_size_t()
+    assert L.sdd_weights_bytes(C.byref(cfg), C.byref(out)) == S.OK
+    h = C.c_void_p()
+    assert L.sdd_model_create(C.byref(cfg), C.c_void_p(1 << 20), out.value, C.byref(h)) == S.OK
+    off, nb = C.c_size_t(), C.c_size_t()
+    kt, g, ng, nwg, sc = C.c_int(), C.c_int(), C.c_int(), C.c_int(), C.c_int()
+    seen = set()
+    for kind, layer in [(S.T_LM_HEAD, 0), (S.T_WQ, 0), (S.T_WO, 0), (S.T_WGATE, 0), (S.T_WDOWN, shape.n_layers - 1)]:
+        assert L.sdd_model_matrix_layout(h, kind, layer, C.byref(off), C.byref(nb), C.byref(kt), C.byref(g),
+                                         C.byref(ng), C.byref(nwg), C.byref(sc)) == S.OK
+        KT, G, n, c = kt.value, g.value, nwg.value, sc.value
+        st = share_starts(KT, G, c, n)
+        shares = np.diff(st)
+        assert st[0] == 0 and st[-1] == G * KT and shares.min() >= 1
+        assert nb.value == shares.max() * n * ng.value * 1024
+        if G > n:
+            assert c > 0
+            segs = (st[1:] - 1) // KT - st[:-1] // KT + 1
+            cost = shares + c * (segs - 1)
+            assert cost.max() - cost.min() <= c + 1, (kind, cost.min(), cost.max())
+        else:
+            split = n // G
+            assert c == 0 and n % G == 0 and np.isin(shares, [KT // split, -(-KT // split)]).all()
+            # one segment per workgroup: a share never crosses a group boundary
+            assert ((st[1:] - 1) // KT == st[:-1] // KT).all()
+        seen.add("streamk" if G > n else "split")
+    assert seen == {"streamk", "split"}
+    assert L.sdd_model_destroy(h) == S.OK
