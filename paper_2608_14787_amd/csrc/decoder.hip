@@ -410,7 +410,7 @@ __global__ void __launch_bounds__(kGemmThreads, 1) gemm_kernel(GemmArgs a) {
 // flight) where the 4-wave kernel keeps 4.
 constexpr int kWsThreads = 512;
 // LDS waits give up after this many polls (about 0.2 s): a broken hand-off
-// ends the kernel with wrong results instead of hanging it
+// ends the kernel, with bit3 of the sticky error word set, instead of hanging it
 constexpr int kWsSpinMax = 1 << 22;
 
 __device__ inline bool ws_wait_geq(int* p, int target) {
