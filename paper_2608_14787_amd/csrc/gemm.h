@@ -145,7 +145,9 @@ __device__ inline void prefetch_next(const GemmArgs& a, int wave, int lane) {
 }
 
 // Epilogues run on the final [rows][C] tile of one column group (LDS, row
-// stride C + 4).  Each wave owns rows wave, wave + 4, ... (R / 4 of them, the
+// stride C + 4), on 4 waves (wave index taken mod 4, so that the two halves of
+// an 8-wave workgroup can run two chunks of a tile at once).  Each wave owns
+// rows wave, wave + 4, ... (R / 4 of them, the
 // padded ones included: their results are computed and not stored), so the
 // rows' work is straight-line code that the compiler interleaves.  A row's
 // reductions run over its columns lane, lane + 64 and then across the wave,
@@ -186,7 +188,7 @@ __device__ inline void qkv_pre_load(const GemmArgs& a, int g, const RowInfo* ri_
   using S = QkvShape<NG, R>;
   constexpr int C = S::C;
   if constexpr (C == 64 || C == 128) {
-    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave), lane = threadIdx.x % kWave;
+    const int wave = __builtin_amdgcn_readfirstlane((threadIdx.x / kWave) & 3), lane = threadIdx.x % kWave;
     const int rsub = lane / S::LPR, d0 = 8 * (lane % S::LPR);
     const bool is_q = g < a.hq;
     p.gn[0] = p.gn[1] = f32x4{1.f, 1.f, 1.f, 1.f};
@@ -214,7 +216,7 @@ __device__ void epilogue_qkv(const GemmArgs& a, const float* tile, int g, const 
   constexpr int C = NG * 16;  // == head_dim
   constexpr int CP = C + 4, RPW = R / 4;
   if constexpr (C == 64 || C == 128) {
-    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave), lane = threadIdx.x % kWave;
+    const int wave = __builtin_amdgcn_readfirstlane((threadIdx.x / kWave) & 3), lane = threadIdx.x % kWave;
     const int h = g;
     const bool is_q = h < a.hq, is_k = !is_q && h < a.hq + a.hkv;
     if (!is_q && !is_k) {
@@ -318,7 +320,7 @@ __device__ void epilogue_resid(const GemmArgs& a, const float* tile, int g) {
 #pragma clang fp contract(off)
   constexpr int C = NG * 16, CP = C + 4, RPW = R / 4;
   constexpr int LPR = C / 8, RPI = kWave / LPR, NIT = (RPW + RPI - 1) / RPI;
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave), lane = threadIdx.x % kWave;
+  const int wave = __builtin_amdgcn_readfirstlane((threadIdx.x / kWave) & 3), lane = threadIdx.x % kWave;
   const int rsub = lane / LPR, c0 = 8 * (lane % LPR);
   const int64_t n0 = (int64_t)g * C + c0;
   const f32x4 gv0 = *reinterpret_cast<const f32x4*>(a.g_next + n0), gv1 = *reinterpret_cast<const f32x4*>(a.g_next + n0 + 4);
@@ -382,7 +384,7 @@ __device__ void epilogue_swiglu(const GemmArgs& a, const float* tile, int g, con
   constexpr int C = NG * 16, CP = C + 4, P = NG / 2, RPW = R / 4;
   constexpr int LPR = P * 2, RPI = kWave / LPR, NIT = (RPW + RPI - 1) / RPI;
   static_assert(NG % 2 == 0, "gate/up groups hold whole pairs");
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave), lane = threadIdx.x % kWave;
+  const int wave = __builtin_amdgcn_readfirstlane((threadIdx.x / kWave) & 3), lane = threadIdx.x % kWave;
   const int rsub = lane / LPR, h0 = 8 * (lane % LPR);      // first hidden column of the lane
   const int cg = (h0 / 16) * 32 + h0 % 16, cu = cg + 16;  // its gate and up tile columns
 #pragma unroll
@@ -451,7 +453,7 @@ __device__ void epilogue_logits(const GemmArgs& a, const float* tile, int g, con
   constexpr int C = NG * 16, CP = C + 4, RPW = R / 4;
   constexpr int LPR = C / 8, RPI = kWave / LPR, NIT = (RPW + RPI - 1) / RPI;
   static_assert(LPR <= 16, "a row's lanes must lie in one DPP row");
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave), lane = threadIdx.x % kWave;
+  const int wave = __builtin_amdgcn_readfirstlane((threadIdx.x / kWave) & 3), lane = threadIdx.x % kWave;
   const int rsub = lane / LPR, c0 = 8 * (lane % LPR), n0 = g * C + c0;
   const bool vec = (a.V & 3) == 0 && n0 + 8 <= a.V;
   float bv[NIT];
@@ -524,7 +526,7 @@ __device__ void epilogue_logits(const GemmArgs& a, const float* tile, int g, con
 // SDD_EUNSUPPORTED (other group widths, too many rows).
 constexpr int kRowsMaxTBW = 5;     // row tiles per computing wave
 constexpr int kRowsMaxRows = 288;  // rows per launch: the final tile of 288 x 132 fp32 fits the 160 KB of LDS
-constexpr size_t kRowsPartBytes = (size_t)2 * kRowsMaxTBW * 8 * 4 * 64 * 16;
+constexpr size_t kRowsPartBytes = (size_t)2 * 2 * kRowsMaxTBW * 8 * 4 * 64 * 16;  // 2 slots x a pair of 8-tile groups
 int launch_gemm_rows(int ng, int epi, const GemmArgs& a, int nblocks, hipStream_t st);
 
 }  // namespace sdd
