@@ -274,6 +274,15 @@ def test_batched_verify_over_64_rows(S, n):
     _batched(S, MID_BF16, lens, 32, seed=91 + n)
 
 
+def test_batched_verify_full_width(S):
+    """Three sequences (99 rows) through one full-width Qwen3-32B layer and the real LM head: gate/up and the
+    LM head run the column-group-pair kernel at their real sizes (400 groups, one pair per workgroup; 1187
+    groups, an odd count, so the last pair holds one group, stream-K over the workgroup budget), qkv, o_proj
+    and down the many-row kernel on their stored split plans."""
+    lens = W.rng(97).integers(16, 48, size=3)
+    _batched(S, W.QWEN32B.with_layers(1), lens, 32, seed=98)
+
+
 def test_batched_ragged_long_with_skip_mask(S):
     """The batched workload at a narrow width: 8 prompts of U[256, 4096] tokens, skip mask at tau 0.7 and
     K_min 6, one verify call over the remaining sequences (variable effective batch)."""
