@@ -223,8 +223,8 @@ __device__ inline ThreadStats stats_init() { return ThreadStats{-INFINITY, -INFI
 template <int VEC, bool kSum, bool kCount, bool kIdx = true>
 __device__ __attribute__((always_inline)) inline void stats_update(ThreadStats& st, const float* v, bool valid, int e0,
                                                                    float zx, int x) {
-  // branch-free: every element takes the same instructions (selects; an invalid vector changes nothing), so
-  // the streaming loop has no divergent blocks and its loads stay in flight.  The max and first argmax are
+  // branch-free per element (selects; an invalid vector changes nothing), so the streaming loop has no
+  // divergent blocks and its loads stay in flight; two wave-uniform branches skip work no lane needs.  The max and first argmax are
   // taken per vector: vx = the vector's max over non-NaN values (fmaxf skips NaN); it replaces the running
   // max when greater (or when none is held yet), at the vector's first element equal to it -- the same
   // result as visiting the elements one by one in index order.  kIdx = false (drafter rows, whose argmax is
@@ -232,7 +232,8 @@ __device__ __attribute__((always_inline)) inline void stats_update(ThreadStats& 
   float vm = -INFINITY;  // max over finite values (reference of the sum)
   float vx = -INFINITY;  // max over non-NaN values (comparisons with NaN are false)
   float zf[VEC];         // the finite values of a valid vector, -inf elsewhere (exp(-inf - m) adds exactly 0)
-  bool nonfin = false, has = false;
+  bool nonfin = false, has = false, tie = false;
+  int gt = 0;
 #pragma unroll
   for (int t = 0; t < VEC; ++t) {
     const float z = v[t];
@@ -242,14 +243,30 @@ __device__ __attribute__((always_inline)) inline void stats_update(ThreadStats& 
     zf[t] = (valid && fin) ? z : -INFINITY;
     vm = fmaxf(vm, zf[t]);
     vx = z > vx ? z : vx;
-    if (kCount) st.cnt += (valid && (z > zx || (z == zx && e0 + t < x))) ? 1 : 0;
+    if (kCount) {
+      gt += z > zx ? 1 : 0;
+      tie |= z == zx;
+    }
+  }
+  if (kCount) {
+    // rank count: values above the draft token's, plus equal values at a lower index; the index test runs
+    // only for vectors where some lane holds an equal value (wave-uniform branch, rare for real logits)
+    st.cnt += valid ? gt : 0;
+    if (__builtin_amdgcn_ballot_w64(valid && tie)) {
+#pragma unroll
+      for (int t = 0; t < VEC; ++t) st.cnt += (valid && v[t] == zx && e0 + t < x) ? 1 : 0;
+    }
   }
   st.fl |= (valid && nonfin) ? 1 : 0;
   const bool take = valid && has && (st.a < 0 || vx > st.m);
   int idx = 0;
   if (kIdx) {
+    // the first index of the vector's max, searched only for vectors where some lane takes a new max
+    // (wave-uniform branch: after a row's first vectors a new running max is rare)
+    if (__builtin_amdgcn_ballot_w64(take)) {
 #pragma unroll
-    for (int t = VEC - 1; t >= 0; --t) idx = v[t] == vx ? t : idx;
+      for (int t = VEC - 1; t >= 0; --t) idx = v[t] == vx ? t : idx;
+    }
   }
   st.m = take ? vx : st.m;
   st.a = take ? e0 + idx : st.a;
