@@ -342,8 +342,8 @@ __global__ void __launch_bounds__(kRowsThreads, 1) gemm_rows_kernel(GemmArgs a) 
 // Column-group pairs (8-tile groups): a workgroup computes the tiles of two adjacent column groups 2p and
 // 2p + 1 over its rows, so that every k-step's activation fragments are loaded into LDS once for 256 columns
 // instead of once per 128 (halving the activation bytes a launch moves, the bulk of its loads above 64 rows).
-// All 8 waves load and compute: wave v loads weight tile v of both groups and the activation fragments of row
-// tiles v, v + 8, ... into the ring, and computes group v / 4 on row tiles v % 4 + 4 j.  The pairs are
+// All 8 waves load and compute: wave v computes group v / 4 on row tiles v % 4 + 4 j; the loads into LDS
+// are split between the waves as described at the ring constants below.  The pairs are
 // partitioned over the launch's workgroups as P x KT stream-K units with equal shares (P = ceil(G / 2) pairs,
 // P * split workgroups when P is below the workgroup budget, else that budget); each weight tile is read where
 // the matrix's own streaming plan stores it.  A row's sum runs over the k-steps in order, split pairs' partials
@@ -353,14 +353,25 @@ __global__ void __launch_bounds__(kRowsThreads, 1) gemm_pair_kernel(GemmArgs a) 
   using T = uint16_t;
   constexpr int NG = 8, C = NG * 16, CP = C + 4;
   static_assert(TBW >= 2 && TBW <= kRowsMaxTBW, "row tiles per wave");
-  constexpr int NX = 4 * TBW;                     // activation row tiles per ring stage
-  constexpr int kStage = (2 * NG + NX) * 1024;    // weight tiles of both groups, then the activation fragments
+  constexpr int NX = 4 * TBW;                     // activation row tiles per k-step
+  // Up to 256 rows (TBW <= 4) two rings: waves 0-3 load only weight tiles, into a deep ring, and waves 4-7
+  // only activation fragments, into a 3-stage one (a wave's loads complete in order, so separate depths need
+  // separate waves): the weights, from HBM, run further ahead.  At 257-288 rows the activation stages are
+  // too large for that split and one ring holds both: each wave loads weight tile v of both groups and the
+  // fragments of row tiles v, v + 8, ...
+  constexpr bool kTwo = TBW <= 4;
+  constexpr int kStage = (2 * NG + NX) * 1024;    // one ring: weight tiles of both groups, then the fragments
   constexpr int RS = std::min<int>(12, (int)(kRingBudget / kStage));
-  constexpr int XQ = NX / 8, XR = NX % 8;         // wave v loads XQ + (v < XR) activation fragments per k-step
+  constexpr int XQ = NX / 8, XR = NX % 8;         // one ring: wave v loads XQ + (v < XR) fragments per k-step
   constexpr int DHI = 2 + XQ + (XR ? 1 : 0), DLO = 2 + XQ;
+  constexpr int kWS = 2 * NG * 1024, kXS = NX * 1024;  // two rings: weight stage, activation stage
+  constexpr int RX = 3;
+  constexpr int RW = std::min<int>(12, (int)((kRingBudget - RX * kXS) / kWS));
   static_assert(XR == 0 || XR == 4, "row tiles per stage");
-  static_assert(RS >= 3 && (RS - 2) * DHI <= 63, "ring depth within the memory counter");
-  constexpr size_t kPartOff = (size_t)RS * kStage;
+  static_assert(kTwo || (RS >= 3 && (RS - 2) * DHI <= 63), "ring depth within the memory counter");
+  static_assert(!kTwo || (RW >= 3 && (RW - 2) * 4 <= 63 && (RX - 2) * TBW <= 63), "ring depths within the memory counter");
+  constexpr size_t kXOff = (size_t)RW * kWS;
+  constexpr size_t kPartOff = kTwo ? kXOff + (size_t)RX * kXS : (size_t)RS * kStage;
   constexpr size_t kBig = std::max((size_t)kRowsMaxRows * CP * 4, kPartOff + (size_t)4 * kRowsMaxRows * 4);
   __shared__ __align__(16) char s_big[kBig];
   __shared__ RowInfo s_ri[kRowsMaxRows];
@@ -373,6 +384,8 @@ __global__ void __launch_bounds__(kRowsThreads, 1) gemm_pair_kernel(GemmArgs a) 
   const int v = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave), lane = threadIdx.x % kWave;
   const int half = v >> 2, wave = v & 3;
   const bool xhi = v < XR;
+  const bool wload = v < 4;                        // two rings: this wave loads weights (else fragments)
+  const int RL = kTwo ? (wload ? RW : RX) : RS;    // depth of the ring this wave fills
   const int w = blockIdx.x;
   // storage plan of the matrix (the 33-row kernels' stream-K partition)
   const uint32_t KT = (uint32_t)a.KT, G = (uint32_t)a.G, SC = (uint32_t)a.segc, NW = (uint32_t)a.n_wg;
@@ -386,9 +399,15 @@ __global__ void __launch_bounds__(kRowsThreads, 1) gemm_pair_kernel(GemmArgs a) 
   const __amdgpu_buffer_rsrc_t nrs = __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(a.W), 0, 0, kBufferRsrcWord3);
   const __amdgpu_buffer_rsrc_t xrs = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<char*>(a.X), 0, (a.m0 + a.M) * a.ldx * (int)sizeof(T), kBufferRsrcWord3);
-  int xl[XQ + 1];  // byte offset of this lane's fragment of row tile v + 8 j (< 2^31: checked on the host)
+  // byte offset of this lane's fragment of each row tile the wave loads (< 2^31: checked on the host): one
+  // ring, row tiles v + 8 j; two rings, row tiles wave + 4 j
+  constexpr int NXL = kTwo ? TBW : XQ + 1;
+  int xl[NXL];
 #pragma unroll
-  for (int j = 0; j <= XQ; ++j) xl[j] = ((a.m0 + 16 * (v + 8 * j) + lane % 16) * a.ldx + (lane / 16) * 8) * 2;
+  for (int j = 0; j < NXL; ++j) {
+    const int rt = kTwo ? wave + 4 * j : v + 8 * j;
+    xl[j] = ((a.m0 + 16 * rt + lane % 16) * a.ldx + (lane / 16) * 8) * 2;
+  }
 
   // Where the storage plan keeps k-step k of column group g: unit g KT + k of owner o at slot
   // (g KT + k - start(o)) n_wg + o.  A tracker follows one group's owners as k rises.
@@ -419,27 +438,49 @@ __global__ void __launch_bounds__(kRowsThreads, 1) gemm_pair_kernel(GemmArgs a) 
     s.xo = (uint32_t)s.kb * 64;
     return s;
   };
-  // this wave's loads of local k-step kt into ring slot kt % RS; a k-step past the segment goes through the
-  // empty descriptor (no memory access) so that the memory-counter waits count alike on every path
+  // this wave's loads of local k-step kt (one ring: weight tile v of both groups and its fragments; two
+  // rings: a weight wave tiles 4 (v & 1) .. + 3 of group 2p + (v >> 1), an activation wave its TBW
+  // fragments).  A k-step past the segment goes through the empty descriptor (no memory access) so that the
+  // memory-counter waits count alike on every path.
   auto issue = [&](const Seg& s, bool has_b, int kt, Trk& ta, Trk& tb) {
-    char* slot = s_big + (kt % RS) * kStage;
     const bool in = kt < s.nk;
     const int k = s.kb + kt;
-    int oa = 0, ob = 0;
-    if (in) {
-      trk_adv(ta, 2 * s.p, k);
-      oa = __builtin_amdgcn_readfirstlane((ta.base + k * (int)NW) * NG * 1024 + v * 1024);
-      if (has_b) {
-        trk_adv(tb, 2 * s.p + 1, k);
-        ob = __builtin_amdgcn_readfirstlane((tb.base + k * (int)NW) * NG * 1024 + v * 1024);
+    if constexpr (!kTwo) {
+      char* slot = s_big + (kt % RS) * kStage;
+      int oa = 0, ob = 0;
+      if (in) {
+        trk_adv(ta, 2 * s.p, k);
+        oa = __builtin_amdgcn_readfirstlane((ta.base + k * (int)NW) * NG * 1024 + v * 1024);
+        if (has_b) {
+          trk_adv(tb, 2 * s.p + 1, k);
+          ob = __builtin_amdgcn_readfirstlane((tb.base + k * (int)NW) * NG * 1024 + v * 1024);
+        }
       }
-    }
-    load_lds16<kNtCpol>(in ? wrs : nrs, slot + v * 1024, lane * 16, oa);
-    load_lds16<kNtCpol>(in && has_b ? wrs : nrs, slot + (NG + v) * 1024, lane * 16, ob);
-    const __amdgpu_buffer_rsrc_t xd = in ? xrs : nrs;
+      load_lds16<kNtCpol>(in ? wrs : nrs, slot + v * 1024, lane * 16, oa);
+      load_lds16<kNtCpol>(in && has_b ? wrs : nrs, slot + (NG + v) * 1024, lane * 16, ob);
+      const __amdgpu_buffer_rsrc_t xd = in ? xrs : nrs;
 #pragma unroll
-    for (int j = 0; j <= XQ; ++j)
-      if (j < XQ || xhi) load_lds16<0>(xd, slot + (2 * NG + v + 8 * j) * 1024, xl[j], (int)(s.xo + (uint32_t)kt * 64));
+      for (int j = 0; j <= XQ; ++j)
+        if (j < XQ || xhi) load_lds16<0>(xd, slot + (2 * NG + v + 8 * j) * 1024, xl[j], (int)(s.xo + (uint32_t)kt * 64));
+    } else if (wload) {
+      char* slot = s_big + (kt % RW) * kWS;
+      const int h = v >> 1, q = 4 * (v & 1);
+      const bool valid = in && (h == 0 || has_b);
+      int off = 0;
+      if (valid) {
+        Trk& t = h ? tb : ta;
+        trk_adv(t, 2 * s.p + h, k);
+        off = __builtin_amdgcn_readfirstlane((t.base + k * (int)NW) * NG * 1024 + q * 1024);
+      }
+      const __amdgpu_buffer_rsrc_t wd = valid ? wrs : nrs;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) load_lds16<kNtCpol>(wd, slot + (h * NG + q + i) * 1024, lane * 16, off + i * 1024);
+    } else {
+      char* slot = s_big + kXOff + (kt % RX) * kXS;
+      const __amdgpu_buffer_rsrc_t xd = in ? xrs : nrs;
+#pragma unroll
+      for (int j = 0; j < TBW; ++j) load_lds16<0>(xd, slot + (wave + 4 * j) * 1024, xl[j], (int)(s.xo + (uint32_t)kt * 64));
+    }
   };
   // Row info and RMSNorm row scales, as in gemm_rows_kernel (the 33-row kernel's summation order).
   auto prologue = [&]() {
@@ -505,10 +546,10 @@ __global__ void __launch_bounds__(kRowsThreads, 1) gemm_pair_kernel(GemmArgs a) 
     const Seg s = make_seg(u);
     const bool has_b = (uint32_t)(2 * s.p + 1) < G;
     const bool mine = half == 0 || has_b;  // this wave's group exists
-    Trk ta, tb{0, 0, 0};
-    trk_at(ta, 2 * s.p, s.kb);
-    if (has_b) trk_at(tb, 2 * s.p + 1, s.kb);
-    for (int kt = 0; kt < RS - 1; ++kt) issue(s, has_b, kt, ta, tb);  // RS - 1 k-steps in flight
+    Trk ta{0, 0, 0}, tb{0, 0, 0};
+    if (!kTwo || v < 2) trk_at(ta, 2 * s.p, s.kb);
+    if (has_b && (!kTwo || (v >= 2 && v < 4))) trk_at(tb, 2 * s.p + 1, s.kb);
+    for (int kt = 0; kt < RL - 1; ++kt) issue(s, has_b, kt, ta, tb);  // RL - 1 k-steps in flight
     if (first) prologue();
     f32x4 acc[NG][TBW];
 #pragma unroll
@@ -517,23 +558,32 @@ __global__ void __launch_bounds__(kRowsThreads, 1) gemm_pair_kernel(GemmArgs a) 
       for (int j = 0; j < TBW; ++j) acc[nt][j] = f32x4{0.f, 0.f, 0.f, 0.f};
     for (int kt = 0; kt < s.nk; ++kt) {
       // this wave's loads of k-step kt have landed and its LDS reads of k-step kt - 1 are complete; after the
-      // barrier every wave's are: slot kt % RS is whole and slot (kt - 1) % RS free
-      if (xhi)
-        __builtin_amdgcn_s_waitcnt(wait_vmcnt((RS - 2) * DHI));
-      else
-        __builtin_amdgcn_s_waitcnt(wait_vmcnt((RS - 2) * DLO));
+      // barrier every wave's are: k-step kt is whole in the ring(s) and k-step kt - 1's slots are free
+      if constexpr (kTwo) {
+        if (wload)
+          __builtin_amdgcn_s_waitcnt(wait_vmcnt((RW - 2) * 4));
+        else
+          __builtin_amdgcn_s_waitcnt(wait_vmcnt((RX - 2) * TBW));
+      } else {
+        if (xhi)
+          __builtin_amdgcn_s_waitcnt(wait_vmcnt((RS - 2) * DHI));
+        else
+          __builtin_amdgcn_s_waitcnt(wait_vmcnt((RS - 2) * DLO));
+      }
       __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
       bare_barrier();
-      issue(s, has_b, kt + RS - 1, ta, tb);
+      issue(s, has_b, kt + RL - 1, ta, tb);
       // The fragments are read by LDS instructions the compiler does not see: it cannot tell them from reads of
       // the slots this wave's direct-to-LDS loads are still filling, and would wait for all of those loads
       // (the barrier above already orders them).  One wait for all of them, tied to the registers it fills.
-      const uint32_t sl = lds_ring + (uint32_t)((kt % RS) * kStage) + (uint32_t)lane * 16;
+      const uint32_t slw = lds_ring + (uint32_t)(kTwo ? (kt % RW) * kWS : (kt % RS) * kStage) + (uint32_t)lane * 16;
+      const uint32_t slx = kTwo ? lds_ring + (uint32_t)(kXOff + (kt % RX) * kXS) + (uint32_t)lane * 16
+                                : slw + (uint32_t)(2 * NG * 1024);
       u32x4 wf[NG], xf[TBW];
 #pragma unroll
-      for (int nt = 0; nt < NG; ++nt) wf[nt] = lds_read16(sl + (uint32_t)((half * NG + nt) * 1024));
+      for (int nt = 0; nt < NG; ++nt) wf[nt] = lds_read16(slw + (uint32_t)((half * NG + nt) * 1024));
 #pragma unroll
-      for (int j = 0; j < TBW; ++j) xf[j] = lds_read16(sl + (uint32_t)((2 * NG + wave + 4 * j) * 1024));
+      for (int j = 0; j < TBW; ++j) xf[j] = lds_read16(slx + (uint32_t)((wave + 4 * j) * 1024));
       asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
 #pragma unroll
       for (int nt = 0; nt < NG; ++nt) asm volatile("" : "+v"(wf[nt]));
