@@ -175,3 +175,67 @@ def test_streaming_plans_of_the_real_shapes(S, which):
         seen.add("streamk" if G > n else "split")
     assert seen == {"streamk", "split"}
     assert L.sdd_model_destroy(h) == S.OK
+
+
+@pytest.mark.parametrize("which", ["QWEN32B", "QWEN7B"])
+def test_pair_partition_reads_every_stored_tile(S, which):
+    """Host-only: the many-row kernel for the wide matrices (gate/up, LM head) covers pairs of adjacent
+    8-tile column groups, P = ceil(G / 2) pairs as P x KT units split evenly over P x min(n_wg / P, KT)
+    workgroups (or stream-K over n_wg when P >= n_wg), and finds each weight tile where the matrix's own
+    plan stores it by following the storing workgroup as k rises.  Replayed here against the documented
+    storage formula (slot (u - start(w)) n_wg + w of unit u = g KT + k, owner w): every tile of the matrix
+    is read exactly once, from its stored slot, and every pair's contributors are contiguous workgroups."""
+    import workloads as W
+    shape = getattr(W, which)
+    L = S.lib()
+    cfg = S.ModelConfig.from_shape(shape)
+    out = C.c_size_t()
+    assert L.sdd_weights_bytes(C.byref(cfg), C.byref(out)) == S.OK
+    h = C.c_void_p()
+    assert L.sdd_model_create(C.byref(cfg), C.c_void_p(1 << 20), out.value, C.byref(h)) == S.OK
+    off, nb = C.c_size_t(), C.c_size_t()
+    kt, g, ng, nwg, sc = C.c_int(), C.c_int(), C.c_int(), C.c_int(), C.c_int()
+    for kind in (S.T_WGATE, S.T_LM_HEAD):
+        assert L.sdd_model_matrix_layout(h, kind, 0, C.byref(off), C.byref(nb), C.byref(kt), C.byref(g), C.byref(ng),
+                                         C.byref(nwg), C.byref(sc)) == S.OK
+        KT, G, n, c = kt.value, g.value, nwg.value, sc.value
+        assert ng.value == 8
+        st = share_starts(KT, G, c, n)  # storage plan
+        P = (G + 1) // 2
+        NP = n if P >= n else P * min(n // P, KT)
+        pst = np.arange(NP + 1, dtype=np.int64) * (P * KT) // NP  # pair partition, equal shares
+        assert (np.diff(pst) >= 1).all()
+        seen = np.zeros(G * KT, np.int32)
+
+        def owner(u):
+            return int(np.searchsorted(st, u, side="right")) - 1
+
+        for w in range(NP):
+            u = int(pst[w])
+            while u < pst[w + 1]:
+                p = u // KT
+                kb = u - p * KT
+                ke = min(KT, kb + int(pst[w + 1]) - u)
+                for gg in (2 * p, 2 * p + 1):
+                    if gg >= G:
+                        continue
+                    o = owner(gg * KT + kb)  # tracker: owner of the segment's first k-step, then advance
+                    kend = int(st[o + 1]) - gg * KT
+                    base = (gg * KT - int(st[o])) * n + o
+                    for k in range(kb, ke):
+                        while k >= kend:
+                            o += 1
+                            kend = int(st[o + 1]) - gg * KT
+                            base = (gg * KT - int(st[o])) * n + o
+                        uu = gg * KT + k
+                        ref = (uu - int(st[owner(uu)])) * n + owner(uu)
+                        assert base + k * n == ref
+                        assert 0 <= ref * 8 * 1024 < nb.value
+                        seen[uu] += 1
+                if not (kb == 0 and ke == KT):  # a split pair: its contributors are w's neighbours
+                    wf = int(np.searchsorted(pst, p * KT, side="right")) - 1
+                    wl = int(np.searchsorted(pst, (p + 1) * KT - 1, side="right")) - 1
+                    assert wf <= w <= wl
+                u += ke - kb
+        assert (seen == 1).all(), kind
+    assert L.sdd_model_destroy(h) == S.OK
